@@ -1,0 +1,263 @@
+/*
+ * oracle.c -- plain fp64 CPU oracle for the block-hybrid attention layer of
+ * "Retrofitting Linear Attention into Diffusion Language Models".
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the library path may link, load or
+ * call this file; only the tests, the smoke check and the CPU-baseline leg of
+ * the benchmark do.  It shares no source with the HIP library: every index
+ * below is written from the documented buffer layouts, not from the kernels.
+ *
+ * Every quantity is evaluated in double precision, literally as the paper
+ * defines it (no max-shift, no blocking, no reordering).  The only guard is
+ * that a softmax exponent must stay below 700 in magnitude, so that exp()
+ * cannot overflow a double; a call that would break it returns 1.
+ *
+ * Layouts (row-major, contiguous, indices outermost first):
+ *   q, out        [B][L][Hq][d]      (prefill: [B][T][Hq][d])
+ *   k, v          [B][L][Hkv][d]     (prefill: [B][T][Hkv][d])
+ *   Wt            [Hq][F][d]         Wt[h][j][i] = W_h[i][j], W_h in R^{d x F}
+ *   alpha         [Hq]               gate logit, w = sigmoid(alpha)
+ *   S             [n_slots][Hq][2F][d]
+ *   z             [n_slots][Hq][2F]
+ *   slots         [B] or NULL        state slot of request b (NULL: slot b)
+ *   k_cache,v_cache [B][Pmax][Hkv][d], request b uses its first plen[b] rows
+ * Query head h reads KV head h / (Hq / Hkv).
+ *
+ * Build: gcc -O2 -fopenmp -shared -fPIC oracle.c -o liboracle.so -lm
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#define EXP_LIMIT 700.0
+
+/* Feature map of Section 3.1 ("Across blocks"):
+ *   phi(x) = [ softmax(x W), softmax(-x W) ]  in R^{2F},
+ * with the softmax taken over the F entries of the row vector x W.
+ * The paper fixes no stabilising shift; the literal exp is used and the
+ * exponent is checked.  Returns 1 if |x W|_inf >= EXP_LIMIT. */
+static int feature_map(const double *x, const double *Wt, int d, int F,
+                       double *phi) {
+  double *pos = phi, *neg = phi + F;
+  double sum_pos = 0.0, sum_neg = 0.0;
+  for (int j = 0; j < F; ++j) {
+    double u = 0.0; /* (x W)_j = sum_i x_i W[i][j] */
+    for (int i = 0; i < d; ++i) u += x[i] * Wt[(size_t)j * d + i];
+    if (fabs(u) >= EXP_LIMIT) return 1;
+    pos[j] = exp(u);
+    neg[j] = exp(-u);
+    sum_pos += pos[j];
+    sum_neg += neg[j];
+  }
+  for (int j = 0; j < F; ++j) {
+    pos[j] /= sum_pos;
+    neg[j] /= sum_neg;
+  }
+  return 0;
+}
+
+/* w = sigma(alpha), the per-head gate of Section 3.1 ("Combining the two
+ * branches"). */
+static double gate(double alpha) { return 1.0 / (1.0 + exp(-alpha)); }
+
+/* One query of the block-hybrid output (Section 3.1):
+ *   a_j     = exp(q . k_j / sqrt(d))                   over the active block
+ *   sm_num  = sum_j a_j v_j,    sm_den = sum_j a_j
+ *   lin_num = phi(q)^T S,       lin_den = phi(q)^T Z
+ *   out     = (w sm_num + lin_num) / (w sm_den + lin_den)
+ * kblk/vblk point at the first block token; consecutive block tokens are
+ * tok_stride doubles apart.  scratch holds 2F + d doubles. */
+static int hybrid_query(const double *q, const double *kblk,
+                        const double *vblk, size_t tok_stride, int L, int d,
+                        int F, const double *Wt, double w, const double *S,
+                        const double *z, double *scratch, double *out) {
+  const int f = 2 * F;
+  double *phi = scratch, *sm_num = scratch + f;
+  double sm_den = 0.0;
+  for (int c = 0; c < d; ++c) sm_num[c] = 0.0;
+  for (int j = 0; j < L; ++j) {
+    const double *kj = kblk + (size_t)j * tok_stride;
+    const double *vj = vblk + (size_t)j * tok_stride;
+    double s = 0.0;
+    for (int i = 0; i < d; ++i) s += q[i] * kj[i];
+    s /= sqrt((double)d);
+    if (fabs(s) >= EXP_LIMIT) return 1;
+    double a = exp(s);
+    sm_den += a;
+    for (int c = 0; c < d; ++c) sm_num[c] += a * vj[c];
+  }
+  if (feature_map(q, Wt, d, F, phi)) return 1;
+  double lin_den = 0.0;
+  for (int r = 0; r < f; ++r) lin_den += phi[r] * z[r];
+  double den = w * sm_den + lin_den;
+  for (int c = 0; c < d; ++c) {
+    double lin_num = 0.0;
+    for (int r = 0; r < f; ++r) lin_num += phi[r] * S[(size_t)r * d + c];
+    out[c] = (w * sm_num[c] + lin_num) / den;
+  }
+  return 0;
+}
+
+/* Commit of one token (Section 3.1 state update):
+ *   S += phi(k) v^T,   Z += phi(k). */
+static int commit_token(const double *kt, const double *vt, int d, int F,
+                        const double *Wt, double *S, double *z,
+                        double *phi) {
+  const int f = 2 * F;
+  if (feature_map(kt, Wt, d, F, phi)) return 1;
+  for (int r = 0; r < f; ++r) {
+    z[r] += phi[r];
+    for (int c = 0; c < d; ++c) S[(size_t)r * d + c] += phi[r] * vt[c];
+  }
+  return 0;
+}
+
+static int slot_of(const int32_t *slots, int b) { return slots ? slots[b] : b; }
+
+/* hybrid step: every query of the active block of every request and head. */
+int oracle_step(int B, int Hq, int Hkv, int d, int L, int F, const double *q,
+                const double *k, const double *v, const double *Wt,
+                const double *alpha, const double *S, const double *z,
+                const int32_t *slots, double *out) {
+  const int G = Hq / Hkv, f = 2 * F;
+  int err = 0;
+#pragma omp parallel for schedule(dynamic) reduction(| : err)
+  for (long u = 0; u < (long)B * Hq; ++u) {
+    const int b = (int)(u / Hq), h = (int)(u % Hq), g = h / G;
+    const int slot = slot_of(slots, b);
+    const double *Sh = S + ((size_t)slot * Hq + h) * f * d;
+    const double *zh = z + ((size_t)slot * Hq + h) * f;
+    const double *Wh = Wt + (size_t)h * F * d;
+    const double w = gate(alpha[h]);
+    double *scratch = (double *)malloc(sizeof(double) * (f + d));
+    const double *kblk = k + ((size_t)b * L * Hkv + g) * d;
+    const double *vblk = v + ((size_t)b * L * Hkv + g) * d;
+    for (int i = 0; i < L; ++i) {
+      const size_t qo = (((size_t)b * L + i) * Hq + h) * d;
+      err |= hybrid_query(q + qo, kblk, vblk, (size_t)Hkv * d, L, d, F, Wh, w,
+                          Sh, zh, scratch, out + qo);
+    }
+    free(scratch);
+  }
+  return err;
+}
+
+/* commit: fold every token of the given block into the state of its slot. */
+int oracle_commit(int B, int Hq, int Hkv, int d, int L, int F, const double *k,
+                  const double *v, const double *Wt, double *S, double *z,
+                  const int32_t *slots) {
+  const int G = Hq / Hkv, f = 2 * F;
+  int err = 0;
+#pragma omp parallel for schedule(dynamic) reduction(| : err)
+  for (long u = 0; u < (long)B * Hq; ++u) {
+    const int b = (int)(u / Hq), h = (int)(u % Hq), g = h / G;
+    const int slot = slot_of(slots, b);
+    double *Sh = S + ((size_t)slot * Hq + h) * f * d;
+    double *zh = z + ((size_t)slot * Hq + h) * f;
+    const double *Wh = Wt + (size_t)h * F * d;
+    double *phi = (double *)malloc(sizeof(double) * f);
+    for (int t = 0; t < L; ++t) {
+      const size_t ko = (((size_t)b * L + t) * Hkv + g) * d;
+      err |= commit_token(k + ko, v + ko, d, F, Wh, Sh, zh, phi);
+    }
+    free(phi);
+  }
+  return err;
+}
+
+/* prefill of T = nblk * L tokens with the block-causal pattern of Figure 2:
+ * block c is first read against the state of blocks 0..c-1 (hybrid step),
+ * then committed.  out may be NULL (state only); q is then unused.  The state
+ * starts from whatever S, z hold, so a prefill continues an earlier one. */
+int oracle_prefill(int B, int T, int Hq, int Hkv, int d, int L, int F,
+                   const double *q, const double *k, const double *v,
+                   const double *Wt, const double *alpha, double *S, double *z,
+                   const int32_t *slots, double *out) {
+  const int G = Hq / Hkv, f = 2 * F;
+  if (L <= 0 || T % L != 0) return 2;
+  const int nblk = T / L;
+  int err = 0;
+#pragma omp parallel for schedule(dynamic) reduction(| : err)
+  for (long u = 0; u < (long)B * Hq; ++u) {
+    const int b = (int)(u / Hq), h = (int)(u % Hq), g = h / G;
+    const int slot = slot_of(slots, b);
+    double *Sh = S + ((size_t)slot * Hq + h) * f * d;
+    double *zh = z + ((size_t)slot * Hq + h) * f;
+    const double *Wh = Wt + (size_t)h * F * d;
+    const double w = gate(alpha[h]);
+    double *scratch = (double *)malloc(sizeof(double) * (f + d));
+    for (int c = 0; c < nblk; ++c) {
+      const size_t t0 = (size_t)c * L;
+      const double *kblk = k + (((size_t)b * T + t0) * Hkv + g) * d;
+      const double *vblk = v + (((size_t)b * T + t0) * Hkv + g) * d;
+      if (out) {
+        for (int i = 0; i < L; ++i) {
+          const size_t qo = (((size_t)b * T + t0 + i) * Hq + h) * d;
+          err |= hybrid_query(q + qo, kblk, vblk, (size_t)Hkv * d, L, d, F,
+                              Wh, w, Sh, zh, scratch, out + qo);
+        }
+      }
+      for (int t = 0; t < L; ++t) {
+        const size_t ko = (((size_t)b * T + t0 + t) * Hkv + g) * d;
+        err |= commit_token(k + ko, v + ko, d, F, Wh, Sh, zh, scratch);
+      }
+    }
+    free(scratch);
+  }
+  return err;
+}
+
+/* Exact softmax attention (Section 2.2 display, without the causal mask
+ * inside the block) of every block query over the request's cached prefix
+ * plus all L block keys:
+ *   out_i = sum_j exp(s_ij) v_j / sum_j exp(s_ij),  s_ij = q_i . k_j / sqrt(d)
+ * j runs over k_cache[b][0 .. plen[b]-1] followed by the block keys. */
+int oracle_softmax_prefix(int B, int Hq, int Hkv, int d, int L, int Pmax,
+                          const double *q, const double *k, const double *v,
+                          const double *k_cache, const double *v_cache,
+                          const int32_t *plen, double *out) {
+  const int G = Hq / Hkv;
+  int err = 0;
+#pragma omp parallel for schedule(dynamic) reduction(| : err)
+  for (long u = 0; u < (long)B * Hq * L; ++u) {
+    const int i = (int)(u % L);
+    const int h = (int)((u / L) % Hq), b = (int)(u / ((long)L * Hq));
+    const int g = h / G, P = plen[b];
+    const size_t qo = (((size_t)b * L + i) * Hq + h) * d;
+    const double *qi = q + qo;
+    double *acc = (double *)calloc((size_t)d, sizeof(double));
+    double den = 0.0;
+    for (int j = 0; j < P + L; ++j) {
+      const double *kj, *vj;
+      if (j < P) {
+        const size_t o = (((size_t)b * Pmax + j) * Hkv + g) * d;
+        kj = k_cache + o;
+        vj = v_cache + o;
+      } else {
+        const size_t o = (((size_t)b * L + (j - P)) * Hkv + g) * d;
+        kj = k + o;
+        vj = v + o;
+      }
+      double s = 0.0;
+      for (int t = 0; t < d; ++t) s += qi[t] * kj[t];
+      s /= sqrt((double)d);
+      if (fabs(s) >= EXP_LIMIT) err = 1;
+      double a = exp(s);
+      den += a;
+      for (int c = 0; c < d; ++c) acc[c] += a * vj[c];
+    }
+    for (int c = 0; c < d; ++c) out[qo + c] = acc[c] / den;
+    free(acc);
+  }
+  return err;
+}
+
+/* The feature map alone, for pinning it: X [n][d] -> PHI [n][2F]. */
+int oracle_feature_map(int n, int d, int F, const double *X, const double *Wt,
+                       double *PHI) {
+  int err = 0;
+  for (int t = 0; t < n; ++t)
+    err |= feature_map(X + (size_t)t * d, Wt, d, F, PHI + (size_t)t * 2 * F);
+  return err;
+}
