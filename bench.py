@@ -1,0 +1,362 @@
+#!/usr/bin/env python3
+"""Benchmark of the block-hybrid attention hot path on one MI355X.
+
+Workload (serving): 64 concurrent requests, 16 query / 4 KV heads, head_dim
+128, 32-token active block, feature dim f = 128 (W_h is 128 x 64), bf16
+activations, fp32 states of per-request committed prefixes of 1k..32k tokens
+(built by hybrid_state_prefill before timing).  The serving cadence of block
+diffusion is 8 denoising steps of the active block, then one commit.
+
+One benchmark step = one block cycle over R = 8 rotating state sets ("lanes",
+as many as the hybrid layers of the model, 6 in the paper, rounded up): for
+each of the 8 denoising steps, hybrid_attn_step on every lane, then
+hybrid_state_commit on every lane.  Every lane owns its states and block
+buffers, so each kernel reads its 64 MiB of state from HBM rather than from
+the 256 MB Infinity Cache, as in a real model forward.
+
+value = query tokens through the hybrid layer per second
+      = 8 steps * R lanes * B * L / (time of one block cycle).
+
+The roofline object is for the step kernel: algorithmic bytes per launch
+(every tensor counted once) over its mean duration, measured with HIP events
+around each launch on the stream the kernel runs on.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+import torch
+
+from paper_2608_06628_amd import binding as hb
+from paper_2608_06628_amd import synth
+
+HBM_PEAK_GBPS = 8000.0
+BF16_MFMA_PEAK_TFLOPS = 2500.0
+METRIC = ("hybrid denoise-step tokens/sec + achieved HBM GB/s "
+          "(B=64,Hq16/Hkv4,d128,blk32)")
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def step_bytes(B, Hq, Hkv, d, L, f, es=2):
+    """Algorithmic bytes of one hybrid_attn_step launch."""
+    F = f // 2
+    q = o = B * L * Hq * d * es
+    kv = 2 * B * L * Hkv * d * es
+    S = B * Hq * f * d * 4
+    z = B * Hq * f * 4
+    W = Hq * F * d * es
+    return q + kv + S + z + o + W + Hq * 4
+
+
+def commit_bytes(B, Hq, Hkv, d, L, f, es=2):
+    """Algorithmic bytes of one hybrid_state_commit launch (S, z read + written)."""
+    F = f // 2
+    kv = 2 * B * L * Hkv * d * es
+    S = 2 * B * Hq * f * d * 4
+    z = 2 * B * Hq * f * 4
+    W = Hq * F * d * es
+    return kv + S + z + W
+
+
+def step_flops(B, Hq, d, L, f):
+    F = f // 2
+    per = 2 * L * d * F + 2 * L * L * d + 2 * L * L * d + 2 * L * f * d + 2 * L * f
+    return B * Hq * per
+
+
+def prefill_flops(B, T, Hq, d, L, f):
+    """Block-causal prefill: per block the step work plus phi(K) and the update."""
+    F = f // 2
+    nblk = T // L
+    per_blk = (2 * L * d * F) * 2 + 2 * L * L * d * 2 + 2 * L * f * d * 2
+    return B * Hq * nblk * per_blk
+
+
+class Lane:
+    """One rotating set of states and per-step block buffers."""
+
+    def __init__(self, dims, S, z, qkv_sets):
+        self.S = S.clone()
+        self.z = z.clone()
+        self.qkv = [(q.clone(), k.clone(), v.clone(), torch.empty_like(q)) for q, k, v in qkv_sets]
+
+
+def build_states(dims, plens, W, gen, dev):
+    """Per-request states of synthetic bf16 prefixes, built by the GPU prefill."""
+    S = torch.zeros((dims.B, dims.Hq, dims.f, dims.d), device=dev)
+    z = torch.zeros((dims.B, dims.Hq, dims.f), device=dev)
+    scale = 1.0 / math.sqrt(dims.d)
+    for b, P in enumerate(plens.tolist()):
+        kp = (torch.randn((1, P, dims.Hkv, dims.d), generator=gen, device=dev) * scale).to(torch.bfloat16)
+        vp = (torch.randn((1, P, dims.Hkv, dims.d), generator=gen, device=dev) * scale).to(torch.bfloat16)
+        hb.hybrid_state_prefill(None, kp, vp, W, None, S[b:b + 1], z[b:b + 1], dims.L,
+                                want_out=False)
+    torch.cuda.synchronize()
+    return S, z
+
+
+def time_region(fn, iters):
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record()
+    for _ in range(iters):
+        fn()
+    b.record()
+    torch.cuda.synchronize()
+    return a.elapsed_time(b) / iters
+
+
+def cpu_baseline(dims, n_req, plens, budget_s=10.0):
+    """The fp64 oracle timed on the host cores: whole block cycles (8 steps +
+    1 commit) over n_req requests, repeated until about budget_s seconds."""
+    import oracle
+    rng = np.random.default_rng(1234)
+    sub = dims.with_(B=n_req)
+    q, k, v = synth.block_qkv(sub, 5, 1.0 / math.sqrt(dims.d))
+    Wt, alpha = synth.feature_weights(sub, 6, 7)
+    S = rng.standard_normal((n_req, dims.Hq, dims.f, dims.d)) * 0.05
+    z = np.abs(rng.standard_normal((n_req, dims.Hq, dims.f))) * float(np.mean(plens)) / dims.F
+    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    cycles = 0
+    t0 = time.perf_counter()
+    while True:
+        for _ in range(synth.SERVE64_STEPS_PER_BLOCK):
+            oracle.step(q, k, v, Wt, alpha, S, z)
+        S, z = oracle.commit(k, v, Wt, S, z)
+        cycles += 1
+        el = time.perf_counter() - t0
+        if el >= budget_s:
+            break
+    tokens = cycles * synth.SERVE64_STEPS_PER_BLOCK * n_req * dims.L
+    return {"value": tokens / el, "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"{cycles} block cycles (8 steps + 1 commit) of {n_req} requests x 16 heads "
+                      f"in {el:.1f} s, fp64, OpenMP over (request, head)"}
+
+
+def run(args):
+    dev = "cuda"
+    dims = synth.SERVE64
+    B, Hq, Hkv, d, L, f = dims.B, dims.Hq, dims.Hkv, dims.d, dims.L, dims.f
+    R, NSTEP = args.lanes, synth.SERVE64_STEPS_PER_BLOCK
+    gen = torch.Generator(device=dev)
+    gen.manual_seed(3)
+    plens = synth.serve_prefix_lengths(B)
+    Wt_np, alpha_np = synth.feature_weights(dims, 1, 2)
+    W = torch.from_numpy(Wt_np).to(dev).to(torch.bfloat16)
+    alpha = torch.from_numpy(alpha_np).to(dev)
+
+    log(f"building {B} states from {int(plens.sum())} prefix tokens by prefill")
+    t0 = time.time()
+    S0, z0 = build_states(dims, plens, W, gen, dev)
+    log(f"states built in {time.time() - t0:.1f} s")
+    scale = 1.0 / math.sqrt(d)
+    qkv_sets = []
+    for s in range(NSTEP):
+        q = (torch.randn((B, L, Hq, d), generator=gen, device=dev) * scale).to(torch.bfloat16)
+        k = (torch.randn((B, L, Hkv, d), generator=gen, device=dev) * scale).to(torch.bfloat16)
+        v = (torch.randn((B, L, Hkv, d), generator=gen, device=dev) * scale).to(torch.bfloat16)
+        qkv_sets.append((q, k, v))
+    lanes = [Lane(dims, S0, z0, qkv_sets) for _ in range(R)]
+    del S0, z0
+    torch.cuda.synchronize()
+    log(f"{R} lanes allocated ({torch.cuda.memory_allocated() / 2**30:.2f} GiB in use)")
+
+    ev_pairs = []
+
+    def cycle(record):
+        for s in range(NSTEP):
+            for ln in lanes:
+                q, k, v, o = ln.qkv[s]
+                if record:
+                    e0 = torch.cuda.Event(enable_timing=True)
+                    e1 = torch.cuda.Event(enable_timing=True)
+                    e0.record()
+                hb.hybrid_attn_step(q, k, v, W, alpha, ln.S, ln.z, out=o)
+                if record:
+                    e1.record()
+                    ev_pairs.append(("step", e0, e1))
+        for ln in lanes:
+            q, k, v, o = ln.qkv[NSTEP - 1]
+            if record:
+                e0 = torch.cuda.Event(enable_timing=True)
+                e1 = torch.cuda.Event(enable_timing=True)
+                e0.record()
+            hb.hybrid_state_commit(k, v, W, ln.S, ln.z)
+            if record:
+                e1.record()
+                ev_pairs.append(("commit", e0, e1))
+
+    for _ in range(args.warmup):
+        cycle(False)
+    torch.cuda.synchronize()
+    log(f"warmup done ({args.warmup} cycles); timing {args.steps} cycles")
+    # Whole-cycle time without per-kernel events.
+    a = torch.cuda.Event(enable_timing=True)
+    b = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    a.record()
+    for _ in range(args.steps):
+        cycle(False)
+    b.record()
+    torch.cuda.synchronize()
+    ms_cycle = a.elapsed_time(b) / args.steps
+    # Per-kernel durations, bracketed by events on the launch stream.
+    for _ in range(args.steps):
+        cycle(True)
+    torch.cuda.synchronize()
+    durs = {"step": [], "commit": []}
+    for kind, e0, e1 in ev_pairs:
+        durs[kind].append(e0.elapsed_time(e1))
+    t_step = float(np.mean(durs["step"])) * 1e-3
+    t_commit = float(np.mean(durs["commit"])) * 1e-3
+    sb = step_bytes(B, Hq, Hkv, d, L, f)
+    cb = commit_bytes(B, Hq, Hkv, d, L, f)
+    step_gbps = sb / t_step / 1e9
+    commit_gbps = cb / t_commit / 1e9
+    for ln in lanes:
+        assert torch.isfinite(ln.qkv[0][3].float()).all(), "non-finite step output"
+    log(f"cycle {ms_cycle:.3f} ms; step {t_step * 1e6:.2f} us ({step_gbps:.0f} GB/s); "
+        f"commit {t_commit * 1e6:.2f} us ({commit_gbps:.0f} GB/s)")
+
+    tokens = NSTEP * R * B * L
+    value = tokens / (ms_cycle * 1e-3)
+    result = {
+        "metric": METRIC, "value": value, "unit": "tokens/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_cycle,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": "serve64: B=64 requests, Hq=16, Hkv=4, d=128, block 32, f=128, "
+                               "prefixes 1k-32k tokens, 8 denoising steps then 1 commit",
+                   "global_batch": B, "seq_len": L, "lanes": R, "parallelism": "none (1 GPU)",
+                   "state_dtype": "fp32", "prefix_tokens": int(plens.sum())},
+        "roofline": {"bound": "hbm", "achieved": step_gbps, "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": step_gbps / HBM_PEAK_GBPS, "traffic": None,
+                     "kernel": "hyb_step_kernel<bf16,128,64>",
+                     "algorithmic_bytes_per_launch": sb, "mean_launch_us": t_step * 1e6},
+        "step_kernel": {"mean_us": t_step * 1e6, "p10_us": float(np.percentile(durs["step"], 10)) * 1e3,
+                        "p90_us": float(np.percentile(durs["step"], 90)) * 1e3,
+                        "gbps": step_gbps, "tokens_per_s": B * L / t_step,
+                        "tflops": step_flops(B, Hq, d, L, f) / t_step / 1e12},
+        "commit_kernel": {"mean_us": t_commit * 1e6, "gbps": commit_gbps,
+                          "bytes_per_launch": cb, "frac": commit_gbps / HBM_PEAK_GBPS},
+    }
+    del lanes
+    torch.cuda.empty_cache()
+
+    if not args.no_extras:
+        result["prefill"] = bench_prefill(gen, dev)
+        result["softmax_prefix"] = bench_mix(gen, dev)
+    if not args.no_cpu_baseline:
+        log("timing the fp64 oracle on the host cores")
+        result["cpu_baseline"] = cpu_baseline(dims, args.cpu_requests, plens)
+    print(json.dumps(result), flush=True)
+
+
+def bench_prefill(gen, dev):
+    dims = synth.PREFILL8
+    B, Hq, Hkv, d, L, f, T = dims.B, dims.Hq, dims.Hkv, dims.d, dims.L, dims.f, synth.PREFILL8_T
+    scale = 1.0 / math.sqrt(d)
+    q = (torch.randn((B, T, Hq, d), generator=gen, device=dev) * scale).to(torch.bfloat16)
+    k = (torch.randn((B, T, Hkv, d), generator=gen, device=dev) * scale).to(torch.bfloat16)
+    v = (torch.randn((B, T, Hkv, d), generator=gen, device=dev) * scale).to(torch.bfloat16)
+    Wt, alpha = synth.feature_weights(dims, 1, 2)
+    W = torch.from_numpy(Wt).to(dev).to(torch.bfloat16)
+    al = torch.from_numpy(alpha).to(dev)
+    S = torch.zeros((B, Hq, f, d), device=dev)
+    z = torch.zeros((B, Hq, f), device=dev)
+    out = torch.empty_like(q)
+
+    def once():
+        S.zero_()
+        z.zero_()
+        hb.hybrid_state_prefill(q, k, v, W, al, S, z, L, out=out)
+
+    once()
+    ms = time_region(once, 5)
+    byts = (q.numel() + k.numel() + v.numel() + out.numel()) * 2 + 2 * S.numel() * 4
+    fl = prefill_flops(B, T, Hq, d, L, f)
+    log(f"prefill8 {ms:.3f} ms")
+    return {"workload": "prefill8: B=8 x 8192 tokens, 16q/4kv, d=128, f=128, blocks of 32",
+            "ms": ms, "prompt_tokens_per_s": B * T / (ms * 1e-3),
+            "gbps": byts / (ms * 1e-3) / 1e9, "hbm_frac": byts / (ms * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+            "tflops": fl / (ms * 1e-3) / 1e12,
+            "mfma_frac": fl / (ms * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS,
+            "note": "includes two zero-fills of the 8 MiB state"}
+
+
+def bench_mix(gen, dev):
+    dims = synth.MIX128
+    B, Hq, Hkv, d, L, f, P = dims.B, dims.Hq, dims.Hkv, dims.d, dims.L, dims.f, synth.MIX128_PREFIX
+    scale = 1.0 / math.sqrt(d)
+    kc = (torch.randn((B, P, Hkv, d), generator=gen, device=dev) * scale).to(torch.bfloat16)
+    vc = (torch.randn((B, P, Hkv, d), generator=gen, device=dev) * scale).to(torch.bfloat16)
+    q = (torch.randn((B, L, Hq, d), generator=gen, device=dev) * scale).to(torch.bfloat16)
+    k = (torch.randn((B, L, Hkv, d), generator=gen, device=dev) * scale).to(torch.bfloat16)
+    v = (torch.randn((B, L, Hkv, d), generator=gen, device=dev) * scale).to(torch.bfloat16)
+    plen = torch.full((B,), P, dtype=torch.int32, device=dev)
+    out = torch.empty_like(q)
+    ws = torch.empty(hb.workspace_bytes(hb.make_dims(B, Hq, Hkv, d, L, 64, hb.HYB_BF16, 1),
+                                        hb.OP_SOFTMAX_PREFIX, P), dtype=torch.uint8, device=dev)
+    sm = lambda: hb.softmax_prefix_step(q, k, v, kc, vc, plen, out=out, ws=ws)
+    sm()
+    ms_sm = time_region(sm, 5)
+    del kc, vc
+    torch.cuda.empty_cache()
+    # hybrid step at the same batch; 4 rotating state sets keep it cache-cold
+    Wt, alpha = synth.feature_weights(dims, 1, 2)
+    W = torch.from_numpy(Wt).to(dev).to(torch.bfloat16)
+    al = torch.from_numpy(alpha).to(dev)
+    states = [(torch.rand((B, Hq, f, d), generator=gen, device=dev) * 0.01,
+               torch.rand((B, Hq, f), generator=gen, device=dev) * P / 64 + 1.0) for _ in range(4)]
+    i = [0]
+
+    def hy():
+        S, z = states[i[0] % 4]
+        i[0] += 1
+        hb.hybrid_attn_step(q, k, v, W, al, S, z, out=out)
+
+    hy()
+    ms_hy = time_region(hy, 40)
+    sm_bytes = 2 * B * P * Hkv * d * 2 + (2 * B * L * Hq * d + 2 * B * L * Hkv * d) * 2
+    sm_flops = 4 * B * Hq * L * (P + L) * d
+    hy_bytes = step_bytes(B, Hq, Hkv, d, L, f)
+    log(f"mix128: softmax {ms_sm:.3f} ms, hybrid {ms_hy * 1e3:.1f} us")
+    return {"workload": "mix128: B=128, 16q/4kv, d=128, block 32, prefix 32768, bf16 KV cache",
+            "softmax_ms": ms_sm, "softmax_gbps": sm_bytes / (ms_sm * 1e-3) / 1e9,
+            "softmax_hbm_frac": sm_bytes / (ms_sm * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+            "softmax_tflops": sm_flops / (ms_sm * 1e-3) / 1e12,
+            "hybrid_us": ms_hy * 1e3, "hybrid_gbps": hy_bytes / (ms_hy * 1e-3) / 1e9,
+            "speedup": ms_sm / ms_hy,
+            "mix_6h14s_vs_20s": (20 * ms_sm) / (6 * ms_hy + 14 * ms_sm)}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--lanes", type=int, default=8)
+    ap.add_argument("--cpu-requests", type=int, default=64)
+    ap.add_argument("--no-extras", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: the hybrid layer shards by request or KV-head "
+              "group with no exchange, and this build runs on a single MI355X only.",
+              file=sys.stderr)
+        sys.exit(2)
+    run(args)
+
+
+if __name__ == "__main__":
+    main()

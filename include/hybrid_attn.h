@@ -1,0 +1,162 @@
+/*
+ * hybrid_attn.h -- C ABI of libhybattn, the MI355X (gfx950) block-hybrid
+ * attention library.
+ *
+ * Method: "Retrofitting Linear Attention into Diffusion Language Models",
+ * Section 3.1.  For a query q of the active block, with a per-query-head
+ * feature map phi(x) = [softmax(xW), softmax(-xW)] (W in R^{d x F}, so phi has
+ * f = 2F entries) and a committed-context state S (f x d), Z (f):
+ *   sm_num  = sum_j exp(q.k_j/sqrt(d)) v_j,   sm_den = sum_j exp(q.k_j/sqrt(d))
+ *             (j over all L tokens of the active block, no mask)
+ *   lin_num = phi(q)^T S,                     lin_den = phi(q)^T Z
+ *   out     = (w sm_num + lin_num) / (w sm_den + lin_den),  w = sigmoid(alpha)
+ * and committing a block adds sum_t phi(k_t) v_t^T to S and sum_t phi(k_t)
+ * to Z.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * Memory.  Every pointer argument is a device pointer (hipMalloc'ed or
+ *   equivalent), owned by the caller.  The library never allocates or frees
+ *   device memory; a scratch buffer, where one is needed, is the caller's
+ *   workspace of at least hybrid_workspace_bytes() bytes.
+ * Alignment.  Every pointer must be 16-byte aligned.
+ * Layouts.  Row-major, contiguous, outermost index first:
+ *   q, out        [B][L][Hq][d]        (prefill: [B][T][Hq][d])
+ *   k, v          [B][L][Hkv][d]       (prefill: [B][T][Hkv][d])
+ *   W             [Hq][F][d]           row j of head h is column j of W_h;
+ *                                      this is the weight layout of a linear
+ *                                      layer d -> F
+ *   alpha         [Hq] float           gate logits; the library forms sigmoid
+ *   S             [n_slots][Hq][f][d] float   S_h as defined above (rows =
+ *                                      features, columns = value dims)
+ *   z             [n_slots][Hq][f] float
+ *   slots         [B] int32 or NULL    state slot of request b; NULL means
+ *                                      slot b.  A slot outside [0, n_slots)
+ *                                      makes that request's outputs NaN and
+ *                                      leaves every state untouched.
+ *   k_cache, v_cache [B][max_prefix][Hkv][d]; request b uses rows
+ *                                      0 .. prefix_len[b]-1.
+ *   Query head h reads KV head h / (Hq / Hkv).
+ * Types.  q, k, v, W and the KV cache share dims->dtype (fp32 or bf16), and so
+ *   does out unless dims->flags has HYB_OUT_F32; alpha, S and z are always
+ *   fp32.  All accumulation is fp32.  On the bf16 path the matrix-core
+ *   operands are bf16: phi(q) and the state read by a step are rounded to
+ *   bf16 (round to nearest even), while the block softmax weights and phi(k)
+ *   in a state update are carried as a bf16 pair hi + lo (about 16 bits).
+ *   A bf16 out is the rounded fp32 result.
+ * Execution.  Work is enqueued on `stream` (a hipStream_t; NULL = the null
+ *   stream) and the call returns without synchronising.  Results are
+ *   bitwise reproducible from run to run (no atomics).
+ * Validation.  Every check below runs on the host before anything is
+ *   enqueued.  On failure the call returns the status, enqueues nothing,
+ *   touches no output and sets a message readable with hybrid_last_error().
+ *   Values that live in device memory (slots, prefix_len) cannot be checked
+ *   on the host; the kernels clamp or mask them as documented per call.
+ * Errors after launch.  HYB_ELAUNCH reports a failed kernel launch; outputs,
+ *   and for commit/prefill the state, are then undefined.
+ * Threading.  Calls are reentrant; the error message is thread-local.
+ */
+#ifndef HYBRID_ATTN_H
+#define HYBRID_ATTN_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  HYB_OK = 0,
+  HYB_ENULL = 1,        /* a required pointer is NULL                       */
+  HYB_EINVAL = 2,       /* a size is out of range or inconsistent           */
+  HYB_EALIGN = 3,       /* a pointer is not 16-byte aligned                 */
+  HYB_EDTYPE = 4,       /* dims->dtype is not a hyb_dtype_t                 */
+  HYB_EUNSUPPORTED = 5, /* no kernel for this (dtype, head_dim, feat_dim)   */
+  HYB_EWORKSPACE = 6,   /* workspace missing or smaller than required       */
+  HYB_ELAUNCH = 7       /* the HIP runtime rejected a launch                */
+} hyb_status_t;
+
+typedef enum { HYB_F32 = 0, HYB_BF16 = 1 } hyb_dtype_t;
+
+typedef enum {
+  HYB_OP_STEP = 0,
+  HYB_OP_COMMIT = 1,
+  HYB_OP_PREFILL = 2,
+  HYB_OP_SOFTMAX_PREFIX = 3
+} hyb_op_t;
+
+typedef struct {
+  int32_t batch;      /* B, requests in this call, >= 0 (0: nothing to do)   */
+  int32_t n_q_heads;  /* Hq, >= 1                                            */
+  int32_t n_kv_heads; /* Hkv, >= 1, divides Hq                               */
+  int32_t head_dim;   /* d: 64 or 128                                        */
+  int32_t block;      /* L, active-block tokens: 1..32                       */
+  int32_t feat_dim;   /* f = 2F, rows of S: 64, 128 or 256                   */
+  int32_t dtype;      /* hyb_dtype_t                                         */
+  int32_t n_slots;    /* rows of the state pool S, z; >= 1 when batch > 0   */
+  int32_t flags;      /* 0 or HYB_OUT_F32; any other bit is rejected        */
+} hyb_dims_t;
+
+/* flags: out is fp32 whatever dtype is (default: out has dtype).  The bf16
+ * output of a call equals the round-to-nearest-even bf16 of its fp32 output
+ * bit for bit. */
+#define HYB_OUT_F32 1
+
+/* One denoising step of the active block (Section 3.1: within-block
+ * softmax branch, linear readout of the committed state, gated merge with a
+ * shared normaliser).  Reads S and z, writes out.  q, k, v, W, alpha, S, z
+ * and out are required; slots may be NULL.  out must not overlap an input.
+ * Empty context (z = 0) gives plain block softmax. */
+int hybrid_attn_step(const hyb_dims_t* dims, const void* q, const void* k,
+                     const void* v, const void* W, const float* alpha,
+                     const float* S, const float* z, const int32_t* slots,
+                     void* out, void* stream);
+
+/* Commit of a finished block (Section 3.1 state update):
+ * S_h += sum_t phi_h(k_t) v_t^T and z_h += sum_t phi_h(k_t) over the L block
+ * tokens, in place, for every request and query head.  Two requests of one
+ * call must not share a slot. */
+int hybrid_state_commit(const hyb_dims_t* dims, const void* k, const void* v,
+                        const void* W, float* S, float* z,
+                        const int32_t* slots, void* stream);
+
+/* Block-causal prefill of seq_len tokens (Figure 2 pattern): the tokens are
+ * cut into seq_len / L blocks; block c is answered against the state of the
+ * blocks before it (as hybrid_attn_step) and then committed.  The state
+ * starts from what S, z hold, so successive calls continue one prompt.
+ * seq_len must be a positive multiple of L.  out may be NULL (state only; q
+ * is then ignored and may be NULL).  ws/ws_bytes: workspace of at least
+ * hybrid_workspace_bytes(dims, HYB_OP_PREFILL, seq_len) bytes (may be NULL
+ * when that is 0).  Two requests of one call must not share a slot. */
+int hybrid_state_prefill(const hyb_dims_t* dims, int32_t seq_len,
+                         const void* q, const void* k, const void* v,
+                         const void* W, const float* alpha, float* S, float* z,
+                         const int32_t* slots, void* out, void* ws,
+                         size_t ws_bytes, void* stream);
+
+/* Exact softmax attention of the active block's queries over each request's
+ * cached prefix plus the block itself (the softmax teacher the hybrid layer
+ * replaces; Section 2.2, without a mask inside the block).  prefix_len is a
+ * device array [B]; values are clamped to [0, max_prefix].  ws/ws_bytes: at
+ * least hybrid_workspace_bytes(dims, HYB_OP_SOFTMAX_PREFIX, max_prefix). */
+int softmax_prefix_step(const hyb_dims_t* dims, const void* q, const void* k,
+                        const void* v, const void* k_cache,
+                        const void* v_cache, const int32_t* prefix_len,
+                        int32_t max_prefix, void* out, void* ws,
+                        size_t ws_bytes, void* stream);
+
+/* Workspace bytes the given op needs for these dims; `extent` is seq_len for
+ * HYB_OP_PREFILL and max_prefix for HYB_OP_SOFTMAX_PREFIX, ignored otherwise.
+ * Returns 0 for invalid dims. */
+size_t hybrid_workspace_bytes(const hyb_dims_t* dims, int32_t op,
+                              int32_t extent);
+
+/* Message of the last failed call on this thread ("" if none). */
+const char* hybrid_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HYBRID_ATTN_H */

@@ -1,0 +1,266 @@
+// api.cpp -- the C ABI of libhybattn: host-side validation, then dispatch to
+// the kernel launchers.  Every check runs before any HIP call, so a rejected
+// call enqueues nothing and touches no buffer.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "../../include/hybrid_attn.h"
+#include "launch.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int ok() {
+  g_err.clear();
+  return HYB_OK;
+}
+
+size_t elem_bytes(int dtype) { return dtype == HYB_BF16 ? 2 : 4; }
+size_t out_bytes(const hyb::Shape& s) { return s.out_f32 ? 4 : elem_bytes(s.dtype); }
+
+// Shape checks common to every entry point.  need_state: the call reads a
+// state pool.
+int check_dims(const hyb_dims_t* d, bool need_state, hyb::Shape* s) {
+  if (!d) return fail(HYB_ENULL, "dims is NULL");
+  if (d->dtype != HYB_F32 && d->dtype != HYB_BF16)
+    return fail(HYB_EDTYPE, "dtype %d is neither HYB_F32 nor HYB_BF16",
+                d->dtype);
+  if (d->batch < 0) return fail(HYB_EINVAL, "batch %d < 0", d->batch);
+  if (d->n_q_heads < 1 || d->n_kv_heads < 1)
+    return fail(HYB_EINVAL, "head counts must be >= 1 (Hq=%d, Hkv=%d)",
+                d->n_q_heads, d->n_kv_heads);
+  if (d->n_q_heads % d->n_kv_heads != 0)
+    return fail(HYB_EINVAL, "n_kv_heads %d does not divide n_q_heads %d",
+                d->n_kv_heads, d->n_q_heads);
+  if (d->head_dim <= 0 || d->block <= 0 || d->feat_dim <= 0)
+    return fail(HYB_EINVAL, "head_dim, block and feat_dim must be positive");
+  if (d->head_dim != 64 && d->head_dim != 128)
+    return fail(HYB_EUNSUPPORTED, "head_dim %d not supported (64 or 128)",
+                d->head_dim);
+  if (d->feat_dim != 64 && d->feat_dim != 128 && d->feat_dim != 256)
+    return fail(HYB_EUNSUPPORTED,
+                "feat_dim %d not supported (64, 128 or 256)", d->feat_dim);
+  if (d->block > 32)
+    return fail(HYB_EUNSUPPORTED, "block %d not supported (1..32)", d->block);
+  if (need_state && d->batch > 0 && d->n_slots < 1)
+    return fail(HYB_EINVAL, "n_slots %d < 1", d->n_slots);
+  if ((long long)d->batch * d->n_q_heads > 0x7fffffffLL)
+    return fail(HYB_EINVAL, "batch * n_q_heads exceeds the grid limit");
+  if (d->flags & ~HYB_OUT_F32)
+    return fail(HYB_EINVAL, "unknown flags 0x%x", d->flags);
+  *s = hyb::Shape{d->batch,    d->n_q_heads,    d->n_kv_heads,
+                  d->head_dim, d->block,        d->feat_dim / 2,
+                  d->dtype,    d->n_slots,      (d->flags & HYB_OUT_F32) ? 1 : 0};
+  return HYB_OK;
+}
+
+int check_ptr(const void* p, const char* name, bool required = true) {
+  if (!p) return required ? fail(HYB_ENULL, "%s is NULL", name) : HYB_OK;
+  if (reinterpret_cast<uintptr_t>(p) & 15)
+    return fail(HYB_EALIGN, "%s is not 16-byte aligned", name);
+  return HYB_OK;
+}
+
+bool overlap(const void* a, size_t na, const void* b, size_t nb) {
+  if (!a || !b || na == 0 || nb == 0) return false;
+  const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+  return x < y + nb && y < x + na;
+}
+
+int launched(hipError_t e, const char* what) {
+  if (e != hipSuccess)
+    return fail(HYB_ELAUNCH, "%s launch failed: %s", what,
+                hipGetErrorString(e));
+  return ok();
+}
+
+#define TRY(x)               \
+  do {                       \
+    int _rc = (x);           \
+    if (_rc != HYB_OK) return _rc; \
+  } while (0)
+
+}  // namespace
+
+extern "C" {
+
+int hybrid_attn_step(const hyb_dims_t* dims, const void* q, const void* k,
+                     const void* v, const void* W, const float* alpha,
+                     const float* S, const float* z, const int32_t* slots,
+                     void* out, void* stream) {
+  hyb::Shape s;
+  TRY(check_dims(dims, true, &s));
+  if (s.B == 0) return ok();
+  TRY(check_ptr(q, "q"));
+  TRY(check_ptr(k, "k"));
+  TRY(check_ptr(v, "v"));
+  TRY(check_ptr(W, "W"));
+  TRY(check_ptr(alpha, "alpha"));
+  TRY(check_ptr(S, "S"));
+  TRY(check_ptr(z, "z"));
+  TRY(check_ptr(slots, "slots", false));
+  TRY(check_ptr(out, "out"));
+  const size_t es = elem_bytes(s.dtype), f = 2 * (size_t)s.F;
+  const size_t nq = (size_t)s.B * s.L * s.Hq * s.D * es;
+  const size_t no = (size_t)s.B * s.L * s.Hq * s.D * out_bytes(s);
+  const size_t nkv = (size_t)s.B * s.L * s.Hkv * s.D * es;
+  const size_t nS = (size_t)s.n_slots * s.Hq * f * s.D * 4;
+  const size_t nz = (size_t)s.n_slots * s.Hq * f * 4;
+  const size_t nW = (size_t)s.Hq * s.F * s.D * es;
+  if (overlap(out, no, q, nq) || overlap(out, no, k, nkv) ||
+      overlap(out, no, v, nkv) || overlap(out, no, W, nW) ||
+      overlap(out, no, S, nS) || overlap(out, no, z, nz) ||
+      overlap(out, no, alpha, (size_t)s.Hq * 4) ||
+      overlap(out, no, slots, (size_t)s.B * 4))
+    return fail(HYB_EINVAL, "out overlaps an input");
+  hyb::StepArgs a{s, q, k, v, W, alpha, S, z, slots, out};
+  (void)hipGetLastError();
+  return launched(hyb::launch_step(a, (hipStream_t)stream), "step");
+}
+
+int hybrid_state_commit(const hyb_dims_t* dims, const void* k, const void* v,
+                        const void* W, float* S, float* z,
+                        const int32_t* slots, void* stream) {
+  hyb::Shape s;
+  TRY(check_dims(dims, true, &s));
+  if (s.B == 0) return ok();
+  TRY(check_ptr(k, "k"));
+  TRY(check_ptr(v, "v"));
+  TRY(check_ptr(W, "W"));
+  TRY(check_ptr(S, "S"));
+  TRY(check_ptr(z, "z"));
+  TRY(check_ptr(slots, "slots", false));
+  const size_t f = 2 * (size_t)s.F;
+  const size_t nS = (size_t)s.n_slots * s.Hq * f * s.D * 4;
+  const size_t nz = (size_t)s.n_slots * s.Hq * f * 4;
+  if (overlap(S, nS, z, nz)) return fail(HYB_EINVAL, "S and z overlap");
+  hyb::CommitArgs a{s, k, v, W, S, z, slots};
+  (void)hipGetLastError();
+  return launched(hyb::launch_commit(a, (hipStream_t)stream), "commit");
+}
+
+int hybrid_state_prefill(const hyb_dims_t* dims, int32_t seq_len,
+                         const void* q, const void* k, const void* v,
+                         const void* W, const float* alpha, float* S, float* z,
+                         const int32_t* slots, void* out, void* ws,
+                         size_t ws_bytes, void* stream) {
+  hyb::Shape s;
+  TRY(check_dims(dims, true, &s));
+  if (seq_len <= 0 || seq_len % s.L != 0)
+    return fail(HYB_EINVAL, "seq_len %d is not a positive multiple of block %d",
+                seq_len, s.L);
+  if (s.B == 0) return ok();
+  TRY(check_ptr(k, "k"));
+  TRY(check_ptr(v, "v"));
+  TRY(check_ptr(W, "W"));
+  TRY(check_ptr(S, "S"));
+  TRY(check_ptr(z, "z"));
+  TRY(check_ptr(slots, "slots", false));
+  TRY(check_ptr(out, "out", false));
+  if (out) {
+    TRY(check_ptr(q, "q"));
+    TRY(check_ptr(alpha, "alpha"));
+  }
+  const size_t need = hybrid_workspace_bytes(dims, HYB_OP_PREFILL, seq_len);
+  if (need > 0 && (!ws || ws_bytes < need))
+    return fail(HYB_EWORKSPACE, "prefill needs %zu workspace bytes, got %zu",
+                need, ws ? ws_bytes : (size_t)0);
+  TRY(check_ptr(ws, "ws", false));
+  const size_t es = elem_bytes(s.dtype), f = 2 * (size_t)s.F;
+  const size_t nq = (size_t)s.B * seq_len * s.Hq * s.D * es;
+  const size_t no = (size_t)s.B * seq_len * s.Hq * s.D * out_bytes(s);
+  const size_t nkv = (size_t)s.B * seq_len * s.Hkv * s.D * es;
+  const size_t nS = (size_t)s.n_slots * s.Hq * f * s.D * 4;
+  const size_t nz = (size_t)s.n_slots * s.Hq * f * 4;
+  if (overlap(S, nS, z, nz)) return fail(HYB_EINVAL, "S and z overlap");
+  if (out && (overlap(out, no, q, nq) || overlap(out, no, k, nkv) ||
+              overlap(out, no, v, nkv) || overlap(out, no, S, nS) ||
+              overlap(out, no, z, nz)))
+    return fail(HYB_EINVAL, "out overlaps an input");
+  hyb::PrefillArgs a{s, seq_len, q, k, v, W, alpha, S, z, slots, out};
+  (void)hipGetLastError();
+  return launched(hyb::launch_prefill(a, (hipStream_t)stream), "prefill");
+}
+
+int softmax_prefix_step(const hyb_dims_t* dims, const void* q, const void* k,
+                        const void* v, const void* k_cache,
+                        const void* v_cache, const int32_t* prefix_len,
+                        int32_t max_prefix, void* out, void* ws,
+                        size_t ws_bytes, void* stream) {
+  hyb::Shape s;
+  TRY(check_dims(dims, false, &s));
+  if (max_prefix < 0)
+    return fail(HYB_EINVAL, "max_prefix %d < 0", max_prefix);
+  if (s.Hq / s.Hkv > 8)
+    return fail(HYB_EUNSUPPORTED,
+                "softmax_prefix_step supports up to 8 query heads per KV head");
+  if (s.B == 0) return ok();
+  TRY(check_ptr(q, "q"));
+  TRY(check_ptr(k, "k"));
+  TRY(check_ptr(v, "v"));
+  TRY(check_ptr(out, "out"));
+  TRY(check_ptr(prefix_len, "prefix_len"));
+  if (max_prefix > 0) {
+    TRY(check_ptr(k_cache, "k_cache"));
+    TRY(check_ptr(v_cache, "v_cache"));
+  }
+  const size_t need =
+      hybrid_workspace_bytes(dims, HYB_OP_SOFTMAX_PREFIX, max_prefix);
+  if (need > 0 && (!ws || ws_bytes < need))
+    return fail(HYB_EWORKSPACE,
+                "softmax_prefix_step needs %zu workspace bytes, got %zu", need,
+                ws ? ws_bytes : (size_t)0);
+  TRY(check_ptr(ws, "ws", false));
+  const size_t es = elem_bytes(s.dtype);
+  const size_t nq = (size_t)s.B * s.L * s.Hq * s.D * es;
+  const size_t no = (size_t)s.B * s.L * s.Hq * s.D * out_bytes(s);
+  const size_t nkv = (size_t)s.B * s.L * s.Hkv * s.D * es;
+  const size_t nc = (size_t)s.B * max_prefix * s.Hkv * s.D * es;
+  if (overlap(out, no, q, nq) || overlap(out, no, k, nkv) ||
+      overlap(out, no, v, nkv) || overlap(out, no, k_cache, nc) ||
+      overlap(out, no, v_cache, nc) || overlap(out, no, ws, need))
+    return fail(HYB_EINVAL, "out overlaps an input or the workspace");
+  hyb::SoftmaxPrefixArgs a{s,         q,   k,  v,
+                           k_cache,   v_cache, prefix_len, max_prefix,
+                           out,       ws,  hyb::softmax_prefix_splits(s, max_prefix)};
+  (void)hipGetLastError();
+  return launched(hyb::launch_softmax_prefix(a, (hipStream_t)stream),
+                  "softmax_prefix_step");
+}
+
+size_t hybrid_workspace_bytes(const hyb_dims_t* dims, int32_t op,
+                              int32_t extent) {
+  hyb::Shape s;
+  const std::string saved = g_err;
+  const int rc = check_dims(dims, false, &s);
+  g_err = saved;
+  if (rc != HYB_OK || extent < 0) return 0;
+  switch (op) {
+    case HYB_OP_STEP:
+    case HYB_OP_COMMIT:
+    case HYB_OP_PREFILL:
+      return 0;
+    case HYB_OP_SOFTMAX_PREFIX:
+      return hyb::softmax_prefix_ws_bytes(
+          s, hyb::softmax_prefix_splits(s, extent));
+  }
+  return 0;
+}
+
+const char* hybrid_last_error(void) { return g_err.c_str(); }
+
+}  // extern "C"

@@ -1,0 +1,258 @@
+// device.h -- gfx950 building blocks shared by the block-hybrid kernels.
+//
+// Matrix-core conventions.  All products use 32x32 MFMA tiles with fp32
+// accumulators:
+//   bf16 path:  v_mfma_f32_32x32x16_bf16  (16-deep contraction, 8 bf16/lane)
+//   fp32 path:  v_mfma_f32_32x32x2_f32    ( 2-deep contraction, 1 fp32/lane)
+// For both, a lane l of the 64-wide wave is split as li = l & 31 and
+// hh = l >> 5.  Operand A (M x K) lane (li, hh) holds row li and the E
+// contraction indices k = ks*KW + hh*E + e (e < E) of k-step ks; operand B
+// (K x N) lane (li, hh) holds column li and the same contraction indices.
+// The 16 accumulator registers of lane (li, hh) hold column li and rows
+// row_of(i, hh) = (i/4)*8 + hh*4 + i%4, i = 0..15.
+//
+// Because a contraction does not care in which order its index is visited,
+// an accumulator tile can feed the next product directly as an operand:
+// register i of lane (li, hh) becomes contraction element e = i % E of
+// k-step i / E, provided the other operand is loaded with the same
+// (k-step, e, hh) -> index map.  The kernels use this to chain QK^T into
+// P V and to read the state straight from its accumulator layout.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hyb {
+
+typedef __bf16 bf16;
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kWave = 64;
+constexpr int kTile = 32;  // MFMA tile edge, also the largest active block
+constexpr int kNumXcd = 8;
+
+template <typename T>
+struct Mma;
+
+template <>
+struct Mma<bf16> {
+  static constexpr int KW = 16;  // contraction depth of one instruction
+  static constexpr int E = 8;    // operand elements per lane
+  typedef bf16x8 op_t;
+  __device__ static inline f32x16 mma(op_t a, op_t b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+  __device__ static inline op_t zero() { return op_t{}; }
+};
+
+template <>
+struct Mma<float> {
+  static constexpr int KW = 2;
+  static constexpr int E = 1;
+  typedef float op_t;
+  __device__ static inline f32x16 mma(op_t a, op_t b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+  __device__ static inline op_t zero() { return 0.0f; }
+};
+
+// 16x16 tiles (gfx950):
+//   bf16 path:  v_mfma_f32_16x16x32_bf16  (32-deep contraction, 8 bf16/lane)
+//   fp32 path:  v_mfma_f32_16x16x4_f32    ( 4-deep contraction, 1 fp32/lane)
+// Lane l is split as c16 = l & 15 and quad = l >> 4.  Operand A (16 x K)
+// lane (c16, quad) holds row c16 and contraction indices ks*KW + quad*E + e;
+// operand B (K x 16) holds column c16 and the same indices; the 4 accumulator
+// registers hold column c16 and rows quad*4 + r.  Four consecutive lanes
+// read 64 contiguous bytes of one row, so operands come straight from global
+// memory with every 64-byte access fully used.
+template <typename T>
+struct Mma16;
+
+template <>
+struct Mma16<bf16> {
+  static constexpr int KW = 32;
+  static constexpr int E = 8;
+  typedef bf16x8 op_t;
+  __device__ static inline f32x4 mma(op_t a, op_t b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+  }
+  __device__ static inline op_t zero() { return op_t{}; }
+};
+
+template <>
+struct Mma16<float> {
+  static constexpr int KW = 4;
+  static constexpr int E = 1;
+  typedef float op_t;
+  __device__ static inline f32x4 mma(op_t a, op_t b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+  }
+  __device__ static inline op_t zero() { return 0.0f; }
+};
+
+__device__ inline float xor16(float x) { return __shfl_xor(x, 16); }
+
+// Row of accumulator register i (0..15) held by lane half hh.
+__device__ __host__ constexpr int row_of(int i, int hh) {
+  return (i >> 2) * 8 + hh * 4 + (i & 3);
+}
+
+// E consecutive elements of T starting at p (16-byte aligned for bf16).
+template <typename T>
+__device__ inline typename Mma<T>::op_t load_op(const T* p);
+template <>
+__device__ inline bf16x8 load_op<bf16>(const bf16* p) {
+  return *reinterpret_cast<const bf16x8*>(p);
+}
+template <>
+__device__ inline float load_op<float>(const float* p) {
+  return *p;
+}
+
+// E fp32 values converted to an operand (bf16 round-to-nearest-even).
+template <typename T>
+__device__ inline typename Mma<T>::op_t cvt_op(const float* x);
+template <>
+__device__ inline bf16x8 cvt_op<bf16>(const float* x) {
+  bf16x8 r;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) r[e] = (bf16)x[e];
+  return r;
+}
+template <>
+__device__ inline float cvt_op<float>(const float* x) {
+  return x[0];
+}
+
+// x, or a zero operand when ok is false (a select, not a branch).
+template <typename T>
+__device__ inline typename Mma<T>::op_t keep_if(bool ok,
+                                               typename Mma<T>::op_t x) {
+  return ok ? x : Mma<T>::zero();
+}
+
+// Operand whose element e is base[key(e) * stride] for the token
+// key(e) = row_of(ks*E + e, hh) (accumulator-row order) or, when natural is
+// set, key(e) = ks*KW + hh*E + e; tokens at or beyond L read row L-1 (always
+// in bounds) and are replaced by zero.
+template <typename T>
+__device__ inline typename Mma<T>::op_t load_rows_op(const T* base,
+                                                     size_t stride, int ks,
+                                                     int hh, int L,
+                                                     bool natural) {
+  typedef Mma<T> M;
+  typename M::op_t x;
+  if constexpr (M::E == 1) {
+    const int key = natural ? ks * M::KW + hh : row_of(ks, hh);
+    const float v = (float)base[(size_t)min(key, L - 1) * stride];
+    x = key < L ? v : 0.0f;
+  } else {
+#pragma unroll
+    for (int e = 0; e < M::E; ++e) {
+      const int key = natural ? ks * M::KW + hh * M::E + e : row_of(ks * M::E + e, hh);
+      const T v = base[(size_t)min(key, L - 1) * stride];
+      x[e] = key < L ? v : (T)0.0f;
+    }
+  }
+  return x;
+}
+
+// Operand whose element e is row[off + row_of(ks*E + e, hh)]: the LDS copy
+// of a tile read in accumulator-register order.  For E = 8 these are two runs
+// of 4 consecutive elements.
+template <typename T>
+__device__ inline typename Mma<T>::op_t lds_op_perm(const T* row, int ks,
+                                                    int hh, int off);
+template <>
+__device__ inline bf16x8 lds_op_perm<bf16>(const bf16* row, int ks, int hh,
+                                           int off) {
+  const bf16x4 lo = *reinterpret_cast<const bf16x4*>(row + off + 16 * ks + 4 * hh);
+  const bf16x4 hi =
+      *reinterpret_cast<const bf16x4*>(row + off + 16 * ks + 8 + 4 * hh);
+  return bf16x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+}
+template <>
+__device__ inline float lds_op_perm<float>(const float* row, int ks, int hh,
+                                           int off) {
+  return row[off + row_of(ks, hh)];
+}
+
+template <typename T>
+__device__ inline float to_f32(T x) {
+  return (float)x;
+}
+
+// The value x takes once it is stored as a T operand (identity for fp32).
+template <typename T>
+__device__ inline float as_operand(float x) {
+  return (float)(T)x;
+}
+
+// acc += A * x as T operands, where the E fp32 values x are carried as a
+// bf16 pair hi + lo (two products) on the bf16 path: about 16 significant
+// bits of x instead of 8.  One product on the fp32 path.
+template <typename T>
+__device__ inline f32x16 mma_split_b(typename Mma<T>::op_t a, const float* x,
+                                     f32x16 acc) {
+  typedef Mma<T> M;
+  acc = M::mma(a, cvt_op<T>(x), acc);
+  if constexpr (M::E > 1) {
+    float lo[M::E];
+#pragma unroll
+    for (int e = 0; e < M::E; ++e) lo[e] = x[e] - as_operand<T>(x[e]);
+    acc = M::mma(a, cvt_op<T>(lo), acc);
+  }
+  return acc;
+}
+
+template <typename T>
+__device__ inline T from_f32(float x) {
+  return (T)x;
+}
+
+// Four consecutive outputs at element index idx: fp32 when the call asked
+// for fp32 outputs (or computes in fp32), else rounded to T.
+template <typename T>
+__device__ inline void store_out4(void* out, size_t idx, const float* v,
+                                  bool f32) {
+  if (sizeof(T) == 4 || f32) {
+    *reinterpret_cast<f32x4*>((float*)out + idx) = f32x4{v[0], v[1], v[2], v[3]};
+  } else {
+    *reinterpret_cast<bf16x4*>((bf16*)out + idx) =
+        bf16x4{(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3]};
+  }
+}
+
+template <typename T>
+__device__ inline void store_out1(void* out, size_t idx, float v, bool f32) {
+  if (sizeof(T) == 4 || f32)
+    ((float*)out)[idx] = v;
+  else
+    ((bf16*)out)[idx] = (bf16)v;
+}
+
+__device__ inline float xor32(float x) { return __shfl_xor(x, 32); }
+
+__device__ inline float fast_exp(float x) {
+  // e^x = 2^(x log2 e); v_exp_f32 is exact to about 1 ulp.
+  return __builtin_amdgcn_exp2f(x * 1.4426950408889634f);
+}
+
+// log(sigmoid(a)) without overflow for any a.
+__device__ inline float log_sigmoid(float a) {
+  return a >= 0.0f ? -log1pf(expf(-a)) : a - log1pf(expf(a));
+}
+
+// Work-unit index for the workgroup: consecutive units land on one XCD.
+// Workgroups are handed to the 8 XCDs round-robin by blockIdx, so unit
+// u = (bid % 8) * (n / 8) + bid / 8 keeps units u..u+n/8-1 on one XCD (and
+// in its L2) when n is a multiple of 8.
+__device__ inline int xcd_unit(int bid, int n) {
+  if ((n & (kNumXcd - 1)) != 0) return bid;
+  return (bid & (kNumXcd - 1)) * (n / kNumXcd) + bid / kNumXcd;
+}
+
+}  // namespace hyb

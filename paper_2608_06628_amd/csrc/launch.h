@@ -1,0 +1,63 @@
+// launch.h -- internal interface between the C-ABI layer (api.cpp) and the
+// kernel translation units.  Arguments arrive here already validated.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace hyb {
+
+struct Shape {
+  int B, Hq, Hkv, D, L, F, dtype, n_slots;  // F = feat_dim / 2
+  int out_f32;                              // out is fp32 whatever dtype is
+};
+
+struct StepArgs {
+  Shape s;
+  const void *q, *k, *v, *W;
+  const float* alpha;
+  const float *S, *z;
+  const int32_t* slots;
+  void* out;
+};
+
+struct CommitArgs {
+  Shape s;
+  const void *k, *v, *W;
+  float *S, *z;
+  const int32_t* slots;
+};
+
+struct PrefillArgs {
+  Shape s;
+  int T;
+  const void *q, *k, *v, *W;
+  const float* alpha;
+  float *S, *z;
+  const int32_t* slots;
+  void* out;  // may be null
+};
+
+struct SoftmaxPrefixArgs {
+  Shape s;
+  const void *q, *k, *v, *k_cache, *v_cache;
+  const int32_t* prefix_len;
+  int max_prefix;
+  void* out;
+  void* ws;
+  int n_split;  // KV splits per (request, KV head)
+};
+
+// Each returns false when no kernel exists for the shape's variant.
+bool step_supported(const Shape& s);
+hipError_t launch_step(const StepArgs& a, hipStream_t st);
+hipError_t launch_commit(const CommitArgs& a, hipStream_t st);
+hipError_t launch_prefill(const PrefillArgs& a, hipStream_t st);
+hipError_t launch_softmax_prefix(const SoftmaxPrefixArgs& a, hipStream_t st);
+
+// Workspace of softmax_prefix_step for n_split splits.
+size_t softmax_prefix_ws_bytes(const Shape& s, int n_split);
+int softmax_prefix_splits(const Shape& s, int max_prefix);
+
+}  // namespace hyb

@@ -1,0 +1,279 @@
+// prefill.hip -- block-causal prefill of a prompt into the recurrent state
+// (Figure 2 pattern): block c is answered against the state of blocks
+// 0..c-1 -- exact softmax inside the block, linear readout of the state,
+// gated merge (Section 3.1) -- and is then committed,
+// S += phi(K_c)^T V_c, z += sum phi(K_c).
+//
+// One workgroup per (request b, query head h) walks the blocks in order.
+// Wave w of NW = D/32 keeps state columns 32w .. 32w+31 of all f rows in fp32
+// MFMA accumulators for the whole prompt, so the state is read from HBM once
+// and written once.  The accumulator tile doubles as the A operand of the
+// readout O_lin^T = S^T phi(Q)^T: register j of the flattened tile is
+// contraction element j % E of k-step j / E, i.e. state row
+// r = 32*(j/16) + row_of(j%16, hh), and phi(Q) is read from LDS in that
+// order.  Block tokens enter every product in the accumulator order of the
+// score tile (token row_of(ks*E+e, hh)), so one set of V registers serves
+// both P V and the commit.  As in the commit kernel, phi(K) enters the state
+// update as a bf16 pair hi + lo on the bf16 path.
+#include "device.h"
+#include "featmap.h"
+#include "launch.h"
+
+namespace hyb {
+
+template <typename T, int D, int F>
+struct PrefillCfg {
+  typedef Mma<T> M;
+  typedef typename M::op_t op_t;
+  static constexpr int NW = D / kTile;
+  static constexpr int f = 2 * F;
+  static constexpr int NRT = f / kTile;
+  static constexpr int KD = D / M::KW;
+  static constexpr int KF = f / M::KW;
+  static constexpr int KL = kTile / M::KW;
+  static constexpr int PHI_LD = f + 16 / (int)sizeof(T);
+  static constexpr int PT_LD = kTile + 16 / (int)sizeof(T);
+  static constexpr int NPART = sizeof(T) == 2 ? 2 : 1;  // hi (+ lo) parts
+  typedef FeatMap<T, D, F, NW> FM;
+  struct alignas(16) Smem {
+    T phiQ[kTile][PHI_LD];         // phi(q_i)[r] at [i][r]
+    T phiKT[NPART][f][PT_LD];      // phi(k_t)[r] at [part][r][t]
+    float z[f];
+    typename FM::Smem fq, fk;
+  };
+};
+
+template <typename T, int D, int F>
+__global__ __launch_bounds__(kWave*(D / kTile)) void hyb_prefill_kernel(
+    PrefillArgs a) {
+  typedef PrefillCfg<T, D, F> C;
+  typedef typename C::M M;
+  typedef typename C::op_t op_t;
+  typedef typename C::FM FM;
+  constexpr int f = C::f, E = M::E, KW = M::KW;
+  __shared__ typename C::Smem sh;
+
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+  const int li = lane & 31, hh = lane >> 5;
+  const int Hq = a.s.Hq, Hkv = a.s.Hkv, L = a.s.L, T_ = a.T;
+  const int u = xcd_unit(blockIdx.x, a.s.B * Hq);
+  const int b = u / Hq, h = u % Hq, g = h / (Hq / Hkv);
+  const int slot = a.slots ? a.slots[b] : b;
+  const bool want_out = a.out != nullptr;
+  const size_t qstride = (size_t)Hq * D, kstride = (size_t)Hkv * D;
+  const int col = w * kTile + li;
+  if (slot < 0 || slot >= a.s.n_slots) {  // uniform per workgroup
+    if (want_out) {
+      const size_t ob = ((size_t)b * T_ * Hq + h) * D;
+      for (int t = 0; t < T_; ++t)
+        for (int c = tid; c < D; c += blockDim.x)
+          store_out1<T>(a.out, ob + (size_t)t * qstride + c, __builtin_nanf(""),
+                        a.s.out_f32);
+    }
+    return;
+  }
+  const size_t sbase = (size_t)slot * Hq + h;
+  float* __restrict__ Sh = a.S + sbase * f * D;
+  float* __restrict__ zh = a.z + sbase * f;
+
+  f32x16 sacc[C::NRT];
+#pragma unroll
+  for (int rt = 0; rt < C::NRT; ++rt)
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      sacc[rt][i] = Sh[(size_t)(rt * kTile + row_of(i, hh)) * D + col];
+  for (int r = tid; r < f; r += blockDim.x) sh.z[r] = zh[r];
+
+  const T* __restrict__ Wt_h = (const T*)a.W + (size_t)h * F * D;
+  op_t wop[FM::PPW][C::KD];  // W_h^T operands, kept for the whole prompt
+  FM::load_w(Wt_h, w, li, hh, wop);
+  const float scale = 1.0f / sqrtf((float)D);
+  const float lw = want_out ? log_sigmoid(a.alpha[h]) : 0.0f;
+  const bool row_ok = li < L;
+  const int nblk = T_ / L;
+
+  for (int blk = 0; blk < nblk; ++blk) {
+    const size_t t0 = (size_t)blk * L;
+    const T* kb = (const T*)a.k + (((size_t)b * T_ + t0) * Hkv + g) * D;
+    const T* vb = (const T*)a.v + (((size_t)b * T_ + t0) * Hkv + g) * D;
+    // Unconditional, in-bounds loads: padding rows read row L-1 and are
+    // zeroed by a select.
+    op_t kop[C::KD], qop[C::KD], vop[C::KL];
+    const int lrow = min(li, L - 1);
+    {
+      const T* krow = kb + (size_t)lrow * kstride + hh * E;
+#pragma unroll
+      for (int ks = 0; ks < C::KD; ++ks) kop[ks] = load_op<T>(krow + ks * KW);
+    }
+#pragma unroll
+    for (int ks = 0; ks < C::KL; ++ks)
+      vop[ks] = load_rows_op<T>(vb + col, kstride, ks, hh, L, false);
+    if (want_out) {
+      const T* qrow = (const T*)a.q + (((size_t)b * T_ + t0) * Hq + h) * D +
+                      (size_t)lrow * qstride + hh * E;
+#pragma unroll
+      for (int ks = 0; ks < C::KD; ++ks) qop[ks] = load_op<T>(qrow + ks * KW);
+    }
+#pragma unroll
+    for (int ks = 0; ks < C::KD; ++ks) {
+      kop[ks] = keep_if<T>(row_ok, kop[ks]);
+      qop[ks] = keep_if<T>(row_ok, qop[ks]);
+    }
+
+    __syncthreads();  // previous block's LDS readers are done
+    float vk[FM::PPW][16], vq[FM::PPW][16];
+    FM::logits(wop, kop, w, li, hh, vk, sh.fk);
+    if (want_out) FM::logits(wop, qop, w, li, hh, vq, sh.fq);
+
+    // In-block softmax branch (keys in rows, queries in columns).
+    f32x16 acc_sm = {};
+    float m = 0.0f, den = 1.0f;
+    if (want_out) {
+      f32x16 sc = {};
+#pragma unroll
+      for (int ks = 0; ks < C::KD; ++ks) sc = M::mma(kop[ks], qop[ks], sc);
+      float p[16];
+      m = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        p[i] = row_of(i, hh) < L ? sc[i] * scale : -INFINITY;
+        m = fmaxf(m, p[i]);
+      }
+      m = fmaxf(m, xor32(m));
+      den = 0.0f;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        p[i] = row_of(i, hh) < L ? fast_exp(p[i] - m) : 0.0f;
+        den += p[i];
+      }
+      den += xor32(den);
+#pragma unroll
+      for (int ks = 0; ks < C::KL; ++ks)
+        acc_sm = mma_split_b<T>(vop[ks], &p[ks * E], acc_sm);
+    }
+
+    __syncthreads();
+    FM::exps(w, li, hh, vk, sh.fk);
+    if (want_out) FM::exps(w, li, hh, vq, sh.fq);
+    __syncthreads();
+    FM::normalise(w, li, hh, vk, sh.fk, [&](int f0, const float* x4) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float x = row_ok ? x4[e] : 0.0f;
+        const T hi = from_f32<T>(x);
+        sh.phiKT[0][f0 + e][li] = hi;
+        if constexpr (C::NPART == 2)
+          sh.phiKT[1][f0 + e][li] = from_f32<T>(x - to_f32(hi));
+      }
+    });
+    if (want_out)
+      FM::normalise(w, li, hh, vq, sh.fq, [&](int f0, const float* x4) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) sh.phiQ[li][f0 + e] = from_f32<T>(x4[e]);
+      });
+    __syncthreads();
+
+    if (want_out) {
+      // Readout against the state of the blocks before this one.
+      f32x16 acc_lin = {};
+      float lden = 0.0f;
+#pragma unroll
+      for (int ks = 0; ks < C::KF; ++ks) {
+        const op_t pb = lds_op_perm<T>(&sh.phiQ[li][0], ks, hh, 0);
+        op_t sa;
+        if constexpr (E == 1) {
+          sa = sacc[ks / 16][ks % 16];
+          lden += pb * sh.z[row_of(ks, hh)];
+        } else {
+#pragma unroll
+          for (int e = 0; e < E; ++e) {
+            const int j = ks * E + e;  // flattened accumulator register
+            sa[e] = (T)sacc[j / 16][j % 16];
+            lden += to_f32(pb[e]) * sh.z[row_of(j, hh)];
+          }
+        }
+        acc_lin = M::mma(sa, pb, acc_lin);
+      }
+      lden += xor32(lden);
+      if (row_ok) {
+        float ca = 1.0f, cz = 0.0f, rz = 0.0f;
+        if (lden > 0.0f) {
+          const float la = lw + m, lb = logf(lden);
+          const float c = fmaxf(la, lb);
+          ca = expf(la - c);
+          cz = expf(lb - c);
+          rz = 1.0f / lden;
+        }
+        const float inv = 1.0f / (ca * den + cz);
+        const size_t obase = (((size_t)b * T_ + t0 + li) * Hq + h) * D;
+#pragma unroll
+        for (int i = 0; i < 16; i += 4) {
+          float o[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            o[e] = (ca * acc_sm[i + e] + cz * (acc_lin[i + e] * rz)) * inv;
+          store_out4<T>(a.out, obase + w * kTile + row_of(i, hh), o, a.s.out_f32);
+        }
+      }
+    }
+
+    // Commit the block: S += phi(K)^T V in the accumulators.
+#pragma unroll
+    for (int rt = 0; rt < C::NRT; ++rt)
+#pragma unroll
+      for (int ks = 0; ks < C::KL; ++ks)
+#pragma unroll
+        for (int part = 0; part < C::NPART; ++part)
+          sacc[rt] = M::mma(
+              lds_op_perm<T>(&sh.phiKT[part][rt * kTile + li][0], ks, hh, 0),
+              vop[ks], sacc[rt]);
+    __syncthreads();  // every wave has read z for this block
+    for (int r = tid; r < f; r += blockDim.x) {
+      float s = 0.0f;
+      for (int t = 0; t < L; ++t)
+#pragma unroll
+        for (int part = 0; part < C::NPART; ++part) s += to_f32(sh.phiKT[part][r][t]);
+      sh.z[r] += s;
+    }
+  }
+
+#pragma unroll
+  for (int rt = 0; rt < C::NRT; ++rt)
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      Sh[(size_t)(rt * kTile + row_of(i, hh)) * D + col] = sacc[rt][i];
+  __syncthreads();
+  for (int r = tid; r < f; r += blockDim.x) zh[r] = sh.z[r];
+}
+
+template <typename T, int D, int F>
+static hipError_t prefill_go(const PrefillArgs& a, hipStream_t st) {
+  hipLaunchKernelGGL((hyb_prefill_kernel<T, D, F>), dim3(a.s.B * a.s.Hq),
+                     dim3(kWave * (D / kTile)), 0, st, a);
+  return hipGetLastError();
+}
+
+template <typename T, int D>
+static hipError_t prefill_f(const PrefillArgs& a, hipStream_t st) {
+  switch (a.s.F) {
+    case 32: return prefill_go<T, D, 32>(a, st);
+    case 64: return prefill_go<T, D, 64>(a, st);
+    case 128: return prefill_go<T, D, 128>(a, st);
+  }
+  return hipErrorInvalidValue;
+}
+
+template <typename T>
+static hipError_t prefill_d(const PrefillArgs& a, hipStream_t st) {
+  switch (a.s.D) {
+    case 64: return prefill_f<T, 64>(a, st);
+    case 128: return prefill_f<T, 128>(a, st);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_prefill(const PrefillArgs& a, hipStream_t st) {
+  return a.s.dtype == 1 ? prefill_d<bf16>(a, st) : prefill_d<float>(a, st);
+}
+
+}  // namespace hyb

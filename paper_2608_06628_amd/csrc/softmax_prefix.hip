@@ -1,0 +1,215 @@
+// softmax_prefix.hip -- exact softmax attention of the active block over a
+// request's cached prefix plus the block itself: the softmax layer that the
+// hybrid layer replaces (Section 2.2 attention without a mask inside the
+// block; the comparison of the paper's kernel benchmark, Appendix A).
+//
+// Split-KV flash decoding.  Keys are indexed in the concatenation
+// [k_cache[b][0 .. P_b-1]; k_block[b][0 .. L-1]] and cut into n_split ranges.
+// One workgroup per (request b, KV head g, range s) with one wave per query
+// head of the group (GQA packing: the G heads share every K/V tile through
+// LDS).  Each 32-key tile gives Sc^T = K Q^T (keys in rows, one query per
+// lane column), an online-softmax update, and O^T += V^T P^T, with P rounded
+// once to the operand type and the running sum taken over the rounded
+// weights.  A second kernel merges the ranges with their log-sum-exp weights.
+#include "device.h"
+#include "launch.h"
+
+namespace hyb {
+
+template <typename T, int D>
+struct SpCfg {
+  typedef Mma<T> M;
+  typedef typename M::op_t op_t;
+  static constexpr int KD = D / M::KW;
+  static constexpr int KL = kTile / M::KW;
+  static constexpr int NCT = D / kTile;
+  static constexpr int LD = D + 16 / (int)sizeof(T);
+  static constexpr int EPC = 16 / (int)sizeof(T);  // elements per 16 bytes
+  struct alignas(16) Smem {
+    T k[kTile][LD];
+    T v[kTile][LD];
+  };
+};
+
+constexpr int kMaxGroup = 8;  // query heads per KV head handled by one WG
+
+template <typename T, int D>
+__global__ __launch_bounds__(kWave* kMaxGroup) void hyb_sp_partial_kernel(
+    SoftmaxPrefixArgs a, int chunk) {
+  typedef SpCfg<T, D> C;
+  typedef typename C::M M;
+  typedef typename C::op_t op_t;
+  constexpr int E = M::E, KW = M::KW;
+  __shared__ typename C::Smem sh;
+
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+  const int li = lane & 31, hh = lane >> 5;
+  const int Hq = a.s.Hq, Hkv = a.s.Hkv, L = a.s.L, G = Hq / Hkv;
+  const int ns = a.n_split, Pmax = a.max_prefix;
+  const int s = blockIdx.x % ns;
+  const int bg = blockIdx.x / ns;
+  const int b = bg / Hkv, g = bg % Hkv, h = g * G + w;
+  int P = a.prefix_len[b];
+  P = P < 0 ? 0 : (P > Pmax ? Pmax : P);
+  const int N = P + L;
+  const int lo = s * chunk;
+  const int hi = min(lo + chunk, N);
+  const size_t qstride = (size_t)Hq * D, kstride = (size_t)Hkv * D;
+
+  op_t qop[C::KD];
+  {
+    const T* qrow = (const T*)a.q + ((size_t)b * L * Hq + h) * D +
+                    (size_t)li * qstride + hh * E;
+#pragma unroll
+    for (int ks = 0; ks < C::KD; ++ks)
+      qop[ks] = li < L ? load_op<T>(qrow + ks * KW) : M::zero();
+  }
+  const T* kc = (const T*)a.k_cache + ((size_t)b * Pmax * Hkv + g) * D;
+  const T* vc = (const T*)a.v_cache + ((size_t)b * Pmax * Hkv + g) * D;
+  const T* kbk = (const T*)a.k + ((size_t)b * L * Hkv + g) * D;
+  const T* vbk = (const T*)a.v + ((size_t)b * L * Hkv + g) * D;
+
+  const float scale = 1.0f / sqrtf((float)D);
+  float m = -INFINITY, l = 0.0f;
+  f32x16 acc[C::NCT];
+#pragma unroll
+  for (int ct = 0; ct < C::NCT; ++ct) acc[ct] = f32x16{};
+
+  constexpr int CPR = D / C::EPC;  // 16-byte chunks per key row
+  for (int j0 = lo; j0 < hi; j0 += kTile) {
+    __syncthreads();
+    // Keys past the range read the range's last key (in bounds) and are
+    // masked out of the scores below.
+    for (int c = tid; c < kTile * CPR; c += blockDim.x) {
+      const int key = c / CPR, part = c % CPR, j = min(j0 + key, hi - 1);
+      const size_t o = (size_t)part * C::EPC;
+      const T* ks = j < P ? kc + (size_t)j * kstride : kbk + (size_t)(j - P) * kstride;
+      const T* vs = j < P ? vc + (size_t)j * kstride : vbk + (size_t)(j - P) * kstride;
+      *reinterpret_cast<uint4*>(&sh.k[key][part * C::EPC]) =
+          *reinterpret_cast<const uint4*>(ks + o);
+      *reinterpret_cast<uint4*>(&sh.v[key][part * C::EPC]) =
+          *reinterpret_cast<const uint4*>(vs + o);
+    }
+    __syncthreads();
+
+    f32x16 sc = {};
+#pragma unroll
+    for (int ks = 0; ks < C::KD; ++ks)
+      sc = M::mma(load_op<T>(&sh.k[li][ks * KW + hh * E]), qop[ks], sc);
+    float p[16];
+    float mt = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      p[i] = j0 + row_of(i, hh) < hi ? sc[i] * scale : -INFINITY;
+      mt = fmaxf(mt, p[i]);
+    }
+    mt = fmaxf(mt, xor32(mt));
+    const float mn = fmaxf(m, mt);
+    const float corr = fast_exp(m - mn);
+    float ps = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      p[i] = j0 + row_of(i, hh) < hi ? as_operand<T>(fast_exp(p[i] - mn)) : 0.0f;
+      ps += p[i];
+    }
+    ps += xor32(ps);
+    l = l * corr + ps;
+    m = mn;
+#pragma unroll
+    for (int ct = 0; ct < C::NCT; ++ct) {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) acc[ct][i] *= corr;
+#pragma unroll
+      for (int ks = 0; ks < C::KL; ++ks) {
+        op_t va;
+        if constexpr (E == 1) {
+          va = to_f32(sh.v[row_of(ks, hh)][ct * kTile + li]);
+        } else {
+#pragma unroll
+          for (int e = 0; e < E; ++e)
+            va[e] = sh.v[row_of(ks * E + e, hh)][ct * kTile + li];
+        }
+        acc[ct] = M::mma(va, cvt_op<T>(&p[ks * E]), acc[ct]);
+      }
+    }
+  }
+
+  // Partial result of this range: unnormalised O, running max and sum.
+  if (li >= L) return;
+  const size_t row = (((size_t)b * Hq + h) * ns + s) * L + li;
+  float* wacc = (float*)a.ws + row * D;
+  float* wml = (float*)a.ws + (size_t)a.s.B * Hq * ns * L * D + row * 2;
+#pragma unroll
+  for (int ct = 0; ct < C::NCT; ++ct)
+#pragma unroll
+    for (int i = 0; i < 16; i += 4)
+      *reinterpret_cast<f32x4*>(wacc + ct * kTile + row_of(i, hh)) =
+          f32x4{acc[ct][i], acc[ct][i + 1], acc[ct][i + 2], acc[ct][i + 3]};
+  if (hh == 0) {
+    wml[0] = m;
+    wml[1] = l;
+  }
+}
+
+// Merge of the n_split partial results of one (request, head, query).
+template <typename T, int D>
+__global__ __launch_bounds__(D) void hyb_sp_combine_kernel(
+    SoftmaxPrefixArgs a) {
+  const int Hq = a.s.Hq, L = a.s.L, ns = a.n_split;
+  const int i = blockIdx.x % L, bh = blockIdx.x / L;
+  const int b = bh / Hq, h = bh % Hq, c = threadIdx.x;
+  const size_t row0 = ((size_t)bh * ns) * L + i;
+  const float* wacc = (const float*)a.ws;
+  const float* wml = wacc + (size_t)a.s.B * Hq * ns * L * D;
+  float M = -INFINITY;
+  for (int s = 0; s < ns; ++s) M = fmaxf(M, wml[(row0 + (size_t)s * L) * 2]);
+  float num = 0.0f, den = 0.0f;
+  for (int s = 0; s < ns; ++s) {
+    const size_t r = row0 + (size_t)s * L;
+    const float ms = wml[r * 2];
+    if (ms == -INFINITY) continue;
+    const float wgt = expf(ms - M);
+    num += wgt * wacc[r * D + c];
+    den += wgt * wml[r * 2 + 1];
+  }
+  store_out1<T>(a.out, (((size_t)b * L + i) * Hq + h) * D + c, num / den,
+                a.s.out_f32);
+}
+
+int softmax_prefix_splits(const Shape& s, int max_prefix) {
+  const long units = (long)s.B * s.Hkv;
+  long want = units > 0 ? (2048 + units - 1) / units : 1;
+  const long cap = ((long)max_prefix + s.L + 511) / 512;
+  if (want > cap) want = cap;
+  if (want < 1) want = 1;
+  return (int)want;
+}
+
+size_t softmax_prefix_ws_bytes(const Shape& s, int n_split) {
+  return (size_t)s.B * s.Hq * n_split * s.L * (s.D + 2) * sizeof(float);
+}
+
+template <typename T, int D>
+static hipError_t sp_go(const SoftmaxPrefixArgs& a, hipStream_t st) {
+  const int ns = a.n_split;
+  int chunk = (a.max_prefix + a.s.L + ns - 1) / ns;
+  chunk = (chunk + kTile - 1) / kTile * kTile;
+  const int G = a.s.Hq / a.s.Hkv;
+  hipLaunchKernelGGL((hyb_sp_partial_kernel<T, D>),
+                     dim3(a.s.B * a.s.Hkv * ns), dim3(kWave * G), 0, st, a,
+                     chunk);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL((hyb_sp_combine_kernel<T, D>), dim3(a.s.B * a.s.Hq * a.s.L),
+                     dim3(D), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_softmax_prefix(const SoftmaxPrefixArgs& a, hipStream_t st) {
+  if (a.s.Hq / a.s.Hkv > kMaxGroup) return hipErrorInvalidValue;
+  if (a.s.dtype == 1)
+    return a.s.D == 64 ? sp_go<bf16, 64>(a, st) : sp_go<bf16, 128>(a, st);
+  return a.s.D == 64 ? sp_go<float, 64>(a, st) : sp_go<float, 128>(a, st);
+}
+
+}  // namespace hyb

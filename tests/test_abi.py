@@ -1,0 +1,122 @@
+"""The C ABI on the CPU: the library loads, exports every symbol the header
+declares, and rejects bad arguments before any HIP call.
+
+Every call here is built to fail validation, so nothing is ever launched:
+the pointers are small fake addresses that no kernel may see.
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2608_06628_amd import binding as hb
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "hybrid_attn.h")
+
+FAKE = ctypes.c_void_p(0x1000)      # aligned, never dereferenced
+MISALIGNED = ctypes.c_void_p(0x1008)
+
+
+def _declared():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^(?:int|size_t|const char\*)\s+(\w+)\s*\(", text, re.M)))
+
+
+def test_exports_match_header():
+    lib = hb.load()
+    names = _declared()
+    assert set(names) == set(hb.EXPORTS)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def _dims(**kw):
+    base = dict(batch=2, n_q_heads=16, n_kv_heads=4, head_dim=128, block=32,
+                feat_dim=128, dtype=hb.HYB_BF16, n_slots=2, flags=0)
+    base.update(kw)
+    return hb.Dims(*[base[n] for n, _ in hb.Dims._fields_])
+
+
+def _step(dims, ptrs=None):
+    lib = hb.load()
+    p = ptrs or [FAKE] * 9
+    return lib.hybrid_attn_step(ctypes.byref(dims) if dims is not None else None, *p, None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(head_dim=96), 5), (dict(feat_dim=96), 5), (dict(block=33), 5),
+    (dict(block=0), 2), (dict(n_kv_heads=3), 2), (dict(batch=-1), 2),
+    (dict(dtype=7), 4), (dict(n_slots=0), 2), (dict(n_q_heads=0), 2),
+    (dict(flags=2), 2), (dict(flags=-1), 2),
+])
+def test_step_rejects_bad_dims(kw, code):
+    assert _step(_dims(**kw)) == code
+    assert hb.last_error()
+
+
+def test_null_and_alignment():
+    assert _step(None) == 1
+    for i in range(9):
+        if i == 7:   # slots may be NULL; misaligned is still rejected
+            p = [FAKE] * 9
+            p[i] = MISALIGNED
+            assert _step(_dims(), p) == 3
+            continue
+        p = [FAKE] * 9
+        p[i] = None
+        assert _step(_dims(), p) == 1, i
+        p[i] = MISALIGNED
+        assert _step(_dims(), p) == 3, i
+
+
+def test_out_aliasing_rejected():
+    p = [FAKE] * 9
+    p[8] = p[0]     # out == q
+    assert _step(_dims(), p) == 2
+    assert "overlap" in hb.last_error()
+
+
+def test_zero_batch_is_a_noop():
+    assert _step(_dims(batch=0), [None] * 9) == 0
+    assert hb.last_error() == ""
+
+
+def test_commit_prefill_softmax_validation():
+    lib = hb.load()
+    d = _dims()
+    assert lib.hybrid_state_commit(ctypes.byref(d), FAKE, FAKE, FAKE, None, FAKE, None, None) == 1
+    assert lib.hybrid_state_commit(ctypes.byref(_dims(feat_dim=48)), FAKE, FAKE, FAKE, FAKE,
+                                   FAKE, None, None) == 5
+    # S and z overlapping
+    assert lib.hybrid_state_commit(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, None, None) == 2
+    # prefill: seq_len not a multiple of the block
+    assert lib.hybrid_state_prefill(ctypes.byref(d), 40, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                    FAKE, None, None, None, 0, None) == 2
+    assert lib.hybrid_state_prefill(ctypes.byref(d), 0, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                    FAKE, None, None, None, 0, None) == 2
+    # softmax prefix: missing workspace
+    need = lib.hybrid_workspace_bytes(ctypes.byref(d), hb.OP_SOFTMAX_PREFIX, 4096)
+    assert need > 0
+    assert lib.softmax_prefix_step(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 4096,
+                                   FAKE, None, 0, None) == 6
+    assert lib.softmax_prefix_step(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 4096,
+                                   ctypes.c_void_p(0x100000), FAKE, need - 1, None) == 6
+    assert lib.softmax_prefix_step(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, -1,
+                                   FAKE, FAKE, need, None) == 2
+    # more than 8 query heads per KV head
+    assert lib.softmax_prefix_step(ctypes.byref(_dims(n_kv_heads=1)), FAKE, FAKE, FAKE, FAKE,
+                                   FAKE, FAKE, 64, FAKE, FAKE, need, None) == 5
+
+
+def test_workspace_query():
+    lib = hb.load()
+    d = _dims(batch=128)
+    assert lib.hybrid_workspace_bytes(ctypes.byref(d), hb.OP_STEP, 0) == 0
+    assert lib.hybrid_workspace_bytes(ctypes.byref(d), hb.OP_COMMIT, 0) == 0
+    ws = lib.hybrid_workspace_bytes(ctypes.byref(d), hb.OP_SOFTMAX_PREFIX, 32768)
+    # n_split partial rows of (d + 2) floats per (request, head, query)
+    assert ws % (128 * 16 * 32 * 130 * 4) == 0 and ws > 0
+    assert lib.hybrid_workspace_bytes(ctypes.byref(_dims(head_dim=5)), hb.OP_STEP, 0) == 0
+    assert lib.hybrid_workspace_bytes(None, hb.OP_STEP, 0) == 0
