@@ -92,7 +92,7 @@ class Lane:
 
 def build_states(dims, plens, W, gen, dev):
     """Per-request states of synthetic bf16 prefixes, built by the GPU prefill."""
-    S = torch.zeros((dims.B, dims.Hq, dims.f, dims.d), device=dev)
+    S = torch.zeros((dims.B, dims.Hq, dims.d, dims.f), device=dev)   # S_h transposed
     z = torch.zeros((dims.B, dims.Hq, dims.f), device=dev)
     scale = 1.0 / math.sqrt(dims.d)
     for b, P in enumerate(plens.tolist()):
@@ -171,30 +171,28 @@ def run(args):
     torch.cuda.synchronize()
     log(f"{R} lanes allocated ({torch.cuda.memory_allocated() / 2**30:.2f} GiB in use)")
 
-    ev_pairs = []
+    phases = []  # (kind, start event, end event, launches between them)
 
     def cycle(record):
+        # The R*NSTEP step launches, then the R commits, each phase bracketed
+        # by one event pair on the launch stream: launches inside a phase run
+        # back to back, so elapsed / launches is the per-launch duration.
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)] if record else None
+        if record:
+            ev[0].record()
         for s in range(NSTEP):
             for ln in lanes:
                 q, k, v, o = ln.qkv[s]
-                if record:
-                    e0 = torch.cuda.Event(enable_timing=True)
-                    e1 = torch.cuda.Event(enable_timing=True)
-                    e0.record()
                 hb.hybrid_attn_step(q, k, v, W, alpha, ln.S, ln.z, out=o)
-                if record:
-                    e1.record()
-                    ev_pairs.append(("step", e0, e1))
+        if record:
+            ev[1].record()
         for ln in lanes:
             q, k, v, o = ln.qkv[NSTEP - 1]
-            if record:
-                e0 = torch.cuda.Event(enable_timing=True)
-                e1 = torch.cuda.Event(enable_timing=True)
-                e0.record()
             hb.hybrid_state_commit(k, v, W, ln.S, ln.z)
-            if record:
-                e1.record()
-                ev_pairs.append(("commit", e0, e1))
+        if record:
+            ev[2].record()
+            phases.append(("step", ev[0], ev[1], NSTEP * len(lanes)))
+            phases.append(("commit", ev[1], ev[2], len(lanes)))
 
     for _ in range(args.warmup):
         cycle(False)
@@ -210,13 +208,13 @@ def run(args):
     b.record()
     torch.cuda.synchronize()
     ms_cycle = a.elapsed_time(b) / args.steps
-    # Per-kernel durations, bracketed by events on the launch stream.
+    # Per-kernel durations: one event pair per phase of each cycle.
     for _ in range(args.steps):
         cycle(True)
     torch.cuda.synchronize()
     durs = {"step": [], "commit": []}
-    for kind, e0, e1 in ev_pairs:
-        durs[kind].append(e0.elapsed_time(e1))
+    for kind, e0, e1, n in phases:
+        durs[kind].append(e0.elapsed_time(e1) / n)
     t_step = float(np.mean(durs["step"])) * 1e-3
     t_commit = float(np.mean(durs["commit"])) * 1e-3
     sb = step_bytes(B, Hq, Hkv, d, L, f)
@@ -243,8 +241,9 @@ def run(args):
                      "unit": "GB/s", "frac": step_gbps / HBM_PEAK_GBPS, "traffic": None,
                      "kernel": "hyb_step_kernel<bf16,128,64>",
                      "algorithmic_bytes_per_launch": sb, "mean_launch_us": t_step * 1e6},
-        "step_kernel": {"mean_us": t_step * 1e6, "p10_us": float(np.percentile(durs["step"], 10)) * 1e3,
-                        "p90_us": float(np.percentile(durs["step"], 90)) * 1e3,
+        "step_kernel": {"mean_us": t_step * 1e6,
+                        "min_cycle_mean_us": float(np.min(durs["step"])) * 1e3,
+                        "max_cycle_mean_us": float(np.max(durs["step"])) * 1e3,
                         "gbps": step_gbps, "tokens_per_s": B * L / t_step,
                         "tflops": step_flops(B, Hq, d, L, f) / t_step / 1e12},
         "commit_kernel": {"mean_us": t_commit * 1e6, "gbps": commit_gbps,
@@ -272,7 +271,7 @@ def bench_prefill(gen, dev):
     Wt, alpha = synth.feature_weights(dims, 1, 2)
     W = torch.from_numpy(Wt).to(dev).to(torch.bfloat16)
     al = torch.from_numpy(alpha).to(dev)
-    S = torch.zeros((B, Hq, f, d), device=dev)
+    S = torch.zeros((B, Hq, d, f), device=dev)   # S_h transposed
     z = torch.zeros((B, Hq, f), device=dev)
     out = torch.empty_like(q)
 

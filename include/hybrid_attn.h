@@ -27,8 +27,10 @@
  *                                      this is the weight layout of a linear
  *                                      layer d -> F
  *   alpha         [Hq] float           gate logits; the library forms sigmoid
- *   S             [n_slots][Hq][f][d] float   S_h as defined above (rows =
- *                                      features, columns = value dims)
+ *   S             [n_slots][Hq][d][f] float   S_h stored transposed:
+ *                                      entry (feature r, value dim c) of S_h
+ *                                      is at c*f + r, so the f features of
+ *                                      one value dim are contiguous
  *   z             [n_slots][Hq][f] float
  *   slots         [B] int32 or NULL    state slot of request b; NULL means
  *                                      slot b.  A slot outside [0, n_slots)

@@ -118,13 +118,13 @@ def _out_flags(out, act, out_f32):
 def hybrid_attn_step(q, k, v, W, alpha, S, z, slots=None, out=None, out_f32=False,
                      stream=None):
     """q [B][L][Hq][d], k/v [B][L][Hkv][d], W [Hq][F][d], alpha [Hq] f32,
-    S [n_slots][Hq][f][d] f32, z [n_slots][Hq][f] f32 -> out [B][L][Hq][d]
+    S [n_slots][Hq][d][f] f32 (S_h transposed), z [n_slots][Hq][f] f32 -> out [B][L][Hq][d]
     in q's dtype (fp32 with out_f32)."""
     lib = load()
     B, L, Hq, d = q.shape
     act = q.dtype
     flags, odt = _out_flags(out, act, out_f32)
-    dims = make_dims(B, Hq, k.shape[2], d, L, S.shape[2], _dt(q), S.shape[0], flags)
+    dims = make_dims(B, Hq, k.shape[2], d, L, z.shape[2], _dt(q), S.shape[0], flags)
     if out is None:
         out = torch.empty(q.shape, dtype=odt, device=q.device)
     _check(lib.hybrid_attn_step(
@@ -139,7 +139,7 @@ def hybrid_state_commit(k, v, W, S, z, slots=None, stream=None):
     """Folds the block k/v [B][L][Hkv][d] into S, z in place."""
     lib = load()
     B, L, Hkv, d = k.shape
-    dims = make_dims(B, W.shape[0], Hkv, d, L, S.shape[2], _dt(k), S.shape[0])
+    dims = make_dims(B, W.shape[0], Hkv, d, L, z.shape[2], _dt(k), S.shape[0])
     act = k.dtype
     _check(lib.hybrid_state_commit(
         ctypes.byref(dims), _ptr(k, "k"), _ptr(v, "v", act), _ptr(W, "W", act),
@@ -160,7 +160,7 @@ def hybrid_state_prefill(q, k, v, W, alpha, S, z, block, slots=None, out=None,
     Hq = W.shape[0]
     act = k.dtype
     flags, odt = _out_flags(out, act, out_f32)
-    dims = make_dims(B, Hq, Hkv, d, block, S.shape[2], _dt(k), S.shape[0], flags)
+    dims = make_dims(B, Hq, Hkv, d, block, z.shape[2], _dt(k), S.shape[0], flags)
     if want_out and out is None:
         out = torch.empty((B, T, Hq, d), dtype=odt, device=k.device)
     if not want_out:

@@ -246,6 +246,17 @@ __device__ inline float log_sigmoid(float a) {
   return a >= 0.0f ? -log1pf(expf(-a)) : a - log1pf(expf(a));
 }
 
+// Workgroup barrier that orders LDS accesses only.  __syncthreads() carries a
+// workgroup fence over every address space, which makes each wave wait for
+// all of its outstanding global loads before the barrier; restricting the
+// fences to the local address space keeps loads issued before the barrier in
+// flight (LDS writes are still complete and visible after it).
+__device__ inline void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 // Work-unit index for the workgroup: consecutive units land on one XCD.
 // Workgroups are handed to the 8 XCDs round-robin by blockIdx, so unit
 // u = (bid % 8) * (n / 8) + bid / 8 keeps units u..u+n/8-1 on one XCD (and

@@ -49,8 +49,6 @@ struct SoftmaxPrefixArgs {
   int n_split;  // KV splits per (request, KV head)
 };
 
-// Each returns false when no kernel exists for the shape's variant.
-bool step_supported(const Shape& s);
 hipError_t launch_step(const StepArgs& a, hipStream_t st);
 hipError_t launch_commit(const CommitArgs& a, hipStream_t st);
 hipError_t launch_prefill(const PrefillArgs& a, hipStream_t st);

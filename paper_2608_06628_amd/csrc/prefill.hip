@@ -80,8 +80,12 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_prefill_kernel(
 #pragma unroll
   for (int rt = 0; rt < C::NRT; ++rt)
 #pragma unroll
-    for (int i = 0; i < 16; ++i)
-      sacc[rt][i] = Sh[(size_t)(rt * kTile + row_of(i, hh)) * D + col];
+    for (int j = 0; j < 4; ++j) {  // rows rt*32 + j*8 + hh*4 .. +3: 16 bytes
+      const f32x4 x = *reinterpret_cast<const f32x4*>(
+          Sh + (size_t)col * f + rt * kTile + row_of(4 * j, hh));
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sacc[rt][4 * j + r] = x[r];
+    }
   for (int r = tid; r < f; r += blockDim.x) sh.z[r] = zh[r];
 
   const T* __restrict__ Wt_h = (const T*)a.W + (size_t)h * F * D;
@@ -240,8 +244,9 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_prefill_kernel(
 #pragma unroll
   for (int rt = 0; rt < C::NRT; ++rt)
 #pragma unroll
-    for (int i = 0; i < 16; ++i)
-      Sh[(size_t)(rt * kTile + row_of(i, hh)) * D + col] = sacc[rt][i];
+    for (int j = 0; j < 4; ++j)
+      *reinterpret_cast<f32x4*>(Sh + (size_t)col * f + rt * kTile + row_of(4 * j, hh)) =
+          f32x4{sacc[rt][4 * j], sacc[rt][4 * j + 1], sacc[rt][4 * j + 2], sacc[rt][4 * j + 3]};
   __syncthreads();
   for (int r = tid; r < f; r += blockDim.x) zh[r] = sh.z[r];
 }

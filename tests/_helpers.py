@@ -45,6 +45,19 @@ def host(t: torch.Tensor) -> np.ndarray:
     return t.detach().float().cpu().numpy().astype(np.float64)
 
 
+# The oracle keeps each S_h as the f x d matrix of the paper; the library
+# stores it transposed ([..][d][f], features contiguous).  These two convert
+# between the layouts and do nothing else.
+def state_dev(S) -> torch.Tensor:
+    """Oracle-layout state [..][f][d] -> device tensor in the library layout."""
+    return f32(np.swapaxes(np.asarray(S), -1, -2))
+
+
+def state_host(S: torch.Tensor) -> np.ndarray:
+    """Library-layout device state -> fp64 array in the oracle layout."""
+    return np.ascontiguousarray(np.swapaxes(host(S), -1, -2))
+
+
 def tol_for(ref: np.ndarray, dtype: str) -> float:
     if dtype == "f32":
         return 1e-5

@@ -8,7 +8,8 @@ import torch
 import oracle
 from paper_2608_06628_amd import binding as hb
 from paper_2608_06628_amd import synth
-from _helpers import act, announce, assert_close, check_outputs, f32, host, i32, make_case
+from _helpers import (act, announce, assert_close, check_outputs, f32, host, i32, make_case,
+                      state_dev, state_host)
 
 pytestmark = pytest.mark.gpu
 
@@ -36,11 +37,11 @@ def test_commit(shape):
     dims = synth.Dims(B=B, Hq=Hq, Hkv=Hkv, d=d, L=L, F=F, dtype=dt)
     announce(f"commit {shape}")
     c = make_case(dims, P, seed=7, peaky=True)
-    S, z = f32(c["S"]), f32(c["z"])
+    S, z = state_dev(c["S"]), f32(c["z"])
     hb.hybrid_state_commit(act(c["k"], dt), act(c["v"], dt), act(c["Wt"], dt), S, z)
     torch.cuda.synchronize()
     Sr, zr = oracle.commit(c["k"], c["v"], c["Wt"], c["S"], c["z"])
-    assert_state_delta(host(S), host(z), c["S"], c["z"], Sr, zr, dt, f"commit {shape}")
+    assert_state_delta(state_host(S), host(z), c["S"], c["z"], Sr, zr, dt, f"commit {shape}")
 
 
 def test_commit_slots_and_bad_slot():
@@ -48,17 +49,17 @@ def test_commit_slots_and_bad_slot():
     slots = np.array([3, 0, 5], np.int32)
     announce("commit slots")
     c = make_case(dims, 32, seed=8, peaky=True, n_slots=6, slots=slots)
-    S, z = f32(c["S"]), f32(c["z"])
+    S, z = state_dev(c["S"]), f32(c["z"])
     bad = np.array([3, 9, 5], np.int32)   # request 1 has no valid slot
     hb.hybrid_state_commit(act(c["k"], "bf16"), act(c["v"], "bf16"), act(c["Wt"], "bf16"),
                            S, z, slots=i32(bad))
     torch.cuda.synchronize()
     k, v = c["k"][[0, 2]], c["v"][[0, 2]]
     Sr, zr = oracle.commit(k, v, c["Wt"], c["S"], c["z"], slots=np.array([3, 5], np.int32))
-    assert_state_delta(host(S), host(z), c["S"], c["z"], Sr, zr, "bf16", "commit slots")
+    assert_state_delta(state_host(S), host(z), c["S"], c["z"], Sr, zr, "bf16", "commit slots")
     # untouched slots are bit-identical
     for s in (0, 1, 2, 4):
-        assert torch.equal(S[s].cpu(), torch.from_numpy(c["S"][s]))
+        assert torch.equal(S[s].cpu(), state_dev(c["S"][s]).cpu())
 
 
 PREFILL_SHAPES = [
@@ -86,20 +87,20 @@ def test_prefill(shape):
     states = []
 
     def call(out_f32):
-        S, z = f32(c0["S"]), f32(c0["z"])
+        S, z = state_dev(c0["S"]), f32(c0["z"])
         states.append((S, z))
         return hb.hybrid_state_prefill(act(q, dt), act(k, dt), act(v, dt), act(Wt, dt),
                                        f32(alpha), S, z, L, out_f32=out_f32)
 
     check_outputs(call, o_r, dt, f"prefill out {shape}")
     S, z = states[-1]
-    assert_state_delta(host(S), host(z), c0["S"], c0["z"], Sr, zr, dt, f"prefill {shape}")
+    assert_state_delta(state_host(S), host(z), c0["S"], c0["z"], Sr, zr, dt, f"prefill {shape}")
     # state only
-    S2, z2 = f32(c0["S"]), f32(c0["z"])
+    S2, z2 = state_dev(c0["S"]), f32(c0["z"])
     assert hb.hybrid_state_prefill(None, act(k, dt), act(v, dt), act(Wt, dt), None, S2, z2, L,
                                    want_out=False) is None
     torch.cuda.synchronize()
-    assert_state_delta(host(S2), host(z2), c0["S"], c0["z"], Sr, zr, dt, f"prefill-state {shape}")
+    assert_state_delta(state_host(S2), host(z2), c0["S"], c0["z"], Sr, zr, dt, f"prefill-state {shape}")
 
 
 def test_prefill_equals_commits_and_resume():
@@ -113,7 +114,7 @@ def test_prefill_equals_commits_and_resume():
     _, k, v = synth.block_qkv(seq, 61, 1.0 / np.sqrt(dims.d))
     Wt, _ = synth.feature_weights(dims, 62, 63)
     kd, vd, Wd = act(k, "bf16"), act(v, "bf16"), act(Wt, "bf16")
-    S1 = torch.zeros((2, 16, 128, 128), device="cuda")
+    S1 = torch.zeros((2, 16, 128, 128), device="cuda")   # [B][Hq][d][f]
     z1 = torch.zeros((2, 16, 128), device="cuda")
     hb.hybrid_state_prefill(None, kd, vd, Wd, None, S1, z1, dims.L, want_out=False)
     S2, z2 = torch.zeros_like(S1), torch.zeros_like(z1)
@@ -126,8 +127,8 @@ def test_prefill_equals_commits_and_resume():
     torch.cuda.synchronize()
     S0, z0 = oracle.empty_state(2, 16, 128, 128)
     Sr, zr = oracle.commit(k, v, Wt, S0, z0)
-    assert_close(host(S1), Sr, "bf16", "prefill state 8192")
-    assert_close(host(S2), Sr, "bf16", "256 commits state")
+    assert_close(state_host(S1), Sr, "bf16", "prefill state 8192")
+    assert_close(state_host(S2), Sr, "bf16", "256 commits state")
     assert_close(host(z1), zr, "bf16", "prefill z 8192")
     # resume from the checkpoint in fresh buffers
     S3, z3 = ck[0].cuda(), ck[1].cuda()
@@ -142,4 +143,4 @@ def test_prefill_equals_commits_and_resume():
         sl = slice(blk * dims.L, (blk + 1) * dims.L)
         hb.hybrid_state_commit(kd[:, sl].contiguous(), vd[:, sl].contiguous(), Wd, S4, z4)
     torch.cuda.synchronize()
-    assert_close(host(S4), Sr, "bf16", "reverse-order commits state")
+    assert_close(state_host(S4), Sr, "bf16", "reverse-order commits state")

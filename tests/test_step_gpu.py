@@ -8,14 +8,15 @@ import torch
 import oracle
 from paper_2608_06628_amd import binding as hb
 from paper_2608_06628_amd import synth
-from _helpers import act, announce, assert_close, check_outputs, f32, host, i32, make_case
+from _helpers import (act, announce, assert_close, check_outputs, f32, host, i32, make_case,
+                      state_dev)
 
 pytestmark = pytest.mark.gpu
 
 
 def step_call(c, dims, slots=None):
     args = (act(c["q"], dims.dtype), act(c["k"], dims.dtype), act(c["v"], dims.dtype),
-            act(c["Wt"], dims.dtype), f32(c["alpha"]), f32(c["S"]), f32(c["z"]))
+            act(c["Wt"], dims.dtype), f32(c["alpha"]), state_dev(c["S"]), f32(c["z"]))
     sl = None if slots is None else i32(slots)
     return lambda out_f32: hb.hybrid_attn_step(*args, slots=sl, out_f32=out_f32)
 
@@ -136,7 +137,7 @@ def test_deterministic_and_guarded():
     announce("step determinism")
     c = make_case(dims, 128, seed=30, peaky=True)
     q, k, v = (act(c[n], "bf16") for n in ("q", "k", "v"))
-    W, al, S, z = act(c["Wt"], "bf16"), f32(c["alpha"]), f32(c["S"]), f32(c["z"])
+    W, al, S, z = act(c["Wt"], "bf16"), f32(c["alpha"]), state_dev(c["S"]), f32(c["z"])
     n = q.numel()
     guard = 4096
     buf = torch.full((n + 2 * guard,), float("nan"), dtype=torch.bfloat16, device="cuda")
