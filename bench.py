@@ -37,6 +37,25 @@ from paper_2608_06628_amd import binding as hb
 from paper_2608_06628_amd import synth
 
 HBM_PEAK_GBPS = 8000.0
+# HBM bytes per step launch from rocprofv3 FETCH_SIZE and WRITE_SIZE on the
+# serve64 workload, scaled by the counts the same counters give on a 256 MiB
+# copy (x2.0 for FETCH_SIZE, x1.0 for WRITE_SIZE).  Keyed by the SHA-256 of
+# the step kernel's sources: after any change the entry no longer matches and
+# the bench reports the traffic as unknown until the counters are read again.
+STEP_TRAFFIC = {
+    "5c17b169e57e5eb49be0de951380b34457f47ca2a314eba95ed99a367eb91e82": {"read": 40329.5 * 1024 * 2.0, "written": 8192.0 * 1024 * 1.0},
+}
+STEP_SOURCES = ("csrc/step.hip", "csrc/device.h", "csrc/launch.h")
+
+
+def step_source_hash() -> str:
+    import hashlib
+    here = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2608_06628_amd")
+    h = hashlib.sha256()
+    for rel in STEP_SOURCES:
+        with open(os.path.join(here, rel), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
 BF16_MFMA_PEAK_TFLOPS = 2500.0
 METRIC = ("hybrid denoise-step tokens/sec + achieved HBM GB/s "
           "(B=64,Hq16/Hkv4,d128,blk32)")
@@ -218,6 +237,8 @@ def run(args):
     t_step = float(np.mean(durs["step"])) * 1e-3
     t_commit = float(np.mean(durs["commit"])) * 1e-3
     sb = step_bytes(B, Hq, Hkv, d, L, f)
+    tr = STEP_TRAFFIC.get(step_source_hash())
+    traffic = None if tr is None else tr["read"] + tr["written"]
     cb = commit_bytes(B, Hq, Hkv, d, L, f)
     step_gbps = sb / t_step / 1e9
     commit_gbps = cb / t_commit / 1e9
@@ -238,7 +259,7 @@ def run(args):
                    "global_batch": B, "seq_len": L, "lanes": R, "parallelism": "none (1 GPU)",
                    "state_dtype": "fp32", "prefix_tokens": int(plens.sum())},
         "roofline": {"bound": "hbm", "achieved": step_gbps, "peak": HBM_PEAK_GBPS,
-                     "unit": "GB/s", "frac": step_gbps / HBM_PEAK_GBPS, "traffic": None,
+                     "unit": "GB/s", "frac": step_gbps / HBM_PEAK_GBPS, "traffic": traffic,
                      "kernel": "hyb_step_kernel<bf16,128,64>",
                      "algorithmic_bytes_per_launch": sb, "mean_launch_us": t_step * 1e6},
         "step_kernel": {"mean_us": t_step * 1e6,
@@ -339,6 +360,19 @@ def bench_mix(gen, dev):
             "mix_6h14s_vs_20s": (20 * ms_sm) / (6 * ms_hy + 14 * ms_sm)}
 
 
+def copy_calibration():
+    """A plain device-to-device copy of a known size: 256 MiB read, 256 MiB
+    written per launch.  Byte counters read on it give the scale factor that
+    converts the same counters on the hybrid kernels into bytes."""
+    n = (256 << 20) // 4
+    src = torch.rand(n, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(5):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": n * 4, "copy_bytes_written": n * 4, "launches": 5}))
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -348,12 +382,18 @@ def main():
     ap.add_argument("--cpu-requests", type=int, default=64)
     ap.add_argument("--no-extras", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only copy 256 MiB device to device five times (the reference "
+                         "kernel for scaling HBM byte counters), then exit")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: the hybrid layer shards by request or KV-head "
-              "group with no exchange, and this build runs on a single MI355X only.",
+        print("bench.py measures one GPU only (run it without --gpus, or with --gpus 1); "
+              "the hybrid layer shards by request or by KV-head group with no exchange.",
               file=sys.stderr)
         sys.exit(2)
+    if args.copy_calibration:
+        copy_calibration()
+        return
     run(args)
 
 
