@@ -226,6 +226,24 @@ __device__ inline void store_out4(void* out, size_t idx, const float* v,
   }
 }
 
+// Eight consecutive outputs at element index idx (16-byte aligned), written
+// with non-temporal stores: fp32 as two 16-byte stores, bf16 as one.
+template <typename T>
+__device__ inline void store_out8_nt(void* out, size_t idx, const float* v,
+                                     bool f32) {
+  if (sizeof(T) == 4 || f32) {
+    f32x4* o = reinterpret_cast<f32x4*>((float*)out + idx);
+    __builtin_nontemporal_store(f32x4{v[0], v[1], v[2], v[3]}, o);
+    __builtin_nontemporal_store(f32x4{v[4], v[5], v[6], v[7]}, o + 1);
+  } else {
+    typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+    const bf16x8 x{(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3],
+                   (bf16)v[4], (bf16)v[5], (bf16)v[6], (bf16)v[7]};
+    __builtin_nontemporal_store(*reinterpret_cast<const u32x4*>(&x),
+                                reinterpret_cast<u32x4*>((bf16*)out + idx));
+  }
+}
+
 template <typename T>
 __device__ inline void store_out1(void* out, size_t idx, float v, bool f32) {
   if (sizeof(T) == 4 || f32)

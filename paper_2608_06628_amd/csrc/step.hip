@@ -70,6 +70,7 @@ struct StepCfg {
     T vt[D][VT_LD];
     f32x4 apv[CB][QB][kWave];
   };
+  static_assert(CB % 2 == 0, "output columns are stored in pairs of blocks");
   struct alignas(16) Smem {
     HeadLds hd[NW];
     op_t phib[NW][QB][KF][kWave];  // b phi(Q) as the readout's B operand
@@ -82,6 +83,13 @@ struct StepCfg {
   // Block key held by P register j (j < 8): j = kb*4 + r.
   __device__ static constexpr int key(int j, int quad) {
     return (j / 4) * 16 + quad * 4 + (j % 4);
+  }
+  // Output column carried by row i of the accumulator tile of column block
+  // cb.  Pairs of blocks (2p, 2p+1) cover columns 32p .. 32p+31 so that the
+  // lane holding rows quad*4 .. +3 of both blocks owns the 8 consecutive
+  // columns 32p + 8 quad .. +7 and stores them with one 16-byte write.
+  __device__ static constexpr int column(int cb, int i) {
+    return (cb >> 1) * 32 + (i >> 2) * 8 + (cb & 1) * 4 + (i & 3);
   }
 };
 
@@ -153,14 +161,14 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
   const size_t sbase = (size_t)(slot_ok ? slot : 0) * Hq + h;
 
   // State wave: column block cb of S_h^T; lane (c16, quad) reads the RUNS
-  // 16-byte runs of column cb*16 + c16 at features feature(4 rn, quad).
+  // 16-byte runs of column column(cb, c16) at features feature(4 rn, quad).
   f32x4 buf[NBUF][RUNS];
-  const float* __restrict__ St = a.S + sbase * f * D + (size_t)c16 * f;
+  const float* __restrict__ St = a.S + sbase * f * D;
   auto issue = [&](int cb) {
 #pragma unroll
     for (int rn = 0; rn < RUNS; ++rn)
       buf[cb % NBUF][rn] = *reinterpret_cast<const f32x4*>(
-          St + (size_t)(cb * 16) * f + C::feature(rn * 4, quad));
+          St + (size_t)C::column(cb, c16) * f + C::feature(rn * 4, quad));
   };
 
   if (state_wave) {
@@ -329,7 +337,7 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
 #pragma unroll
         for (int ks = 0; ks < C::KL; ++ks)
           acc[cbk][qb] = mma16_split_b<T>(
-              lds_keys_op<T>(&vt[cbk * 16 + c16][0], ks, quad), &p[qb][ks * E],
+              lds_keys_op<T>(&vt[C::column(cbk, c16)][0], ks, quad), &p[qb][ks * E],
               acc[cbk][qb]);
       }
 #pragma unroll
@@ -367,16 +375,18 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
     if (cbk + NBUF < CB) issue(cbk + NBUF);
   }
 
-  // 8. Store: the lane holds query qb*16 + c16, columns cb*16 + quad*4 .. +3.
+  // 8. Store: the lane holds query qb*16 + c16 and, for each block pair p,
+  //    the 8 consecutive columns 32p + 8 quad .. +7 (see column()).  The
+  //    output is not read again by this kernel: non-temporal stores.
 #pragma unroll
   for (int qb = 0; qb < QB; ++qb) {
     if (qb * 16 + c16 >= L) continue;
     const size_t obase = (((size_t)b * L + qb * 16 + c16) * Hq + h) * D;
 #pragma unroll
-    for (int cbk = 0; cbk < CB; ++cbk) {
-      const float o[4] = {acc[cbk][qb][0], acc[cbk][qb][1], acc[cbk][qb][2],
-                          acc[cbk][qb][3]};
-      store_out4<T>(a.out, obase + cbk * 16 + quad * 4, o, a.s.out_f32);
+    for (int pr = 0; pr < CB / 2; ++pr) {
+      const f32x4 lo = acc[2 * pr][qb], hi = acc[2 * pr + 1][qb];
+      const float o[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+      store_out8_nt<T>(a.out, obase + pr * 32 + quad * 8, o, a.s.out_f32);
     }
   }
 }
