@@ -130,7 +130,10 @@ int hybrid_state_commit(const hyb_dims_t* dims, const void* k, const void* v,
  * seq_len must be a positive multiple of L.  out may be NULL (state only; q
  * is then ignored and may be NULL).  ws/ws_bytes: workspace of at least
  * hybrid_workspace_bytes(dims, HYB_OP_PREFILL, seq_len) bytes (may be NULL
- * when that is 0).  Two requests of one call must not share a slot. */
+ * when that is 0); the prompt is processed in sequence segments whose state
+ * increments pass through it, so results equal the block-by-block ones up to
+ * the order of fp32 additions.  It must not overlap any other argument.  Two
+ * requests of one call must not share a slot. */
 int hybrid_state_prefill(const hyb_dims_t* dims, int32_t seq_len,
                          const void* q, const void* k, const void* v,
                          const void* W, const float* alpha, float* S, float* z,

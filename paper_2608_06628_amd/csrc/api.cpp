@@ -191,7 +191,11 @@ int hybrid_state_prefill(const hyb_dims_t* dims, int32_t seq_len,
               overlap(out, no, v, nkv) || overlap(out, no, S, nS) ||
               overlap(out, no, z, nz)))
     return fail(HYB_EINVAL, "out overlaps an input");
-  hyb::PrefillArgs a{s, seq_len, q, k, v, W, alpha, S, z, slots, out};
+  if (need > 0 && (overlap(ws, need, S, nS) || overlap(ws, need, z, nz) ||
+                   overlap(ws, need, k, nkv) || overlap(ws, need, v, nkv) ||
+                   (out && (overlap(ws, need, out, no) || overlap(ws, need, q, nq)))))
+    return fail(HYB_EINVAL, "the workspace overlaps an argument");
+  hyb::PrefillArgs a{s, seq_len, q, k, v, W, alpha, S, z, slots, out, (float*)ws};
   (void)hipGetLastError();
   return launched(hyb::launch_prefill(a, (hipStream_t)stream), "prefill");
 }
@@ -252,8 +256,10 @@ size_t hybrid_workspace_bytes(const hyb_dims_t* dims, int32_t op,
   switch (op) {
     case HYB_OP_STEP:
     case HYB_OP_COMMIT:
-    case HYB_OP_PREFILL:
       return 0;
+    case HYB_OP_PREFILL:
+      if (extent == 0 || extent % s.L != 0) return 0;
+      return hyb::prefill_ws_bytes(s, extent);
     case HYB_OP_SOFTMAX_PREFIX:
       return hyb::softmax_prefix_ws_bytes(
           s, hyb::softmax_prefix_splits(s, extent));

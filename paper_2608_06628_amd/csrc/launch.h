@@ -37,6 +37,7 @@ struct PrefillArgs {
   float *S, *z;
   const int32_t* slots;
   void* out;  // may be null
+  float* ws;  // per-segment state deltas (nseg > 1), caller's workspace
 };
 
 struct SoftmaxPrefixArgs {
@@ -53,6 +54,10 @@ hipError_t launch_step(const StepArgs& a, hipStream_t st);
 hipError_t launch_commit(const CommitArgs& a, hipStream_t st);
 hipError_t launch_prefill(const PrefillArgs& a, hipStream_t st);
 hipError_t launch_softmax_prefix(const SoftmaxPrefixArgs& a, hipStream_t st);
+
+// Prefill: number of sequence segments and the workspace they need.
+int prefill_segments(const Shape& s, int T);
+size_t prefill_ws_bytes(const Shape& s, int T);
 
 // Workspace of softmax_prefix_step for n_split splits.
 size_t softmax_prefix_ws_bytes(const Shape& s, int n_split);

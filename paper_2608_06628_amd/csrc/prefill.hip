@@ -4,7 +4,18 @@
 // gated merge (Section 3.1) -- and is then committed,
 // S += phi(K_c)^T V_c, z += sum phi(K_c).
 //
-// One workgroup per (request b, query head h) walks the blocks in order.
+// Sequence segments.  The prompt's blocks are cut into nseg segments so that
+// the grid fills the chip.  A first launch (delta mode) computes each
+// segment's own state increment dS_s = sum_{c in s} phi(K_c)^T V_c and dz_s
+// into the caller's workspace (the last segment's is not needed); the second
+// launch (walk mode) starts segment s from S + sum_{s' < s} dS_s' and walks
+// its blocks as below; the last segment writes the final state.  Only the
+// associativity of the sum is used, so the result is the sequential one up to
+// rounding order.  Without outputs, only the last segment walks.
+//
+// Within a segment, one workgroup per (request b, query head h) walks the
+// blocks in order, with the next block's Q, K and V in flight while the
+// current one is computed.
 // Wave w of NW = D/32 keeps state columns 32w .. 32w+31 of all f rows in fp32
 // MFMA accumulators for the whole prompt, so the state is read from HBM once
 // and written once.  The accumulator tile doubles as the A operand of the
@@ -45,7 +56,7 @@ struct PrefillCfg {
 
 template <typename T, int D, int F>
 __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_prefill_kernel(
-    PrefillArgs a) {
+    PrefillArgs a, int nseg, int seg_blocks, int delta) {
   typedef PrefillCfg<T, D, F> C;
   typedef typename C::M M;
   typedef typename C::op_t op_t;
@@ -56,16 +67,24 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_prefill_kernel(
   const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
   const int li = lane & 31, hh = lane >> 5;
   const int Hq = a.s.Hq, Hkv = a.s.Hkv, L = a.s.L, T_ = a.T;
-  const int u = xcd_unit(blockIdx.x, a.s.B * Hq);
+  // Unit u = (b, h) varies fastest, so the heads of one KV group and segment
+  // are neighbours (on one XCD) and share K and V in L2.
+  const int units = a.s.B * Hq, nseg_here = delta ? nseg - 1 : nseg;
+  const int vix = xcd_unit(blockIdx.x, units * nseg_here);
+  const int u = vix % units, seg = vix / units;
   const int b = u / Hq, h = u % Hq, g = h / (Hq / Hkv);
   const int slot = a.slots ? a.slots[b] : b;
-  const bool want_out = a.out != nullptr;
+  const bool want_out = !delta && a.out != nullptr;
+  const bool last = seg == nseg - 1;
   const size_t qstride = (size_t)Hq * D, kstride = (size_t)Hkv * D;
   const int col = w * kTile + li;
+  const int nblk = T_ / L;
+  const int blk0 = seg * seg_blocks, blk1 = min(nblk, blk0 + seg_blocks);
+  if (!delta && !want_out && !last) return;  // state only: the last segment walks
   if (slot < 0 || slot >= a.s.n_slots) {  // uniform per workgroup
     if (want_out) {
       const size_t ob = ((size_t)b * T_ * Hq + h) * D;
-      for (int t = 0; t < T_; ++t)
+      for (int t = blk0 * L; t < blk1 * L; ++t)
         for (int c = tid; c < D; c += blockDim.x)
           store_out1<T>(a.out, ob + (size_t)t * qstride + c, __builtin_nanf(""),
                         a.s.out_f32);
@@ -75,18 +94,38 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_prefill_kernel(
   const size_t sbase = (size_t)slot * Hq + h;
   float* __restrict__ Sh = a.S + sbase * f * D;
   float* __restrict__ zh = a.z + sbase * f;
+  // Workspace: dS [units][nseg-1][D][f] (transposed, as S), then dz
+  // [units][nseg-1][f].
+  float* __restrict__ wsS = a.ws + (size_t)u * (nseg - 1) * D * f;
+  float* __restrict__ wsz = a.ws + (size_t)units * (nseg - 1) * D * f + (size_t)u * (nseg - 1) * f;
 
+  // Starting state: zero for a delta, else S plus the earlier segments'
+  // increments, all in the accumulator layout.
   f32x16 sacc[C::NRT];
+  auto add_state = [&](const float* src, bool first) {
 #pragma unroll
-  for (int rt = 0; rt < C::NRT; ++rt)
+    for (int rt = 0; rt < C::NRT; ++rt)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {  // rows rt*32 + j*8 + hh*4 .. +3: 16 bytes
-      const f32x4 x = *reinterpret_cast<const f32x4*>(
-          Sh + (size_t)col * f + rt * kTile + row_of(4 * j, hh));
+      for (int j = 0; j < 4; ++j) {  // rows rt*32 + j*8 + hh*4 .. +3: 16 bytes
+        const f32x4 x = *reinterpret_cast<const f32x4*>(
+            src + (size_t)col * f + rt * kTile + row_of(4 * j, hh));
 #pragma unroll
-      for (int r = 0; r < 4; ++r) sacc[rt][4 * j + r] = x[r];
+        for (int r = 0; r < 4; ++r) sacc[rt][4 * j + r] = first ? x[r] : sacc[rt][4 * j + r] + x[r];
+      }
+  };
+  if (delta) {
+#pragma unroll
+    for (int rt = 0; rt < C::NRT; ++rt) sacc[rt] = f32x16{};
+    for (int r = tid; r < f; r += blockDim.x) sh.z[r] = 0.0f;
+  } else {
+    add_state(Sh, true);
+    for (int s = 0; s < seg; ++s) add_state(wsS + (size_t)s * D * f, false);
+    for (int r = tid; r < f; r += blockDim.x) {
+      float zr = zh[r];
+      for (int s = 0; s < seg; ++s) zr += wsz[(size_t)s * f + r];
+      sh.z[r] = zr;
     }
-  for (int r = tid; r < f; r += blockDim.x) sh.z[r] = zh[r];
+  }
 
   const T* __restrict__ Wt_h = (const T*)a.W + (size_t)h * F * D;
   op_t wop[FM::PPW][C::KD];  // W_h^T operands, kept for the whole prompt
@@ -94,37 +133,47 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_prefill_kernel(
   const float scale = 1.0f / sqrtf((float)D);
   const float lw = want_out ? log_sigmoid(a.alpha[h]) : 0.0f;
   const bool row_ok = li < L;
-  const int nblk = T_ / L;
+  const int lrow = min(li, L - 1);
 
-  for (int blk = 0; blk < nblk; ++blk) {
+  // Block operands.  Unconditional, in-bounds loads: padding rows read row
+  // L-1 and are zeroed by a select later; the prefetch past the segment's
+  // last block re-reads that block.
+  auto load_block = [&](int blk, op_t (&ko)[C::KD], op_t (&qo)[C::KD],
+                        op_t (&vo)[C::KL]) {
     const size_t t0 = (size_t)blk * L;
     const T* kb = (const T*)a.k + (((size_t)b * T_ + t0) * Hkv + g) * D;
     const T* vb = (const T*)a.v + (((size_t)b * T_ + t0) * Hkv + g) * D;
-    // Unconditional, in-bounds loads: padding rows read row L-1 and are
-    // zeroed by a select.
-    op_t kop[C::KD], qop[C::KD], vop[C::KL];
-    const int lrow = min(li, L - 1);
-    {
-      const T* krow = kb + (size_t)lrow * kstride + hh * E;
+    const T* krow = kb + (size_t)lrow * kstride + hh * E;
 #pragma unroll
-      for (int ks = 0; ks < C::KD; ++ks) kop[ks] = load_op<T>(krow + ks * KW);
-    }
+    for (int ks = 0; ks < C::KD; ++ks) ko[ks] = load_op<T>(krow + ks * KW);
 #pragma unroll
     for (int ks = 0; ks < C::KL; ++ks)
-      vop[ks] = load_rows_op<T>(vb + col, kstride, ks, hh, L, false);
+      vo[ks] = load_rows_op<T>(vb + col, kstride, ks, hh, L, false);
     if (want_out) {
       const T* qrow = (const T*)a.q + (((size_t)b * T_ + t0) * Hq + h) * D +
                       (size_t)lrow * qstride + hh * E;
 #pragma unroll
-      for (int ks = 0; ks < C::KD; ++ks) qop[ks] = load_op<T>(qrow + ks * KW);
+      for (int ks = 0; ks < C::KD; ++ks) qo[ks] = load_op<T>(qrow + ks * KW);
     }
+  };
+  op_t kop[C::KD], qop[C::KD], vop[C::KL];
+#pragma unroll
+  for (int ks = 0; ks < C::KD; ++ks) qop[ks] = M::zero();
+  if (blk0 < blk1) load_block(blk0, kop, qop, vop);
+
+  for (int blk = blk0; blk < blk1; ++blk) {
+    const size_t t0 = (size_t)blk * L;
+    op_t kn[C::KD], qn[C::KD], vn[C::KL];
+#pragma unroll
+    for (int ks = 0; ks < C::KD; ++ks) qn[ks] = M::zero();
+    load_block(min(blk + 1, blk1 - 1), kn, qn, vn);
 #pragma unroll
     for (int ks = 0; ks < C::KD; ++ks) {
       kop[ks] = keep_if<T>(row_ok, kop[ks]);
       qop[ks] = keep_if<T>(row_ok, qop[ks]);
     }
 
-    __syncthreads();  // previous block's LDS readers are done
+    lds_barrier();  // previous block's LDS readers are done
     float vk[FM::PPW][16], vq[FM::PPW][16];
     FM::logits(wop, kop, w, li, hh, vk, sh.fk);
     if (want_out) FM::logits(wop, qop, w, li, hh, vq, sh.fq);
@@ -156,10 +205,10 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_prefill_kernel(
         acc_sm = mma_split_b<T>(vop[ks], &p[ks * E], acc_sm);
     }
 
-    __syncthreads();
+    lds_barrier();
     FM::exps(w, li, hh, vk, sh.fk);
     if (want_out) FM::exps(w, li, hh, vq, sh.fq);
-    __syncthreads();
+    lds_barrier();
     FM::normalise(w, li, hh, vk, sh.fk, [&](int f0, const float* x4) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -175,7 +224,7 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_prefill_kernel(
 #pragma unroll
         for (int e = 0; e < 4; ++e) sh.phiQ[li][f0 + e] = from_f32<T>(x4[e]);
       });
-    __syncthreads();
+    lds_barrier();
 
     if (want_out) {
       // Readout against the state of the blocks before this one.
@@ -231,7 +280,7 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_prefill_kernel(
           sacc[rt] = M::mma(
               lds_op_perm<T>(&sh.phiKT[part][rt * kTile + li][0], ks, hh, 0),
               vop[ks], sacc[rt]);
-    __syncthreads();  // every wave has read z for this block
+    lds_barrier();  // every wave has read z for this block
     for (int r = tid; r < f; r += blockDim.x) {
       float s = 0.0f;
       for (int t = 0; t < L; ++t)
@@ -239,23 +288,66 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_prefill_kernel(
         for (int part = 0; part < C::NPART; ++part) s += to_f32(sh.phiKT[part][r][t]);
       sh.z[r] += s;
     }
+#pragma unroll
+    for (int ks = 0; ks < C::KD; ++ks) {
+      kop[ks] = kn[ks];
+      qop[ks] = qn[ks];
+    }
+#pragma unroll
+    for (int ks = 0; ks < C::KL; ++ks) vop[ks] = vn[ks];
   }
 
+  // A delta goes to the workspace; the last segment's walk writes the state.
+  if (!delta && !last) return;
+  float* dstS = delta ? wsS + (size_t)seg * D * f : Sh;
+  float* dstz = delta ? wsz + (size_t)seg * f : zh;
 #pragma unroll
   for (int rt = 0; rt < C::NRT; ++rt)
 #pragma unroll
     for (int j = 0; j < 4; ++j)
-      *reinterpret_cast<f32x4*>(Sh + (size_t)col * f + rt * kTile + row_of(4 * j, hh)) =
+      *reinterpret_cast<f32x4*>(dstS + (size_t)col * f + rt * kTile + row_of(4 * j, hh)) =
           f32x4{sacc[rt][4 * j], sacc[rt][4 * j + 1], sacc[rt][4 * j + 2], sacc[rt][4 * j + 3]};
-  __syncthreads();
-  for (int r = tid; r < f; r += blockDim.x) zh[r] = sh.z[r];
+  lds_barrier();
+  for (int r = tid; r < f; r += blockDim.x) dstz[r] = sh.z[r];
 }
 
 template <typename T, int D, int F>
 static hipError_t prefill_go(const PrefillArgs& a, hipStream_t st) {
-  hipLaunchKernelGGL((hyb_prefill_kernel<T, D, F>), dim3(a.s.B * a.s.Hq),
-                     dim3(kWave * (D / kTile)), 0, st, a);
+  const int units = a.s.B * a.s.Hq, nblk = a.T / a.s.L;
+  const int nseg = prefill_segments(a.s, a.T);
+  const int seg_blocks = (nblk + nseg - 1) / nseg;
+  const dim3 block(kWave * (D / kTile));
+  if (nseg > 1) {
+    hipLaunchKernelGGL((hyb_prefill_kernel<T, D, F>), dim3(units * (nseg - 1)), block, 0, st,
+                       a, nseg, seg_blocks, 1);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL((hyb_prefill_kernel<T, D, F>), dim3(units * nseg), block, 0, st, a, nseg,
+                     seg_blocks, 0);
   return hipGetLastError();
+}
+
+// Segments: enough (request, head, segment) workgroups to cover the chip
+// about twice, at most 8 segments (the walk of segment s reads the s earlier
+// increments) and at least 4 blocks per segment.
+int prefill_segments(const Shape& s, int T) {
+  const int units = s.B * s.Hq, nblk = T / s.L;
+  int nseg = (512 + units - 1) / units;
+  if (nseg > 8) nseg = 8;
+  if (nseg > nblk / 4) nseg = nblk / 4;
+  if (nseg < 1) nseg = 1;
+  // Every segment must own at least one block at the rounded-up length.
+  for (; nseg > 1; --nseg)
+    if ((nseg - 1) * ((nblk + nseg - 1) / nseg) < nblk) break;
+  return nseg;
+}
+
+size_t prefill_ws_bytes(const Shape& s, int T) {
+  const int nseg = prefill_segments(s, T);
+  if (nseg <= 1) return 0;
+  const size_t f = 2 * (size_t)s.F;
+  return (size_t)s.B * s.Hq * (nseg - 1) * ((size_t)s.D * f + f) * 4;
 }
 
 template <typename T, int D>

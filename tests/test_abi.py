@@ -96,6 +96,17 @@ def test_commit_prefill_softmax_validation():
                                     FAKE, None, None, None, 0, None) == 2
     assert lib.hybrid_state_prefill(ctypes.byref(d), 0, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
                                     FAKE, None, None, None, 0, None) == 2
+    # prefill over many blocks for few (request, head) units needs a workspace
+    dp = _dims(batch=1, n_q_heads=4, n_kv_heads=1, n_slots=1)
+    need_p = lib.hybrid_workspace_bytes(ctypes.byref(dp), hb.OP_PREFILL, 32 * 64)
+    assert need_p > 0
+    assert lib.hybrid_state_prefill(ctypes.byref(dp), 32 * 64, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                    ctypes.c_void_p(0x100000), ctypes.c_void_p(0x200000),
+                                    None, None, None, 0, None) == 6
+    assert lib.hybrid_state_prefill(ctypes.byref(dp), 32 * 64, FAKE, FAKE, FAKE, FAKE, FAKE,
+                                    ctypes.c_void_p(0x100000), ctypes.c_void_p(0x200000),
+                                    None, None, ctypes.c_void_p(0x300000), need_p - 1,
+                                    None) == 6
     # softmax prefix: missing workspace
     need = lib.hybrid_workspace_bytes(ctypes.byref(d), hb.OP_SOFTMAX_PREFIX, 4096)
     assert need > 0

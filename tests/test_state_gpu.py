@@ -144,3 +144,50 @@ def test_prefill_equals_commits_and_resume():
         hb.hybrid_state_commit(kd[:, sl].contiguous(), vd[:, sl].contiguous(), Wd, S4, z4)
     torch.cuda.synchronize()
     assert_close(state_host(S4), Sr, "bf16", "reverse-order commits state")
+
+
+SEGMENT_CASES = [
+    # (B, Hq, Hkv, d, L, F, dtype, nblk): few (request, head) units, so the
+    # prompt is cut into several sequence segments; 37 blocks leave the last
+    # segment short.
+    (1, 4, 1, 64, 8, 32, "f32", 40),
+    (1, 4, 2, 64, 8, 32, "bf16", 37),
+    (2, 2, 1, 128, 32, 64, "bf16", 33),
+]
+
+
+@pytest.mark.parametrize("shape", SEGMENT_CASES, ids=lambda s: "x".join(map(str, s)))
+def test_prefill_segments(shape):
+    """Segmented prefill (state increments through the workspace) equals the
+    oracle's block-by-block prefill, outputs and state, and the state-only
+    call agrees with it."""
+    B, Hq, Hkv, d, L, F, dt, nblk = shape
+    dims = synth.Dims(B=B, Hq=Hq, Hkv=Hkv, d=d, L=L, F=F, dtype=dt)
+    T = nblk * L
+    ws_need = hb.workspace_bytes(hb.make_dims(B, Hq, Hkv, d, L, 2 * F, hb.HYB_BF16 if dt == "bf16"
+                                              else hb.HYB_F32, B), hb.OP_PREFILL, T)
+    assert ws_need > 0, "case must exercise more than one segment"
+    announce(f"prefill segments {shape}")
+    seq = dims.with_(L=T)
+    q, k, v = synth.block_qkv(seq, 91, 1.0)
+    Wt, alpha = synth.feature_weights(dims, 92, 93, 1.0 / np.sqrt(d))
+    c0 = make_case(dims, 16, seed=94, peaky=True)
+    o_r, Sr, zr = oracle.prefill(q, k, v, Wt, alpha, c0["S"], c0["z"], L)
+    states = []
+
+    def call(out_f32):
+        S, z = state_dev(c0["S"]), f32(c0["z"])
+        states.append((S, z))
+        return hb.hybrid_state_prefill(act(q, dt), act(k, dt), act(v, dt), act(Wt, dt),
+                                       f32(alpha), S, z, L, out_f32=out_f32)
+
+    check_outputs(call, o_r, dt, f"prefill segments out {shape}")
+    S, z = states[-1]
+    assert_state_delta(state_host(S), host(z), c0["S"], c0["z"], Sr, zr, dt,
+                       f"prefill segments {shape}")
+    S2, z2 = state_dev(c0["S"]), f32(c0["z"])
+    hb.hybrid_state_prefill(None, act(k, dt), act(v, dt), act(Wt, dt), None, S2, z2, L,
+                            want_out=False)
+    torch.cuda.synchronize()
+    assert_state_delta(state_host(S2), host(z2), c0["S"], c0["z"], Sr, zr, dt,
+                       f"prefill segments state-only {shape}")
