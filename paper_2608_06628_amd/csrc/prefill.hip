@@ -50,6 +50,7 @@ struct PrefillCfg {
     T phiQ[kTile][PHI_LD];         // phi(q_i)[r] at [i][r]
     T phiKT[NPART][f][PT_LD];      // phi(k_t)[r] at [part][r][t]
     float z[f];
+    float lden[NW][kTile];         // per-wave partial phi(q_i) . z
     typename FM::Smem fq, fk;
   };
 };
@@ -219,11 +220,20 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_prefill_kernel(
           sh.phiKT[1][f0 + e][li] = from_f32<T>(x - to_f32(hi));
       }
     });
-    if (want_out)
+    if (want_out) {
+      // phi(q) to LDS and this wave's part of lin_den = phi(q) . z (the
+      // features of the pairs it owns), summed over the waves below.
+      float lz = 0.0f;
       FM::normalise(w, li, hh, vq, sh.fq, [&](int f0, const float* x4) {
 #pragma unroll
-        for (int e = 0; e < 4; ++e) sh.phiQ[li][f0 + e] = from_f32<T>(x4[e]);
+        for (int e = 0; e < 4; ++e) {
+          sh.phiQ[li][f0 + e] = from_f32<T>(x4[e]);
+          lz += x4[e] * sh.z[f0 + e];
+        }
       });
+      lz += xor32(lz);
+      if (hh == 0) sh.lden[w][li] = lz;
+    }
     lds_barrier();
 
     if (want_out) {
@@ -231,23 +241,22 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_prefill_kernel(
       f32x16 acc_lin = {};
       float lden = 0.0f;
 #pragma unroll
+      for (int ww = 0; ww < C::NW; ++ww) lden += sh.lden[ww][li];
+#pragma unroll
       for (int ks = 0; ks < C::KF; ++ks) {
         const op_t pb = lds_op_perm<T>(&sh.phiQ[li][0], ks, hh, 0);
         op_t sa;
         if constexpr (E == 1) {
           sa = sacc[ks / 16][ks % 16];
-          lden += pb * sh.z[row_of(ks, hh)];
         } else {
 #pragma unroll
           for (int e = 0; e < E; ++e) {
             const int j = ks * E + e;  // flattened accumulator register
             sa[e] = (T)sacc[j / 16][j % 16];
-            lden += to_f32(pb[e]) * sh.z[row_of(j, hh)];
           }
         }
         acc_lin = M::mma(sa, pb, acc_lin);
       }
-      lden += xor32(lden);
       if (row_ok) {
         float ca = 1.0f, cz = 0.0f, rz = 0.0f;
         if (lden > 0.0f) {
@@ -281,11 +290,19 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_prefill_kernel(
               lds_op_perm<T>(&sh.phiKT[part][rt * kTile + li][0], ks, hh, 0),
               vop[ks], sacc[rt]);
     lds_barrier();  // every wave has read z for this block
+    // z += sum_t phi(k_t): row r of phiKT holds the 32 tokens contiguously
+    // (zero past the block length), read 16 bytes at a time.
     for (int r = tid; r < f; r += blockDim.x) {
       float s = 0.0f;
-      for (int t = 0; t < L; ++t)
 #pragma unroll
-        for (int part = 0; part < C::NPART; ++part) s += to_f32(sh.phiKT[part][r][t]);
+      for (int part = 0; part < C::NPART; ++part)
+#pragma unroll
+        for (int t0 = 0; t0 < kTile; t0 += 16 / (int)sizeof(T)) {
+          const uint4 x = *reinterpret_cast<const uint4*>(&sh.phiKT[part][r][t0]);
+          const T* xt = reinterpret_cast<const T*>(&x);
+#pragma unroll
+          for (int e = 0; e < 16 / (int)sizeof(T); ++e) s += to_f32(xt[e]);
+        }
       sh.z[r] += s;
     }
 #pragma unroll
