@@ -98,9 +98,9 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_commit_kernel(
   // 2. phi(K), transposed into LDS; padding tokens contribute nothing.
   float val[FM::PPW][16];
   FM::logits(wop, kop, w, li, hh, val, sh.fm);
-  __syncthreads();
+  lds_barrier();
   FM::exps(w, li, hh, val, sh.fm);
-  __syncthreads();
+  lds_barrier();
   FM::normalise(w, li, hh, val, sh.fm, [&](int f0, const float* x4) {
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -110,7 +110,7 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_commit_kernel(
       if constexpr (C::NPART == 2) sh.phiT[1][f0 + e][li] = from_f32<T>(x - to_f32(hi));
     }
   });
-  __syncthreads();
+  lds_barrier();
 
   // 3. S += phi(K)^T V, one accumulate per 32-row tile, stored in place.
 #pragma unroll

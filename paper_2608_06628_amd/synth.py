@@ -53,6 +53,27 @@ def gaussian(seed: int, shape, std: float = 1.0) -> np.ndarray:
     return (rng.standard_normal(shape) * std).astype(np.float32)
 
 
+def device_gaussian(shape, seed: int, std: float = 1.0, dtype: str = "bf16",
+                    device: str = "cuda", chunk_rows: int = 1 << 14):
+    """Seeded N(0, std^2) tensor drawn on the device with torch's generator, in
+    the activation dtype (bf16 values are rounded once, on creation).  Used for
+    inputs too large to draw on the host; a test hands the same tensor to the
+    library and copies the rows it checks to the host for the oracle.  Drawn
+    in slices along the first axis so that no full-size fp32 copy exists."""
+    import torch
+    gen = torch.Generator(device=device)
+    gen.manual_seed(seed)
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    out = torch.empty(shape, dtype=tdt, device=device)
+    flat = out.view(shape[0], -1)
+    step = max(1, chunk_rows // max(1, flat.shape[1] // 4096 + 1))
+    for r0 in range(0, shape[0], step):
+        r1 = min(shape[0], r0 + step)
+        x = torch.randn((r1 - r0, flat.shape[1]), generator=gen, device=device) * std
+        flat[r0:r1] = x.to(tdt)
+    return out
+
+
 def block_qkv(dims: Dims, seed: int, scale: float = 1.0):
     """Active-block q [B][L][Hq][d], k, v [B][L][Hkv][d] ~ N(0, scale^2)."""
     rng = np.random.default_rng(seed)
