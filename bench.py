@@ -145,7 +145,7 @@ def cpu_baseline(dims, n_req, plens, budget_s=10.0):
     Wt, alpha = synth.feature_weights(sub, 6, 7)
     S = rng.standard_normal((n_req, dims.Hq, dims.f, dims.d)) * 0.05
     z = np.abs(rng.standard_normal((n_req, dims.Hq, dims.f))) * float(np.mean(plens)) / dims.F
-    threads = int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+    threads = _omp_threads()
     cycles = 0
     t0 = time.perf_counter()
     while True:
@@ -279,7 +279,56 @@ def run(args):
     if not args.no_cpu_baseline:
         log("timing the fp64 oracle on the host cores")
         result["cpu_baseline"] = cpu_baseline(dims, args.cpu_requests, plens)
+        if not args.no_extras:
+            result["prefill"]["cpu_oracle"] = cpu_prefill()
+            result["softmax_prefix"]["cpu_oracle"] = cpu_softmax_prefix()
+    # The paper's own headline number, for context only: a different metric
+    # (end-to-end decoding throughput of the whole model) on other hardware.
+    result["paper_context"] = {
+        "end_to_end_decoding_speedup_up_to": 1.7,
+        "setting": "LLaDA-Hybrid (6 of 20 attention layers hybrid) vs its softmax teacher, "
+                   "SGLang continuous batching on one H200 (Table 2)",
+        "comparable": False}
     print(json.dumps(result), flush=True)
+
+
+def _omp_threads():
+    return int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+
+
+def cpu_prefill():
+    """The fp64 oracle's block-by-block prefill of one 8192-token prompt (all
+    16 heads), timed on the host cores."""
+    import oracle
+    dims = synth.PREFILL8.with_(B=1)
+    T = synth.PREFILL8_T
+    q, k, v = synth.block_qkv(dims.with_(L=T), 11, 1.0 / math.sqrt(dims.d))
+    Wt, alpha = synth.feature_weights(dims, 12, 13)
+    S, z = oracle.empty_state(1, dims.Hq, dims.f, dims.d)
+    t0 = time.perf_counter()
+    oracle.prefill(q, k, v, Wt, alpha, S, z, dims.L)
+    el = time.perf_counter() - t0
+    return {"prompt_tokens_per_s": T / el, "cores": _omp_threads(), "kind": "oracle",
+            "sample": f"1 prompt x {T} tokens, 16 heads, in {el:.1f} s, fp64"}
+
+
+def cpu_softmax_prefix():
+    """The fp64 oracle's exact softmax step over a 32768-token prefix for one
+    request (all 16 heads), timed on the host cores; per-step time at B=128
+    extrapolated linearly."""
+    import oracle
+    dims = synth.MIX128.with_(B=1)
+    P = synth.MIX128_PREFIX
+    sc = 1.0 / math.sqrt(dims.d)
+    q, k, v = synth.block_qkv(dims, 21, sc)
+    kc, vc = synth.prefix_kv(1, P, dims.Hkv, dims.d, 22, sc, "bf16")
+    t0 = time.perf_counter()
+    oracle.softmax_prefix(q, k, v, kc, vc, np.array([P], np.int32))
+    el = time.perf_counter() - t0
+    return {"ms_per_request": el * 1e3, "ms_per_step_b128": el * 1e3 * synth.MIX128.B,
+            "cores": _omp_threads(), "kind": "oracle",
+            "sample": f"1 request x 16 heads over a {P}-token prefix in {el:.2f} s, fp64; "
+                      f"B=128 extrapolated x128"}
 
 
 def bench_prefill(gen, dev):
