@@ -11,14 +11,20 @@
 //                  operands) and a P V (fp32 accumulators) to the state wave
 //                  through LDS, then exits.
 //   state wave  -- streams the head's state.  Its first NBUF column blocks
-//                  are requested at kernel entry, before anything else, so
-//                  the state -- most of the bytes -- is in flight while the
-//                  block wave computes; after the single barrier it folds
-//                  S^T (b phi)^T onto a P V block by block, requesting the
-//                  next column block as each buffer frees, and stores.
+//                  are requested at kernel entry, before anything else.  On
+//                  the bf16 path each column block is converted to MFMA
+//                  operands as it lands (the fold uses S rounded to bf16
+//                  anyway), which frees its buffer for the next request, so
+//                  the whole state is requested while the block wave
+//                  computes.  After the barrier it folds S^T (b phi)^T onto
+//                  a P V column block by column block, the later blocks as
+//                  they arrive, and stages the outputs in LDS.
 //
-// The barrier orders LDS only (a workgroup fence restricted to the local
-// address space), so the state loads issued before it stay in flight.
+// Then all waves write the outputs: a token's NW heads are contiguous in the
+// output, so each token is one or two full-wave 16-byte-per-lane stores.
+//
+// The barriers order LDS only (a workgroup fence restricted to the local
+// address space), so the state loads issued before them stay in flight.
 //
 // Every product is computed transposed (columns = queries), so each lane owns
 // one query and the per-query softmax, normaliser and merge are per-lane
@@ -61,15 +67,22 @@ struct StepCfg {
   // Column blocks a state wave keeps in flight: 128 registers' worth.
   static constexpr int NBUF0 = 128 / (RUNS * 4);
   static constexpr int NBUF = NBUF0 < 1 ? 1 : (NBUF0 > CB ? CB : NBUF0);
+  // Column blocks converted to operands before the barrier (bf16 only):
+  // enough to have every column block requested, within 64 registers.
+  static constexpr int KPK0 = CB - NBUF, KPK1 = 64 / (KF * 4);
+  static constexpr int KPACK = E == 1 ? 0 : (KPK0 < KPK1 ? KPK0 : KPK1);
   static constexpr int EPC = 16 / (int)sizeof(T);  // elements per 16 bytes
   static constexpr int VT_LD = 36;        // V^T row length (keys, padded)
   static constexpr int VITEMS = 16 * (D / EPC);    // (key pair, column group)
   static constexpr int VPT = (VITEMS + kWave - 1) / kWave;  // items per lane
-  // Per head: V^T while the block wave runs, then its a P V accumulators.
+  // Per head: V^T while the block wave runs, then its a P V accumulators;
+  // each pair of column blocks of a P V, once read back, holds the pair's
+  // outputs ([32 queries][32 columns], output type).
   union alignas(16) HeadLds {
     T vt[D][VT_LD];
     f32x4 apv[CB][QB][kWave];
   };
+  static_assert(2 * QB * kWave * 16 >= 32 * 32 * 4, "output staging");
   static_assert(CB % 2 == 0, "output columns are stored in pairs of blocks");
   struct alignas(16) Smem {
     HeadLds hd[NW];
@@ -171,9 +184,31 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
           St + (size_t)C::column(cb, c16) * f + C::feature(rn * 4, quad));
   };
 
+  // Column blocks 0 .. KPACK-1 as bf16 operands (S^T A operands).
+  op_t sop[C::KPACK > 0 ? C::KPACK : 1][C::KF];
+  auto convert = [&](int cb, int ks) {
+    float sv[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) sv[e] = buf[cb % NBUF][(ks * E + e) / 4][(ks * E + e) % 4];
+    return cvt_op<T>(sv);
+  };
+
   if (state_wave) {
 #pragma unroll
     for (int cb = 0; cb < NBUF; ++cb) issue(cb);
+#pragma unroll
+    for (int cb = 0; cb < C::KPACK; ++cb) {
+#pragma unroll
+      for (int ks = 0; ks < C::KF; ++ks) sop[cb][ks] = convert(cb, ks);
+      // Keep the refill below this block's conversion: otherwise the
+      // compiler hoists every load to the top and runs out of registers.
+#pragma unroll
+      for (int ks = 0; ks < C::KF; ++ks) {
+        const uint4 t = *reinterpret_cast<const uint4*>(&sop[cb][ks]);
+        asm volatile("" ::"v"(t.x), "v"(t.y), "v"(t.z), "v"(t.w) : "memory");
+      }
+      if (cb + NBUF < CB) issue(cb + NBUF);
+    }
   } else {
     // ---------------- block wave ----------------
     // 1. Loads, all unconditional and in bounds (rows past the block length
@@ -346,47 +381,74 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
       for (int qb = 0; qb < QB; ++qb) sh.hd[w].apv[cbk][qb][lane] = acc[cbk][qb];
   }
   lds_barrier();
-  if (!state_wave) return;
 
-  // ---------------- state wave ----------------
-  // 7. out^T = a P V + S^T (b phi)^T, column block by column block; each
-  //    consumed buffer is refilled with column block cb + NBUF.
-  op_t phib[QB][C::KF];
+  const bool of32 = sizeof(T) == 4 || a.s.out_f32;
+  if (state_wave) {
+    // 7. out^T = a P V + S^T (b phi)^T, a pair of column blocks at a time;
+    //    column blocks past KPACK are converted as they land, and each such
+    //    buffer is refilled with column block cb + NBUF if not yet requested.
+    op_t phib[QB][C::KF];
 #pragma unroll
-  for (int qb = 0; qb < QB; ++qb)
+    for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
-    for (int ks = 0; ks < C::KF; ++ks) phib[qb][ks] = sh.phib[w][qb][ks][lane];
-  f32x4 acc[CB][QB];
-#pragma unroll
-  for (int cbk = 0; cbk < CB; ++cbk) {
-#pragma unroll
-    for (int qb = 0; qb < QB; ++qb) acc[cbk][qb] = sh.hd[w].apv[cbk][qb][lane];
-#pragma unroll
-    for (int ks = 0; ks < C::KF; ++ks) {
-      float sv[E];
-#pragma unroll
-      for (int e = 0; e < E; ++e)
-        sv[e] = buf[cbk % NBUF][(ks * E + e) / 4][(ks * E + e) % 4];
-      const op_t sa = cvt_op<T>(sv);
-#pragma unroll
-      for (int qb = 0; qb < QB; ++qb)
-        acc[cbk][qb] = M::mma(sa, phib[qb][ks], acc[cbk][qb]);
-    }
-    if (cbk + NBUF < CB) issue(cbk + NBUF);
-  }
-
-  // 8. Store: the lane holds query qb*16 + c16 and, for each block pair p,
-  //    the 8 consecutive columns 32p + 8 quad .. +7 (see column()).  The
-  //    output is not read again by this kernel: non-temporal stores.
-#pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    if (qb * 16 + c16 >= L) continue;
-    const size_t obase = (((size_t)b * L + qb * 16 + c16) * Hq + h) * D;
+      for (int ks = 0; ks < C::KF; ++ks) phib[qb][ks] = sh.phib[w][qb][ks][lane];
 #pragma unroll
     for (int pr = 0; pr < CB / 2; ++pr) {
-      const f32x4 lo = acc[2 * pr][qb], hi = acc[2 * pr + 1][qb];
-      const float o[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-      store_out8_nt<T>(a.out, obase + pr * 32 + quad * 8, o, a.s.out_f32);
+      f32x4 acc[2][QB];
+#pragma unroll
+      for (int h2 = 0; h2 < 2; ++h2) {
+        const int cbk = 2 * pr + h2;
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb) acc[h2][qb] = sh.hd[w].apv[cbk][qb][lane];
+#pragma unroll
+        for (int ks = 0; ks < C::KF; ++ks) {
+          const op_t sa = cbk < C::KPACK ? sop[cbk < C::KPACK ? cbk : 0][ks] : convert(cbk, ks);
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb)
+            acc[h2][qb] = M::mma(sa, phib[qb][ks], acc[h2][qb]);
+        }
+        if (cbk >= C::KPACK && cbk + NBUF < CB) issue(cbk + NBUF);
+      }
+      // The lane holds query qb*16 + c16 and the 8 consecutive columns
+      // 32 pr + 8 quad .. +7 (see column()); they go to the pair's staging
+      // area, over its a P V just read.
+      char* stg = reinterpret_cast<char*>(&sh.hd[w].apv[2 * pr][0][0]);
+#pragma unroll
+      for (int qb = 0; qb < QB; ++qb) {
+        const f32x4 lo = acc[0][qb], hi = acc[1][qb];
+        const int row = qb * 16 + c16;
+        if (of32) {
+          f32x4* d = reinterpret_cast<f32x4*>(stg + (row * 32 + quad * 8) * 4);
+          d[0] = lo;
+          d[1] = hi;
+        } else {
+          *reinterpret_cast<bf16x8*>(stg + (row * 32 + quad * 8) * 2) =
+              bf16x8{(bf16)lo[0], (bf16)lo[1], (bf16)lo[2], (bf16)lo[3],
+                     (bf16)hi[0], (bf16)hi[1], (bf16)hi[2], (bf16)hi[3]};
+        }
+      }
+    }
+  }
+  lds_barrier();
+
+  // 8. Store: each wave writes whole tokens (the NW heads of a token are
+  //    contiguous, NW * D outputs), 16 bytes per lane; the output is not read
+  //    again by this kernel: non-temporal stores.
+  {
+    typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+    const int osz = of32 ? 4 : 2;
+    const int cph = D * osz / 16;  // 16-byte chunks per head
+    for (int t = wv; t < L; t += 2 * NW) {
+      char* orow = reinterpret_cast<char*>(a.out) +
+                   (((size_t)b * L + t) * Hq + hg * NW) * D * osz;
+      for (int c = lane; c < NW * cph; c += kWave) {
+        const int hh = c / cph, col0 = (c % cph) * (16 / osz);
+        const char* src = reinterpret_cast<const char*>(&sh.hd[hh].apv[2 * (col0 / 32)][0][0]) +
+                          (t * 32 + col0 % 32) * osz;
+        __builtin_nontemporal_store(*reinterpret_cast<const u32x4*>(src),
+                                    reinterpret_cast<u32x4*>(orow + (size_t)hh * D * osz +
+                                                             (size_t)col0 * osz));
+      }
     }
   }
 }
