@@ -84,9 +84,24 @@ struct StepCfg {
   };
   static_assert(2 * QB * kWave * 16 >= 32 * 32 * 4, "output staging");
   static_assert(CB % 2 == 0, "output columns are stored in pairs of blocks");
+  // bf16: the block wave's Q, K and (when it fits the head area) W_h rows
+  // reach LDS by direct global->LDS copies whose every instruction reads
+  // whole rows, 16 bytes per lane; the MFMA operands are then read from LDS.
+  static constexpr int CPR = D / EPC;          // 16-byte chunks per row
+  static constexpr int RPI = kWave / CPR;      // rows per copy instruction
+  static constexpr int RP256 = 256 / (D * (int)sizeof(T)) > 0 ? 256 / (D * (int)sizeof(T)) : 1;
+  static constexpr bool DMA_QK = sizeof(T) == 2;
+  static constexpr bool DMA_W = DMA_QK && F * D * sizeof(T) <= sizeof(HeadLds);
+  // Chunk c of a staged row t sits at position c ^ swz(t), so the 16 rows an
+  // operand read takes at one chunk fall in distinct LDS banks.
+  __device__ static constexpr int swz(int t) { return (t / RP256) % CPR; }
+  union alignas(16) WaveLds {
+    op_t phib[QB][KF][kWave];  // b phi(Q) as the readout's B operand
+    T qk[DMA_QK ? 2 * 32 * D : 1];  // staged Q and K rows, until read
+  };
   struct alignas(16) Smem {
-    HeadLds hd[NW];
-    op_t phib[NW][QB][KF][kWave];  // b phi(Q) as the readout's B operand
+    HeadLds hd[NW];  // W_h rows (staged), then V^T, then a P V and outputs
+    WaveLds wl[NW];
   };
   // Feature held by phi register j (j < NPHI) of a lane in quarter `quad`:
   // j = (sign * FB + fb) * 4 + r -> sign*F + fb*16 + quad*4 + r.
@@ -228,29 +243,74 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
       vhi[j] = *reinterpret_cast<const uint4*>(
           vb0 + (size_t)min(2 * kp + 1, L - 1) * kstride + cg * C::EPC);
     }
-    op_t qop[QB][C::KD], kop[KB][C::KD];
+    const float alpha_h = a.alpha[h];
+    op_t qop[QB][C::KD], kop[KB][C::KD], wop[FB][C::KD];
+    T* const wst = reinterpret_cast<T*>(&sh.hd[w]);
+    T* const qst = sh.wl[w].qk;
+    T* const kst = sh.wl[w].qk + (C::DMA_QK ? 32 * D : 0);
+    // Rows 0 .. n-1 of a row-major operand (row t at base + min(t, tmax) *
+    // stride) into LDS at dst, chunk-swizzled; copy i takes rows i*RPI ..
+    auto stage = [&](const T* base, size_t stride, int n, int tmax, T* dst) {
 #pragma unroll
-    for (int r = 0; r < 2; ++r) {
-      const T* qrow = qb0 + (size_t)min(r * 16 + c16, L - 1) * qstride + quad * E;
-      const T* krow = kb0 + (size_t)min(r * 16 + c16, L - 1) * kstride + quad * E;
+      for (int i = 0; i < n / C::RPI; ++i) {
+        const int t = i * C::RPI + lane / C::CPR, pos = lane % C::CPR;
+        __builtin_amdgcn_global_load_lds(
+            (const __attribute__((address_space(1))) void*)(base + (size_t)min(t, tmax) * stride +
+                                                           (pos ^ C::swz(t)) * C::EPC),
+            (__attribute__((address_space(3))) void*)(dst + i * C::RPI * D), 16, 0, 0);
+      }
+    };
+    auto staged_op = [&](const T* src, int t, int c) {
+      return load_op<T>(src + t * D + (c ^ C::swz(t)) * C::EPC);
+    };
+    if constexpr (C::DMA_W) stage(Wt_h, D, F, F - 1, wst);
+    if constexpr (C::DMA_QK) {
+      stage(qb0, qstride, 32, L - 1, qst);
+      stage(kb0, kstride, 32, L - 1, kst);
+    } else {
 #pragma unroll
-      for (int ks = 0; ks < C::KD; ++ks) {
-        qop[r][ks] = load_op<T>(qrow + ks * KW);
-        kop[r][ks] = load_op<T>(krow + ks * KW);
+      for (int r = 0; r < 2; ++r) {
+        const T* qrow = qb0 + (size_t)min(r * 16 + c16, L - 1) * qstride + quad * E;
+        const T* krow = kb0 + (size_t)min(r * 16 + c16, L - 1) * kstride + quad * E;
+#pragma unroll
+        for (int ks = 0; ks < C::KD; ++ks) {
+          qop[r][ks] = load_op<T>(qrow + ks * KW);
+          kop[r][ks] = load_op<T>(krow + ks * KW);
+        }
       }
     }
-    op_t wop[FB][C::KD];
+    if constexpr (!C::DMA_W) {
 #pragma unroll
-    for (int fb = 0; fb < FB; ++fb) {
-      const T* wrow = Wt_h + (size_t)(fb * 16 + c16) * D + quad * E;
+      for (int fb = 0; fb < FB; ++fb) {
+        const T* wrow = Wt_h + (size_t)(fb * 16 + c16) * D + quad * E;
 #pragma unroll
-      for (int ks = 0; ks < C::KD; ++ks) wop[fb][ks] = load_op<T>(wrow + ks * KW);
+        for (int ks = 0; ks < C::KD; ++ks) wop[fb][ks] = load_op<T>(wrow + ks * KW);
+      }
     }
     f32x4 zr[RUNS];  // z at this lane's features, in phi-register order
 #pragma unroll
     for (int rn = 0; rn < RUNS; ++rn)
       zr[rn] = *reinterpret_cast<const f32x4*>(zh + C::feature(rn * 4, quad));
-    const float lw = log_sigmoid(a.alpha[h]);
+    const float lw = log_sigmoid(alpha_h);
+    if constexpr (C::DMA_QK) {
+      // The copies are counted by vmcnt alone and the compiler does not
+      // track them: wait for every load of this wave, then read the operands.
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+#pragma unroll
+      for (int r = 0; r < 2; ++r)
+#pragma unroll
+        for (int ks = 0; ks < C::KD; ++ks) {
+          qop[r][ks] = staged_op(qst, r * 16 + c16, quad + 4 * ks);
+          kop[r][ks] = staged_op(kst, r * 16 + c16, quad + 4 * ks);
+        }
+      if constexpr (C::DMA_W) {
+#pragma unroll
+        for (int fb = 0; fb < FB; ++fb)
+#pragma unroll
+          for (int ks = 0; ks < C::KD; ++ks)
+            wop[fb][ks] = staged_op(wst, fb * 16 + c16, quad + 4 * ks);
+      }
+    }
 
     // 2. V^T of the KV head into this wave's LDS area (keys padded to 0).
     T(*vt)[C::VT_LD] = sh.hd[w].vt;
@@ -359,7 +419,7 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
       for (int j = 0; j < NPHI; ++j) phi[j] *= j < 4 * FB ? sbp : sbn;
 #pragma unroll
       for (int ks = 0; ks < C::KF; ++ks)
-        sh.phib[w][qb][ks][lane] = cvt_op<T>(&phi[ks * E]);
+        sh.wl[w].phib[qb][ks][lane] = cvt_op<T>(&phi[ks * E]);
     }
 
     // 6. a P V into accumulators, then over this wave's (consumed) V^T area.
@@ -391,7 +451,7 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
-      for (int ks = 0; ks < C::KF; ++ks) phib[qb][ks] = sh.phib[w][qb][ks][lane];
+      for (int ks = 0; ks < C::KF; ++ks) phib[qb][ks] = sh.wl[w].phib[qb][ks][lane];
 #pragma unroll
     for (int pr = 0; pr < CB / 2; ++pr) {
       f32x4 acc[2][QB];
