@@ -84,9 +84,10 @@ struct StepCfg {
   };
   static_assert(2 * QB * kWave * 16 >= 32 * 32 * 4, "output staging");
   static_assert(CB % 2 == 0, "output columns are stored in pairs of blocks");
-  // bf16: the block wave's Q, K and (when it fits the head area) W_h rows
+  // bf16: the block wave's Q, K, V and (when it fits the head area) W_h rows
   // reach LDS by direct global->LDS copies whose every instruction reads
-  // whole rows, 16 bytes per lane; the MFMA operands are then read from LDS.
+  // whole rows, 16 bytes per lane; the MFMA operands are then read from LDS,
+  // those of V^T by transposing reads.
   static constexpr int CPR = D / EPC;          // 16-byte chunks per row
   static constexpr int RPI = kWave / CPR;      // rows per copy instruction
   static constexpr int RP256 = 256 / (D * (int)sizeof(T)) > 0 ? 256 / (D * (int)sizeof(T)) : 1;
@@ -95,9 +96,15 @@ struct StepCfg {
   // Chunk c of a staged row t sits at position c ^ swz(t), so the 16 rows an
   // operand read takes at one chunk fall in distinct LDS banks.
   __device__ static constexpr int swz(int t) { return (t / RP256) % CPR; }
-  union alignas(16) WaveLds {
-    op_t phib[QB][KF][kWave];  // b phi(Q) as the readout's B operand
-    T qk[DMA_QK ? 2 * 32 * D : 1];  // staged Q and K rows, until read
+  // Staged Q and K rows are read into registers before b phi(Q) is written
+  // over them; the staged V rows are read after that, so they have their own
+  // space.
+  struct alignas(16) WaveLds {
+    union alignas(16) {
+      op_t phib[QB][KF][kWave];  // b phi(Q) as the readout's B operand
+      T qk[DMA_QK ? 2 * 32 * D : 1];
+    };
+    T v[DMA_QK ? 32 * D : 1];
   };
   struct alignas(16) Smem {
     HeadLds hd[NW];  // W_h rows (staged), then V^T, then a P V and outputs
@@ -235,19 +242,22 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
     const T* __restrict__ Wt_h = (const T*)a.W + (size_t)h * F * D;
     const float* __restrict__ zh = a.z + sbase * f;
     uint4 vlo[C::VPT], vhi[C::VPT];  // rows 2kp, 2kp+1 of a 16-byte column group
+    if constexpr (!C::DMA_QK) {
 #pragma unroll
-    for (int j = 0; j < C::VPT; ++j) {
-      const int it = min(lane + j * kWave, C::VITEMS - 1), kp = it % 16, cg = it / 16;
-      vlo[j] = *reinterpret_cast<const uint4*>(
-          vb0 + (size_t)min(2 * kp, L - 1) * kstride + cg * C::EPC);
-      vhi[j] = *reinterpret_cast<const uint4*>(
-          vb0 + (size_t)min(2 * kp + 1, L - 1) * kstride + cg * C::EPC);
+      for (int j = 0; j < C::VPT; ++j) {
+        const int it = min(lane + j * kWave, C::VITEMS - 1), kp = it % 16, cg = it / 16;
+        vlo[j] = *reinterpret_cast<const uint4*>(
+            vb0 + (size_t)min(2 * kp, L - 1) * kstride + cg * C::EPC);
+        vhi[j] = *reinterpret_cast<const uint4*>(
+            vb0 + (size_t)min(2 * kp + 1, L - 1) * kstride + cg * C::EPC);
+      }
     }
     const float alpha_h = a.alpha[h];
     op_t qop[QB][C::KD], kop[KB][C::KD], wop[FB][C::KD];
     T* const wst = reinterpret_cast<T*>(&sh.hd[w]);
     T* const qst = sh.wl[w].qk;
     T* const kst = sh.wl[w].qk + (C::DMA_QK ? 32 * D : 0);
+    T* const vst = sh.wl[w].v;
     // Rows 0 .. n-1 of a row-major operand (row t at base + min(t, tmax) *
     // stride) into LDS at dst, chunk-swizzled; copy i takes rows i*RPI ..
     auto stage = [&](const T* base, size_t stride, int n, int tmax, T* dst) {
@@ -267,6 +277,7 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
     if constexpr (C::DMA_QK) {
       stage(qb0, qstride, 32, L - 1, qst);
       stage(kb0, kstride, 32, L - 1, kst);
+      stage(vb0, kstride, 32, L - 1, vst);
     } else {
 #pragma unroll
       for (int r = 0; r < 2; ++r) {
@@ -312,10 +323,11 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
       }
     }
 
-    // 2. V^T of the KV head into this wave's LDS area (keys padded to 0).
+    // 2. Without the staged copies: V^T of the KV head into this wave's LDS
+    //    area (keys padded to 0).
     T(*vt)[C::VT_LD] = sh.hd[w].vt;
 #pragma unroll
-    for (int j = 0; j < C::VPT; ++j) {
+    for (int j = 0; j < (C::DMA_QK ? 0 : C::VPT); ++j) {
       const int it = lane + j * kWave, kp = it % 16, cg = it / 16;
       if (C::VITEMS % kWave != 0 && it >= C::VITEMS) break;
       const T* x0 = reinterpret_cast<const T*>(&vlo[j]);
@@ -422,19 +434,42 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
         sh.wl[w].phib[qb][ks][lane] = cvt_op<T>(&phi[ks * E]);
     }
 
-    // 6. a P V into accumulators, then over this wave's (consumed) V^T area.
+    // 6. a P V into accumulators, then over this wave's head area.  The
+    //    V^T operand of column block cbk holds, in lane (c16, quad), column
+    //    column(cbk, c16) at keys key(0..7, quad).  From staged V rows: in
+    //    each 16-lane quarter the transposing read gives lane i element i%4 of
+    //    the 8-byte pieces addressed by lanes i/4 + 4j (j = 0..3), so lane
+    //    (i, quad) addresses key quad*4 + i/4 at columns column(cbk, 4*(i%4))
+    //    .. +3, four consecutive columns.
+    auto vt_op = [&](int cbk, int ks) -> op_t {
+      if constexpr (C::DMA_QK) {
+        static_assert(C::KL == 1, "one k-step over the block keys");
+        typedef short s16x4 __attribute__((ext_vector_type(4)));
+        const int col = C::column(cbk, 4 * (c16 % 4));
+        auto piece = [&](int t) {
+          const T* src = vst + t * D + ((col / C::EPC) ^ C::swz(t)) * C::EPC + col % C::EPC;
+          return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+              (__attribute__((address_space(3))) s16x4*)src);
+        };
+        const s16x4 lo = piece(quad * 4 + c16 / 4), hi = piece(16 + quad * 4 + c16 / 4);
+        return __builtin_bit_cast(op_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+      } else {
+        return lds_keys_op<T>(&vt[C::column(cbk, c16)][0], ks, quad);
+      }
+    };
     f32x4 acc[CB][QB];
 #pragma unroll
-    for (int cbk = 0; cbk < CB; ++cbk)
+    for (int cbk = 0; cbk < CB; ++cbk) {
 #pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
-        acc[cbk][qb] = f32x4{};
+      for (int qb = 0; qb < QB; ++qb) acc[cbk][qb] = f32x4{};
 #pragma unroll
-        for (int ks = 0; ks < C::KL; ++ks)
-          acc[cbk][qb] = mma16_split_b<T>(
-              lds_keys_op<T>(&vt[C::column(cbk, c16)][0], ks, quad), &p[qb][ks * E],
-              acc[cbk][qb]);
+      for (int ks = 0; ks < C::KL; ++ks) {
+        const op_t va = vt_op(cbk, ks);
+#pragma unroll
+        for (int qb = 0; qb < QB; ++qb)
+          acc[cbk][qb] = mma16_split_b<T>(va, &p[qb][ks * E], acc[cbk][qb]);
       }
+    }
 #pragma unroll
     for (int cbk = 0; cbk < CB; ++cbk)
 #pragma unroll
