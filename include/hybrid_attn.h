@@ -115,6 +115,20 @@ int hybrid_attn_step(const hyb_dims_t* dims, const void* q, const void* k,
                      const float* S, const float* z, const int32_t* slots,
                      void* out, void* stream);
 
+/* The last denoising step of a block fused with its commit, in one launch
+ * (the single kernel of Section 3.3: within-block softmax, readout, gated
+ * merge and the causal state update).  out is exactly what hybrid_attn_step
+ * gives on the state as it was; then, as hybrid_state_commit,
+ * S_h += sum_t phi_h(k_t) v_t^T and z_h += sum_t phi_h(k_t), in place.
+ * Arguments as for hybrid_attn_step, with S and z writable.  out, S and z
+ * must not overlap each other or any input; two requests of one call must
+ * not share a slot.  A request whose slot is out of range gets NaN outputs
+ * and leaves the state untouched. */
+int hybrid_attn_step_commit(const hyb_dims_t* dims, const void* q,
+                            const void* k, const void* v, const void* W,
+                            const float* alpha, float* S, float* z,
+                            const int32_t* slots, void* out, void* stream);
+
 /* Commit of a finished block (Section 3.1 state update):
  * S_h += sum_t phi_h(k_t) v_t^T and z_h += sum_t phi_h(k_t) over the L block
  * tokens, in place, for every request and query head.  Two requests of one

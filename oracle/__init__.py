@@ -136,6 +136,17 @@ def commit(k, v, Wt, S, z, slots=None):
     return S, z
 
 
+def step_commit(q, k, v, Wt, alpha, S, z, slots=None):
+    """The last denoising step of a block fused with its commit (Section 3.3:
+    one pass computes the within-block softmax, the readout, the gated merge
+    and the causal state update).  By definition: the step's output on the
+    state as it was, then the commit of the same block's keys and values.
+    Returns (out, S', z') (copies)."""
+    out = step(q, k, v, Wt, alpha, S, z, slots)
+    S1, z1 = commit(k, v, Wt, S, z, slots)
+    return out, S1, z1
+
+
 def prefill(q, k, v, Wt, alpha, S, z, L, slots=None, want_out=True):
     """Block-causal prefill of T tokens in blocks of L.
 

@@ -22,8 +22,9 @@ OP_STEP, OP_COMMIT, OP_PREFILL, OP_SOFTMAX_PREFIX = 0, 1, 2, 3
 STATUS = {0: "HYB_OK", 1: "HYB_ENULL", 2: "HYB_EINVAL", 3: "HYB_EALIGN",
           4: "HYB_EDTYPE", 5: "HYB_EUNSUPPORTED", 6: "HYB_EWORKSPACE",
           7: "HYB_ELAUNCH"}
-EXPORTS = ("hybrid_attn_step", "hybrid_state_commit", "hybrid_state_prefill",
-           "softmax_prefix_step", "hybrid_workspace_bytes", "hybrid_last_error")
+EXPORTS = ("hybrid_attn_step", "hybrid_attn_step_commit", "hybrid_state_commit",
+           "hybrid_state_prefill", "softmax_prefix_step", "hybrid_workspace_bytes",
+           "hybrid_last_error")
 
 
 class HybError(RuntimeError):
@@ -54,6 +55,7 @@ def load():
     vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
     P = ctypes.POINTER(Dims)
     lib.hybrid_attn_step.argtypes = [P] + [vp] * 10
+    lib.hybrid_attn_step_commit.argtypes = [P] + [vp] * 10
     lib.hybrid_state_commit.argtypes = [P] + [vp] * 7
     lib.hybrid_state_prefill.argtypes = [P, i32] + [vp] * 10 + [sz, vp]
     lib.softmax_prefix_step.argtypes = [P] + [vp] * 6 + [i32, vp, vp, sz, vp]
@@ -61,7 +63,7 @@ def load():
     lib.hybrid_workspace_bytes.restype = sz
     lib.hybrid_last_error.argtypes = []
     lib.hybrid_last_error.restype = ctypes.c_char_p
-    for n in ("hybrid_attn_step", "hybrid_state_commit", "hybrid_state_prefill",
+    for n in ("hybrid_attn_step", "hybrid_attn_step_commit", "hybrid_state_commit", "hybrid_state_prefill",
               "softmax_prefix_step"):
         getattr(lib, n).restype = ctypes.c_int
     _lib = lib
@@ -128,6 +130,25 @@ def hybrid_attn_step(q, k, v, W, alpha, S, z, slots=None, out=None, out_f32=Fals
     if out is None:
         out = torch.empty(q.shape, dtype=odt, device=q.device)
     _check(lib.hybrid_attn_step(
+        ctypes.byref(dims), _ptr(q, "q"), _ptr(k, "k", act), _ptr(v, "v", act),
+        _ptr(W, "W", act), _ptr(alpha, "alpha", torch.float32),
+        _ptr(S, "S", torch.float32), _ptr(z, "z", torch.float32),
+        _ptr(slots, "slots", torch.int32), _ptr(out, "out", odt), _stream(stream)))
+    return out
+
+
+def hybrid_attn_step_commit(q, k, v, W, alpha, S, z, slots=None, out=None, out_f32=False,
+                            stream=None):
+    """The step of hybrid_attn_step on the state as it is, then the commit of
+    k/v into S, z in place, in one launch; returns out."""
+    lib = load()
+    B, L, Hq, d = q.shape
+    act = q.dtype
+    flags, odt = _out_flags(out, act, out_f32)
+    dims = make_dims(B, Hq, k.shape[2], d, L, z.shape[2], _dt(q), S.shape[0], flags)
+    if out is None:
+        out = torch.empty(q.shape, dtype=odt, device=q.device)
+    _check(lib.hybrid_attn_step_commit(
         ctypes.byref(dims), _ptr(q, "q"), _ptr(k, "k", act), _ptr(v, "v", act),
         _ptr(W, "W", act), _ptr(alpha, "alpha", torch.float32),
         _ptr(S, "S", torch.float32), _ptr(z, "z", torch.float32),

@@ -132,6 +132,51 @@ int hybrid_attn_step(const hyb_dims_t* dims, const void* q, const void* k,
   return launched(hyb::launch_step(a, (hipStream_t)stream), "step");
 }
 
+int hybrid_attn_step_commit(const hyb_dims_t* dims, const void* q,
+                            const void* k, const void* v, const void* W,
+                            const float* alpha, float* S, float* z,
+                            const int32_t* slots, void* out, void* stream) {
+  hyb::Shape s;
+  TRY(check_dims(dims, true, &s));
+  if (s.B == 0) return ok();
+  TRY(check_ptr(q, "q"));
+  TRY(check_ptr(k, "k"));
+  TRY(check_ptr(v, "v"));
+  TRY(check_ptr(W, "W"));
+  TRY(check_ptr(alpha, "alpha"));
+  TRY(check_ptr(S, "S"));
+  TRY(check_ptr(z, "z"));
+  TRY(check_ptr(slots, "slots", false));
+  TRY(check_ptr(out, "out"));
+  const size_t es = elem_bytes(s.dtype), f = 2 * (size_t)s.F;
+  const size_t nq = (size_t)s.B * s.L * s.Hq * s.D * es;
+  const size_t no = (size_t)s.B * s.L * s.Hq * s.D * out_bytes(s);
+  const size_t nkv = (size_t)s.B * s.L * s.Hkv * s.D * es;
+  const size_t nS = (size_t)s.n_slots * s.Hq * f * s.D * 4;
+  const size_t nz = (size_t)s.n_slots * s.Hq * f * 4;
+  const size_t nW = (size_t)s.Hq * s.F * s.D * es;
+  // Everything the kernel writes (out, S, z) is disjoint from everything it
+  // reads and from each other.
+  struct Buf {
+    const void* p;
+    size_t n;
+  };
+  const Buf written[3] = {{out, no}, {S, nS}, {z, nz}};
+  const Buf read_only[6] = {{q, nq}, {k, nkv}, {v, nkv}, {W, nW},
+                            {alpha, (size_t)s.Hq * 4}, {slots, (size_t)s.B * 4}};
+  for (int i = 0; i < 3; ++i) {
+    for (const Buf& r : read_only)
+      if (overlap(written[i].p, written[i].n, r.p, r.n))
+        return fail(HYB_EINVAL, "an output (out, S or z) overlaps an input");
+    for (int j = i + 1; j < 3; ++j)
+      if (overlap(written[i].p, written[i].n, written[j].p, written[j].n))
+        return fail(HYB_EINVAL, "out, S and z overlap");
+  }
+  hyb::StepArgs a{s, q, k, v, W, alpha, S, z, slots, out};
+  (void)hipGetLastError();
+  return launched(hyb::launch_step_commit(a, (hipStream_t)stream), "step_commit");
+}
+
 int hybrid_state_commit(const hyb_dims_t* dims, const void* k, const void* v,
                         const void* W, float* S, float* z,
                         const int32_t* slots, void* stream) {

@@ -51,6 +51,10 @@ struct SoftmaxPrefixArgs {
 };
 
 hipError_t launch_step(const StepArgs& a, hipStream_t st);
+// The step fused with the commit of the same block: S and z are updated in
+// place after the step has read them (the StepArgs state pointers must be
+// writable).
+hipError_t launch_step_commit(const StepArgs& a, hipStream_t st);
 hipError_t launch_commit(const CommitArgs& a, hipStream_t st);
 hipError_t launch_prefill(const PrefillArgs& a, hipStream_t st);
 hipError_t launch_softmax_prefix(const SoftmaxPrefixArgs& a, hipStream_t st);

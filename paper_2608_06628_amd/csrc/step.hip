@@ -44,12 +44,14 @@
 // State layout: S_h is stored transposed (element (feature r, column c) at
 // c*f + r), so the A operand of S^T -- column c16 of a block, four features
 // per lane per run -- is one 16-byte load per run.
+#include <type_traits>
+
 #include "device.h"
 #include "launch.h"
 
 namespace hyb {
 
-template <typename T, int D, int F, int NW>
+template <typename T, int D, int F, int NW, bool CM = false>
 struct StepCfg {
   typedef Mma16<T> M;
   typedef typename M::op_t op_t;
@@ -96,20 +98,33 @@ struct StepCfg {
   // Chunk c of a staged row t sits at position c ^ swz(t), so the 16 rows an
   // operand read takes at one chunk fall in distinct LDS banks.
   __device__ static constexpr int swz(int t) { return (t / RP256) % CPR; }
+  // With the commit (CM): phi(K)^T as A operands of phi(K)^T V, per
+  // 16-feature block: NPART parts (bf16 hi + lo) x KL key steps.
+  static constexpr int NFB = f / 16;
+  static constexpr int NPART = E > 1 ? 2 : 1;
+  static constexpr int NPK = NPART * KL;
   // Staged Q and K rows are read into registers before b phi(Q) is written
-  // over them; the staged V rows are read after that, so they have their own
-  // space.
+  // over them, and phi(K)^T is written there once b phi(Q) has been read;
+  // the staged V rows are read until the end, so they have their own space.
   struct alignas(16) WaveLds {
     union alignas(16) {
       op_t phib[QB][KF][kWave];  // b phi(Q) as the readout's B operand
       T qk[DMA_QK ? 2 * 32 * D : 1];
+      op_t pk[CM ? NFB : 1][CM ? NPK : 1][kWave];  // phi(K)^T operands
     };
     T v[DMA_QK ? 32 * D : 1];
   };
-  struct alignas(16) Smem {
+  // Without staged V rows the commit keeps V^T in a space of its own (the
+  // head area takes a P V over it).
+  static constexpr bool VT_OWN = CM && !DMA_QK;
+  struct alignas(16) SmemBase {
     HeadLds hd[NW];  // W_h rows (staged), then V^T, then a P V and outputs
     WaveLds wl[NW];
   };
+  struct alignas(16) SmemVt : SmemBase {
+    T vt_own[NW][D][VT_LD];
+  };
+  typedef std::conditional_t<VT_OWN, SmemVt, SmemBase> Smem;
   // Feature held by phi register j (j < NPHI) of a lane in quarter `quad`:
   // j = (sign * FB + fb) * 4 + r -> sign*F + fb*16 + quad*4 + r.
   __device__ static constexpr int feature(int j, int quad) {
@@ -170,10 +185,26 @@ __device__ inline float qsum(float x) {
   x += xor16(x);
   return x + xor32(x);
 }
+// max / min / sum over the 16 lanes of a lane quarter (lanes c16 = 0..15).
+__device__ inline float rmax16(float x) {
+#pragma unroll
+  for (int m = 1; m < 16; m *= 2) x = fmaxf(x, __shfl_xor(x, m));
+  return x;
+}
+__device__ inline float rmin16(float x) {
+#pragma unroll
+  for (int m = 1; m < 16; m *= 2) x = fminf(x, __shfl_xor(x, m));
+  return x;
+}
+__device__ inline float rsum16(float x) {
+#pragma unroll
+  for (int m = 1; m < 16; m *= 2) x += __shfl_xor(x, m);
+  return x;
+}
 
-template <typename T, int D, int F, int NW>
+template <typename T, int D, int F, int NW, bool CM>
 __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a) {
-  typedef StepCfg<T, D, F, NW> C;
+  typedef StepCfg<T, D, F, NW, CM> C;
   typedef typename C::M M;
   typedef typename C::op_t op_t;
   constexpr int f = C::f, E = C::E, KW = C::KW, FB = C::FB, QB = C::QB,
@@ -205,6 +236,44 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
       buf[cb % NBUF][rn] = *reinterpret_cast<const f32x4*>(
           St + (size_t)C::column(cb, c16) * f + C::feature(rn * 4, quad));
   };
+
+  // Staged V rows (bf16) or V^T (fp32) of this head's KV head.
+  T* const vst = sh.wl[w].v;
+  T(*vt)[C::VT_LD];
+  if constexpr (C::VT_OWN)
+    vt = sh.vt_own[w];
+  else
+    vt = sh.hd[w].vt;
+  // V^T operands, of a P V and (with the commit) of phi(K)^T V.  The operand
+  // of column block cbk holds, in lane (c16, quad), column column(cbk, c16)
+  // at keys key(0..7, quad).  From staged V rows: in each 16-lane quarter the
+  // transposing read gives lane i element i%4 of the 8-byte pieces addressed
+  // by lanes i/4 + 4j (j = 0..3), so lane (i, quad) addresses key
+  // quad*4 + i/4 at columns column(cbk, 4*(i%4)) .. +3, four consecutive
+  // columns.
+  auto vt_op = [&](int cbk, int ks) -> op_t {
+    if constexpr (C::DMA_QK) {
+      static_assert(C::KL == 1, "one k-step over the block keys");
+      typedef short s16x4 __attribute__((ext_vector_type(4)));
+      const int col = C::column(cbk, 4 * (c16 % 4));
+      auto piece = [&](int t) {
+        const T* src = vst + t * D + ((col / C::EPC) ^ C::swz(t)) * C::EPC + col % C::EPC;
+        return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) s16x4*)src);
+      };
+      const s16x4 lo = piece(quad * 4 + c16 / 4), hi = piece(16 + quad * 4 + c16 / 4);
+      return __builtin_bit_cast(op_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    } else {
+      return lds_keys_op<T>(&vt[C::column(cbk, c16)][0], ks, quad);
+    }
+  };
+
+  // Block wave operands that outlive its step work: K and W_h (for phi(K)
+  // in the commit), z at this lane's features in phi-register order; with
+  // the commit, phi(K)^T operands.
+  op_t kop[KB][C::KD], wop[FB][C::KD];
+  f32x4 zr[RUNS];
+  op_t pk[C::NFB][C::NPK];
 
   // Column blocks 0 .. KPACK-1 as bf16 operands (S^T A operands).
   op_t sop[C::KPACK > 0 ? C::KPACK : 1][C::KF];
@@ -253,11 +322,10 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
       }
     }
     const float alpha_h = a.alpha[h];
-    op_t qop[QB][C::KD], kop[KB][C::KD], wop[FB][C::KD];
+    op_t qop[QB][C::KD];
     T* const wst = reinterpret_cast<T*>(&sh.hd[w]);
     T* const qst = sh.wl[w].qk;
     T* const kst = sh.wl[w].qk + (C::DMA_QK ? 32 * D : 0);
-    T* const vst = sh.wl[w].v;
     // Rows 0 .. n-1 of a row-major operand (row t at base + min(t, tmax) *
     // stride) into LDS at dst, chunk-swizzled; copy i takes rows i*RPI ..
     auto stage = [&](const T* base, size_t stride, int n, int tmax, T* dst) {
@@ -298,7 +366,6 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
         for (int ks = 0; ks < C::KD; ++ks) wop[fb][ks] = load_op<T>(wrow + ks * KW);
       }
     }
-    f32x4 zr[RUNS];  // z at this lane's features, in phi-register order
 #pragma unroll
     for (int rn = 0; rn < RUNS; ++rn)
       zr[rn] = *reinterpret_cast<const f32x4*>(zh + C::feature(rn * 4, quad));
@@ -325,7 +392,6 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
 
     // 2. Without the staged copies: V^T of the KV head into this wave's LDS
     //    area (keys padded to 0).
-    T(*vt)[C::VT_LD] = sh.hd[w].vt;
 #pragma unroll
     for (int j = 0; j < (C::DMA_QK ? 0 : C::VPT); ++j) {
       const int it = lane + j * kWave, kp = it % 16, cg = it / 16;
@@ -434,29 +500,7 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
         sh.wl[w].phib[qb][ks][lane] = cvt_op<T>(&phi[ks * E]);
     }
 
-    // 6. a P V into accumulators, then over this wave's head area.  The
-    //    V^T operand of column block cbk holds, in lane (c16, quad), column
-    //    column(cbk, c16) at keys key(0..7, quad).  From staged V rows: in
-    //    each 16-lane quarter the transposing read gives lane i element i%4 of
-    //    the 8-byte pieces addressed by lanes i/4 + 4j (j = 0..3), so lane
-    //    (i, quad) addresses key quad*4 + i/4 at columns column(cbk, 4*(i%4))
-    //    .. +3, four consecutive columns.
-    auto vt_op = [&](int cbk, int ks) -> op_t {
-      if constexpr (C::DMA_QK) {
-        static_assert(C::KL == 1, "one k-step over the block keys");
-        typedef short s16x4 __attribute__((ext_vector_type(4)));
-        const int col = C::column(cbk, 4 * (c16 % 4));
-        auto piece = [&](int t) {
-          const T* src = vst + t * D + ((col / C::EPC) ^ C::swz(t)) * C::EPC + col % C::EPC;
-          return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-              (__attribute__((address_space(3))) s16x4*)src);
-        };
-        const s16x4 lo = piece(quad * 4 + c16 / 4), hi = piece(16 + quad * 4 + c16 / 4);
-        return __builtin_bit_cast(op_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-      } else {
-        return lds_keys_op<T>(&vt[C::column(cbk, c16)][0], ks, quad);
-      }
-    };
+    // 6. a P V into accumulators, then over this wave's head area.
     f32x4 acc[CB][QB];
 #pragma unroll
     for (int cbk = 0; cbk < CB; ++cbk) {
@@ -476,6 +520,98 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
       for (int qb = 0; qb < QB; ++qb) sh.hd[w].apv[cbk][qb][lane] = acc[cbk][qb];
   }
   lds_barrier();
+
+  // With the commit: phi(K) of the block keys, from U_K = K W_h^T so
+  // that lane (c16, quad) holds feature fb*16 + c16 of keys
+  // kb*16 + quad*4 + r, which is the A-operand layout of phi(K)^T V (keys
+  // in the order key(j, quad)); each key's softmax over the features of a
+  // sign reduces across the 16 lanes of its quarter.  Padding keys get
+  // phi = 0.  z += sum_t phi(k_t) is written here (z was read before),
+  // from the same rounded values that enter S.  The block wave does this
+  // while the state waves fold.
+  if constexpr (CM) {
+    if (!state_wave) {
+      float ph[2][KB][FB][4];  // [sign][kb][fb][r]
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+        for (int fb = 0; fb < FB; ++fb) {
+          f32x4 acc = {};
+#pragma unroll
+          for (int ks = 0; ks < C::KD; ++ks) acc = M::mma(kop[kb][ks], wop[fb][ks], acc);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) ph[0][kb][fb][r] = acc[r];
+        }
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float mx = -INFINITY, mn = INFINITY;
+#pragma unroll
+          for (int fb = 0; fb < FB; ++fb) {
+            mx = fmaxf(mx, ph[0][kb][fb][r]);
+            mn = fminf(mn, ph[0][kb][fb][r]);
+          }
+          mx = rmax16(mx);
+          mn = rmin16(mn);
+          float sp = 0.0f, sn = 0.0f;
+#pragma unroll
+          for (int fb = 0; fb < FB; ++fb) {
+            const float u = ph[0][kb][fb][r];
+            ph[0][kb][fb][r] = fast_exp(u - mx);
+            ph[1][kb][fb][r] = fast_exp(mn - u);
+            sp += ph[0][kb][fb][r];
+            sn += ph[1][kb][fb][r];
+          }
+          const bool kv = kb * 16 + quad * 4 + r < L;
+          const float ip = kv ? 1.0f / rsum16(sp) : 0.0f, in = kv ? 1.0f / rsum16(sn) : 0.0f;
+#pragma unroll
+          for (int fb = 0; fb < FB; ++fb) {
+            ph[0][kb][fb][r] *= ip;
+            ph[1][kb][fb][r] *= in;
+          }
+        }
+      float zs[C::NFB];
+#pragma unroll
+      for (int fbk = 0; fbk < C::NFB; ++fbk) {
+        const int sg = fbk / FB, fb = fbk % FB;
+        zs[fbk] = 0.0f;
+#pragma unroll
+        for (int ks = 0; ks < C::KL; ++ks) {
+          float x[E], lo[E];
+#pragma unroll
+          for (int e = 0; e < E; ++e) {
+            const int j = ks * E + e;  // key(j, quad)
+            x[e] = ph[sg][j / 4][fb][j % 4];
+          }
+          pk[fbk][ks] = cvt_op<T>(x);
+#pragma unroll
+          for (int e = 0; e < E; ++e) {
+            lo[e] = x[e] - as_operand<T>(x[e]);
+            zs[fbk] += as_operand<T>(x[e]);
+          }
+          if constexpr (C::NPART == 2) {
+            pk[fbk][C::KL + ks] = cvt_op<T>(lo);
+#pragma unroll
+            for (int e = 0; e < E; ++e) zs[fbk] += as_operand<T>(lo[e]);
+          }
+        }
+        zs[fbk] = qsum(zs[fbk]);  // feature fbk*16 + c16, in every quarter
+      }
+      // z (this lane holds z_old at features fbk*16 + quad*4 + r in zr):
+      // lanes c16 == 0 write 16 bytes per block.
+      if (slot_ok) {
+        float* __restrict__ zw = const_cast<float*>(a.z) + sbase * f;
+#pragma unroll
+        for (int fbk = 0; fbk < C::NFB; ++fbk) {
+          f32x4 zn;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) zn[r] = zr[fbk][r] + __shfl(zs[fbk], quad * 4 + r);
+          if (c16 == 0) *reinterpret_cast<f32x4*>(zw + fbk * 16 + quad * 4) = zn;
+        }
+      }
+    }
+  }
 
   const bool of32 = sizeof(T) == 4 || a.s.out_f32;
   if (state_wave) {
@@ -546,58 +682,105 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
       }
     }
   }
+
+  // 9. With the commit: S_h += phi(K)^T V.  The block wave hands its phi(K)^T
+  //    operands over through its per-wave area (b phi(Q) has been read); the
+  //    state wave reads the state again, column block by column block, and
+  //    accumulates onto it in place: run rn of column block cb holds, in lane
+  //    (c16, quad), features rn*16 + quad*4 .. +3 of column column(cb, c16),
+  //    the accumulator layout of the 16 x 16 tile (features rn*16 .., columns
+  //    of cb).  The step above used the state as it was.
+  if constexpr (CM) {
+    if (!state_wave) {
+#pragma unroll
+      for (int fbk = 0; fbk < C::NFB; ++fbk)
+#pragma unroll
+        for (int j = 0; j < C::NPK; ++j) sh.wl[w].pk[fbk][j][lane] = pk[fbk][j];
+    }
+    lds_barrier();
+    if (state_wave && slot_ok) {
+      static_assert(RUNS == C::NFB, "one state run per 16-feature block");
+      float* __restrict__ Sw = const_cast<float*>(a.S) + sbase * f * D;
+#pragma unroll
+      for (int cb = 0; cb < NBUF; ++cb) issue(cb);
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb) {
+        op_t va[C::KL];
+#pragma unroll
+        for (int ks = 0; ks < C::KL; ++ks) va[ks] = vt_op(cb, ks);
+#pragma unroll
+        for (int rn = 0; rn < RUNS; ++rn) {
+          f32x4 acc = buf[cb % NBUF][rn];
+#pragma unroll
+          for (int j = 0; j < C::NPK; ++j)
+            acc = M::mma(sh.wl[w].pk[rn][j][lane], va[j % C::KL], acc);
+          *reinterpret_cast<f32x4*>(Sw + (size_t)C::column(cb, c16) * f + C::feature(rn * 4, quad)) =
+              acc;
+        }
+        if (cb + NBUF < CB) issue(cb + NBUF);
+      }
+    }
+  }
 }
 
-// Heads per workgroup: as many (up to 4) as share one KV head; fp32 and the
-// widest feature map use at most 2, which keeps their two waves per head
-// within one SIMD's register file and their LDS within 160 KiB.
-template <typename T, int F>
+// Heads per workgroup: as many (up to 4) as share one KV head; fp32, the
+// widest feature map and the fused commit use at most 2, which keeps their
+// two waves per head within one SIMD's register file and their LDS within
+// 160 KiB.
+template <typename T, int F, bool CM>
 constexpr int step_max_heads() {
-  return (sizeof(T) == 4 || F == 128) ? 2 : 4;
+  return (sizeof(T) == 4 || F == 128 || CM) ? 2 : 4;
 }
 
-template <typename T, int D, int F>
+template <typename T, int D, int F, bool CM>
 static hipError_t step_go(const StepArgs& a, hipStream_t st) {
   const int G = a.s.Hq / a.s.Hkv;
   int nw = G % 4 == 0 ? 4 : (G % 2 == 0 ? 2 : 1);
-  if (nw > step_max_heads<T, F>()) nw = step_max_heads<T, F>();
+  if (nw > step_max_heads<T, F, CM>()) nw = step_max_heads<T, F, CM>();
   const dim3 grid(a.s.B * (a.s.Hq / nw));
-  if constexpr (step_max_heads<T, F>() >= 4) {
-    static_assert(sizeof(typename StepCfg<T, D, F, 4>::Smem) <= 160 * 1024, "LDS");
+  if constexpr (step_max_heads<T, F, CM>() >= 4) {
+    static_assert(sizeof(typename StepCfg<T, D, F, 4, CM>::Smem) <= 160 * 1024, "LDS");
     if (nw == 4) {
-      hipLaunchKernelGGL((hyb_step_kernel<T, D, F, 4>), grid, dim3(kWave * 8), 0, st, a);
+      hipLaunchKernelGGL((hyb_step_kernel<T, D, F, 4, CM>), grid, dim3(kWave * 8), 0, st, a);
       return hipGetLastError();
     }
   }
-  static_assert(sizeof(typename StepCfg<T, D, F, 2>::Smem) <= 160 * 1024, "LDS");
+  static_assert(sizeof(typename StepCfg<T, D, F, 2, CM>::Smem) <= 160 * 1024, "LDS");
   if (nw == 2)
-    hipLaunchKernelGGL((hyb_step_kernel<T, D, F, 2>), grid, dim3(kWave * 4), 0, st, a);
+    hipLaunchKernelGGL((hyb_step_kernel<T, D, F, 2, CM>), grid, dim3(kWave * 4), 0, st, a);
   else
-    hipLaunchKernelGGL((hyb_step_kernel<T, D, F, 1>), grid, dim3(kWave * 2), 0, st, a);
+    hipLaunchKernelGGL((hyb_step_kernel<T, D, F, 1, CM>), grid, dim3(kWave * 2), 0, st, a);
   return hipGetLastError();
 }
 
-template <typename T, int D>
+template <typename T, int D, bool CM>
 static hipError_t step_f(const StepArgs& a, hipStream_t st) {
   switch (a.s.F) {
-    case 32: return step_go<T, D, 32>(a, st);
-    case 64: return step_go<T, D, 64>(a, st);
-    case 128: return step_go<T, D, 128>(a, st);
+    case 32: return step_go<T, D, 32, CM>(a, st);
+    case 64: return step_go<T, D, 64, CM>(a, st);
+    case 128: return step_go<T, D, 128, CM>(a, st);
   }
   return hipErrorInvalidValue;
 }
 
-template <typename T>
+template <typename T, bool CM>
 static hipError_t step_d(const StepArgs& a, hipStream_t st) {
   switch (a.s.D) {
-    case 64: return step_f<T, 64>(a, st);
-    case 128: return step_f<T, 128>(a, st);
+    case 64: return step_f<T, 64, CM>(a, st);
+    case 128: return step_f<T, 128, CM>(a, st);
   }
   return hipErrorInvalidValue;
 }
 
 hipError_t launch_step(const StepArgs& a, hipStream_t st) {
-  return a.s.dtype == 1 ? step_d<bf16>(a, st) : step_d<float>(a, st);
+  return a.s.dtype == 1 ? step_d<bf16, false>(a, st) : step_d<float, false>(a, st);
+}
+
+// The step of a block's last denoising pass fused with its commit (the
+// single launch of Section 3.3): the outputs use the state as it was, then
+// S and z take the block's keys and values.  S and z are written in place.
+hipError_t launch_step_commit(const StepArgs& a, hipStream_t st) {
+  return a.s.dtype == 1 ? step_d<bf16, true>(a, st) : step_d<float, true>(a, st);
 }
 
 }  // namespace hyb

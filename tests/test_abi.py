@@ -83,6 +83,38 @@ def test_zero_batch_is_a_noop():
     assert hb.last_error() == ""
 
 
+def _addr(i):
+    return ctypes.c_void_p(0x100000 * (i + 1))   # disjoint, aligned, never dereferenced
+
+
+def test_step_commit_validation():
+    """The fused step+commit: null, alignment and every written/read overlap."""
+    lib = hb.load()
+    d = _dims()
+    call = lambda p, dims=d: lib.hybrid_attn_step_commit(ctypes.byref(dims), *p, None)
+    ok = [_addr(i) for i in range(9)]
+    ok[7] = None                                    # slots may be NULL
+    for i in range(9):
+        if i == 7:
+            continue
+        p = list(ok)
+        p[i] = None
+        assert call(p) == 1, i
+        p[i] = MISALIGNED
+        assert call(p) == 3, i
+    assert call(list(ok), _dims(head_dim=96)) == 5
+    # written buffers: out (8), S (5), z (6); read: q k v W alpha (0-4), slots (7)
+    for w_i in (5, 6, 8):
+        for r_i in (0, 1, 2, 3, 4, 5, 6, 8):
+            if r_i == w_i:
+                continue
+            p = list(ok)
+            p[w_i] = p[r_i]
+            assert call(p) == 2, (w_i, r_i)
+            assert "overlap" in hb.last_error()
+    assert lib.hybrid_attn_step_commit(ctypes.byref(_dims(batch=0)), *([None] * 9), None) == 0
+
+
 def test_commit_prefill_softmax_validation():
     lib = hb.load()
     d = _dims()

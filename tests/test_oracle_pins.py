@@ -304,6 +304,30 @@ def test_prefill_is_dense_block_causal(dims):
     np.testing.assert_allclose(z3, z, atol=0)
 
 
+# ------------------------------------------------- fused step + commit ----
+
+@pytest.mark.parametrize("dims", [CASES[1], CASES[2]])
+def test_step_commit_walk_is_dense_block_causal(dims):
+    """Serving a prompt block by block with the fused step+commit (Section 3.3)
+    from an empty state gives the dense Figure 2 outputs and the dense state:
+    each block's output must come from the state before its own commit."""
+    T = 4 * dims.L
+    q, k, v = synth.block_qkv(dims.with_(L=T), 34)
+    Wt, alpha = synth.feature_weights(dims, 35, 36, 1.0 / math.sqrt(dims.d))
+    S, z = oracle.empty_state(dims.B, dims.Hq, dims.f, dims.d)
+    outs = []
+    for c in range(T // dims.L):
+        sl = slice(c * dims.L, (c + 1) * dims.L)
+        o, S, z = oracle.step_commit(q[:, sl], k[:, sl], v[:, sl], Wt, alpha, S, z)
+        outs.append(o)
+    np.testing.assert_allclose(np.concatenate(outs, 1),
+                               brute.block_causal_brute(q, k, v, Wt, alpha, dims.L),
+                               rtol=1e-12, atol=1e-13)
+    Sb, zb = brute.state_brute(k, v, Wt, dims.Hq)
+    np.testing.assert_allclose(S, Sb, rtol=1e-12, atol=1e-13)
+    np.testing.assert_allclose(z, zb, rtol=1e-12, atol=1e-13)
+
+
 # ------------------------------------------------ softmax-prefix step ----
 
 def test_softmax_prefix_equals_sdpa():
