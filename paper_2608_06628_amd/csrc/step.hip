@@ -104,13 +104,12 @@ struct StepCfg {
   static constexpr int NPART = E > 1 ? 2 : 1;
   static constexpr int NPK = NPART * KL;
   // Staged Q and K rows are read into registers before b phi(Q) is written
-  // over them, and phi(K)^T is written there once b phi(Q) has been read;
-  // the staged V rows are read until the end, so they have their own space.
+  // over them; the staged V rows are read until the end, so they have their
+  // own space.
   struct alignas(16) WaveLds {
     union alignas(16) {
       op_t phib[QB][KF][kWave];  // b phi(Q) as the readout's B operand
       T qk[DMA_QK ? 2 * 32 * D : 1];
-      op_t pk[CM ? NFB : 1][CM ? NPK : 1][kWave];  // phi(K)^T operands
     };
     T v[DMA_QK ? 32 * D : 1];
   };
@@ -268,9 +267,9 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
     }
   };
 
-  // Block wave operands that outlive its step work: K and W_h (for phi(K)
-  // in the commit), z at this lane's features in phi-register order; with
-  // the commit, phi(K)^T operands.
+  // K and W_h operands (the block wave's step; the state wave's phi(K) in
+  // the commit), z at this lane's features in phi-register order (block
+  // wave), phi(K)^T operands (commit, state wave).
   op_t kop[KB][C::KD], wop[FB][C::KD];
   f32x4 zr[RUNS];
   op_t pk[C::NFB][C::NPK];
@@ -521,98 +520,6 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
   }
   lds_barrier();
 
-  // With the commit: phi(K) of the block keys, from U_K = K W_h^T so
-  // that lane (c16, quad) holds feature fb*16 + c16 of keys
-  // kb*16 + quad*4 + r, which is the A-operand layout of phi(K)^T V (keys
-  // in the order key(j, quad)); each key's softmax over the features of a
-  // sign reduces across the 16 lanes of its quarter.  Padding keys get
-  // phi = 0.  z += sum_t phi(k_t) is written here (z was read before),
-  // from the same rounded values that enter S.  The block wave does this
-  // while the state waves fold.
-  if constexpr (CM) {
-    if (!state_wave) {
-      float ph[2][KB][FB][4];  // [sign][kb][fb][r]
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-        for (int fb = 0; fb < FB; ++fb) {
-          f32x4 acc = {};
-#pragma unroll
-          for (int ks = 0; ks < C::KD; ++ks) acc = M::mma(kop[kb][ks], wop[fb][ks], acc);
-#pragma unroll
-          for (int r = 0; r < 4; ++r) ph[0][kb][fb][r] = acc[r];
-        }
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          float mx = -INFINITY, mn = INFINITY;
-#pragma unroll
-          for (int fb = 0; fb < FB; ++fb) {
-            mx = fmaxf(mx, ph[0][kb][fb][r]);
-            mn = fminf(mn, ph[0][kb][fb][r]);
-          }
-          mx = rmax16(mx);
-          mn = rmin16(mn);
-          float sp = 0.0f, sn = 0.0f;
-#pragma unroll
-          for (int fb = 0; fb < FB; ++fb) {
-            const float u = ph[0][kb][fb][r];
-            ph[0][kb][fb][r] = fast_exp(u - mx);
-            ph[1][kb][fb][r] = fast_exp(mn - u);
-            sp += ph[0][kb][fb][r];
-            sn += ph[1][kb][fb][r];
-          }
-          const bool kv = kb * 16 + quad * 4 + r < L;
-          const float ip = kv ? 1.0f / rsum16(sp) : 0.0f, in = kv ? 1.0f / rsum16(sn) : 0.0f;
-#pragma unroll
-          for (int fb = 0; fb < FB; ++fb) {
-            ph[0][kb][fb][r] *= ip;
-            ph[1][kb][fb][r] *= in;
-          }
-        }
-      float zs[C::NFB];
-#pragma unroll
-      for (int fbk = 0; fbk < C::NFB; ++fbk) {
-        const int sg = fbk / FB, fb = fbk % FB;
-        zs[fbk] = 0.0f;
-#pragma unroll
-        for (int ks = 0; ks < C::KL; ++ks) {
-          float x[E], lo[E];
-#pragma unroll
-          for (int e = 0; e < E; ++e) {
-            const int j = ks * E + e;  // key(j, quad)
-            x[e] = ph[sg][j / 4][fb][j % 4];
-          }
-          pk[fbk][ks] = cvt_op<T>(x);
-#pragma unroll
-          for (int e = 0; e < E; ++e) {
-            lo[e] = x[e] - as_operand<T>(x[e]);
-            zs[fbk] += as_operand<T>(x[e]);
-          }
-          if constexpr (C::NPART == 2) {
-            pk[fbk][C::KL + ks] = cvt_op<T>(lo);
-#pragma unroll
-            for (int e = 0; e < E; ++e) zs[fbk] += as_operand<T>(lo[e]);
-          }
-        }
-        zs[fbk] = qsum(zs[fbk]);  // feature fbk*16 + c16, in every quarter
-      }
-      // z (this lane holds z_old at features fbk*16 + quad*4 + r in zr):
-      // lanes c16 == 0 write 16 bytes per block.
-      if (slot_ok) {
-        float* __restrict__ zw = const_cast<float*>(a.z) + sbase * f;
-#pragma unroll
-        for (int fbk = 0; fbk < C::NFB; ++fbk) {
-          f32x4 zn;
-#pragma unroll
-          for (int r = 0; r < 4; ++r) zn[r] = zr[fbk][r] + __shfl(zs[fbk], quad * 4 + r);
-          if (c16 == 0) *reinterpret_cast<f32x4*>(zw + fbk * 16 + quad * 4) = zn;
-        }
-      }
-    }
-  }
-
   const bool of32 = sizeof(T) == 4 || a.s.out_f32;
   if (state_wave) {
     // 7. out^T = a P V + S^T (b phi)^T, a pair of column blocks at a time;
@@ -683,23 +590,117 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
     }
   }
 
-  // 9. With the commit: S_h += phi(K)^T V.  The block wave hands its phi(K)^T
-  //    operands over through its per-wave area (b phi(Q) has been read); the
-  //    state wave reads the state again, column block by column block, and
-  //    accumulates onto it in place: run rn of column block cb holds, in lane
-  //    (c16, quad), features rn*16 + quad*4 .. +3 of column column(cb, c16),
-  //    the accumulator layout of the 16 x 16 tile (features rn*16 .., columns
-  //    of cb).  The step above used the state as it was.
+  // 9. With the commit: S_h += phi(K)^T V and z_h += sum_t phi(k_t), by the
+  //    state wave once the outputs are out.  It loads K and W_h (from L2),
+  //    computes phi(K) of the block keys from U_K = K W_h^T so that lane
+  //    (c16, quad) holds feature fb*16 + c16 of keys kb*16 + quad*4 + r:
+  //    the A-operand layout of phi(K)^T V (keys in the order key(j, quad)).
+  //    Each key's softmax over the features of a sign reduces across the 16
+  //    lanes of its quarter; padding keys get phi = 0.  z takes the sum of
+  //    the same rounded values that enter S.  Then it reads the state again,
+  //    column block by column block, and accumulates onto it in place: run
+  //    rn of column block cb holds, in lane (c16, quad), features
+  //    rn*16 + quad*4 .. +3 of column column(cb, c16), the accumulator layout
+  //    of the 16 x 16 tile (features rn*16 .., columns of cb).  The step above
+  //    used the state as it was.
   if constexpr (CM) {
-    if (!state_wave) {
-#pragma unroll
-      for (int fbk = 0; fbk < C::NFB; ++fbk)
-#pragma unroll
-        for (int j = 0; j < C::NPK; ++j) sh.wl[w].pk[fbk][j][lane] = pk[fbk][j];
-    }
-    lds_barrier();
     if (state_wave && slot_ok) {
       static_assert(RUNS == C::NFB, "one state run per 16-feature block");
+      {
+        const size_t kstride = (size_t)Hkv * D;
+        const T* __restrict__ kb0 = (const T*)a.k + ((size_t)b * L * Hkv + g) * D;
+        const T* __restrict__ Wt_h = (const T*)a.W + (size_t)h * F * D;
+#pragma unroll
+        for (int r = 0; r < KB; ++r) {
+          const T* krow = kb0 + (size_t)min(r * 16 + c16, L - 1) * kstride + quad * E;
+#pragma unroll
+          for (int ks = 0; ks < C::KD; ++ks) kop[r][ks] = load_op<T>(krow + ks * KW);
+        }
+#pragma unroll
+        for (int fb = 0; fb < FB; ++fb) {
+          const T* wrow = Wt_h + (size_t)(fb * 16 + c16) * D + quad * E;
+#pragma unroll
+          for (int ks = 0; ks < C::KD; ++ks) wop[fb][ks] = load_op<T>(wrow + ks * KW);
+        }
+      }
+      float ph[2][KB][FB][4];  // [sign][kb][fb][r]
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+        for (int fb = 0; fb < FB; ++fb) {
+          f32x4 acc = {};
+#pragma unroll
+          for (int ks = 0; ks < C::KD; ++ks) acc = M::mma(kop[kb][ks], wop[fb][ks], acc);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) ph[0][kb][fb][r] = acc[r];
+        }
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float mx = -INFINITY, mn = INFINITY;
+#pragma unroll
+          for (int fb = 0; fb < FB; ++fb) {
+            mx = fmaxf(mx, ph[0][kb][fb][r]);
+            mn = fminf(mn, ph[0][kb][fb][r]);
+          }
+          mx = rmax16(mx);
+          mn = rmin16(mn);
+          float sp = 0.0f, sn = 0.0f;
+#pragma unroll
+          for (int fb = 0; fb < FB; ++fb) {
+            const float u = ph[0][kb][fb][r];
+            ph[0][kb][fb][r] = fast_exp(u - mx);
+            ph[1][kb][fb][r] = fast_exp(mn - u);
+            sp += ph[0][kb][fb][r];
+            sn += ph[1][kb][fb][r];
+          }
+          const bool kv = kb * 16 + quad * 4 + r < L;
+          const float ip = kv ? 1.0f / rsum16(sp) : 0.0f, in = kv ? 1.0f / rsum16(sn) : 0.0f;
+#pragma unroll
+          for (int fb = 0; fb < FB; ++fb) {
+            ph[0][kb][fb][r] *= ip;
+            ph[1][kb][fb][r] *= in;
+          }
+        }
+      float zs[C::NFB];
+#pragma unroll
+      for (int fbk = 0; fbk < C::NFB; ++fbk) {
+        const int sg = fbk / FB, fb = fbk % FB;
+        zs[fbk] = 0.0f;
+#pragma unroll
+        for (int ks = 0; ks < C::KL; ++ks) {
+          float x[E], lo[E];
+#pragma unroll
+          for (int e = 0; e < E; ++e) {
+            const int j = ks * E + e;  // key(j, quad)
+            x[e] = ph[sg][j / 4][fb][j % 4];
+          }
+          pk[fbk][ks] = cvt_op<T>(x);
+#pragma unroll
+          for (int e = 0; e < E; ++e) {
+            lo[e] = x[e] - as_operand<T>(x[e]);
+            zs[fbk] += as_operand<T>(x[e]);
+          }
+          if constexpr (C::NPART == 2) {
+            pk[fbk][C::KL + ks] = cvt_op<T>(lo);
+#pragma unroll
+            for (int e = 0; e < E; ++e) zs[fbk] += as_operand<T>(lo[e]);
+          }
+        }
+        zs[fbk] = qsum(zs[fbk]);  // feature fbk*16 + c16, in every quarter
+      }
+      // z: lanes c16 == 0 write 16 bytes per 16-feature block.
+      {
+        float* __restrict__ zw = const_cast<float*>(a.z) + sbase * f;
+#pragma unroll
+        for (int fbk = 0; fbk < C::NFB; ++fbk) {
+          f32x4 zn = *reinterpret_cast<const f32x4*>(zw + fbk * 16 + quad * 4);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) zn[r] += __shfl(zs[fbk], quad * 4 + r);
+          if (c16 == 0) *reinterpret_cast<f32x4*>(zw + fbk * 16 + quad * 4) = zn;
+        }
+      }
       float* __restrict__ Sw = const_cast<float*>(a.S) + sbase * f * D;
 #pragma unroll
       for (int cb = 0; cb < NBUF; ++cb) issue(cb);
@@ -712,8 +713,7 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
         for (int rn = 0; rn < RUNS; ++rn) {
           f32x4 acc = buf[cb % NBUF][rn];
 #pragma unroll
-          for (int j = 0; j < C::NPK; ++j)
-            acc = M::mma(sh.wl[w].pk[rn][j][lane], va[j % C::KL], acc);
+          for (int j = 0; j < C::NPK; ++j) acc = M::mma(pk[rn][j], va[j % C::KL], acc);
           *reinterpret_cast<f32x4*>(Sw + (size_t)C::column(cb, c16) * f + C::feature(rn * 4, quad)) =
               acc;
         }
@@ -723,13 +723,12 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
   }
 }
 
-// Heads per workgroup: as many (up to 4) as share one KV head; fp32, the
-// widest feature map and the fused commit use at most 2, which keeps their
-// two waves per head within one SIMD's register file and their LDS within
-// 160 KiB.
+// Heads per workgroup: as many (up to 4) as share one KV head; fp32 and the
+// widest feature map use at most 2, which keeps their two waves per head
+// within one SIMD's register file and their LDS within 160 KiB.
 template <typename T, int F, bool CM>
 constexpr int step_max_heads() {
-  return (sizeof(T) == 4 || F == 128 || CM) ? 2 : 4;
+  return (sizeof(T) == 4 || F == 128) ? 2 : 4;
 }
 
 template <typename T, int D, int F, bool CM>
