@@ -275,6 +275,17 @@ __device__ inline void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
+// The same ordering for kernels that issue global->LDS copies: the compiler
+// counts such a copy as an LDS write until it sees the wave's vmcnt reach 0,
+// so before a local fence it waits for every outstanding global load of the
+// wave, on whatever path the wave took.  Written out instead: the wave's LDS
+// operations complete (lgkmcnt 0), then the barrier; the "memory" clobber
+// keeps LDS accesses on their side.  The copies must be waited for
+// explicitly (s_waitcnt vmcnt) by the wave that issued them.
+__device__ inline void lds_barrier_nodrain() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 // Work-unit index for the workgroup: consecutive units land on one XCD.
 // Workgroups are handed to the 8 XCDs round-robin by blockIdx, so unit
 // u = (bid % 8) * (n / 8) + bid / 8 keeps units u..u+n/8-1 on one XCD (and

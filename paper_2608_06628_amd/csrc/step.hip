@@ -116,6 +116,16 @@ struct StepCfg {
   // Without staged V rows the commit keeps V^T in a space of its own (the
   // head area takes a P V over it).
   static constexpr bool VT_OWN = CM && !DMA_QK;
+  // The commit on arrival of the state (bf16, f <= d): the block wave
+  // computes phi(K) as soon as its copies land and leaves its operands in
+  // consumed staging space -- the bf16 hi parts in the K-staging area (64 d
+  // bytes; b phi(Q), 64 f bytes, stays within the Q-staging area before
+  // it), the lo parts in the head area (free from the W_h operand reads
+  // until a P V) -- so the state wave updates each column block in fp32 as
+  // it arrives and never reads the state twice.  Other shapes update in a
+  // second pass after the outputs.
+  static constexpr bool EARLY = CM && DMA_QK && f <= D;
+  static_assert(!EARLY || f * 64 <= (int)sizeof(HeadLds), "phi(K) lo parts in the head area");
   struct alignas(16) SmemBase {
     HeadLds hd[NW];  // W_h rows (staged), then V^T, then a P V and outputs
     WaveLds wl[NW];
@@ -274,6 +284,103 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
   f32x4 zr[RUNS];
   op_t pk[C::NFB][C::NPK];
 
+  // phi(K) of the block keys from kop, wop: U_K = K W_h^T puts feature
+  // fb*16 + c16 of keys kb*16 + quad*4 + r in lane (c16, quad), which is the
+  // A-operand layout of phi(K)^T V (keys in the order key(j, quad)).  Each
+  // key's softmax over the features of a sign reduces across the 16 lanes of
+  // its quarter; padding keys get phi = 0.  The operand parts of 16-feature
+  // block fbk and key step ks (bf16 hi, + lo when NP = 2) go to
+  // sink(fbk, part, ks, operand); zs[fbk] sums the same rounded values over
+  // the block keys (feature fbk*16 + c16, in every quarter).
+  auto phi_k = [&](auto np, float* zs, auto&& sink) {
+    constexpr int NP = decltype(np)::value;
+    float ph[2][KB][FB][4];  // [sign][kb][fb][r]
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+      for (int fb = 0; fb < FB; ++fb) {
+        f32x4 acc = {};
+#pragma unroll
+        for (int ks = 0; ks < C::KD; ++ks) acc = M::mma(kop[kb][ks], wop[fb][ks], acc);
+#pragma unroll
+        for (int r = 0; r < 4; ++r) ph[0][kb][fb][r] = acc[r];
+      }
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float mx = -INFINITY, mn = INFINITY;
+#pragma unroll
+        for (int fb = 0; fb < FB; ++fb) {
+          mx = fmaxf(mx, ph[0][kb][fb][r]);
+          mn = fminf(mn, ph[0][kb][fb][r]);
+        }
+        mx = rmax16(mx);
+        mn = rmin16(mn);
+        float sp = 0.0f, sn = 0.0f;
+#pragma unroll
+        for (int fb = 0; fb < FB; ++fb) {
+          const float u = ph[0][kb][fb][r];
+          ph[0][kb][fb][r] = fast_exp(u - mx);
+          ph[1][kb][fb][r] = fast_exp(mn - u);
+          sp += ph[0][kb][fb][r];
+          sn += ph[1][kb][fb][r];
+        }
+        const bool kv = kb * 16 + quad * 4 + r < L;
+        const float ip = kv ? 1.0f / rsum16(sp) : 0.0f, in = kv ? 1.0f / rsum16(sn) : 0.0f;
+#pragma unroll
+        for (int fb = 0; fb < FB; ++fb) {
+          ph[0][kb][fb][r] *= ip;
+          ph[1][kb][fb][r] *= in;
+        }
+      }
+#pragma unroll
+    for (int fbk = 0; fbk < C::NFB; ++fbk) {
+      const int sg = fbk / FB, fb = fbk % FB;
+      zs[fbk] = 0.0f;
+#pragma unroll
+      for (int ks = 0; ks < C::KL; ++ks) {
+        float x[E], lo[E];
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          const int j = ks * E + e;  // key(j, quad)
+          x[e] = ph[sg][j / 4][fb][j % 4];
+        }
+        sink(fbk, 0, ks, cvt_op<T>(x));
+#pragma unroll
+        for (int e = 0; e < E; ++e) {
+          lo[e] = x[e] - as_operand<T>(x[e]);
+          zs[fbk] += as_operand<T>(x[e]);
+        }
+        if constexpr (NP == 2) {
+          sink(fbk, 1, ks, cvt_op<T>(lo));
+#pragma unroll
+          for (int e = 0; e < E; ++e) zs[fbk] += as_operand<T>(lo[e]);
+        }
+      }
+      zs[fbk] = qsum(zs[fbk]);  // feature fbk*16 + c16, in every quarter
+    }
+  };
+
+  // EARLY commit of column block cb (fp32 state in buf): S^T of the block
+  // += (phi(K)^T V)^T, the phi(K)^T operands (hi, lo) read from the block
+  // wave's staging space.  Run rn of the block holds, in lane (c16, quad),
+  // features rn*16 + quad*4 .. +3 of column column(cb, c16): the accumulator
+  // layout of the 16 x 16 tile (features rn*16 .., columns of cb).
+  auto update = [&](int cb) {
+    if (!slot_ok) return;
+    const op_t* __restrict__ pkh = reinterpret_cast<const op_t*>(sh.wl[w].qk + 32 * D);
+    const op_t* __restrict__ pkl = reinterpret_cast<const op_t*>(&sh.hd[w]);
+    float* __restrict__ Sw = const_cast<float*>(a.S) + sbase * f * D;
+    const op_t va = vt_op(cb, 0);
+#pragma unroll
+    for (int rn = 0; rn < RUNS; ++rn) {
+      f32x4 acc = M::mma(pkh[rn * kWave + lane], va, buf[cb % NBUF][rn]);
+      acc = M::mma(pkl[rn * kWave + lane], va, acc);
+      *reinterpret_cast<f32x4*>(Sw + (size_t)C::column(cb, c16) * f + C::feature(rn * 4, quad)) = acc;
+    }
+  };
+
   // Column blocks 0 .. KPACK-1 as bf16 operands (S^T A operands).
   op_t sop[C::KPACK > 0 ? C::KPACK : 1][C::KF];
   auto convert = [&](int cb, int ks) {
@@ -284,10 +391,13 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
   };
 
   if (state_wave) {
+    if constexpr (C::EARLY) __builtin_amdgcn_s_barrier();  // block requests first
 #pragma unroll
     for (int cb = 0; cb < NBUF; ++cb) issue(cb);
+    if constexpr (C::EARLY) lds_barrier_nodrain();  // phi(K) is in LDS
 #pragma unroll
     for (int cb = 0; cb < C::KPACK; ++cb) {
+      if constexpr (C::EARLY) update(cb);
 #pragma unroll
       for (int ks = 0; ks < C::KF; ++ks) sop[cb][ks] = convert(cb, ks);
       // Keep the refill below this block's conversion: otherwise the
@@ -298,6 +408,16 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
         asm volatile("" ::"v"(t.x), "v"(t.y), "v"(t.z), "v"(t.w) : "memory");
       }
       if (cb + NBUF < CB) issue(cb + NBUF);
+    }
+    if constexpr (C::EARLY) {
+      // The rest as it arrives (kept in fp32 for the readout), then the
+      // head area may take a P V.
+#pragma unroll
+      for (int cb = C::KPACK; cb < CB; ++cb) {
+        update(cb);
+        if (cb + NBUF < CB) issue(cb + NBUF);
+      }
+      lds_barrier_nodrain();
     }
   } else {
     // ---------------- block wave ----------------
@@ -368,6 +488,10 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
 #pragma unroll
     for (int rn = 0; rn < RUNS; ++rn)
       zr[rn] = *reinterpret_cast<const f32x4*>(zh + C::feature(rn * 4, quad));
+    // Early commit: the state waves wait for phi(K), which needs these
+    // loads first; a plain barrier (no fence, no wait) holds their stream
+    // until the block waves' requests are queued ahead of it.
+    if constexpr (C::EARLY) __builtin_amdgcn_s_barrier();
     const float lw = log_sigmoid(alpha_h);
     if constexpr (C::DMA_QK) {
       // The copies are counted by vmcnt alone and the compiler does not
@@ -376,10 +500,7 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
 #pragma unroll
       for (int r = 0; r < 2; ++r)
 #pragma unroll
-        for (int ks = 0; ks < C::KD; ++ks) {
-          qop[r][ks] = staged_op(qst, r * 16 + c16, quad + 4 * ks);
-          kop[r][ks] = staged_op(kst, r * 16 + c16, quad + 4 * ks);
-        }
+        for (int ks = 0; ks < C::KD; ++ks) kop[r][ks] = staged_op(kst, r * 16 + c16, quad + 4 * ks);
       if constexpr (C::DMA_W) {
 #pragma unroll
         for (int fb = 0; fb < FB; ++fb)
@@ -387,6 +508,35 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
           for (int ks = 0; ks < C::KD; ++ks)
             wop[fb][ks] = staged_op(wst, fb * 16 + c16, quad + 4 * ks);
       }
+    }
+    if constexpr (C::EARLY) {
+      // phi(K) for the commit, over the K rows just read (Q is read after
+      // it, to keep registers free); z takes the sum of the same values
+      // (z_old is in zr: lane (c16, quad) holds features fbk*16 + quad*4 + r);
+      // then the state waves may start.
+      float zs[C::NFB];
+      op_t* const pkh = reinterpret_cast<op_t*>(kst);
+      op_t* const pkl = reinterpret_cast<op_t*>(&sh.hd[w]);
+      phi_k(std::integral_constant<int, 2>{}, zs, [&](int fbk, int part, int, op_t x) {
+        (part == 0 ? pkh : pkl)[fbk * kWave + lane] = x;
+      });
+      if (slot_ok) {
+        float* __restrict__ zw = const_cast<float*>(a.z) + sbase * f;
+#pragma unroll
+        for (int fbk = 0; fbk < C::NFB; ++fbk) {
+          f32x4 zn;
+#pragma unroll
+          for (int r = 0; r < 4; ++r) zn[r] = zr[fbk][r] + __shfl(zs[fbk], quad * 4 + r);
+          if (c16 == 0) *reinterpret_cast<f32x4*>(zw + fbk * 16 + quad * 4) = zn;
+        }
+      }
+      lds_barrier_nodrain();
+    }
+    if constexpr (C::DMA_QK) {
+#pragma unroll
+      for (int r = 0; r < 2; ++r)
+#pragma unroll
+        for (int ks = 0; ks < C::KD; ++ks) qop[r][ks] = staged_op(qst, r * 16 + c16, quad + 4 * ks);
     }
 
     // 2. Without the staged copies: V^T of the KV head into this wave's LDS
@@ -499,7 +649,9 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
         sh.wl[w].phib[qb][ks][lane] = cvt_op<T>(&phi[ks * E]);
     }
 
-    // 6. a P V into accumulators, then over this wave's head area.
+    // 6. a P V into accumulators, then over this wave's head area (with
+    //    the early commit, once the state wave is done with phi(K)).
+    if constexpr (C::EARLY) lds_barrier_nodrain();
     f32x4 acc[CB][QB];
 #pragma unroll
     for (int cbk = 0; cbk < CB; ++cbk) {
@@ -518,7 +670,10 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) sh.hd[w].apv[cbk][qb][lane] = acc[cbk][qb];
   }
-  lds_barrier();
+  if constexpr (C::EARLY)
+    lds_barrier_nodrain();
+  else
+    lds_barrier();
 
   const bool of32 = sizeof(T) == 4 || a.s.out_f32;
   if (state_wave) {
@@ -545,7 +700,7 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
           for (int qb = 0; qb < QB; ++qb)
             acc[h2][qb] = M::mma(sa, phib[qb][ks], acc[h2][qb]);
         }
-        if (cbk >= C::KPACK && cbk + NBUF < CB) issue(cbk + NBUF);
+        if (!C::EARLY && cbk >= C::KPACK && cbk + NBUF < CB) issue(cbk + NBUF);
       }
       // The lane holds query qb*16 + c16 and the 8 consecutive columns
       // 32 pr + 8 quad .. +7 (see column()); they go to the pair's staging
@@ -603,7 +758,7 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
   //    rn*16 + quad*4 .. +3 of column column(cb, c16), the accumulator layout
   //    of the 16 x 16 tile (features rn*16 .., columns of cb).  The step above
   //    used the state as it was.
-  if constexpr (CM) {
+  if constexpr (CM && !C::EARLY) {
     if (state_wave && slot_ok) {
       static_assert(RUNS == C::NFB, "one state run per 16-feature block");
       {
@@ -623,73 +778,9 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
           for (int ks = 0; ks < C::KD; ++ks) wop[fb][ks] = load_op<T>(wrow + ks * KW);
         }
       }
-      float ph[2][KB][FB][4];  // [sign][kb][fb][r]
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-        for (int fb = 0; fb < FB; ++fb) {
-          f32x4 acc = {};
-#pragma unroll
-          for (int ks = 0; ks < C::KD; ++ks) acc = M::mma(kop[kb][ks], wop[fb][ks], acc);
-#pragma unroll
-          for (int r = 0; r < 4; ++r) ph[0][kb][fb][r] = acc[r];
-        }
-#pragma unroll
-      for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          float mx = -INFINITY, mn = INFINITY;
-#pragma unroll
-          for (int fb = 0; fb < FB; ++fb) {
-            mx = fmaxf(mx, ph[0][kb][fb][r]);
-            mn = fminf(mn, ph[0][kb][fb][r]);
-          }
-          mx = rmax16(mx);
-          mn = rmin16(mn);
-          float sp = 0.0f, sn = 0.0f;
-#pragma unroll
-          for (int fb = 0; fb < FB; ++fb) {
-            const float u = ph[0][kb][fb][r];
-            ph[0][kb][fb][r] = fast_exp(u - mx);
-            ph[1][kb][fb][r] = fast_exp(mn - u);
-            sp += ph[0][kb][fb][r];
-            sn += ph[1][kb][fb][r];
-          }
-          const bool kv = kb * 16 + quad * 4 + r < L;
-          const float ip = kv ? 1.0f / rsum16(sp) : 0.0f, in = kv ? 1.0f / rsum16(sn) : 0.0f;
-#pragma unroll
-          for (int fb = 0; fb < FB; ++fb) {
-            ph[0][kb][fb][r] *= ip;
-            ph[1][kb][fb][r] *= in;
-          }
-        }
       float zs[C::NFB];
-#pragma unroll
-      for (int fbk = 0; fbk < C::NFB; ++fbk) {
-        const int sg = fbk / FB, fb = fbk % FB;
-        zs[fbk] = 0.0f;
-#pragma unroll
-        for (int ks = 0; ks < C::KL; ++ks) {
-          float x[E], lo[E];
-#pragma unroll
-          for (int e = 0; e < E; ++e) {
-            const int j = ks * E + e;  // key(j, quad)
-            x[e] = ph[sg][j / 4][fb][j % 4];
-          }
-          pk[fbk][ks] = cvt_op<T>(x);
-#pragma unroll
-          for (int e = 0; e < E; ++e) {
-            lo[e] = x[e] - as_operand<T>(x[e]);
-            zs[fbk] += as_operand<T>(x[e]);
-          }
-          if constexpr (C::NPART == 2) {
-            pk[fbk][C::KL + ks] = cvt_op<T>(lo);
-#pragma unroll
-            for (int e = 0; e < E; ++e) zs[fbk] += as_operand<T>(lo[e]);
-          }
-        }
-        zs[fbk] = qsum(zs[fbk]);  // feature fbk*16 + c16, in every quarter
-      }
+      phi_k(std::integral_constant<int, C::NPART>{}, zs,
+            [&](int fbk, int part, int ks, op_t x) { pk[fbk][part * C::KL + ks] = x; });
       // z: lanes c16 == 0 write 16 bytes per 16-feature block.
       {
         float* __restrict__ zw = const_cast<float*>(a.z) + sbase * f;
