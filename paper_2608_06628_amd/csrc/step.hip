@@ -126,6 +126,9 @@ struct StepCfg {
   // second pass after the outputs.
   static constexpr bool EARLY = CM && DMA_QK && f <= D;
   static_assert(!EARLY || f * 64 <= (int)sizeof(HeadLds), "phi(K) lo parts in the head area");
+  // Column blocks held as bf16 readout operands: KPACK, or all of them with
+  // the early commit (each is updated and converted as it arrives).
+  static constexpr int NPACK = EARLY ? CB : KPACK;
   struct alignas(16) SmemBase {
     HeadLds hd[NW];  // W_h rows (staged), then V^T, then a P V and outputs
     WaveLds wl[NW];
@@ -180,6 +183,19 @@ __device__ inline f32x4 mma16_split_b(typename Mma16<T>::op_t a, const float* x,
     acc = M::mma(a, cvt_op<T>(lo), acc);
   }
   return acc;
+}
+
+// Element e of an MFMA operand set from an fp32 value (rounded to the
+// operand type).
+template <typename T>
+__device__ inline void set_elem(typename Mma16<T>::op_t& o, int e, float x);
+template <>
+__device__ inline void set_elem<bf16>(bf16x8& o, int e, float x) {
+  o[e] = (bf16)x;
+}
+template <>
+__device__ inline void set_elem<float>(float& o, int, float x) {
+  o = x;
 }
 
 __device__ inline float qmax(float x) {  // max over the 4 lane quarters
@@ -286,80 +302,71 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
 
   // phi(K) of the block keys from kop, wop: U_K = K W_h^T puts feature
   // fb*16 + c16 of keys kb*16 + quad*4 + r in lane (c16, quad), which is the
-  // A-operand layout of phi(K)^T V (keys in the order key(j, quad)).  Each
-  // key's softmax over the features of a sign reduces across the 16 lanes of
-  // its quarter; padding keys get phi = 0.  The operand parts of 16-feature
-  // block fbk and key step ks (bf16 hi, + lo when NP = 2) go to
-  // sink(fbk, part, ks, operand); zs[fbk] sums the same rounded values over
-  // the block keys (feature fbk*16 + c16, in every quarter).
+  // A-operand layout of phi(K)^T V (keys in the order key(j, quad): j =
+  // kb*4 + r).  Each key's softmax over the features of a sign reduces
+  // across the 16 lanes of its quarter; padding keys get phi = 0.  One
+  // 16-key half kb at a time, the four values of 16-feature block fbk go to
+  // sink(fbk, part, kb, x4) as part 0 (to be rounded to the operand type)
+  // and, when NP = 2, part 1 (the bf16 rounding remainder); zs[fbk] sums the
+  // rounded parts over the block keys (feature fbk*16 + c16, every quarter).
   auto phi_k = [&](auto np, float* zs, auto&& sink) {
     constexpr int NP = decltype(np)::value;
-    float ph[2][KB][FB][4];  // [sign][kb][fb][r]
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb)
+    for (int fbk = 0; fbk < C::NFB; ++fbk) zs[fbk] = 0.0f;
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      float ph[2][FB][4];  // [sign][fb][r]
 #pragma unroll
       for (int fb = 0; fb < FB; ++fb) {
         f32x4 acc = {};
 #pragma unroll
         for (int ks = 0; ks < C::KD; ++ks) acc = M::mma(kop[kb][ks], wop[fb][ks], acc);
 #pragma unroll
-        for (int r = 0; r < 4; ++r) ph[0][kb][fb][r] = acc[r];
+        for (int r = 0; r < 4; ++r) ph[0][fb][r] = acc[r];
       }
-#pragma unroll
-    for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         float mx = -INFINITY, mn = INFINITY;
 #pragma unroll
         for (int fb = 0; fb < FB; ++fb) {
-          mx = fmaxf(mx, ph[0][kb][fb][r]);
-          mn = fminf(mn, ph[0][kb][fb][r]);
+          mx = fmaxf(mx, ph[0][fb][r]);
+          mn = fminf(mn, ph[0][fb][r]);
         }
         mx = rmax16(mx);
         mn = rmin16(mn);
         float sp = 0.0f, sn = 0.0f;
 #pragma unroll
         for (int fb = 0; fb < FB; ++fb) {
-          const float u = ph[0][kb][fb][r];
-          ph[0][kb][fb][r] = fast_exp(u - mx);
-          ph[1][kb][fb][r] = fast_exp(mn - u);
-          sp += ph[0][kb][fb][r];
-          sn += ph[1][kb][fb][r];
+          const float u = ph[0][fb][r];
+          ph[0][fb][r] = fast_exp(u - mx);
+          ph[1][fb][r] = fast_exp(mn - u);
+          sp += ph[0][fb][r];
+          sn += ph[1][fb][r];
         }
         const bool kv = kb * 16 + quad * 4 + r < L;
         const float ip = kv ? 1.0f / rsum16(sp) : 0.0f, in = kv ? 1.0f / rsum16(sn) : 0.0f;
 #pragma unroll
         for (int fb = 0; fb < FB; ++fb) {
-          ph[0][kb][fb][r] *= ip;
-          ph[1][kb][fb][r] *= in;
+          ph[0][fb][r] *= ip;
+          ph[1][fb][r] *= in;
         }
       }
 #pragma unroll
-    for (int fbk = 0; fbk < C::NFB; ++fbk) {
-      const int sg = fbk / FB, fb = fbk % FB;
-      zs[fbk] = 0.0f;
+      for (int fbk = 0; fbk < C::NFB; ++fbk) {
+        const float* x = ph[fbk / FB][fbk % FB];
+        float lo[4];
 #pragma unroll
-      for (int ks = 0; ks < C::KL; ++ks) {
-        float x[E], lo[E];
-#pragma unroll
-        for (int e = 0; e < E; ++e) {
-          const int j = ks * E + e;  // key(j, quad)
-          x[e] = ph[sg][j / 4][fb][j % 4];
+        for (int r = 0; r < 4; ++r) {
+          lo[r] = x[r] - as_operand<T>(x[r]);
+          zs[fbk] += as_operand<T>(x[r]);
+          if constexpr (NP == 2) zs[fbk] += as_operand<T>(lo[r]);
         }
-        sink(fbk, 0, ks, cvt_op<T>(x));
-#pragma unroll
-        for (int e = 0; e < E; ++e) {
-          lo[e] = x[e] - as_operand<T>(x[e]);
-          zs[fbk] += as_operand<T>(x[e]);
-        }
-        if constexpr (NP == 2) {
-          sink(fbk, 1, ks, cvt_op<T>(lo));
-#pragma unroll
-          for (int e = 0; e < E; ++e) zs[fbk] += as_operand<T>(lo[e]);
-        }
+        sink(fbk, 0, kb, x);
+        if constexpr (NP == 2) sink(fbk, 1, kb, lo);
       }
-      zs[fbk] = qsum(zs[fbk]);  // feature fbk*16 + c16, in every quarter
     }
+#pragma unroll
+    for (int fbk = 0; fbk < C::NFB; ++fbk) zs[fbk] = qsum(zs[fbk]);
   };
 
   // EARLY commit of column block cb (fp32 state in buf): S^T of the block
@@ -382,7 +389,7 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
   };
 
   // Column blocks 0 .. KPACK-1 as bf16 operands (S^T A operands).
-  op_t sop[C::KPACK > 0 ? C::KPACK : 1][C::KF];
+  op_t sop[C::NPACK > 0 ? C::NPACK : 1][C::KF];
   auto convert = [&](int cb, int ks) {
     float sv[E];
 #pragma unroll
@@ -410,11 +417,12 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
       if (cb + NBUF < CB) issue(cb + NBUF);
     }
     if constexpr (C::EARLY) {
-      // The rest as it arrives (kept in fp32 for the readout), then the
-      // head area may take a P V.
+      // The rest as it arrives, then the head area may take a P V.
 #pragma unroll
       for (int cb = C::KPACK; cb < CB; ++cb) {
         update(cb);
+#pragma unroll
+        for (int ks = 0; ks < C::KF; ++ks) sop[cb][ks] = convert(cb, ks);
         if (cb + NBUF < CB) issue(cb + NBUF);
       }
       lds_barrier_nodrain();
@@ -517,8 +525,11 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
       float zs[C::NFB];
       op_t* const pkh = reinterpret_cast<op_t*>(kst);
       op_t* const pkl = reinterpret_cast<op_t*>(&sh.hd[w]);
-      phi_k(std::integral_constant<int, 2>{}, zs, [&](int fbk, int part, int, op_t x) {
-        (part == 0 ? pkh : pkl)[fbk * kWave + lane] = x;
+      phi_k(std::integral_constant<int, 2>{}, zs, [&](int fbk, int part, int kb, const float* x4) {
+        typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+        const bf16x4_t v{(bf16)x4[0], (bf16)x4[1], (bf16)x4[2], (bf16)x4[3]};
+        *reinterpret_cast<bf16x4_t*>(reinterpret_cast<char*>(part == 0 ? pkh : pkl) +
+                                     (fbk * kWave + lane) * 16 + kb * 8) = v;
       });
       if (slot_ok) {
         float* __restrict__ zw = const_cast<float*>(a.z) + sbase * f;
@@ -695,7 +706,7 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
         for (int qb = 0; qb < QB; ++qb) acc[h2][qb] = sh.hd[w].apv[cbk][qb][lane];
 #pragma unroll
         for (int ks = 0; ks < C::KF; ++ks) {
-          const op_t sa = cbk < C::KPACK ? sop[cbk < C::KPACK ? cbk : 0][ks] : convert(cbk, ks);
+          const op_t sa = cbk < C::NPACK ? sop[cbk < C::NPACK ? cbk : 0][ks] : convert(cbk, ks);
 #pragma unroll
           for (int qb = 0; qb < QB; ++qb)
             acc[h2][qb] = M::mma(sa, phib[qb][ks], acc[h2][qb]);
@@ -779,8 +790,13 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
         }
       }
       float zs[C::NFB];
-      phi_k(std::integral_constant<int, C::NPART>{}, zs,
-            [&](int fbk, int part, int ks, op_t x) { pk[fbk][part * C::KL + ks] = x; });
+      phi_k(std::integral_constant<int, C::NPART>{}, zs, [&](int fbk, int part, int kb, const float* x4) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int j = kb * 4 + r;  // key(j, quad): operand step j / E, element j % E
+          set_elem<T>(pk[fbk][part * C::KL + j / E], j % E, x4[r]);
+        }
+      });
       // z: lanes c16 == 0 write 16 bytes per 16-feature block.
       {
         float* __restrict__ zw = const_cast<float*>(a.z) + sbase * f;
