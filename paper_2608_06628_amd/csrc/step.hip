@@ -210,21 +210,35 @@ __device__ inline float qsum(float x) {
   x += xor16(x);
   return x + xor32(x);
 }
-// max / min / sum over the 16 lanes of a lane quarter (lanes c16 = 0..15).
+// max / min / sum over the 16 lanes of a lane quarter (a DPP row, lanes
+// c16 = 0..15), on the VALU: swap neighbours, then pairs (quad
+// permutations), then combine the two quads of each half-row (half-row
+// mirror) and the two halves of the row (row mirror); every lane ends with
+// the whole row's result.
+template <int CTRL>
+__device__ inline float dpp(float x) {
+  return __builtin_bit_cast(
+      float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), CTRL, 0xF, 0xF, false));
+}
+constexpr int kDppSwap1 = 0xB1;       // quad_perm [1, 0, 3, 2]
+constexpr int kDppSwap2 = 0x4E;       // quad_perm [2, 3, 0, 1]
+constexpr int kDppHalfMirror = 0x141;  // row_half_mirror
+constexpr int kDppMirror = 0x140;      // row_mirror
+template <typename Op>
+__device__ inline float row_reduce16(float x, Op op) {
+  x = op(x, dpp<kDppSwap1>(x));
+  x = op(x, dpp<kDppSwap2>(x));
+  x = op(x, dpp<kDppHalfMirror>(x));
+  return op(x, dpp<kDppMirror>(x));
+}
 __device__ inline float rmax16(float x) {
-#pragma unroll
-  for (int m = 1; m < 16; m *= 2) x = fmaxf(x, __shfl_xor(x, m));
-  return x;
+  return row_reduce16(x, [](float a, float b) { return fmaxf(a, b); });
 }
 __device__ inline float rmin16(float x) {
-#pragma unroll
-  for (int m = 1; m < 16; m *= 2) x = fminf(x, __shfl_xor(x, m));
-  return x;
+  return row_reduce16(x, [](float a, float b) { return fminf(a, b); });
 }
 __device__ inline float rsum16(float x) {
-#pragma unroll
-  for (int m = 1; m < 16; m *= 2) x += __shfl_xor(x, m);
-  return x;
+  return row_reduce16(x, [](float a, float b) { return a + b; });
 }
 
 template <typename T, int D, int F, int NW, bool CM>
@@ -343,8 +357,9 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
           sp += ph[0][fb][r];
           sn += ph[1][fb][r];
         }
-        const bool kv = kb * 16 + quad * 4 + r < L;
-        const float ip = kv ? 1.0f / rsum16(sp) : 0.0f, in = kv ? 1.0f / rsum16(sn) : 0.0f;
+        // Branch-free: every lane of the row takes part in the reductions.
+        const float kv = kb * 16 + quad * 4 + r < L ? 1.0f : 0.0f;
+        const float ip = kv / rsum16(sp), in = kv / rsum16(sn);
 #pragma unroll
         for (int fb = 0; fb < FB; ++fb) {
           ph[0][fb][r] *= ip;
