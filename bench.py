@@ -43,7 +43,7 @@ HBM_PEAK_GBPS = 8000.0
 # the step kernel's sources: after any change the entry no longer matches and
 # the bench reports the traffic as unknown until the counters are read again.
 STEP_TRAFFIC = {
-    "818dbc6769123aa9fa6d1e7cad94d165c70fd124336f8e411719b871ad397c63": {"read": 40329.77 * 1024 * 2.0, "written": 8192.0 * 1024 * 1.0},
+    "6af3d037a6332b919f3103837da06865431f0b753327129de6777f02cb157ce7": {"read": 40342.53 * 1024 * 2.0, "written": 8192.0 * 1024 * 1.0},
 }
 STEP_SOURCES = ("csrc/step.hip", "csrc/device.h", "csrc/launch.h")
 
@@ -84,6 +84,12 @@ def commit_bytes(B, Hq, Hkv, d, L, f, es=2):
     z = 2 * B * Hq * f * 4
     W = Hq * F * d * es
     return kv + S + z + W
+
+
+def step_commit_bytes(B, Hq, Hkv, d, L, f, es=2):
+    """Algorithmic bytes of one hybrid_attn_step_commit launch: the step's,
+    plus S and z written once."""
+    return step_bytes(B, Hq, Hkv, d, L, f, es) + B * Hq * f * d * 4 + B * Hq * f * 4
 
 
 def step_flops(B, Hq, d, L, f):
@@ -192,14 +198,18 @@ def run(args):
 
     phases = []  # (kind, start event, end event, launches between them)
 
-    def cycle(record):
-        # The R*NSTEP step launches, then the R commits, each phase bracketed
-        # by one event pair on the launch stream: launches inside a phase run
-        # back to back, so elapsed / launches is the per-launch duration.
+    def cycle(record, fused=True):
+        # A block cycle: NSTEP denoising steps on each of the R lanes, the
+        # last one fused with the block's commit (hybrid_attn_step_commit,
+        # one launch) -- or, with fused=False, NSTEP steps then R separate
+        # commits of the same keys and values (the same outputs and states).
+        # Each phase is bracketed by one event pair on the launch stream:
+        # launches inside a phase run back to back, so elapsed / launches is
+        # the per-launch duration.
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)] if record else None
         if record:
             ev[0].record()
-        for s in range(NSTEP):
+        for s in range(NSTEP - 1 if fused else NSTEP):
             for ln in lanes:
                 q, k, v, o = ln.qkv[s]
                 hb.hybrid_attn_step(q, k, v, W, alpha, ln.S, ln.z, out=o)
@@ -207,44 +217,63 @@ def run(args):
             ev[1].record()
         for ln in lanes:
             q, k, v, o = ln.qkv[NSTEP - 1]
-            hb.hybrid_state_commit(k, v, W, ln.S, ln.z)
+            if fused:
+                hb.hybrid_attn_step_commit(q, k, v, W, alpha, ln.S, ln.z, out=o)
+            else:
+                hb.hybrid_state_commit(k, v, W, ln.S, ln.z)
         if record:
             ev[2].record()
-            phases.append(("step", ev[0], ev[1], NSTEP * len(lanes)))
-            phases.append(("commit", ev[1], ev[2], len(lanes)))
+            phases.append(("step", ev[0], ev[1], (NSTEP - 1 if fused else NSTEP) * len(lanes)))
+            phases.append(("step_commit" if fused else "commit", ev[1], ev[2], len(lanes)))
+
+    def timed_cycles(fused):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        a.record()
+        for _ in range(args.steps):
+            cycle(False, fused)
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / args.steps
 
     for _ in range(args.warmup):
         cycle(False)
     torch.cuda.synchronize()
     log(f"warmup done ({args.warmup} cycles); timing {args.steps} cycles")
     # Whole-cycle time without per-kernel events.
-    a = torch.cuda.Event(enable_timing=True)
-    b = torch.cuda.Event(enable_timing=True)
-    torch.cuda.synchronize()
-    a.record()
-    for _ in range(args.steps):
-        cycle(False)
-    b.record()
-    torch.cuda.synchronize()
-    ms_cycle = a.elapsed_time(b) / args.steps
+    ms_cycle = timed_cycles(True)
     # Per-kernel durations: one event pair per phase of each cycle.
     for _ in range(args.steps):
         cycle(True)
     torch.cuda.synchronize()
-    durs = {"step": [], "commit": []}
+    durs = {"step": [], "step_commit": [], "commit": []}
     for kind, e0, e1, n in phases:
         durs[kind].append(e0.elapsed_time(e1) / n)
+    # The same cycle with a separate commit launch, for comparison.
+    phases.clear()
+    ms_cycle_sep = timed_cycles(False)
+    for _ in range(args.steps):
+        cycle(True, False)
+    torch.cuda.synchronize()
+    for kind, e0, e1, n in phases:
+        if kind == "commit":
+            durs[kind].append(e0.elapsed_time(e1) / n)
     t_step = float(np.mean(durs["step"])) * 1e-3
+    t_fused = float(np.mean(durs["step_commit"])) * 1e-3
     t_commit = float(np.mean(durs["commit"])) * 1e-3
     sb = step_bytes(B, Hq, Hkv, d, L, f)
     tr = STEP_TRAFFIC.get(step_source_hash())
     traffic = None if tr is None else tr["read"] + tr["written"]
     cb = commit_bytes(B, Hq, Hkv, d, L, f)
+    fb = step_commit_bytes(B, Hq, Hkv, d, L, f)
     step_gbps = sb / t_step / 1e9
     commit_gbps = cb / t_commit / 1e9
+    fused_gbps = fb / t_fused / 1e9
     for ln in lanes:
         assert torch.isfinite(ln.qkv[0][3].float()).all(), "non-finite step output"
-    log(f"cycle {ms_cycle:.3f} ms; step {t_step * 1e6:.2f} us ({step_gbps:.0f} GB/s); "
+    log(f"cycle {ms_cycle:.3f} ms (separate commit: {ms_cycle_sep:.3f} ms); step {t_step * 1e6:.2f} us "
+        f"({step_gbps:.0f} GB/s); step+commit {t_fused * 1e6:.2f} us ({fused_gbps:.0f} GB/s); "
         f"commit {t_commit * 1e6:.2f} us ({commit_gbps:.0f} GB/s)")
 
     tokens = NSTEP * R * B * L
@@ -255,7 +284,8 @@ def run(args):
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16", "data": "synthetic",
         "config": {"workload": "serve64: B=64 requests, Hq=16, Hkv=4, d=128, block 32, f=128, "
-                               "prefixes 1k-32k tokens, 8 denoising steps then 1 commit",
+                               "prefixes 1k-32k tokens, 8 denoising steps per block, the last fused "
+                               "with the block's commit",
                    "global_batch": B, "seq_len": L, "lanes": R, "parallelism": "none (1 GPU)",
                    "state_dtype": "fp32", "prefix_tokens": int(plens.sum())},
         "roofline": {"bound": "hbm", "achieved": step_gbps, "peak": HBM_PEAK_GBPS,
@@ -267,8 +297,12 @@ def run(args):
                         "max_cycle_mean_us": float(np.max(durs["step"])) * 1e3,
                         "gbps": step_gbps, "tokens_per_s": B * L / t_step,
                         "tflops": step_flops(B, Hq, d, L, f) / t_step / 1e12},
-        "commit_kernel": {"mean_us": t_commit * 1e6, "gbps": commit_gbps,
-                          "bytes_per_launch": cb, "frac": commit_gbps / HBM_PEAK_GBPS},
+        "step_commit_kernel": {"mean_us": t_fused * 1e6, "gbps": fused_gbps,
+                               "bytes_per_launch": fb, "frac": fused_gbps / HBM_PEAK_GBPS},
+        "separate_commit": {"ms_per_cycle": ms_cycle_sep,
+                            "tokens_per_s": NSTEP * R * B * L / (ms_cycle_sep * 1e-3),
+                            "commit_mean_us": t_commit * 1e6, "commit_gbps": commit_gbps,
+                            "commit_bytes_per_launch": cb, "commit_frac": commit_gbps / HBM_PEAK_GBPS},
     }
     del lanes
     torch.cuda.empty_cache()

@@ -71,6 +71,31 @@ def test_serve64_step_and_commit_sampled():
     assert_close(z1 - z[s], zr - z[s], "bf16", f"serve64 commit dz, requests {sample}")
 
 
+def test_serve64_step_commit_sampled():
+    """B=64 fused step+commit (the last denoising pass of a block in the
+    bench's cycle): outputs on the old state, then the committed state."""
+    dims = synth.SERVE64
+    B = dims.B
+    sc = 1.0 / math.sqrt(dims.d)
+    q = synth.device_gaussian((B, dims.L, dims.Hq, dims.d), 441, sc)
+    k = synth.device_gaussian((B, dims.L, dims.Hkv, dims.d), 442, sc)
+    v = synth.device_gaussian((B, dims.L, dims.Hkv, dims.d), 443, sc)
+    Wt, alpha = synth.feature_weights(dims, 442, 443)
+    S, z = _states(dims, B, 64, 441)
+    Sd, zd = state_dev(S), f32(z)
+    announce("serve64: step_commit B=64")
+    o32 = hb.hybrid_attn_step_commit(q, k, v, act(Wt, "bf16"), f32(alpha), Sd, zd, out_f32=True)
+    torch.cuda.synchronize()
+    assert torch.isfinite(o32).all()
+    sample = [0, 31, 63]
+    s = np.array(sample)
+    ref_out, Sr, zr = oracle.step_commit(_bf16_host(q[s]), _bf16_host(k[s]), _bf16_host(v[s]),
+                                         Wt, alpha, S[s], z[s])
+    assert_close(host(o32[s]), ref_out, "bf16", f"serve64 step_commit out, requests {sample}")
+    assert_close(state_host(Sd)[s] - S[s], Sr - S[s], "bf16", f"serve64 step_commit dS {sample}")
+    assert_close(host(zd)[s] - z[s], zr - z[s], "bf16", f"serve64 step_commit dz {sample}")
+
+
 def test_mix128_hybrid_step_sampled():
     """B=128 hybrid step (the hybrid side of the mix128 comparison)."""
     _step_sampled(synth.MIX128, 411, [0, 77, 127], "mix128")
