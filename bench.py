@@ -310,6 +310,7 @@ def run(args):
     if not args.no_extras:
         result["prefill"] = bench_prefill(gen, dev)
         result["softmax_prefix"] = bench_mix(gen, dev)
+        result["table3"] = bench_table3(gen, dev)
     if not args.no_cpu_baseline:
         log("timing the fp64 oracle on the host cores")
         result["cpu_baseline"] = cpu_baseline(dims, args.cpu_requests, plens)
@@ -443,6 +444,95 @@ def bench_mix(gen, dev):
             "mix_6h14s_vs_20s": (20 * ms_sm) / (6 * ms_hy + 14 * ms_sm)}
 
 
+# Per-block kernel latency against prefix length, after the paper's
+# appendix microbenchmark (Table 3): one 32-token block forward of B requests
+# with P tokens of context; the paper's H200 numbers are context only.
+TABLE3_P = (0, 256, 1024, 4096, 8192, 16384, 32768)
+TABLE3_B = (8, 32)
+PAPER_TABLE3_MS = {  # (B, P): (teacher, hybrid), one H200, median of 20
+    (8, 0): (0.090, 0.070), (8, 256): (0.097, 0.069), (8, 1024): (0.136, 0.068),
+    (8, 4096): (0.342, 0.069), (8, 8192): (0.601, 0.070), (8, 16384): (1.108, 0.069),
+    (8, 32768): (2.123, 0.069),
+    (32, 0): (0.094, 0.101), (32, 256): (0.147, 0.100), (32, 1024): (0.319, 0.103),
+    (32, 4096): (1.114, 0.101), (32, 8192): (2.150, 0.103), (32, 16384): (4.204, 0.101),
+    (32, 32768): (8.299, 0.103),
+}
+COLD_BYTES = 384 << 20  # more than the 256 MB memory-side cache
+
+
+def median_ms(fn, n=20, warm=3):
+    """Median of n individually timed calls (HIP events around each)."""
+    for _ in range(warm):
+        fn()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(n)]
+    for a, b in ev:
+        a.record()
+        fn()
+        b.record()
+    torch.cuda.synchronize()
+    return float(np.median([a.elapsed_time(b) for a, b in ev]))
+
+
+def bench_table3(gen, dev):
+    """Hybrid step vs exact softmax over the KV cache, P x B, each timed call
+    on inputs no earlier call has touched recently (copies rotate past the
+    memory-side cache)."""
+    dims0 = synth.SERVE64
+    Hq, Hkv, d, L, f = dims0.Hq, dims0.Hkv, dims0.d, dims0.L, dims0.f
+    scale = 1.0 / math.sqrt(d)
+    Wt, alpha = synth.feature_weights(dims0, 1, 2)
+    W = torch.from_numpy(Wt).to(dev).to(torch.bfloat16)
+    al = torch.from_numpy(alpha).to(dev)
+    rnd = lambda shape: (torch.randn(shape, generator=gen, device=dev) * scale).to(torch.bfloat16)
+    rows = []
+    for B in TABLE3_B:
+        qkv = (rnd((B, L, Hq, d)), rnd((B, L, Hkv, d)), rnd((B, L, Hkv, d)))
+        out = torch.empty_like(qkv[0])
+        n_st = -(-COLD_BYTES // (B * Hq * f * d * 4))
+        states = [(torch.rand((B, Hq, d, f), generator=gen, device=dev) * 0.01,
+                   torch.rand((B, Hq, f), generator=gen, device=dev) + 1.0) for _ in range(n_st)]
+        for P in TABLE3_P:
+            kv_bytes = 2 * B * max(P, 1) * Hkv * d * 2
+            n_kv = min(128, -(-COLD_BYTES // kv_bytes))
+            caches = [(rnd((B, max(P, 1), Hkv, d)), rnd((B, max(P, 1), Hkv, d))) for _ in range(n_kv)]
+            plen = torch.full((B,), P, dtype=torch.int32, device=dev)
+            ws = torch.empty(max(1, hb.workspace_bytes(hb.make_dims(B, Hq, Hkv, d, L, 64, hb.HYB_BF16, 1),
+                                                       hb.OP_SOFTMAX_PREFIX, max(P, 1))),
+                             dtype=torch.uint8, device=dev)
+            it = [0]
+
+            def sm():
+                kc, vc = caches[it[0] % n_kv]
+                it[0] += 1
+                hb.softmax_prefix_step(*qkv, kc, vc, plen, out=out, ws=ws)
+
+            def hy():
+                S, z = states[it[0] % n_st]
+                it[0] += 1
+                hb.hybrid_attn_step(*qkv, W, al, S, z, out=out)
+
+            ms_sm, ms_hy = median_ms(sm), median_ms(hy)
+            del caches
+            torch.cuda.empty_cache()
+            pt, ph = PAPER_TABLE3_MS[(B, P)]
+            rows.append({"B": B, "P": P, "softmax_ms": ms_sm, "hybrid_ms": ms_hy,
+                         "speedup": ms_sm / ms_hy,
+                         # attention time of a 20-layer model with n hybrid layers
+                         "mix_6of20_vs_softmax": 20 * ms_sm / (6 * ms_hy + 14 * ms_sm),
+                         "mix_8of20_vs_softmax": 20 * ms_sm / (8 * ms_hy + 12 * ms_sm),
+                         "paper_h200_teacher_ms": pt, "paper_h200_hybrid_ms": ph,
+                         "paper_h200_speedup": pt / ph})
+            log(f"table3 B={B:2d} P={P:5d}: softmax {ms_sm * 1e3:8.1f} us, hybrid {ms_hy * 1e3:6.1f} us, "
+                f"x{ms_sm / ms_hy:.1f}")
+        del states
+        torch.cuda.empty_cache()
+    return {"workload": "Table 3 analogue: one 32-token block, 16q/4kv, d=128, f=128, bf16; "
+                        "median of 20 calls on cold inputs",
+            "rows": rows}
+
+
 def copy_calibration():
     """A plain device-to-device copy of a known size: 256 MiB read, 256 MiB
     written per launch.  Byte counters read on it give the scale factor that
@@ -465,6 +555,8 @@ def main():
     ap.add_argument("--cpu-requests", type=int, default=64)
     ap.add_argument("--no-extras", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--only-table3", action="store_true",
+                    help="run only the prefix-length x batch latency sweep and print it")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only copy 256 MiB device to device five times (the reference "
                          "kernel for scaling HBM byte counters), then exit")
@@ -476,6 +568,11 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.only_table3:
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(5)
+        print(json.dumps(bench_table3(gen, "cuda")), flush=True)
         return
     run(args)
 
