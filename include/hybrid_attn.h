@@ -36,6 +36,19 @@
  *                                      slot b.  A slot outside [0, n_slots)
  *                                      makes that request's outputs NaN and
  *                                      leaves every state untouched.
+ *   block_len     [B] int32 or NULL    active tokens of request b's block,
+ *                                      clamped to [0, L]; NULL means L for
+ *                                      every request.  Request b then acts
+ *                                      as a call with L = block_len[b] on
+ *                                      its first block_len[b] rows: its
+ *                                      later rows of q, k and v play no part
+ *                                      (their values may be anything, NaN
+ *                                      included) and its later rows of out
+ *                                      are not written.  0 makes the request
+ *                                      a no-op.  This serves a batch whose
+ *                                      requests sit in blocks of different
+ *                                      lengths, e.g. a prompt's last,
+ *                                      partial block.
  *   k_cache, v_cache [B][max_prefix][Hkv][d]; request b uses rows
  *                                      0 .. prefix_len[b]-1.
  *   Query head h reads KV head h / (Hq / Hkv).
@@ -52,7 +65,7 @@
  * Validation.  Every check below runs on the host before anything is
  *   enqueued.  On failure the call returns the status, enqueues nothing,
  *   touches no output and sets a message readable with hybrid_last_error().
- *   Values that live in device memory (slots, prefix_len) cannot be checked
+ *   Values that live in device memory (slots, block_len, prefix_len) cannot be checked
  *   on the host; the kernels clamp or mask them as documented per call.
  * Errors after launch.  HYB_ELAUNCH reports a failed kernel launch; outputs,
  *   and for commit/prefill the state, are then undefined.
@@ -108,12 +121,12 @@ typedef struct {
 /* One denoising step of the active block (Section 3.1: within-block
  * softmax branch, linear readout of the committed state, gated merge with a
  * shared normaliser).  Reads S and z, writes out.  q, k, v, W, alpha, S, z
- * and out are required; slots may be NULL.  out must not overlap an input.
- * Empty context (z = 0) gives plain block softmax. */
+ * and out are required; slots and block_len may be NULL.  out must not
+ * overlap an input.  Empty context (z = 0) gives plain block softmax. */
 int hybrid_attn_step(const hyb_dims_t* dims, const void* q, const void* k,
                      const void* v, const void* W, const float* alpha,
                      const float* S, const float* z, const int32_t* slots,
-                     void* out, void* stream);
+                     const int32_t* block_len, void* out, void* stream);
 
 /* The last denoising step of a block fused with its commit, in one launch
  * (the single kernel of Section 3.3: within-block softmax, readout, gated
@@ -127,15 +140,18 @@ int hybrid_attn_step(const hyb_dims_t* dims, const void* q, const void* k,
 int hybrid_attn_step_commit(const hyb_dims_t* dims, const void* q,
                             const void* k, const void* v, const void* W,
                             const float* alpha, float* S, float* z,
-                            const int32_t* slots, void* out, void* stream);
+                            const int32_t* slots, const int32_t* block_len,
+                            void* out, void* stream);
 
 /* Commit of a finished block (Section 3.1 state update):
- * S_h += sum_t phi_h(k_t) v_t^T and z_h += sum_t phi_h(k_t) over the L block
- * tokens, in place, for every request and query head.  Two requests of one
+ * S_h += sum_t phi_h(k_t) v_t^T and z_h += sum_t phi_h(k_t) over the block
+ * tokens (the first block_len[b] of request b; all L when block_len is
+ * NULL), in place, for every request and query head.  Two requests of one
  * call must not share a slot. */
 int hybrid_state_commit(const hyb_dims_t* dims, const void* k, const void* v,
                         const void* W, float* S, float* z,
-                        const int32_t* slots, void* stream);
+                        const int32_t* slots, const int32_t* block_len,
+                        void* stream);
 
 /* Block-causal prefill of seq_len tokens (Figure 2 pattern): the tokens are
  * cut into seq_len / L blocks; block c is answered against the state of the

@@ -54,9 +54,9 @@ def load():
     lib = ctypes.CDLL(LIB_PATH)
     vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
     P = ctypes.POINTER(Dims)
-    lib.hybrid_attn_step.argtypes = [P] + [vp] * 10
-    lib.hybrid_attn_step_commit.argtypes = [P] + [vp] * 10
-    lib.hybrid_state_commit.argtypes = [P] + [vp] * 7
+    lib.hybrid_attn_step.argtypes = [P] + [vp] * 11
+    lib.hybrid_attn_step_commit.argtypes = [P] + [vp] * 11
+    lib.hybrid_state_commit.argtypes = [P] + [vp] * 8
     lib.hybrid_state_prefill.argtypes = [P, i32] + [vp] * 10 + [sz, vp]
     lib.softmax_prefix_step.argtypes = [P] + [vp] * 6 + [i32, vp, vp, sz, vp]
     lib.hybrid_workspace_bytes.argtypes = [P, i32, i32]
@@ -118,10 +118,11 @@ def _out_flags(out, act, out_f32):
 
 
 def hybrid_attn_step(q, k, v, W, alpha, S, z, slots=None, out=None, out_f32=False,
-                     stream=None):
+                     stream=None, block_len=None):
     """q [B][L][Hq][d], k/v [B][L][Hkv][d], W [Hq][F][d], alpha [Hq] f32,
     S [n_slots][Hq][d][f] f32 (S_h transposed), z [n_slots][Hq][f] f32 -> out [B][L][Hq][d]
-    in q's dtype (fp32 with out_f32)."""
+    in q's dtype (fp32 with out_f32).  block_len [B] int32 (device): active rows
+    per request; rows past it of out are left as they were."""
     lib = load()
     B, L, Hq, d = q.shape
     act = q.dtype
@@ -133,12 +134,13 @@ def hybrid_attn_step(q, k, v, W, alpha, S, z, slots=None, out=None, out_f32=Fals
         ctypes.byref(dims), _ptr(q, "q"), _ptr(k, "k", act), _ptr(v, "v", act),
         _ptr(W, "W", act), _ptr(alpha, "alpha", torch.float32),
         _ptr(S, "S", torch.float32), _ptr(z, "z", torch.float32),
-        _ptr(slots, "slots", torch.int32), _ptr(out, "out", odt), _stream(stream)))
+        _ptr(slots, "slots", torch.int32), _ptr(block_len, "block_len", torch.int32),
+        _ptr(out, "out", odt), _stream(stream)))
     return out
 
 
 def hybrid_attn_step_commit(q, k, v, W, alpha, S, z, slots=None, out=None, out_f32=False,
-                            stream=None):
+                            stream=None, block_len=None):
     """The step of hybrid_attn_step on the state as it is, then the commit of
     k/v into S, z in place, in one launch; returns out."""
     lib = load()
@@ -152,11 +154,12 @@ def hybrid_attn_step_commit(q, k, v, W, alpha, S, z, slots=None, out=None, out_f
         ctypes.byref(dims), _ptr(q, "q"), _ptr(k, "k", act), _ptr(v, "v", act),
         _ptr(W, "W", act), _ptr(alpha, "alpha", torch.float32),
         _ptr(S, "S", torch.float32), _ptr(z, "z", torch.float32),
-        _ptr(slots, "slots", torch.int32), _ptr(out, "out", odt), _stream(stream)))
+        _ptr(slots, "slots", torch.int32), _ptr(block_len, "block_len", torch.int32),
+        _ptr(out, "out", odt), _stream(stream)))
     return out
 
 
-def hybrid_state_commit(k, v, W, S, z, slots=None, stream=None):
+def hybrid_state_commit(k, v, W, S, z, slots=None, stream=None, block_len=None):
     """Folds the block k/v [B][L][Hkv][d] into S, z in place."""
     lib = load()
     B, L, Hkv, d = k.shape
@@ -165,7 +168,8 @@ def hybrid_state_commit(k, v, W, S, z, slots=None, stream=None):
     _check(lib.hybrid_state_commit(
         ctypes.byref(dims), _ptr(k, "k"), _ptr(v, "v", act), _ptr(W, "W", act),
         _ptr(S, "S", torch.float32), _ptr(z, "z", torch.float32),
-        _ptr(slots, "slots", torch.int32), _stream(stream)))
+        _ptr(slots, "slots", torch.int32), _ptr(block_len, "block_len", torch.int32),
+        _stream(stream)))
 
 
 def workspace_bytes(dims: Dims, op: int, extent: int = 0) -> int:

@@ -101,7 +101,7 @@ extern "C" {
 int hybrid_attn_step(const hyb_dims_t* dims, const void* q, const void* k,
                      const void* v, const void* W, const float* alpha,
                      const float* S, const float* z, const int32_t* slots,
-                     void* out, void* stream) {
+                     const int32_t* block_len, void* out, void* stream) {
   hyb::Shape s;
   TRY(check_dims(dims, true, &s));
   if (s.B == 0) return ok();
@@ -113,6 +113,7 @@ int hybrid_attn_step(const hyb_dims_t* dims, const void* q, const void* k,
   TRY(check_ptr(S, "S"));
   TRY(check_ptr(z, "z"));
   TRY(check_ptr(slots, "slots", false));
+  TRY(check_ptr(block_len, "block_len", false));
   TRY(check_ptr(out, "out"));
   const size_t es = elem_bytes(s.dtype), f = 2 * (size_t)s.F;
   const size_t nq = (size_t)s.B * s.L * s.Hq * s.D * es;
@@ -125,9 +126,10 @@ int hybrid_attn_step(const hyb_dims_t* dims, const void* q, const void* k,
       overlap(out, no, v, nkv) || overlap(out, no, W, nW) ||
       overlap(out, no, S, nS) || overlap(out, no, z, nz) ||
       overlap(out, no, alpha, (size_t)s.Hq * 4) ||
-      overlap(out, no, slots, (size_t)s.B * 4))
+      overlap(out, no, slots, (size_t)s.B * 4) ||
+      overlap(out, no, block_len, (size_t)s.B * 4))
     return fail(HYB_EINVAL, "out overlaps an input");
-  hyb::StepArgs a{s, q, k, v, W, alpha, S, z, slots, out};
+  hyb::StepArgs a{s, q, k, v, W, alpha, S, z, slots, out, block_len};
   (void)hipGetLastError();
   return launched(hyb::launch_step(a, (hipStream_t)stream), "step");
 }
@@ -135,7 +137,8 @@ int hybrid_attn_step(const hyb_dims_t* dims, const void* q, const void* k,
 int hybrid_attn_step_commit(const hyb_dims_t* dims, const void* q,
                             const void* k, const void* v, const void* W,
                             const float* alpha, float* S, float* z,
-                            const int32_t* slots, void* out, void* stream) {
+                            const int32_t* slots, const int32_t* block_len,
+                            void* out, void* stream) {
   hyb::Shape s;
   TRY(check_dims(dims, true, &s));
   if (s.B == 0) return ok();
@@ -147,6 +150,7 @@ int hybrid_attn_step_commit(const hyb_dims_t* dims, const void* q,
   TRY(check_ptr(S, "S"));
   TRY(check_ptr(z, "z"));
   TRY(check_ptr(slots, "slots", false));
+  TRY(check_ptr(block_len, "block_len", false));
   TRY(check_ptr(out, "out"));
   const size_t es = elem_bytes(s.dtype), f = 2 * (size_t)s.F;
   const size_t nq = (size_t)s.B * s.L * s.Hq * s.D * es;
@@ -162,8 +166,10 @@ int hybrid_attn_step_commit(const hyb_dims_t* dims, const void* q,
     size_t n;
   };
   const Buf written[3] = {{out, no}, {S, nS}, {z, nz}};
-  const Buf read_only[6] = {{q, nq}, {k, nkv}, {v, nkv}, {W, nW},
-                            {alpha, (size_t)s.Hq * 4}, {slots, (size_t)s.B * 4}};
+  const Buf read_only[7] = {{q, nq},     {k, nkv},
+                            {v, nkv},     {W, nW},
+                            {alpha, (size_t)s.Hq * 4}, {slots, (size_t)s.B * 4},
+                            {block_len, (size_t)s.B * 4}};
   for (int i = 0; i < 3; ++i) {
     for (const Buf& r : read_only)
       if (overlap(written[i].p, written[i].n, r.p, r.n))
@@ -172,14 +178,15 @@ int hybrid_attn_step_commit(const hyb_dims_t* dims, const void* q,
       if (overlap(written[i].p, written[i].n, written[j].p, written[j].n))
         return fail(HYB_EINVAL, "out, S and z overlap");
   }
-  hyb::StepArgs a{s, q, k, v, W, alpha, S, z, slots, out};
+  hyb::StepArgs a{s, q, k, v, W, alpha, S, z, slots, out, block_len};
   (void)hipGetLastError();
   return launched(hyb::launch_step_commit(a, (hipStream_t)stream), "step_commit");
 }
 
 int hybrid_state_commit(const hyb_dims_t* dims, const void* k, const void* v,
                         const void* W, float* S, float* z,
-                        const int32_t* slots, void* stream) {
+                        const int32_t* slots, const int32_t* block_len,
+                        void* stream) {
   hyb::Shape s;
   TRY(check_dims(dims, true, &s));
   if (s.B == 0) return ok();
@@ -189,11 +196,12 @@ int hybrid_state_commit(const hyb_dims_t* dims, const void* k, const void* v,
   TRY(check_ptr(S, "S"));
   TRY(check_ptr(z, "z"));
   TRY(check_ptr(slots, "slots", false));
+  TRY(check_ptr(block_len, "block_len", false));
   const size_t f = 2 * (size_t)s.F;
   const size_t nS = (size_t)s.n_slots * s.Hq * f * s.D * 4;
   const size_t nz = (size_t)s.n_slots * s.Hq * f * 4;
   if (overlap(S, nS, z, nz)) return fail(HYB_EINVAL, "S and z overlap");
-  hyb::CommitArgs a{s, k, v, W, S, z, slots};
+  hyb::CommitArgs a{s, k, v, W, S, z, slots, block_len};
   (void)hipGetLastError();
   return launched(hyb::launch_commit(a, (hipStream_t)stream), "commit");
 }

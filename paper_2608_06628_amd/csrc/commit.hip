@@ -9,8 +9,9 @@
 // once and written once.  phi(K) is built with the shared feature-map code
 // and transposed through LDS (feature-major) to serve as the A operand.
 // On the bf16 path phi is kept as a bf16 pair hi + lo (two products), so the
-// update carries phi to about 16 bits instead of 8.  Tokens beyond the block
-// length get phi = 0 and v = 0.
+// update carries phi to about 16 bits instead of 8.  Tokens beyond the
+// request's block length get phi = 0 and v = 0 (padding rows are never used
+// as values, whatever they hold).
 #include "device.h"
 #include "featmap.h"
 #include "launch.h"
@@ -52,6 +53,9 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_commit_kernel(
   const int b = u / Hq, h = u % Hq, g = h / (Hq / Hkv);
   const int slot = a.slots ? a.slots[b] : b;
   if (slot < 0 || slot >= a.s.n_slots) return;  // uniform per workgroup
+  // Active tokens of this request's block (padding tokens contribute nothing).
+  const int Lb = a.block_len ? min(max(a.block_len[b], 0), L) : L;
+  if (Lb == 0) return;  // nothing to commit (uniform per workgroup)
   const size_t sbase = (size_t)slot * Hq + h;
   float* __restrict__ Sh = a.S + sbase * f * D;
   float* __restrict__ zh = a.z + sbase * f;
@@ -66,10 +70,10 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_commit_kernel(
   FM::load_w(Wt_h, w, li, hh, wop);
   const T* __restrict__ kb = (const T*)a.k + ((size_t)b * L * Hkv + g) * D;
   const T* __restrict__ vb = (const T*)a.v + ((size_t)b * L * Hkv + g) * D;
-  const bool tok_ok = li < L;
+  const bool tok_ok = li < Lb;
   op_t kop[C::KD];
   {
-    const T* krow = kb + (size_t)min(li, L - 1) * kstride + hh * E;
+    const T* krow = kb + (size_t)min(li, Lb - 1) * kstride + hh * E;
 #pragma unroll
     for (int ks = 0; ks < C::KD; ++ks) kop[ks] = load_op<T>(krow + ks * KW);
   }
@@ -77,7 +81,7 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_commit_kernel(
   op_t vop[C::KL];
 #pragma unroll
   for (int ks = 0; ks < C::KL; ++ks)
-    vop[ks] = load_rows_op<T>(vb + col, kstride, ks, hh, L, true);
+    vop[ks] = load_rows_op<T>(vb + col, kstride, ks, hh, Lb, true);
   constexpr int NTH = kWave * C::NW, ZPT = (f + NTH - 1) / NTH;
   float zreg[ZPT];
 #pragma unroll
@@ -134,7 +138,7 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_commit_kernel(
     const int r = tid + j * NTH;
     if (r >= f) continue;
     float s = 0.0f;
-    for (int t = 0; t < L; ++t)
+    for (int t = 0; t < Lb; ++t)
 #pragma unroll
       for (int part = 0; part < C::NPART; ++part) s += to_f32(sh.phiT[part][r][t]);
     zh[r] = zreg[j] + s;

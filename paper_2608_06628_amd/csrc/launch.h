@@ -13,6 +13,8 @@ struct Shape {
   int out_f32;                              // out is fp32 whatever dtype is
 };
 
+// block_len (nullable, device [B]): request b uses its first block_len[b]
+// tokens of the L-token block (clamped to 0 .. L); the rest are padding.
 struct StepArgs {
   Shape s;
   const void *q, *k, *v, *W;
@@ -20,6 +22,7 @@ struct StepArgs {
   const float *S, *z;
   const int32_t* slots;
   void* out;
+  const int32_t* block_len;
 };
 
 struct CommitArgs {
@@ -27,6 +30,7 @@ struct CommitArgs {
   const void *k, *v, *W;
   float *S, *z;
   const int32_t* slots;
+  const int32_t* block_len;
 };
 
 struct PrefillArgs {

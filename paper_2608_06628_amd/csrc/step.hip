@@ -263,6 +263,13 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
   const int h = hg * NW + w, g = (hg * NW) / (Hq / Hkv);
   const int slot = a.slots ? a.slots[b] : b;
   const bool slot_ok = slot >= 0 && slot < a.s.n_slots;
+  // Active tokens of this request's block (the rest are padding: masked as
+  // keys, never written as outputs, never committed).
+  const int Lb = a.block_len ? min(max(a.block_len[b], 0), L) : L;
+  // Rows past Lb read row Lc instead: in bounds, and an active row, so the
+  // padding rows are never read whatever they hold.  A request with Lb = 0
+  // writes no output and commits nothing.
+  const int Lc = max(Lb, 1) - 1;
   const size_t sbase = (size_t)(slot_ok ? slot : 0) * Hq + h;
 
   // State wave: column block cb of S_h^T; lane (c16, quad) reads the RUNS
@@ -358,7 +365,7 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
           sn += ph[1][fb][r];
         }
         // Branch-free: every lane of the row takes part in the reductions.
-        const float kv = kb * 16 + quad * 4 + r < L ? 1.0f : 0.0f;
+        const float kv = kb * 16 + quad * 4 + r < Lb ? 1.0f : 0.0f;
         const float ip = kv / rsum16(sp), in = kv / rsum16(sn);
 #pragma unroll
         for (int fb = 0; fb < FB; ++fb) {
@@ -390,7 +397,7 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
   // features rn*16 + quad*4 .. +3 of column column(cb, c16): the accumulator
   // layout of the 16 x 16 tile (features rn*16 .., columns of cb).
   auto update = [&](int cb) {
-    if (!slot_ok) return;
+    if (!slot_ok || Lb == 0) return;
     const op_t* __restrict__ pkh = reinterpret_cast<const op_t*>(sh.wl[w].qk + 32 * D);
     const op_t* __restrict__ pkl = reinterpret_cast<const op_t*>(&sh.hd[w]);
     float* __restrict__ Sw = const_cast<float*>(a.S) + sbase * f * D;
@@ -444,8 +451,8 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
     }
   } else {
     // ---------------- block wave ----------------
-    // 1. Loads, all unconditional and in bounds (rows past the block length
-    //    read row L-1 and are masked later).
+    // 1. Loads, all unconditional and in bounds (rows past the request's
+    //    block length read row Lc and are masked later).
     const size_t qstride = (size_t)Hq * D, kstride = (size_t)Hkv * D;
     const T* __restrict__ qb0 = (const T*)a.q + ((size_t)b * L * Hq + h) * D;
     const T* __restrict__ kb0 = (const T*)a.k + ((size_t)b * L * Hkv + g) * D;
@@ -458,9 +465,9 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
       for (int j = 0; j < C::VPT; ++j) {
         const int it = min(lane + j * kWave, C::VITEMS - 1), kp = it % 16, cg = it / 16;
         vlo[j] = *reinterpret_cast<const uint4*>(
-            vb0 + (size_t)min(2 * kp, L - 1) * kstride + cg * C::EPC);
+            vb0 + (size_t)min(2 * kp, Lc) * kstride + cg * C::EPC);
         vhi[j] = *reinterpret_cast<const uint4*>(
-            vb0 + (size_t)min(2 * kp + 1, L - 1) * kstride + cg * C::EPC);
+            vb0 + (size_t)min(2 * kp + 1, Lc) * kstride + cg * C::EPC);
       }
     }
     const float alpha_h = a.alpha[h];
@@ -485,14 +492,14 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
     };
     if constexpr (C::DMA_W) stage(Wt_h, D, F, F - 1, wst);
     if constexpr (C::DMA_QK) {
-      stage(qb0, qstride, 32, L - 1, qst);
-      stage(kb0, kstride, 32, L - 1, kst);
-      stage(vb0, kstride, 32, L - 1, vst);
+      stage(qb0, qstride, 32, Lc, qst);
+      stage(kb0, kstride, 32, Lc, kst);
+      stage(vb0, kstride, 32, Lc, vst);
     } else {
 #pragma unroll
       for (int r = 0; r < 2; ++r) {
-        const T* qrow = qb0 + (size_t)min(r * 16 + c16, L - 1) * qstride + quad * E;
-        const T* krow = kb0 + (size_t)min(r * 16 + c16, L - 1) * kstride + quad * E;
+        const T* qrow = qb0 + (size_t)min(r * 16 + c16, Lc) * qstride + quad * E;
+        const T* krow = kb0 + (size_t)min(r * 16 + c16, Lc) * kstride + quad * E;
 #pragma unroll
         for (int ks = 0; ks < C::KD; ++ks) {
           qop[r][ks] = load_op<T>(qrow + ks * KW);
@@ -546,7 +553,7 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
         *reinterpret_cast<bf16x4_t*>(reinterpret_cast<char*>(part == 0 ? pkh : pkl) +
                                      (fbk * kWave + lane) * 16 + kb * 8) = v;
       });
-      if (slot_ok) {
+      if (slot_ok && Lb > 0) {
         float* __restrict__ zw = const_cast<float*>(a.z) + sbase * f;
 #pragma unroll
         for (int fbk = 0; fbk < C::NFB; ++fbk) {
@@ -576,8 +583,8 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
 #pragma unroll
       for (int e = 0; e < C::EPC; ++e) {
         T* dst = &vt[cg * C::EPC + e][2 * kp];
-        dst[0] = 2 * kp < L ? x0[e] : (T)0.0f;
-        dst[1] = 2 * kp + 1 < L ? x1[e] : (T)0.0f;
+        dst[0] = 2 * kp < Lb ? x0[e] : (T)0.0f;
+        dst[1] = 2 * kp + 1 < Lb ? x1[e] : (T)0.0f;
       }
     }
 
@@ -595,7 +602,7 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
         for (int ks = 0; ks < C::KD; ++ks) sc = M::mma(kop[kb][ks], qop[qb][ks], sc);
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const bool kv = C::key(kb * 4 + r, quad) < L;
+          const bool kv = C::key(kb * 4 + r, quad) < Lb;
           p[qb][kb * 4 + r] = kv ? sc[r] * scale : -INFINITY;
           m[qb] = fmaxf(m[qb], p[qb][kb * 4 + r]);
         }
@@ -604,7 +611,7 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
       den[qb] = 0.0f;
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        p[qb][j] = C::key(j, quad) < L ? fast_exp(p[qb][j] - m[qb]) : 0.0f;
+        p[qb][j] = C::key(j, quad) < Lb ? fast_exp(p[qb][j] - m[qb]) : 0.0f;
         den[qb] += p[qb][j];
       }
       den[qb] = qsum(den[qb]);
@@ -757,7 +764,7 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
     typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
     const int osz = of32 ? 4 : 2;
     const int cph = D * osz / 16;  // 16-byte chunks per head
-    for (int t = wv; t < L; t += 2 * NW) {
+    for (int t = wv; t < Lb; t += 2 * NW) {
       char* orow = reinterpret_cast<char*>(a.out) +
                    (((size_t)b * L + t) * Hq + hg * NW) * D * osz;
       for (int c = lane; c < NW * cph; c += kWave) {
@@ -785,7 +792,7 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
   //    of the 16 x 16 tile (features rn*16 .., columns of cb).  The step above
   //    used the state as it was.
   if constexpr (CM && !C::EARLY) {
-    if (state_wave && slot_ok) {
+    if (state_wave && slot_ok && Lb > 0) {
       static_assert(RUNS == C::NFB, "one state run per 16-feature block");
       {
         const size_t kstride = (size_t)Hkv * D;
@@ -793,7 +800,7 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
         const T* __restrict__ Wt_h = (const T*)a.W + (size_t)h * F * D;
 #pragma unroll
         for (int r = 0; r < KB; ++r) {
-          const T* krow = kb0 + (size_t)min(r * 16 + c16, L - 1) * kstride + quad * E;
+          const T* krow = kb0 + (size_t)min(r * 16 + c16, Lc) * kstride + quad * E;
 #pragma unroll
           for (int ks = 0; ks < C::KD; ++ks) kop[r][ks] = load_op<T>(krow + ks * KW);
         }

@@ -41,7 +41,7 @@ def _dims(**kw):
 
 def _step(dims, ptrs=None):
     lib = hb.load()
-    p = ptrs or [FAKE] * 9
+    p = ptrs or [FAKE] * 10
     return lib.hybrid_attn_step(ctypes.byref(dims) if dims is not None else None, *p, None)
 
 
@@ -58,13 +58,13 @@ def test_step_rejects_bad_dims(kw, code):
 
 def test_null_and_alignment():
     assert _step(None) == 1
-    for i in range(9):
-        if i == 7:   # slots may be NULL; misaligned is still rejected
-            p = [FAKE] * 9
+    for i in range(10):
+        if i in (7, 8):   # slots and block_len may be NULL; misaligned is still rejected
+            p = [FAKE] * 10
             p[i] = MISALIGNED
             assert _step(_dims(), p) == 3
             continue
-        p = [FAKE] * 9
+        p = [FAKE] * 10
         p[i] = None
         assert _step(_dims(), p) == 1, i
         p[i] = MISALIGNED
@@ -72,19 +72,23 @@ def test_null_and_alignment():
 
 
 def test_out_aliasing_rejected():
-    p = [FAKE] * 9
-    p[8] = p[0]     # out == q
+    p = [FAKE] * 10
+    p[9] = p[0]     # out == q
+    assert _step(_dims(), p) == 2
+    assert "overlap" in hb.last_error()
+    p = [_addr(i) for i in range(10)]
+    p[9] = p[8]     # out == block_len
     assert _step(_dims(), p) == 2
     assert "overlap" in hb.last_error()
 
 
 def test_zero_batch_is_a_noop():
-    assert _step(_dims(batch=0), [None] * 9) == 0
+    assert _step(_dims(batch=0), [None] * 10) == 0
     assert hb.last_error() == ""
 
 
 def _addr(i):
-    return ctypes.c_void_p(0x100000 * (i + 1))   # disjoint, aligned, never dereferenced
+    return ctypes.c_void_p(0x1000000 * (i + 1))   # 16 MiB apart: disjoint, aligned, never dereferenced
 
 
 def test_step_commit_validation():
@@ -92,10 +96,10 @@ def test_step_commit_validation():
     lib = hb.load()
     d = _dims()
     call = lambda p, dims=d: lib.hybrid_attn_step_commit(ctypes.byref(dims), *p, None)
-    ok = [_addr(i) for i in range(9)]
+    ok = [_addr(i) for i in range(10)]
     ok[7] = None                                    # slots may be NULL
-    for i in range(9):
-        if i == 7:
+    for i in range(10):
+        if i in (7, 8):                             # slots, block_len may be NULL
             continue
         p = list(ok)
         p[i] = None
@@ -103,26 +107,40 @@ def test_step_commit_validation():
         p[i] = MISALIGNED
         assert call(p) == 3, i
     assert call(list(ok), _dims(head_dim=96)) == 5
-    # written buffers: out (8), S (5), z (6); read: q k v W alpha (0-4), slots (7)
-    for w_i in (5, 6, 8):
-        for r_i in (0, 1, 2, 3, 4, 5, 6, 8):
+    # written buffers: out (9), S (5), z (6); read: q k v W alpha (0-4),
+    # block_len (8); slots (7) is NULL here and checked below
+    for w_i in (5, 6, 9):
+        for r_i in (0, 1, 2, 3, 4, 5, 6, 8, 9):
             if r_i == w_i:
                 continue
             p = list(ok)
             p[w_i] = p[r_i]
             assert call(p) == 2, (w_i, r_i)
             assert "overlap" in hb.last_error()
-    assert lib.hybrid_attn_step_commit(ctypes.byref(_dims(batch=0)), *([None] * 9), None) == 0
+    for w_i in (5, 6, 9):
+        p = list(ok)
+        p[7] = _addr(12)
+        p[w_i] = p[7]
+        assert call(p) == 2, ("slots", w_i)
+    p = list(ok)
+    p[8] = MISALIGNED
+    assert call(p) == 3
+    assert lib.hybrid_attn_step_commit(ctypes.byref(_dims(batch=0)), *([None] * 10), None) == 0
 
 
 def test_commit_prefill_softmax_validation():
     lib = hb.load()
     d = _dims()
-    assert lib.hybrid_state_commit(ctypes.byref(d), FAKE, FAKE, FAKE, None, FAKE, None, None) == 1
+    assert lib.hybrid_state_commit(ctypes.byref(d), FAKE, FAKE, FAKE, None, FAKE, None, None,
+                                   None) == 1
     assert lib.hybrid_state_commit(ctypes.byref(_dims(feat_dim=48)), FAKE, FAKE, FAKE, FAKE,
-                                   FAKE, None, None) == 5
+                                   FAKE, None, None, None) == 5
     # S and z overlapping
-    assert lib.hybrid_state_commit(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, None, None) == 2
+    assert lib.hybrid_state_commit(ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, FAKE, None, None,
+                                   None) == 2
+    # block_len misaligned
+    assert lib.hybrid_state_commit(ctypes.byref(d), _addr(0), _addr(1), _addr(2), _addr(3),
+                                   _addr(4), None, MISALIGNED, None) == 3
     # prefill: seq_len not a multiple of the block
     assert lib.hybrid_state_prefill(ctypes.byref(d), 40, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
                                     FAKE, None, None, None, 0, None) == 2
