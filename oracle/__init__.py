@@ -6,7 +6,9 @@ never does.  It shares no code with the HIP library.
 
 ``oracle.c`` evaluates the paper's definitions literally in double precision
 (Section 3.1 for the hybrid step, the state and its update; Section 2.2 for
-softmax attention; Figure 2 for the block-causal prefill pattern).  This module
+softmax attention; Figure 2 for the block-causal prefill pattern), and the
+exact reverse-mode gradient of that prefill with respect to the Stage-1
+parameters {W, alpha} of Section 3.2.  This module
 compiles it with gcc and wraps it with NumPy arrays.  ``brute.py`` holds
 independent dense formulations used to pin it.
 
@@ -54,8 +56,9 @@ def _load():
     lib.oracle_prefill.argtypes = [i] * 7 + [_dp] * 7 + [_ip, _dp]
     lib.oracle_softmax_prefix.argtypes = [i] * 6 + [_dp] * 5 + [_ip, _dp]
     lib.oracle_feature_map.argtypes = [i] * 3 + [_dp] * 3
+    lib.oracle_backward.argtypes = [i] * 7 + [_dp] * 10
     for fn in (lib.oracle_step, lib.oracle_commit, lib.oracle_prefill,
-               lib.oracle_softmax_prefix, lib.oracle_feature_map):
+               lib.oracle_softmax_prefix, lib.oracle_feature_map, lib.oracle_backward):
         fn.restype = ctypes.c_int
     _lib = lib
     return lib
@@ -194,6 +197,44 @@ def softmax_prefix(q, k, v, k_cache, v_cache, plen):
                                      pvc, pl.ctypes.data_as(_ip),
                                      out.ctypes.data_as(_dp)), "softmax_prefix")
     return out
+
+
+def backward(q, k, v, Wt, alpha, L, dout=None, target=None):
+    """Gradient of the block-causal hybrid layer over a training sequence
+    (empty starting state, blocks of L) with respect to W and alpha, the
+    parameters Stage 1 of Section 3.2 trains.
+
+    Exactly one of dout (upstream gradient, objective sum <dout, out>) and
+    target (the softmax teacher's output; objective sum |out - target|^2,
+    the attention-transfer loss) is given.  Returns (dWt [Hq][F][d],
+    dalpha [Hq], loss [Hq] or None); gradients are summed over the batch.
+    """
+    assert (dout is None) != (target is None)
+    lib = _load()
+    q, pq = _d(q)
+    k, pk = _d(k)
+    v, pv = _d(v)
+    Wt, pW = _d(Wt)
+    alpha, pa = _d(alpha)
+    B, T, Hq, d = q.shape
+    Hkv = k.shape[2]
+    F = Wt.shape[1]
+    if dout is not None:
+        g, pg = _d(dout)
+        assert g.shape == q.shape
+        pt = None
+    else:
+        t, pt = _d(target)
+        assert t.shape == q.shape
+        pg = None
+    dW = np.zeros((Hq, F, d))
+    da = np.zeros(Hq)
+    loss = np.zeros(Hq) if target is not None else None
+    _check(lib.oracle_backward(B, T, Hq, Hkv, d, L, F, pq, pk, pv, pW, pa, pg, pt,
+                               dW.ctypes.data_as(_dp), da.ctypes.data_as(_dp),
+                               loss.ctypes.data_as(_dp) if loss is not None else None),
+           "backward")
+    return dW, da, loss
 
 
 def empty_state(n_slots, Hq, f, d):

@@ -261,3 +261,191 @@ int oracle_feature_map(int n, int d, int F, const double *X, const double *Wt,
     err |= feature_map(X + (size_t)t * d, Wt, d, F, PHI + (size_t)t * 2 * F);
   return err;
 }
+
+/* ---------------------------------------------------------------------------
+ * Backward of the block-causal hybrid layer over a training sequence, for the
+ * attention transfer of Section 3.2 (Stage 1): the trainable parameters are
+ * psi = {W, alpha}, so the gradients returned are dL/dW and dL/dalpha.
+ *
+ * Forward (the prefill pattern of Figure 2, from an empty state): block c of
+ * the T = nblk * L tokens is answered as in hybrid_query against S_{c-1},
+ * z_{c-1} (the blocks before it), then committed.
+ *
+ * Objective.  With target == NULL, L = sum_i <dout_i, out_i> (so the result
+ * is the vector-Jacobian product for an upstream gradient dout).  With a
+ * target (the frozen softmax teacher's output a^sm of Section 3.2), L is the
+ * attention-transfer loss sum_i |out_i - target_i|^2 and dout_i =
+ * 2 (out_i - target_i); loss[h] receives its value per query head.
+ *
+ * Reverse mode, written from the definitions (N = w sm_num + lin_num,
+ * D = w sm_den + lin_den, out = N / D, g = dL/dout):
+ *   dL/dN_i      = g_i / D_i
+ *   dL/dD_i      = -(g_i . out_i) / D_i
+ *   dL/dw       += dL/dN_i . sm_num_i + dL/dD_i sm_den_i
+ *   dL/dphi(q_i) = S_{c-1} dL/dN_i + z_{c-1} dL/dD_i          (i in block c)
+ *   dL/dphi(k_t) = sum_{c' > c} sum_{i in c'} phi(q_i) (v_t . dL/dN_i + dL/dD_i)
+ *                = G_c v_t + gz_c                              (t in block c)
+ *     with G_c = sum_{c' > c} sum_{i in c'} phi(q_i) (dL/dN_i)^T, gz_c likewise
+ *   feature map, u = x W (F entries), phi = [p, n], p = softmax(u),
+ *   n = softmax(-u), dphi = [dp, dn]:
+ *     dL/du_j = p_j (dp_j - <dp, p>) - n_j (dn_j - <dn, n>)
+ *     dL/dW[:, j] += x dL/du_j         (x = q_i or k_t, head h's W)
+ *   dL/dalpha = dL/dw * w (1 - w).
+ * Outputs are sums over the batch: dWt [Hq][F][d] (same layout as Wt),
+ * dalpha [Hq], loss [Hq] (may be NULL without a target).
+ * --------------------------------------------------------------------------- */
+
+/* dL/du of the feature map at x (phi already evaluated there), added into
+ * dWt as x dL/du_j. */
+static void feature_map_backward(const double *x, const double *phi,
+                                 const double *dphi, int d, int F,
+                                 double *dWt) {
+  const double *p = phi, *n = phi + F, *dp = dphi, *dn = dphi + F;
+  double sp = 0.0, sn = 0.0;
+  for (int j = 0; j < F; ++j) {
+    sp += dp[j] * p[j];
+    sn += dn[j] * n[j];
+  }
+  for (int j = 0; j < F; ++j) {
+    const double du = p[j] * (dp[j] - sp) - n[j] * (dn[j] - sn);
+    for (int i = 0; i < d; ++i) dWt[(size_t)j * d + i] += du * x[i];
+  }
+}
+
+int oracle_backward(int B, int T, int Hq, int Hkv, int d, int L, int F,
+                    const double *q, const double *k, const double *v,
+                    const double *Wt, const double *alpha, const double *dout,
+                    const double *target, double *dWt, double *dalpha,
+                    double *loss) {
+  const int G = Hq / Hkv, f = 2 * F;
+  if (L <= 0 || T % L != 0) return 2;
+  if ((dout == NULL) == (target == NULL)) return 2;
+  const int nblk = T / L;
+  const long units = (long)B * Hq;
+  /* per-unit results, summed over the batch in a fixed order afterwards */
+  double *u_dW = (double *)calloc((size_t)units * F * d, sizeof(double));
+  double *u_dw = (double *)calloc((size_t)units, sizeof(double));
+  double *u_loss = (double *)calloc((size_t)units, sizeof(double));
+  int err = 0;
+#pragma omp parallel for schedule(dynamic) reduction(| : err)
+  for (long u = 0; u < units; ++u) {
+    const int b = (int)(u / Hq), h = (int)(u % Hq), g = h / G;
+    const double *Wh = Wt + (size_t)h * F * d;
+    const double w = gate(alpha[h]);
+    double *dWu = u_dW + (size_t)u * F * d;
+    /* forward state, then the per-query adjoints kept for the reverse pass */
+    double *S = (double *)calloc((size_t)f * d, sizeof(double));
+    double *z = (double *)calloc((size_t)f, sizeof(double));
+    double *phiq = (double *)malloc(sizeof(double) * (size_t)T * f);
+    double *dN = (double *)malloc(sizeof(double) * (size_t)T * d);
+    double *dD = (double *)malloc(sizeof(double) * (size_t)T);
+    double *phi = (double *)malloc(sizeof(double) * f);
+    double *dphi = (double *)malloc(sizeof(double) * f);
+    double *sm_num = (double *)malloc(sizeof(double) * d);
+    double *o = (double *)malloc(sizeof(double) * d);
+    double *gi = (double *)malloc(sizeof(double) * d);
+    double dw = 0.0, ls = 0.0;
+    for (int c = 0; c < nblk && !err; ++c) {
+      const size_t t0 = (size_t)c * L;
+      for (int i = 0; i < L; ++i) {
+        const size_t qo = (((size_t)b * T + t0 + i) * Hq + h) * d;
+        const double *qi = q + qo;
+        /* the forward quantities of Section 3.1 for query i */
+        double sm_den = 0.0;
+        for (int cc = 0; cc < d; ++cc) sm_num[cc] = 0.0;
+        for (int j = 0; j < L; ++j) {
+          const size_t ko = (((size_t)b * T + t0 + j) * Hkv + g) * d;
+          double s = 0.0;
+          for (int x = 0; x < d; ++x) s += qi[x] * k[ko + x];
+          s /= sqrt((double)d);
+          if (fabs(s) >= EXP_LIMIT) err = 1;
+          const double a = exp(s);
+          sm_den += a;
+          for (int cc = 0; cc < d; ++cc) sm_num[cc] += a * v[ko + cc];
+        }
+        double *ph = phiq + (size_t)(t0 + i) * f;
+        if (feature_map(qi, Wh, d, F, ph)) err = 1;
+        double lin_den = 0.0;
+        for (int r = 0; r < f; ++r) lin_den += ph[r] * z[r];
+        const double D = w * sm_den + lin_den;
+        for (int cc = 0; cc < d; ++cc) {
+          double lin_num = 0.0;
+          for (int r = 0; r < f; ++r) lin_num += ph[r] * S[(size_t)r * d + cc];
+          o[cc] = (w * sm_num[cc] + lin_num) / D;
+        }
+        /* upstream gradient */
+        for (int cc = 0; cc < d; ++cc) {
+          if (target) {
+            const double e = o[cc] - target[qo + cc];
+            ls += e * e;
+            gi[cc] = 2.0 * e;
+          } else {
+            gi[cc] = dout[qo + cc];
+          }
+        }
+        double go = 0.0;
+        for (int cc = 0; cc < d; ++cc) go += gi[cc] * o[cc];
+        double *dNi = dN + (size_t)(t0 + i) * d;
+        const double dDi = -go / D;
+        dD[t0 + i] = dDi;
+        for (int cc = 0; cc < d; ++cc) dNi[cc] = gi[cc] / D;
+        for (int cc = 0; cc < d; ++cc) dw += dNi[cc] * sm_num[cc];
+        dw += dDi * sm_den;
+        /* dL/dphi(q_i) against the state this block read */
+        for (int r = 0; r < f; ++r) {
+          double s = z[r] * dDi;
+          for (int cc = 0; cc < d; ++cc) s += S[(size_t)r * d + cc] * dNi[cc];
+          dphi[r] = s;
+        }
+        feature_map_backward(qi, ph, dphi, d, F, dWu);
+      }
+      for (int t = 0; t < L; ++t) {
+        const size_t ko = (((size_t)b * T + t0 + t) * Hkv + g) * d;
+        err |= commit_token(k + ko, v + ko, d, F, Wh, S, z, phi);
+      }
+    }
+    /* reverse pass over the blocks: G_c, gz_c hold the later blocks' sums */
+    double *Gs = S, *gz = z; /* the forward state is no longer needed */
+    memset(Gs, 0, sizeof(double) * (size_t)f * d);
+    memset(gz, 0, sizeof(double) * (size_t)f);
+    for (int c = nblk - 1; c >= 0 && !err; --c) {
+      const size_t t0 = (size_t)c * L;
+      for (int t = 0; t < L; ++t) {
+        const size_t ko = (((size_t)b * T + t0 + t) * Hkv + g) * d;
+        if (feature_map(k + ko, Wh, d, F, phi)) err = 1;
+        for (int r = 0; r < f; ++r) {
+          double s = gz[r];
+          for (int cc = 0; cc < d; ++cc) s += Gs[(size_t)r * d + cc] * v[ko + cc];
+          dphi[r] = s;
+        }
+        feature_map_backward(k + ko, phi, dphi, d, F, dWu);
+      }
+      for (int i = 0; i < L; ++i) {
+        const double *ph = phiq + (size_t)(t0 + i) * f;
+        const double *dNi = dN + (size_t)(t0 + i) * d;
+        for (int r = 0; r < f; ++r) {
+          gz[r] += ph[r] * dD[t0 + i];
+          for (int cc = 0; cc < d; ++cc) Gs[(size_t)r * d + cc] += ph[r] * dNi[cc];
+        }
+      }
+    }
+    u_dw[u] = dw * w * (1.0 - w);
+    u_loss[u] = ls;
+    free(S); free(z); free(phiq); free(dN); free(dD); free(phi); free(dphi);
+    free(sm_num); free(o); free(gi);
+  }
+  for (int h = 0; h < Hq; ++h) {
+    double *dW = dWt + (size_t)h * F * d;
+    memset(dW, 0, sizeof(double) * (size_t)F * d);
+    dalpha[h] = 0.0;
+    if (loss) loss[h] = 0.0;
+    for (int b = 0; b < B; ++b) {
+      const long u = (long)b * Hq + h;
+      for (size_t x = 0; x < (size_t)F * d; ++x) dW[x] += u_dW[(size_t)u * F * d + x];
+      dalpha[h] += u_dw[u];
+      if (loss) loss[h] += u_loss[u];
+    }
+  }
+  free(u_dW); free(u_dw); free(u_loss);
+  return err;
+}
