@@ -98,7 +98,8 @@ typedef enum {
   HYB_OP_STEP = 0,
   HYB_OP_COMMIT = 1,
   HYB_OP_PREFILL = 2,
-  HYB_OP_SOFTMAX_PREFIX = 3
+  HYB_OP_SOFTMAX_PREFIX = 3,
+  HYB_OP_BACKWARD = 4
 } hyb_op_t;
 
 typedef struct {
@@ -181,9 +182,35 @@ int softmax_prefix_step(const hyb_dims_t* dims, const void* q, const void* k,
                         int32_t max_prefix, void* out, void* ws,
                         size_t ws_bytes, void* stream);
 
+/* Gradient of the block-hybrid layer over a training sequence with respect
+ * to its feature-map weights W and gate logits alpha: the attention transfer
+ * of Section 3.2 (Stage 1), which trains only {W, alpha} with the backbone
+ * frozen.  The forward is the block-causal pattern of Figure 2 from an empty
+ * state (hybrid_state_prefill's outputs for a fresh request): q [B][T][Hq][d],
+ * k, v [B][T][Hkv][d], W, alpha as for hybrid_attn_step, T = seq_len.
+ * Objective, exactly one of:
+ *   dout   [B][T][Hq][d] (dims->dtype): L = sum <dout, out>, i.e. the
+ *          gradient for an upstream gradient dout; loss must be NULL;
+ *   target [B][T][Hq][d] (dims->dtype): the frozen softmax teacher's output;
+ *          L = sum |out - target|^2, the attention-transfer loss, formed
+ *          without writing out; loss (fp32 [Hq], may be NULL) receives L per
+ *          query head.
+ * Outputs (fp32, overwritten, summed over the batch): dW [Hq][F][d] in W's
+ * layout, dalpha [Hq].  seq_len must be a positive multiple of L.  feat_dim
+ * must be 64 or 128 (HYB_EUNSUPPORTED otherwise); dims->flags must be 0;
+ * n_slots is not used.  ws/ws_bytes: at least hybrid_workspace_bytes(dims,
+ * HYB_OP_BACKWARD, seq_len) bytes, not overlapping any argument; outputs
+ * must not overlap each other or an input.  batch 0 writes nothing.
+ * Deterministic: partial sums are added in a fixed order. */
+int hybrid_attn_backward(const hyb_dims_t* dims, int32_t seq_len,
+                         const void* q, const void* k, const void* v,
+                         const void* W, const float* alpha, const void* dout,
+                         const void* target, float* dW, float* dalpha,
+                         float* loss, void* ws, size_t ws_bytes, void* stream);
+
 /* Workspace bytes the given op needs for these dims; `extent` is seq_len for
- * HYB_OP_PREFILL and max_prefix for HYB_OP_SOFTMAX_PREFIX, ignored otherwise.
- * Returns 0 for invalid dims. */
+ * HYB_OP_PREFILL and HYB_OP_BACKWARD, max_prefix for HYB_OP_SOFTMAX_PREFIX,
+ * ignored otherwise.  Returns 0 for invalid dims. */
 size_t hybrid_workspace_bytes(const hyb_dims_t* dims, int32_t op,
                               int32_t extent);
 

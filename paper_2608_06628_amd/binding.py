@@ -18,13 +18,13 @@ LIB_PATH = os.path.join(_PKG, "libhybattn.so")
 
 HYB_F32, HYB_BF16 = 0, 1
 HYB_OUT_F32 = 1
-OP_STEP, OP_COMMIT, OP_PREFILL, OP_SOFTMAX_PREFIX = 0, 1, 2, 3
+OP_STEP, OP_COMMIT, OP_PREFILL, OP_SOFTMAX_PREFIX, OP_BACKWARD = 0, 1, 2, 3, 4
 STATUS = {0: "HYB_OK", 1: "HYB_ENULL", 2: "HYB_EINVAL", 3: "HYB_EALIGN",
           4: "HYB_EDTYPE", 5: "HYB_EUNSUPPORTED", 6: "HYB_EWORKSPACE",
           7: "HYB_ELAUNCH"}
 EXPORTS = ("hybrid_attn_step", "hybrid_attn_step_commit", "hybrid_state_commit",
-           "hybrid_state_prefill", "softmax_prefix_step", "hybrid_workspace_bytes",
-           "hybrid_last_error")
+           "hybrid_state_prefill", "softmax_prefix_step", "hybrid_attn_backward",
+           "hybrid_workspace_bytes", "hybrid_last_error")
 
 
 class HybError(RuntimeError):
@@ -59,6 +59,7 @@ def load():
     lib.hybrid_state_commit.argtypes = [P] + [vp] * 8
     lib.hybrid_state_prefill.argtypes = [P, i32] + [vp] * 10 + [sz, vp]
     lib.softmax_prefix_step.argtypes = [P] + [vp] * 6 + [i32, vp, vp, sz, vp]
+    lib.hybrid_attn_backward.argtypes = [P, i32] + [vp] * 11 + [sz, vp]
     lib.hybrid_workspace_bytes.argtypes = [P, i32, i32]
     lib.hybrid_workspace_bytes.restype = sz
     lib.hybrid_last_error.argtypes = []
@@ -227,3 +228,37 @@ def softmax_prefix_step(q, k, v, k_cache, v_cache, prefix_len, out=None, ws=None
         _ptr(ws, "ws") if ws is not None else None,
         ws.numel() * ws.element_size() if ws is not None else 0, _stream(stream)))
     return out
+
+
+def hybrid_attn_backward(q, k, v, W, alpha, block, dout=None, target=None, dW=None,
+                         dalpha=None, loss=None, ws=None, stream=None):
+    """Gradient of the block-causal hybrid layer over q [B][T][Hq][d],
+    k/v [B][T][Hkv][d] (empty starting state, blocks of `block` tokens) with
+    respect to W [Hq][F][d] and alpha [Hq].  Give dout (upstream gradient) or
+    target (the teacher's output; squared-error loss).  Returns
+    (dW fp32 [Hq][F][d], dalpha fp32 [Hq], loss fp32 [Hq] or None)."""
+    lib = load()
+    B, T, Hq, d = q.shape
+    Hkv = k.shape[2]
+    F = W.shape[1]
+    act = q.dtype
+    dims = make_dims(B, Hq, Hkv, d, block, 2 * F, _dt(q), 1, 0)
+    dev = q.device
+    if dW is None:
+        dW = torch.empty((Hq, F, d), dtype=torch.float32, device=dev)
+    if dalpha is None:
+        dalpha = torch.empty(Hq, dtype=torch.float32, device=dev)
+    if target is not None and loss is None:
+        loss = torch.empty(Hq, dtype=torch.float32, device=dev)
+    need = workspace_bytes(dims, OP_BACKWARD, T)
+    if ws is None and need:
+        ws = torch.empty(need, dtype=torch.uint8, device=dev)
+    _check(lib.hybrid_attn_backward(
+        ctypes.byref(dims), T, _ptr(q, "q"), _ptr(k, "k", act), _ptr(v, "v", act),
+        _ptr(W, "W", act), _ptr(alpha, "alpha", torch.float32),
+        _ptr(dout, "dout", act), _ptr(target, "target", act),
+        _ptr(dW, "dW", torch.float32), _ptr(dalpha, "dalpha", torch.float32),
+        _ptr(loss, "loss", torch.float32),
+        _ptr(ws, "ws") if ws is not None else None,
+        ws.numel() * ws.element_size() if ws is not None else 0, _stream(stream)))
+    return dW, dalpha, loss

@@ -299,6 +299,68 @@ int softmax_prefix_step(const hyb_dims_t* dims, const void* q, const void* k,
                   "softmax_prefix_step");
 }
 
+int hybrid_attn_backward(const hyb_dims_t* dims, int32_t seq_len,
+                         const void* q, const void* k, const void* v,
+                         const void* W, const float* alpha, const void* dout,
+                         const void* target, float* dW, float* dalpha,
+                         float* loss, void* ws, size_t ws_bytes, void* stream) {
+  hyb::Shape s;
+  TRY(check_dims(dims, false, &s));
+  if (dims->flags != 0) return fail(HYB_EINVAL, "flags must be 0 for the backward");
+  if (!hyb::backward_supported(s))
+    return fail(HYB_EUNSUPPORTED, "backward supports feat_dim 64 or 128, not %d",
+                2 * s.F);
+  if (seq_len <= 0 || seq_len % s.L != 0)
+    return fail(HYB_EINVAL, "seq_len %d is not a positive multiple of block %d",
+                seq_len, s.L);
+  if (s.B == 0) return ok();
+  TRY(check_ptr(q, "q"));
+  TRY(check_ptr(k, "k"));
+  TRY(check_ptr(v, "v"));
+  TRY(check_ptr(W, "W"));
+  TRY(check_ptr(alpha, "alpha"));
+  TRY(check_ptr(dout, "dout", false));
+  TRY(check_ptr(target, "target", false));
+  if ((dout == nullptr) == (target == nullptr))
+    return fail(HYB_EINVAL, "exactly one of dout and target must be given");
+  if (dout && loss) return fail(HYB_EINVAL, "loss needs a target");
+  TRY(check_ptr(dW, "dW"));
+  TRY(check_ptr(dalpha, "dalpha"));
+  TRY(check_ptr(loss, "loss", false));
+  const size_t need = hybrid_workspace_bytes(dims, HYB_OP_BACKWARD, seq_len);
+  if (!ws || ws_bytes < need)
+    return fail(HYB_EWORKSPACE, "backward needs %zu workspace bytes, got %zu",
+                need, ws ? ws_bytes : (size_t)0);
+  TRY(check_ptr(ws, "ws"));
+  const size_t es = elem_bytes(s.dtype);
+  const size_t nq = (size_t)s.B * seq_len * s.Hq * s.D * es;
+  const size_t nkv = (size_t)s.B * seq_len * s.Hkv * s.D * es;
+  const size_t nW = (size_t)s.Hq * s.F * s.D * es;
+  struct Buf {
+    const void* p;
+    size_t n;
+  };
+  const Buf written[4] = {{dW, (size_t)s.Hq * s.F * s.D * 4},
+                          {dalpha, (size_t)s.Hq * 4},
+                          {loss, (size_t)s.Hq * 4},
+                          {ws, need}};
+  const Buf read_only[6] = {{q, nq},  {k, nkv}, {v, nkv}, {W, nW},
+                            {alpha, (size_t)s.Hq * 4},
+                            {dout ? dout : target, nq}};
+  for (int i = 0; i < 4; ++i) {
+    for (int j = i + 1; j < 4; ++j)
+      if (overlap(written[i].p, written[i].n, written[j].p, written[j].n))
+        return fail(HYB_EINVAL, "outputs or the workspace overlap each other");
+    for (int j = 0; j < 6; ++j)
+      if (overlap(written[i].p, written[i].n, read_only[j].p, read_only[j].n))
+        return fail(HYB_EINVAL, "an output or the workspace overlaps an input");
+  }
+  hyb::BackwardArgs a{s, seq_len, q, k, v, W, alpha, dout, target,
+                      dW, dalpha, loss, ws};
+  (void)hipGetLastError();
+  return launched(hyb::launch_backward(a, (hipStream_t)stream), "backward");
+}
+
 size_t hybrid_workspace_bytes(const hyb_dims_t* dims, int32_t op,
                               int32_t extent) {
   hyb::Shape s;
@@ -316,6 +378,9 @@ size_t hybrid_workspace_bytes(const hyb_dims_t* dims, int32_t op,
     case HYB_OP_SOFTMAX_PREFIX:
       return hyb::softmax_prefix_ws_bytes(
           s, hyb::softmax_prefix_splits(s, extent));
+    case HYB_OP_BACKWARD:
+      if (extent == 0 || extent % s.L != 0 || !hyb::backward_supported(s)) return 0;
+      return hyb::backward_ws_bytes(s, extent);
   }
   return 0;
 }

@@ -1,0 +1,876 @@
+// backward.hip -- gradient of the block-causal hybrid layer with respect to
+// its feature-map weights W and gate logits alpha: the attention transfer of
+// Section 3.2 (Stage 1), whose only trainable parameters are {W, alpha}.
+//
+// Forward (Figure 2 pattern, from an empty state): block c of the sequence
+// is answered against S_{c-1}, z_{c-1} (exact softmax inside the block,
+// linear readout, shared-normaliser merge of Section 3.1) and then committed.
+// With g = dL/dout, N = w sm_num + lin_num, D = w sm_den + lin_den:
+//   dL/dN_i = g_i / D_i,  dL/dD_i = -(g_i . out_i) / D_i
+//   dL/dw  += dL/dN_i . sm_num_i + dL/dD_i sm_den_i
+//   dL/dphi(q_i) = S_{c-1} dL/dN_i + z_{c-1} dL/dD_i
+//   dL/dphi(k_t) = Gbar_c v_t + gz_c,  Gbar_c = sum over the queries of the
+//                  blocks after c of phi(q_i) dL/dN_i^T (gz_c likewise)
+//   feature map: dL/du_j = p_j (dp_j - <dp,p>) - n_j (dn_j - <dn,n>),
+//                dL/dW[:, j] += x dL/du_j.
+// In attention-transfer mode g_i = 2 (out_i - target_i) is formed in
+// registers from the teacher's output; out itself never reaches memory.
+//
+// Kernels (one workgroup per (request, head, sequence segment), NW = D/32
+// waves; segments as in the prefill, so the grid fills the chip):
+//   1. the prefill's delta launch: each segment's state increment;
+//   2. hyb_bwd_fwd_kernel: forward walk.  Wave w keeps S columns 32w..+31
+//      in fp32 accumulators (the readout operand, as in the prefill).  Each
+//      block also copies S_{c-1} to LDS as [feature][column] operands, for
+//      dL/dphi(Q), which contracts over the head dimension.  Per block it
+//      forms out, dL/dN, dL/dD, dL/dphi(Q) and the query part of dL/dW and
+//      dL/dalpha, and hands dL/dN^T and dL/dD to the workspace;
+//   3. hyb_bwd_rev_kernel, delta mode: each segment's sum of
+//      phi(Q)^T dL/dN (and phi(Q)^T dL/dD);
+//   4. hyb_bwd_rev_kernel, walk mode: reverse walk with Gbar^T in the
+//      accumulators, the key part of dL/dW;
+//   5. hyb_bwd_reduce_kernel: sums the per-(request, segment) partials in a
+//      fixed order (bitwise reproducible, no atomics).
+// On the bf16 path phi(K), phi(Q) (as an update operand) and dL/du enter the
+// matrix products as bf16 pairs hi + lo; the state, Gbar and dL/dN as bf16.
+#include "device.h"
+#include "featmap.h"
+#include "launch.h"
+
+namespace hyb {
+
+template <typename T, int D, int F>
+struct BwdCfg {
+  typedef Mma<T> M;
+  typedef typename M::op_t op_t;
+  static constexpr int NW = D / kTile;      // waves = 32-column slices of d
+  static constexpr int f = 2 * F;
+  static constexpr int NRT = f / kTile;     // 32-feature tiles
+  static constexpr int NT = F / kTile;      // tiles per sign
+  static constexpr int RPW = (NRT + NW - 1) / NW;  // feature tiles per wave
+  static constexpr int KD = D / M::KW;
+  static constexpr int KL = kTile / M::KW;
+  static constexpr int NPART = sizeof(T) == 2 ? 2 : 1;
+  static constexpr int PAD = 16 / (int)sizeof(T);
+  typedef FeatMap<T, D, F, NW> FM;
+  static_assert(FM::PPW == RPW, "one feature-map pair per feature tile");
+  struct alignas(16) SmemF {
+    T st[NPART][f][D + PAD];             // S_{c-1} as operands, [part][r][c]
+    T phiQ[NPART][kTile][f + PAD];       // phi(q_i)[r] at [part][i][r]
+    T phiKT[NPART][f][kTile + PAD];      // phi(k_t)[r] at [part][r][t]
+    T gn[NPART][kTile][D + PAD];         // dL/dN_i[c] at [part][i][c]
+    T duT[2][NPART][F][kTile + PAD];     // +-dL/du from each sign, [j][i]
+    float z[f];
+    float lden[NW][kTile];
+    float red[NW][kTile][2];
+    float jsum[NRT][kTile];
+    float gd[kTile];
+    float fin[NW][2];
+    typename FM::Smem fq, fk;
+  };
+  struct alignas(16) SmemB {
+    T phiQT[NPART][f][kTile + PAD];      // phi(q_i)[r] at [part][r][i]
+    T duT[2][NPART][F][kTile + PAD];
+    float gz[f];
+    float jsum[NRT][kTile];
+    float gd[kTile];
+    typename FM::Smem fq, fk;
+  };
+};
+
+// Workspace layout (floats unless noted), every part 256-byte aligned:
+//   prefill deltas dS [units][nseg-1][D][f], dz [units][nseg-1][f]
+//   Gbar deltas   dG [units][nseg][D][f] (transposed like S), dgz [units][nseg][f]
+//   dL/dN^T        gnT [units][nblk][D][32]
+//   dL/dD          gd  [units][nblk][32]
+//   partial dW     dwq, dwk [units][nseg][F][D]
+//   partial scalars red [units][nseg][2]  (dL/dalpha, loss)
+struct BwdLayout {
+  size_t dS, dG, dgz, gnT, gd, dwq, dwk, red, total;
+};
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+static BwdLayout bwd_layout(const Shape& s, int T) {
+  const size_t units = (size_t)s.B * s.Hq, f = 2 * (size_t)s.F;
+  const int nseg = prefill_segments(s, T), nblk = T / s.L;
+  BwdLayout l;
+  size_t o = 0;
+  l.dS = o;
+  o = align256(o + prefill_ws_bytes(s, T));
+  l.dG = o;
+  o = align256(o + units * nseg * s.D * f * 4);
+  l.dgz = o;
+  o = align256(o + units * nseg * f * 4);
+  l.gnT = o;
+  o = align256(o + units * nblk * s.D * kTile * 4);
+  l.gd = o;
+  o = align256(o + units * nblk * kTile * 4);
+  l.dwq = o;
+  o = align256(o + units * nseg * s.F * s.D * 4);
+  l.dwk = o;
+  o = align256(o + units * nseg * s.F * s.D * 4);
+  l.red = o;
+  o = align256(o + units * nseg * 2 * 4);
+  l.total = o;
+  return l;
+}
+
+size_t backward_ws_bytes(const Shape& s, int T) { return bwd_layout(s, T).total; }
+
+struct BwdKArgs {
+  BackwardArgs a;
+  int nseg, seg_blocks, nblk;
+  float *dS, *dz, *dG, *dgz, *gd, *dwq, *dwk, *red, *gnT;
+};
+
+// Accumulator registers ks*E .. ks*E+E-1 of a tile as a T operand (the tile's
+// rows become the contraction index, in row_of order).
+template <typename T>
+__device__ inline typename Mma<T>::op_t acc_op(const f32x16& x, int ks) {
+  typedef Mma<T> M;
+  typename M::op_t r;
+  if constexpr (M::E == 1) {
+    r = x[ks];
+  } else {
+#pragma unroll
+    for (int e = 0; e < M::E; ++e) r[e] = (T)x[ks * M::E + e];
+  }
+  return r;
+}
+
+// The rounding remainders x - T(x) of the same registers: with acc_op they
+// carry x as a pair hi + lo (about 16 significant bits on the bf16 path).
+template <typename T>
+__device__ inline typename Mma<T>::op_t acc_op_lo(const f32x16& x, int ks) {
+  typedef Mma<T> M;
+  typename M::op_t r;
+  if constexpr (M::E == 1) {
+    r = 0.0f;
+  } else {
+#pragma unroll
+    for (int e = 0; e < M::E; ++e) {
+      const float v = x[ks * M::E + e];
+      r[e] = (T)(v - as_operand<T>(v));
+    }
+  }
+  return r;
+}
+
+// E fp32 values from p as an operand pair hi + lo (lo is zero on fp32).
+template <typename T>
+__device__ inline void load_split_op(const float* p, typename Mma<T>::op_t& hi,
+                                     typename Mma<T>::op_t& lo) {
+  typedef Mma<T> M;
+  if constexpr (M::E == 1) {
+    hi = *p;
+    lo = 0.0f;
+  } else {
+    const f32x4 a = *reinterpret_cast<const f32x4*>(p);
+    const f32x4 b = *reinterpret_cast<const f32x4*>(p + 4);
+    const float x[8] = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      hi[e] = (T)x[e];
+      lo[e] = (T)(x[e] - as_operand<T>(x[e]));
+    }
+  }
+}
+
+// Wave-wide sum (64 lanes).
+__device__ inline float wave_sum(float x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o);
+  return x;
+}
+
+// ---------------------------------------------------------------------------
+// 2. Forward walk.
+// ---------------------------------------------------------------------------
+template <typename T, int D, int F>
+__global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_fwd_kernel(BwdKArgs ka) {
+  typedef BwdCfg<T, D, F> C;
+  typedef typename C::M M;
+  typedef typename C::op_t op_t;
+  typedef typename C::FM FM;
+  constexpr int f = C::f, E = M::E, KW = M::KW, NW = C::NW, RPW = C::RPW;
+  constexpr int NT = C::NT, NRT = C::NRT;
+  __shared__ typename C::SmemF sh;
+  const BackwardArgs& a = ka.a;
+
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+  const int li = lane & 31, hh = lane >> 5;
+  const int Hq = a.s.Hq, Hkv = a.s.Hkv, L = a.s.L, T_ = a.T;
+  const int units = a.s.B * Hq, nseg = ka.nseg;
+  const int vix = xcd_unit(blockIdx.x, units * nseg);
+  const int u = vix % units, seg = vix / units;
+  const int b = u / Hq, h = u % Hq, g = h / (Hq / Hkv);
+  const size_t qstride = (size_t)Hq * D, kstride = (size_t)Hkv * D;
+  const int col = w * kTile + li;
+  const int blk0 = seg * ka.seg_blocks, blk1 = min(ka.nblk, blk0 + ka.seg_blocks);
+  const bool tmode = a.target != nullptr;
+
+  // Starting state: the increments of the earlier segments (the sequence
+  // starts from an empty state).
+  f32x16 sacc[NRT];
+#pragma unroll
+  for (int rt = 0; rt < NRT; ++rt) sacc[rt] = f32x16{};
+  for (int r = tid; r < f; r += blockDim.x) sh.z[r] = 0.0f;
+  for (int sp = 0; sp < seg; ++sp) {
+    const float* src = ka.dS + ((size_t)u * (nseg - 1) + sp) * D * f;
+#pragma unroll
+    for (int rt = 0; rt < NRT; ++rt)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) sacc[rt][i] += src[(size_t)col * f + rt * kTile + row_of(i, hh)];
+    const float* zs = ka.dz + ((size_t)u * (nseg - 1) + sp) * f;
+    for (int r = tid; r < f; r += blockDim.x) sh.z[r] += zs[r];
+  }
+
+  const T* __restrict__ Wt_h = (const T*)a.W + (size_t)h * F * D;
+  op_t wop[FM::PPW][C::KD];
+  FM::load_w(Wt_h, w, li, hh, wop);
+  const float scale = 1.0f / sqrtf((float)D);
+  const float lw = log_sigmoid(a.alpha[h]);
+  const float one_minus_w = expf(log_sigmoid(-a.alpha[h]));
+  const bool row_ok = li < L;
+  const int lrow = min(li, L - 1);
+
+  f32x16 dwacc[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) dwacc[t] = f32x16{};
+  float dal = 0.0f, lss = 0.0f;
+
+  for (int blk = blk0; blk < blk1; ++blk) {
+    const size_t t0 = (size_t)blk * L;
+    const T* kb = (const T*)a.k + (((size_t)b * T_ + t0) * Hkv + g) * D;
+    const T* vb = (const T*)a.v + (((size_t)b * T_ + t0) * Hkv + g) * D;
+    const T* qb = (const T*)a.q + (((size_t)b * T_ + t0) * Hq + h) * D;
+    op_t kop[C::KD], qop[C::KD], vop[C::KL];
+    {
+      const T* krow = kb + (size_t)lrow * kstride + hh * E;
+      const T* qrow = qb + (size_t)lrow * qstride + hh * E;
+#pragma unroll
+      for (int ks = 0; ks < C::KD; ++ks) {
+        kop[ks] = keep_if<T>(row_ok, load_op<T>(krow + ks * KW));
+        qop[ks] = keep_if<T>(row_ok, load_op<T>(qrow + ks * KW));
+      }
+#pragma unroll
+      for (int ks = 0; ks < C::KL; ++ks)
+        vop[ks] = load_rows_op<T>(vb + col, kstride, ks, hh, L, false);
+    }
+
+    lds_barrier();  // the previous block's LDS readers are done
+    // S_{c-1} to LDS as operands (hi + lo): column col of every feature row.
+#pragma unroll
+    for (int rt = 0; rt < NRT; ++rt)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const T hi = from_f32<T>(sacc[rt][i]);
+        sh.st[0][rt * kTile + row_of(i, hh)][col] = hi;
+        if constexpr (C::NPART == 2)
+          sh.st[1][rt * kTile + row_of(i, hh)][col] = from_f32<T>(sacc[rt][i] - to_f32(hi));
+      }
+    float vk[FM::PPW][16], vq[FM::PPW][16];
+    FM::logits(wop, kop, w, li, hh, vk, sh.fk);
+    FM::logits(wop, qop, w, li, hh, vq, sh.fq);
+
+    // In-block softmax branch (keys in rows, queries in columns).
+    f32x16 acc_sm = {};
+    float m, den;
+    {
+      f32x16 sc = {};
+#pragma unroll
+      for (int ks = 0; ks < C::KD; ++ks) sc = M::mma(kop[ks], qop[ks], sc);
+      float p[16];
+      m = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        p[i] = row_of(i, hh) < L ? sc[i] * scale : -INFINITY;
+        m = fmaxf(m, p[i]);
+      }
+      m = fmaxf(m, xor32(m));
+      den = 0.0f;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        p[i] = row_of(i, hh) < L ? fast_exp(p[i] - m) : 0.0f;
+        den += p[i];
+      }
+      den += xor32(den);
+#pragma unroll
+      for (int ks = 0; ks < C::KL; ++ks)
+        acc_sm = mma_split_b<T>(vop[ks], &p[ks * E], acc_sm);
+    }
+
+    lds_barrier();
+    FM::exps(w, li, hh, vk, sh.fk);
+    FM::exps(w, li, hh, vq, sh.fq);
+    lds_barrier();
+    FM::scale(w, li, vk, sh.fk);
+    FM::scale(w, li, vq, sh.fq);
+    {
+      float lz = 0.0f;
+#pragma unroll
+      for (int j = 0; j < RPW; ++j) {
+        const int p = w + j * NW;
+        if (p >= NRT) continue;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int r = p * kTile + row_of(i, hh);
+          const float xk = row_ok ? vk[j][i] : 0.0f;
+          const T hi = from_f32<T>(xk);
+          sh.phiKT[0][r][li] = hi;
+          if constexpr (C::NPART == 2) sh.phiKT[1][r][li] = from_f32<T>(xk - to_f32(hi));
+          const T qh = from_f32<T>(vq[j][i]);
+          sh.phiQ[0][li][r] = qh;
+          if constexpr (C::NPART == 2) sh.phiQ[1][li][r] = from_f32<T>(vq[j][i] - to_f32(qh));
+          lz += vq[j][i] * sh.z[r];
+        }
+      }
+      lz += xor32(lz);
+      if (hh == 0) sh.lden[w][li] = lz;
+    }
+    lds_barrier();
+
+    // Readout against the state of the blocks before this one.
+    f32x16 acc_lin = {};
+    float lden = 0.0f;
+#pragma unroll
+    for (int ww = 0; ww < NW; ++ww) lden += sh.lden[ww][li];
+    // (both operands as hi + lo pairs on the bf16 path: hi*hi + lo*hi + hi*lo)
+#pragma unroll
+    for (int ks = 0; ks < f / KW; ++ks) {
+      const op_t pb = lds_op_perm<T>(&sh.phiQ[0][li][0], ks, hh, 0);
+      const int rt = ks / C::KL, kk = ks % C::KL;
+      acc_lin = M::mma(acc_op<T>(sacc[rt], kk), pb, acc_lin);
+      if constexpr (C::NPART == 2) {
+        acc_lin = M::mma(acc_op_lo<T>(sacc[rt], kk), pb, acc_lin);
+        acc_lin = M::mma(acc_op<T>(sacc[rt], kk), lds_op_perm<T>(&sh.phiQ[1][li][0], ks, hh, 0),
+                         acc_lin);
+      }
+    }
+    // Merge (scaled by exp(-c) so nothing overflows): out = N / D with
+    // w sm_den = exp(la) den, lin_den = exp(lb), c = max(la, lb).
+    float ca = 1.0f, cz = 0.0f, rz = 0.0f, cmax = lw + m;
+    if (lden > 0.0f) {
+      const float la = lw + m, lb = logf(lden);
+      cmax = fmaxf(la, lb);
+      ca = expf(la - cmax);
+      cz = expf(lb - cmax);
+      rz = 1.0f / lden;
+    }
+    const float inv = 1.0f / (ca * den + cz);
+    // upstream gradient (or the teacher's output): query li, columns
+    // 32w + row_of(i, hh)
+    float gq[16];
+    float go_p = 0.0f, gs_p = 0.0f;
+    const T* gsrc = (const T*)(tmode ? a.target : a.dout) +
+                    (((size_t)b * T_ + t0 + lrow) * Hq + h) * D + w * kTile;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const float gin = row_ok ? to_f32(gsrc[row_of(i, hh)]) : 0.0f;
+      const float o = (ca * acc_sm[i] + cz * (acc_lin[i] * rz)) * inv;
+      if (tmode) {
+        const float e = row_ok ? o - gin : 0.0f;
+        lss += e * e;
+        gq[i] = 2.0f * e;
+      } else {
+        gq[i] = gin;
+      }
+      go_p += gq[i] * o;
+      gs_p += gq[i] * acc_sm[i];
+    }
+    go_p += xor32(go_p);
+    gs_p += xor32(gs_p);
+    if (hh == 0) {
+      sh.red[w][li][0] = go_p;
+      sh.red[w][li][1] = gs_p;
+    }
+    lds_barrier();
+    float go = 0.0f, gs = 0.0f;
+#pragma unroll
+    for (int ww = 0; ww < NW; ++ww) {
+      go += sh.red[ww][li][0];
+      gs += sh.red[ww][li][1];
+    }
+    // 1/D = inv exp(-c); dL/dalpha = dL/dw w(1-w), and
+    // dL/dw = exp(m - c) inv (g.acc_sm - (g.out) den) with exp(m - c) w = ca.
+    const float rD = inv * expf(-cmax);
+    const float gD = -rD * go;
+    if (w == 0 && hh == 0 && row_ok) dal += ca * one_minus_w * inv * (gs - go * den);
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const float x = rD * gq[i];
+      const T hi = from_f32<T>(x);
+      sh.gn[0][li][w * kTile + row_of(i, hh)] = hi;
+      if constexpr (C::NPART == 2) sh.gn[1][li][w * kTile + row_of(i, hh)] = from_f32<T>(x - to_f32(hi));
+    }
+    if (w == 0 && hh == 0) sh.gd[li] = row_ok ? gD : 0.0f;
+    lds_barrier();
+
+    // dL/dN^T and dL/dD for the reverse pass: 8 queries of one column per
+    // item, written contiguously.
+    {
+      float* gnT = ka.gnT + ((size_t)u * ka.nblk + blk) * D * kTile;
+      for (int it = tid; it < D * 4; it += blockDim.x) {
+        const int c = it >> 2, i0 = (it & 3) * 8;
+        float x[8];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          x[e] = to_f32(sh.gn[0][i0 + e][c]);
+          if constexpr (C::NPART == 2) x[e] += to_f32(sh.gn[1][i0 + e][c]);
+        }
+        f32x4* dst = reinterpret_cast<f32x4*>(gnT + (size_t)c * kTile + i0);
+        dst[0] = f32x4{x[0], x[1], x[2], x[3]};
+        dst[1] = f32x4{x[4], x[5], x[6], x[7]};
+      }
+      if (tid < kTile) ka.gd[((size_t)u * ka.nblk + blk) * kTile + tid] = sh.gd[tid];
+    }
+
+    // dL/dphi(q_i) for the feature tiles this wave owns: rows r of tile p,
+    // columns i; S_{c-1} rows from LDS are the A operand (contraction over d).
+    float dphi[RPW][16];
+#pragma unroll
+    for (int j = 0; j < RPW; ++j) {
+      const int p = w + j * NW;
+      if (p >= NRT) continue;
+      f32x16 dq = {};
+#pragma unroll
+      for (int s = 0; s < NW; ++s)
+#pragma unroll
+        for (int ks = 0; ks < C::KL; ++ks)
+        {
+          const op_t ah = lds_op_perm<T>(&sh.st[0][p * kTile + li][0], ks, hh, s * kTile);
+          const op_t bh = lds_op_perm<T>(&sh.gn[0][li][0], ks, hh, s * kTile);
+          dq = M::mma(ah, bh, dq);
+          if constexpr (C::NPART == 2) {
+            dq = M::mma(lds_op_perm<T>(&sh.st[1][p * kTile + li][0], ks, hh, s * kTile), bh, dq);
+            dq = M::mma(ah, lds_op_perm<T>(&sh.gn[1][li][0], ks, hh, s * kTile), dq);
+          }
+        }
+      const float gdi = sh.gd[li];
+      float js = 0.0f;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        dphi[j][i] = dq[i] + gdi * sh.z[p * kTile + row_of(i, hh)];
+        js += dphi[j][i] * vq[j][i];
+      }
+      js += xor32(js);
+      if (hh == 0) sh.jsum[p][li] = js;
+    }
+    lds_barrier();
+    // Feature-map backward: dL/du for each sign, transposed into LDS.
+#pragma unroll
+    for (int j = 0; j < RPW; ++j) {
+      const int p = w + j * NW;
+      if (p >= NRT) continue;
+      const int sg = p / NT, t = p % NT;
+      float ssum = 0.0f;
+#pragma unroll
+      for (int tt = 0; tt < NT; ++tt) ssum += sh.jsum[sg * NT + tt][li];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        float du = row_ok ? vq[j][i] * (dphi[j][i] - ssum) : 0.0f;
+        if (sg) du = -du;
+        const int jr = t * kTile + row_of(i, hh);
+        const T hi = from_f32<T>(du);
+        sh.duT[sg][0][jr][li] = hi;
+        if constexpr (C::NPART == 2) sh.duT[sg][1][jr][li] = from_f32<T>(du - to_f32(hi));
+      }
+    }
+    op_t qtop[C::KL];
+#pragma unroll
+    for (int ks = 0; ks < C::KL; ++ks)
+      qtop[ks] = load_rows_op<T>(qb + col, qstride, ks, hh, L, false);
+    lds_barrier();
+    // dW^T tiles (rows j of tile t, columns 32w..): += dL/du^T Q.
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int sg = 0; sg < 2; ++sg)
+#pragma unroll
+        for (int part = 0; part < C::NPART; ++part)
+#pragma unroll
+          for (int ks = 0; ks < C::KL; ++ks)
+            dwacc[t] = M::mma(lds_op_perm<T>(&sh.duT[sg][part][t * kTile + li][0], ks, hh, 0),
+                              qtop[ks], dwacc[t]);
+    // Commit the block into S (columns 32w..).
+#pragma unroll
+    for (int rt = 0; rt < NRT; ++rt)
+#pragma unroll
+      for (int ks = 0; ks < C::KL; ++ks)
+#pragma unroll
+        for (int part = 0; part < C::NPART; ++part)
+          sacc[rt] = M::mma(lds_op_perm<T>(&sh.phiKT[part][rt * kTile + li][0], ks, hh, 0),
+                            vop[ks], sacc[rt]);
+    // z += sum_t phi(k_t) (every reader of z in this block is past the last
+    // barrier).
+    for (int r = tid; r < f; r += blockDim.x) {
+      float s = 0.0f;
+#pragma unroll
+      for (int part = 0; part < C::NPART; ++part)
+        for (int t = 0; t < kTile; ++t) s += to_f32(sh.phiKT[part][r][t]);
+      sh.z[r] += s;
+    }
+  }
+
+  // Partials of this (request, head, segment).
+  float* dwq = ka.dwq + ((size_t)u * nseg + seg) * F * D;
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) dwq[(size_t)(t * kTile + row_of(i, hh)) * D + col] = dwacc[t][i];
+  dal = wave_sum(dal);
+  lss = wave_sum(lss);
+  if (lane == 0) {
+    sh.fin[w][0] = dal;
+    sh.fin[w][1] = lss;
+  }
+  lds_barrier();
+  if (tid == 0) {
+    float x0 = 0.0f, x1 = 0.0f;
+    for (int ww = 0; ww < NW; ++ww) {
+      x0 += sh.fin[ww][0];
+      x1 += sh.fin[ww][1];
+    }
+    ka.red[((size_t)u * nseg + seg) * 2] = x0;
+    ka.red[((size_t)u * nseg + seg) * 2 + 1] = x1;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// 3./4. Reverse walk (delta: only the segment's Gbar sum).
+// ---------------------------------------------------------------------------
+template <typename T, int D, int F>
+__global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_rev_kernel(BwdKArgs ka, int delta) {
+  typedef BwdCfg<T, D, F> C;
+  typedef typename C::M M;
+  typedef typename C::op_t op_t;
+  typedef typename C::FM FM;
+  constexpr int f = C::f, E = M::E, KW = M::KW, NW = C::NW, RPW = C::RPW;
+  constexpr int NT = C::NT, NRT = C::NRT;
+  __shared__ typename C::SmemB sh;
+  const BackwardArgs& a = ka.a;
+
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+  const int li = lane & 31, hh = lane >> 5;
+  const int Hq = a.s.Hq, Hkv = a.s.Hkv, L = a.s.L, T_ = a.T;
+  const int units = a.s.B * Hq, nseg = ka.nseg;
+  // delta covers segments 1 .. nseg-1 (segment 0's sum is never needed)
+  const int nseg_here = delta ? nseg - 1 : nseg;
+  const int vix = xcd_unit(blockIdx.x, units * nseg_here);
+  const int u = vix % units, seg = vix / units + (delta ? 1 : 0);
+  const int b = u / Hq, h = u % Hq, g = h / (Hq / Hkv);
+  const size_t qstride = (size_t)Hq * D, kstride = (size_t)Hkv * D;
+  const int col = w * kTile + li;
+  const int blk0 = seg * ka.seg_blocks, blk1 = min(ka.nblk, blk0 + ka.seg_blocks);
+
+  // Gbar^T tiles (rows c of slice s, columns of feature tile p) and gz:
+  // the sums over the later segments.
+  f32x16 gacc[RPW][NW];
+#pragma unroll
+  for (int j = 0; j < RPW; ++j)
+#pragma unroll
+    for (int s = 0; s < NW; ++s) gacc[j][s] = f32x16{};
+  for (int r = tid; r < f; r += blockDim.x) sh.gz[r] = 0.0f;
+  if (!delta) {
+    for (int sp = seg + 1; sp < nseg; ++sp) {
+      const float* src = ka.dG + ((size_t)u * nseg + sp) * D * f;
+#pragma unroll
+      for (int j = 0; j < RPW; ++j) {
+        const int p = w + j * NW;
+        if (p >= NRT) continue;
+#pragma unroll
+        for (int s = 0; s < NW; ++s)
+#pragma unroll
+          for (int i = 0; i < 16; ++i)
+            gacc[j][s][i] += src[(size_t)(s * kTile + row_of(i, hh)) * f + p * kTile + li];
+      }
+      const float* zs = ka.dgz + ((size_t)u * nseg + sp) * f;
+      for (int r = tid; r < f; r += blockDim.x) sh.gz[r] += zs[r];
+    }
+  }
+
+  const T* __restrict__ Wt_h = (const T*)a.W + (size_t)h * F * D;
+  op_t wop[FM::PPW][C::KD];
+  FM::load_w(Wt_h, w, li, hh, wop);
+  const bool row_ok = li < L;
+  const int lrow = min(li, L - 1);
+  f32x16 dwacc[NT];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) dwacc[t] = f32x16{};
+
+  for (int blk = blk1 - 1; blk >= blk0; --blk) {
+    const size_t t0 = (size_t)blk * L;
+    const T* kb = (const T*)a.k + (((size_t)b * T_ + t0) * Hkv + g) * D;
+    const T* vb = (const T*)a.v + (((size_t)b * T_ + t0) * Hkv + g) * D;
+    const T* qb = (const T*)a.q + (((size_t)b * T_ + t0) * Hq + h) * D;
+    const float* gnT = ka.gnT + ((size_t)u * ka.nblk + blk) * D * kTile;
+    op_t qop[C::KD], kop[C::KD], vrow[NW][C::KL], ktop[C::KL];
+    {
+      const T* qrow = qb + (size_t)lrow * qstride + hh * E;
+#pragma unroll
+      for (int ks = 0; ks < C::KD; ++ks) qop[ks] = keep_if<T>(row_ok, load_op<T>(qrow + ks * KW));
+      if (!delta) {
+        const T* krow = kb + (size_t)lrow * kstride + hh * E;
+        const T* vr = vb + (size_t)lrow * kstride;
+#pragma unroll
+        for (int ks = 0; ks < C::KD; ++ks) kop[ks] = keep_if<T>(row_ok, load_op<T>(krow + ks * KW));
+#pragma unroll
+        for (int s = 0; s < NW; ++s)
+#pragma unroll
+          for (int ks = 0; ks < C::KL; ++ks)
+            vrow[s][ks] = keep_if<T>(row_ok, lds_op_perm<T>(vr, ks, hh, s * kTile));
+#pragma unroll
+        for (int ks = 0; ks < C::KL; ++ks)
+          ktop[ks] = load_rows_op<T>(kb + col, kstride, ks, hh, L, false);
+      }
+    }
+    const float gdl = ka.gd[((size_t)u * ka.nblk + blk) * kTile + li];
+
+    lds_barrier();  // the previous block's LDS readers are done
+    float vq[FM::PPW][16], vk[FM::PPW][16];
+    FM::logits(wop, qop, w, li, hh, vq, sh.fq);
+    if (!delta) FM::logits(wop, kop, w, li, hh, vk, sh.fk);
+    lds_barrier();
+    FM::exps(w, li, hh, vq, sh.fq);
+    if (!delta) FM::exps(w, li, hh, vk, sh.fk);
+    lds_barrier();
+    FM::scale(w, li, vq, sh.fq);
+    if (!delta) FM::scale(w, li, vk, sh.fk);
+#pragma unroll
+    for (int j = 0; j < RPW; ++j) {
+      const int p = w + j * NW;
+      if (p >= NRT) continue;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int r = p * kTile + row_of(i, hh);
+        const float x = row_ok ? vq[j][i] : 0.0f;
+        const T hi = from_f32<T>(x);
+        sh.phiQT[0][r][li] = hi;
+        if constexpr (C::NPART == 2) sh.phiQT[1][r][li] = from_f32<T>(x - to_f32(hi));
+      }
+    }
+    if (w == 0 && hh == 0) sh.gd[li] = gdl;
+
+    float dphi[RPW][16];
+    if (!delta) {
+      // dL/dphi(k_t) = Gbar v_t + gz, with Gbar over the later blocks only.
+#pragma unroll
+      for (int j = 0; j < RPW; ++j) {
+        const int p = w + j * NW;
+        if (p >= NRT) continue;
+        f32x16 dk = {};
+#pragma unroll
+        for (int s = 0; s < NW; ++s)
+#pragma unroll
+          for (int ks = 0; ks < C::KL; ++ks)
+          {
+            dk = M::mma(acc_op<T>(gacc[j][s], ks), vrow[s][ks], dk);
+            if constexpr (C::NPART == 2) dk = M::mma(acc_op_lo<T>(gacc[j][s], ks), vrow[s][ks], dk);
+          }
+        float js = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          dphi[j][i] = dk[i] + sh.gz[p * kTile + row_of(i, hh)];
+          js += dphi[j][i] * vk[j][i];
+        }
+        js += xor32(js);
+        if (hh == 0) sh.jsum[p][li] = js;
+      }
+    }
+    lds_barrier();
+    if (!delta) {
+#pragma unroll
+      for (int j = 0; j < RPW; ++j) {
+        const int p = w + j * NW;
+        if (p >= NRT) continue;
+        const int sg = p / NT, t = p % NT;
+        float ssum = 0.0f;
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt) ssum += sh.jsum[sg * NT + tt][li];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          float du = row_ok ? vk[j][i] * (dphi[j][i] - ssum) : 0.0f;
+          if (sg) du = -du;
+          const int jr = t * kTile + row_of(i, hh);
+          const T hi = from_f32<T>(du);
+          sh.duT[sg][0][jr][li] = hi;
+          if constexpr (C::NPART == 2) sh.duT[sg][1][jr][li] = from_f32<T>(du - to_f32(hi));
+        }
+      }
+    }
+    // gz += sum_i phi(q_i) dL/dD_i (gz is not read again in this block).
+    for (int r = tid; r < f; r += blockDim.x) {
+      float s = 0.0f;
+#pragma unroll
+      for (int part = 0; part < C::NPART; ++part)
+        for (int i = 0; i < kTile; ++i) s += to_f32(sh.phiQT[part][r][i]) * sh.gd[i];
+      sh.gz[r] += s;
+    }
+    // Gbar^T += dL/dN^T phi(Q): rows c of slice s, columns of tile p; the
+    // query index runs in natural order on both operands.
+#pragma unroll
+    for (int j = 0; j < RPW; ++j) {
+      const int p = w + j * NW;
+      if (p >= NRT) continue;
+#pragma unroll
+      for (int s = 0; s < NW; ++s)
+#pragma unroll
+        for (int ks = 0; ks < C::KL; ++ks) {
+          op_t gh, gl;
+          load_split_op<T>(gnT + (size_t)(s * kTile + li) * kTile + ks * KW + hh * E, gh, gl);
+          const op_t ph = load_op<T>(&sh.phiQT[0][p * kTile + li][ks * KW + hh * E]);
+          gacc[j][s] = M::mma(gh, ph, gacc[j][s]);
+          if constexpr (C::NPART == 2) {
+            gacc[j][s] = M::mma(gl, ph, gacc[j][s]);
+            gacc[j][s] = M::mma(gh, load_op<T>(&sh.phiQT[1][p * kTile + li][ks * KW + hh * E]),
+                                gacc[j][s]);
+          }
+        }
+    }
+    if (!delta) {
+      lds_barrier();
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int sg = 0; sg < 2; ++sg)
+#pragma unroll
+          for (int part = 0; part < C::NPART; ++part)
+#pragma unroll
+            for (int ks = 0; ks < C::KL; ++ks)
+              dwacc[t] = M::mma(lds_op_perm<T>(&sh.duT[sg][part][t * kTile + li][0], ks, hh, 0),
+                                ktop[ks], dwacc[t]);
+    }
+  }
+
+  if (delta) {
+    float* dst = ka.dG + ((size_t)u * nseg + seg) * D * f;
+#pragma unroll
+    for (int j = 0; j < RPW; ++j) {
+      const int p = w + j * NW;
+      if (p >= NRT) continue;
+#pragma unroll
+      for (int s = 0; s < NW; ++s)
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          dst[(size_t)(s * kTile + row_of(i, hh)) * f + p * kTile + li] = gacc[j][s][i];
+    }
+    lds_barrier();
+    float* zd = ka.dgz + ((size_t)u * nseg + seg) * f;
+    for (int r = tid; r < f; r += blockDim.x) zd[r] = sh.gz[r];
+  } else {
+    float* dwk = ka.dwk + ((size_t)u * nseg + seg) * F * D;
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) dwk[(size_t)(t * kTile + row_of(i, hh)) * D + col] = dwacc[t][i];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// 5. Sum of the partials over requests and segments, in a fixed order.
+// ---------------------------------------------------------------------------
+__global__ void hyb_bwd_reduce_kernel(BwdKArgs ka) {
+  const BackwardArgs& a = ka.a;
+  const int Hq = a.s.Hq, F = a.s.F, D = a.s.D, nseg = ka.nseg;
+  const size_t per = (size_t)F * D;
+  const size_t idx = (size_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx < (size_t)Hq * per) {
+    const int h = (int)(idx / per);
+    const size_t e = idx % per;
+    float s = 0.0f;
+    for (int b = 0; b < a.s.B; ++b) {
+      const size_t u = (size_t)b * Hq + h;
+      for (int sg = 0; sg < nseg; ++sg) {
+        const size_t o = (u * nseg + sg) * per + e;
+        s += ka.dwq[o] + ka.dwk[o];
+      }
+    }
+    a.dW[idx] = s;
+  }
+  if (idx < (size_t)Hq) {
+    float s0 = 0.0f, s1 = 0.0f;
+    for (int b = 0; b < a.s.B; ++b) {
+      const size_t u = (size_t)b * Hq + idx;
+      for (int sg = 0; sg < nseg; ++sg) {
+        s0 += ka.red[(u * nseg + sg) * 2];
+        s1 += ka.red[(u * nseg + sg) * 2 + 1];
+      }
+    }
+    a.dalpha[idx] = s0;
+    if (a.loss) a.loss[idx] = s1;
+  }
+}
+
+template <typename T, int D, int F>
+static hipError_t bwd_go(const BackwardArgs& a, hipStream_t st) {
+  const Shape& s = a.s;
+  const int units = s.B * s.Hq, nblk = a.T / s.L;
+  const int nseg = prefill_segments(s, a.T);
+  const int seg_blocks = (nblk + nseg - 1) / nseg;
+  const BwdLayout l = bwd_layout(s, a.T);
+  char* ws = (char*)a.ws;
+  const size_t f = 2 * (size_t)s.F;
+  BwdKArgs ka;
+  ka.a = a;
+  ka.nseg = nseg;
+  ka.seg_blocks = seg_blocks;
+  ka.nblk = nblk;
+  ka.dS = (float*)(ws + l.dS);
+  ka.dz = ka.dS + (size_t)units * (nseg - 1) * s.D * f;
+  ka.dG = (float*)(ws + l.dG);
+  ka.dgz = (float*)(ws + l.dgz);
+  ka.gnT = (float*)(ws + l.gnT);
+  ka.gd = (float*)(ws + l.gd);
+  ka.dwq = (float*)(ws + l.dwq);
+  ka.dwk = (float*)(ws + l.dwk);
+  ka.red = (float*)(ws + l.red);
+  const dim3 block(kWave * (D / kTile));
+  hipError_t e;
+  if (nseg > 1) {
+    // 1. each segment's own state increment (the prefill's delta launch)
+    PrefillArgs pa{s, a.T, nullptr, a.k, a.v, a.W, nullptr, nullptr, nullptr,
+                   nullptr, nullptr, ka.dS};
+    pa.s.n_slots = s.B;
+    if ((e = launch_prefill_delta(pa, st)) != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL((hyb_bwd_fwd_kernel<T, D, F>), dim3(units * nseg), block, 0, st, ka);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (nseg > 1) {
+    hipLaunchKernelGGL((hyb_bwd_rev_kernel<T, D, F>), dim3(units * (nseg - 1)), block, 0, st,
+                       ka, 1);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL((hyb_bwd_rev_kernel<T, D, F>), dim3(units * nseg), block, 0, st, ka, 0);
+  if ((e = hipGetLastError()) != hipSuccess) return e;
+  const size_t n = (size_t)s.Hq * s.F * s.D;
+  hipLaunchKernelGGL(hyb_bwd_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
+                     ka);
+  return hipGetLastError();
+}
+
+template <typename T, int D>
+static hipError_t bwd_f(const BackwardArgs& a, hipStream_t st) {
+  switch (a.s.F) {
+    case 32: return bwd_go<T, D, 32>(a, st);
+    case 64: return bwd_go<T, D, 64>(a, st);
+  }
+  return hipErrorInvalidValue;
+}
+
+template <typename T>
+static hipError_t bwd_d(const BackwardArgs& a, hipStream_t st) {
+  switch (a.s.D) {
+    case 64: return bwd_f<T, 64>(a, st);
+    case 128: return bwd_f<T, 128>(a, st);
+  }
+  return hipErrorInvalidValue;
+}
+
+bool backward_supported(const Shape& s) { return s.F == 32 || s.F == 64; }
+
+hipError_t launch_backward(const BackwardArgs& a, hipStream_t st) {
+  return a.s.dtype == 1 ? bwd_d<bf16>(a, st) : bwd_d<float>(a, st);
+}
+
+}  // namespace hyb

@@ -99,6 +99,25 @@ struct FeatMap {
     }
   }
 
+  // After a second barrier: normalise in place.  val[j][i] then holds
+  // feature 32p + row_of(i, hh) of row li, p = w + j*NW (F = 32*NT, so the
+  // pair index is also the 32-feature tile index).
+  __device__ static inline void scale(int w, int li, float (&val)[PPW][16],
+                                      const Smem& sh) {
+#pragma unroll
+    for (int j = 0; j < PPW; ++j) {
+      if (!owns(w, j)) continue;
+      const int p = w + j * NW;
+      const int base = (p / NT) * NT;
+      float s = 0.0f;
+#pragma unroll
+      for (int t = 0; t < NT; ++t) s += sh.sm[base + t][li];
+      const float inv = 1.0f / s;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) val[j][i] *= inv;
+    }
+  }
+
   // After a second barrier: normalise and hand every group of 4 consecutive
   // features of row li to store(first_feature, x[4]).
   template <typename Store>

@@ -44,6 +44,20 @@ struct PrefillArgs {
   float* ws;  // per-segment state deltas (nseg > 1), caller's workspace
 };
 
+// Backward of the block-causal hybrid layer over T tokens (empty starting
+// state) with respect to W and alpha.  Exactly one of dout (upstream
+// gradient) and target (teacher output: squared-error objective) is set.
+struct BackwardArgs {
+  Shape s;
+  int T;
+  const void *q, *k, *v, *W;
+  const float* alpha;
+  const void* dout;
+  const void* target;
+  float *dW, *dalpha, *loss;  // loss may be null
+  void* ws;
+};
+
 struct SoftmaxPrefixArgs {
   Shape s;
   const void *q, *k, *v, *k_cache, *v_cache;
@@ -66,6 +80,13 @@ hipError_t launch_softmax_prefix(const SoftmaxPrefixArgs& a, hipStream_t st);
 // Prefill: number of sequence segments and the workspace they need.
 int prefill_segments(const Shape& s, int T);
 size_t prefill_ws_bytes(const Shape& s, int T);
+// The prefill's first launch alone: each segment's state increment (all
+// segments but the last) into a.ws; a.S, a.z, a.q, a.alpha are not used.
+hipError_t launch_prefill_delta(const PrefillArgs& a, hipStream_t st);
+
+hipError_t launch_backward(const BackwardArgs& a, hipStream_t st);
+bool backward_supported(const Shape& s);
+size_t backward_ws_bytes(const Shape& s, int T);
 
 // Workspace of softmax_prefix_step for n_split splits.
 size_t softmax_prefix_ws_bytes(const Shape& s, int n_split);

@@ -345,6 +345,33 @@ static hipError_t prefill_go(const PrefillArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+template <typename T, int D, int F>
+static hipError_t prefill_delta_go(const PrefillArgs& a, hipStream_t st) {
+  const int units = a.s.B * a.s.Hq, nblk = a.T / a.s.L;
+  const int nseg = prefill_segments(a.s, a.T);
+  const int seg_blocks = (nblk + nseg - 1) / nseg;
+  if (nseg <= 1) return hipSuccess;
+  hipLaunchKernelGGL((hyb_prefill_kernel<T, D, F>), dim3(units * (nseg - 1)),
+                     dim3(kWave * (D / kTile)), 0, st, a, nseg, seg_blocks, 1);
+  return hipGetLastError();
+}
+
+template <typename T, int D>
+static hipError_t prefill_delta_f(const PrefillArgs& a, hipStream_t st) {
+  switch (a.s.F) {
+    case 32: return prefill_delta_go<T, D, 32>(a, st);
+    case 64: return prefill_delta_go<T, D, 64>(a, st);
+    case 128: return prefill_delta_go<T, D, 128>(a, st);
+  }
+  return hipErrorInvalidValue;
+}
+
+hipError_t launch_prefill_delta(const PrefillArgs& a, hipStream_t st) {
+  if (a.s.dtype == 1)
+    return a.s.D == 64 ? prefill_delta_f<bf16, 64>(a, st) : prefill_delta_f<bf16, 128>(a, st);
+  return a.s.D == 64 ? prefill_delta_f<float, 64>(a, st) : prefill_delta_f<float, 128>(a, st);
+}
+
 // Segments: enough (request, head, segment) workgroups to cover the chip
 // about twice, at most 8 segments (the walk of segment s reads the s earlier
 // increments) and at least 4 blocks per segment.

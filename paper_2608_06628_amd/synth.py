@@ -91,6 +91,16 @@ def feature_weights(dims: Dims, seed_w: int, seed_a: int, w_std: float = 0.02):
     return Wt, alpha
 
 
+def sequence_qkv(dims: Dims, T: int, seed: int, scale: float = 1.0):
+    """Training-sequence q [B][T][Hq][d], k, v [B][T][Hkv][d] ~ N(0, scale^2)."""
+    return block_qkv(dims.with_(L=T), seed, scale)
+
+
+def upstream(dims: Dims, T: int, seed: int, std: float = 1.0) -> np.ndarray:
+    """An upstream gradient or a teacher output [B][T][Hq][d] ~ N(0, std^2)."""
+    return to_dtype(gaussian(seed, (dims.B, T, dims.Hq, dims.d), std), dims.dtype)
+
+
 def prefix_kv(B: int, P: int, Hkv: int, d: int, seed: int, scale: float, dtype: str):
     """Committed-prefix keys and values [B][P][Hkv][d] ~ N(0, scale^2)."""
     rng = np.random.default_rng(seed)
@@ -112,6 +122,10 @@ DECODE1 = Dims(B=1, Hq=16, Hkv=4, d=128, L=32, F=64, dtype="bf16")
 SERVE64 = Dims(B=64, Hq=16, Hkv=4, d=128, L=32, F=64, dtype="bf16")
 PREFILL8 = Dims(B=8, Hq=16, Hkv=4, d=128, L=32, F=64, dtype="bf16")
 MIX128 = Dims(B=128, Hq=16, Hkv=4, d=128, L=32, F=64, dtype="bf16")
+# Stage-1 attention transfer: 8 sequences of 2048 tokens (training examples
+# are truncated to 2048 tokens), one linearised layer.
+TRAIN8 = Dims(B=8, Hq=16, Hkv=4, d=128, L=32, F=64, dtype="bf16")
+TRAIN8_T = 2048
 
 TINY_PREFIX = 32            # 4 committed blocks of 8 tokens
 DECODE1_PREFIX = 4096

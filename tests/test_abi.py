@@ -181,3 +181,49 @@ def test_workspace_query():
     assert ws % (128 * 16 * 32 * 130 * 4) == 0 and ws > 0
     assert lib.hybrid_workspace_bytes(ctypes.byref(_dims(head_dim=5)), hb.OP_STEP, 0) == 0
     assert lib.hybrid_workspace_bytes(None, hb.OP_STEP, 0) == 0
+
+
+def test_backward_validation():
+    lib = hb.load()
+    d = _dims(feat_dim=128)
+    T = 64
+    need = lib.hybrid_workspace_bytes(ctypes.byref(d), hb.OP_BACKWARD, T)
+    assert need > 0
+    assert lib.hybrid_workspace_bytes(ctypes.byref(_dims(feat_dim=256)), hb.OP_BACKWARD, T) == 0
+    assert lib.hybrid_workspace_bytes(ctypes.byref(d), hb.OP_BACKWARD, 40) == 0
+    # q k v W alpha dout target dW dalpha loss ws
+    ok = [_addr(i) for i in range(11)]
+    ok[6] = None   # dout mode
+    ok[9] = None   # no loss without a target
+    call = lambda p, dims=d, t=T, n=need: lib.hybrid_attn_backward(
+        ctypes.byref(dims), t, *p[:10], p[10], n, None)
+    for i in (0, 1, 2, 3, 4, 7, 8, 10):
+        p = list(ok)
+        p[i] = None
+        assert call(p) == (6 if i == 10 else 1), i
+        p[i] = MISALIGNED
+        assert call(p) == 3, i
+    p = list(ok)
+    p[6] = _addr(6)                          # dout and target
+    assert call(p) == 2 and "exactly one" in hb.last_error()
+    p = list(ok)
+    p[5] = None                              # neither
+    assert call(p) == 2
+    p = list(ok)
+    p[9] = _addr(9)                          # loss without a target
+    assert call(p) == 2
+    assert call(list(ok), _dims(feat_dim=256)) == 5
+    assert call(list(ok), _dims(feat_dim=128, flags=1)) == 2
+    assert call(list(ok), d, 48) == 2        # not a multiple of the block
+    assert call(list(ok), d, T, need - 1) == 6
+    # written buffers dW (7), dalpha (8), ws (10) against the inputs and each other
+    for w_i in (7, 8, 10):
+        for r_i in (0, 1, 2, 3, 4, 5, 7, 8, 10):
+            if r_i == w_i:
+                continue
+            p = list(ok)
+            p[w_i] = p[r_i]
+            assert call(p) == 2, (w_i, r_i)
+            assert "overlap" in hb.last_error()
+    assert lib.hybrid_attn_backward(ctypes.byref(_dims(batch=0, feat_dim=128)), T,
+                                    *([None] * 11), 0, None) == 0
