@@ -106,6 +106,18 @@ def prefill_flops(B, T, Hq, d, L, f):
     return B * Hq * nblk * per_blk
 
 
+def backward_flops(B, T, Hq, d, L, f):
+    """Stage-1 backward, counted once per product (the forward it needs, then
+    the reverse mode): per block phi(Q), phi(K), QK^T, PV, the readout, the
+    commit; dL/dphi(Q), the query part of dW, dL/dphi(K), the Gbar update and
+    the key part of dW."""
+    F = f // 2
+    nblk = T // L
+    fwd = 2 * (2 * L * d * F) + 2 * (2 * L * L * d) + 2 * (2 * L * f * d)
+    bwd = 2 * L * f * d + 2 * L * F * d + 2 * L * f * d + 2 * L * f * d + 2 * L * F * d
+    return B * Hq * nblk * (fwd + bwd)
+
+
 class Lane:
     """One rotating set of states and per-step block buffers."""
 
@@ -311,12 +323,14 @@ def run(args):
         result["prefill"] = bench_prefill(gen, dev)
         result["softmax_prefix"] = bench_mix(gen, dev)
         result["table3"] = bench_table3(gen, dev)
+        result["backward"] = bench_backward(gen, dev)
     if not args.no_cpu_baseline:
         log("timing the fp64 oracle on the host cores")
         result["cpu_baseline"] = cpu_baseline(dims, args.cpu_requests, plens)
         if not args.no_extras:
             result["prefill"]["cpu_oracle"] = cpu_prefill()
             result["softmax_prefix"]["cpu_oracle"] = cpu_softmax_prefix()
+            result["backward"]["cpu_oracle"] = cpu_backward()
     # The paper's own headline number, for context only: a different metric
     # (end-to-end decoding throughput of the whole model) on other hardware.
     result["paper_context"] = {
@@ -364,6 +378,58 @@ def cpu_softmax_prefix():
             "cores": _omp_threads(), "kind": "oracle",
             "sample": f"1 request x 16 heads over a {P}-token prefix in {el:.2f} s, fp64; "
                       f"B=128 extrapolated x128"}
+
+
+def cpu_backward():
+    """The fp64 oracle's backward (attention-transfer mode) of one 2048-token
+    sequence, all 16 heads, timed on the host cores."""
+    import oracle
+    dims = synth.TRAIN8.with_(B=1)
+    T = synth.TRAIN8_T
+    q, k, v = synth.sequence_qkv(dims, T, 31, 1.0)
+    Wt, alpha = synth.feature_weights(dims, 32, 33, 1.0 / math.sqrt(dims.d))
+    tgt = synth.upstream(dims, T, 34, 0.05)
+    t0 = time.perf_counter()
+    oracle.backward(q, k, v, Wt, alpha, dims.L, target=tgt)
+    el = time.perf_counter() - t0
+    return {"training_tokens_per_s": T / el, "cores": _omp_threads(), "kind": "oracle",
+            "sample": f"1 sequence x {T} tokens, 16 heads, in {el:.1f} s, fp64"}
+
+
+def bench_backward(gen, dev):
+    """Stage-1 attention-transfer gradient (dW, dalpha and the loss against the
+    teacher's output) of one layer over B=8 sequences of 2048 tokens."""
+    dims = synth.TRAIN8
+    B, Hq, Hkv, d, L, f, T = dims.B, dims.Hq, dims.Hkv, dims.d, dims.L, dims.f, synth.TRAIN8_T
+    q = torch.randn((B, T, Hq, d), generator=gen, device=dev).to(torch.bfloat16)
+    k = torch.randn((B, T, Hkv, d), generator=gen, device=dev).to(torch.bfloat16)
+    v = torch.randn((B, T, Hkv, d), generator=gen, device=dev).to(torch.bfloat16)
+    tgt = (torch.randn((B, T, Hq, d), generator=gen, device=dev) * 0.05).to(torch.bfloat16)
+    Wt, alpha = synth.feature_weights(dims, 1, 2, 1.0 / math.sqrt(d))
+    W = torch.from_numpy(Wt).to(dev).to(torch.bfloat16)
+    al = torch.from_numpy(alpha).to(dev)
+    dW = torch.empty((Hq, dims.F, d), device=dev)
+    da = torch.empty(Hq, device=dev)
+    loss = torch.empty(Hq, device=dev)
+    ws = torch.empty(hb.workspace_bytes(hb.make_dims(B, Hq, Hkv, d, L, f, hb.HYB_BF16, 1),
+                                        hb.OP_BACKWARD, T), dtype=torch.uint8, device=dev)
+
+    def once():
+        hb.hybrid_attn_backward(q, k, v, W, al, L, target=tgt, dW=dW, dalpha=da, loss=loss, ws=ws)
+
+    once()
+    ms = time_region(once, 5)
+    fl = backward_flops(B, T, Hq, d, L, f)
+    byts = (q.numel() + k.numel() + v.numel() + tgt.numel()) * 2
+    log(f"backward train8 {ms:.3f} ms")
+    return {"workload": "train8: attention transfer of one layer, B=8 x 2048 tokens, 16q/4kv, "
+                        "d=128, f=128, blocks of 32, bf16, teacher-output target",
+            "ms": ms, "training_tokens_per_s": B * T / (ms * 1e-3),
+            "tflops": fl / (ms * 1e-3) / 1e12,
+            "mfma_frac": fl / (ms * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS,
+            "flops_per_call": fl, "input_bytes": byts,
+            "gbps_inputs": byts / (ms * 1e-3) / 1e9,
+            "ws_bytes": ws.numel()}
 
 
 def bench_prefill(gen, dev):
@@ -557,6 +623,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--only-table3", action="store_true",
                     help="run only the prefix-length x batch latency sweep and print it")
+    ap.add_argument("--only-backward", action="store_true",
+                    help="run only the attention-transfer backward timing and print it")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only copy 256 MiB device to device five times (the reference "
                          "kernel for scaling HBM byte counters), then exit")
@@ -568,6 +636,11 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.only_backward:
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(5)
+        print(json.dumps(bench_backward(gen, "cuda")), flush=True)
         return
     if args.only_table3:
         gen = torch.Generator(device="cuda")
