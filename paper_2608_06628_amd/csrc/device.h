@@ -244,6 +244,54 @@ __device__ inline void store_out8_nt(void* out, size_t idx, const float* v,
   }
 }
 
+// Eight consecutive outputs at element index idx (16-byte aligned): fp32 as
+// two 16-byte stores, bf16 as one.
+template <typename T>
+__device__ inline void store_out8(void* out, size_t idx, const float* v, bool f32) {
+  if (sizeof(T) == 4 || f32) {
+    f32x4* o = reinterpret_cast<f32x4*>((float*)out + idx);
+    o[0] = f32x4{v[0], v[1], v[2], v[3]};
+    o[1] = f32x4{v[4], v[5], v[6], v[7]};
+  } else {
+    *reinterpret_cast<bf16x8*>((bf16*)out + idx) =
+        bf16x8{(bf16)v[0], (bf16)v[1], (bf16)v[2], (bf16)v[3],
+               (bf16)v[4], (bf16)v[5], (bf16)v[6], (bf16)v[7]};
+  }
+}
+
+// x as a bf16 pair in one dword: hi = bf16(x) in the low half, lo =
+// bf16(x - hi) in the high half (about 16 significant bits together).
+__device__ inline uint32_t pack_hi_lo(float x) {
+  const bf16 hi = (bf16)x;
+  const bf16 lo = (bf16)(x - (float)hi);
+  return (uint32_t)__builtin_bit_cast(uint16_t, hi) |
+         ((uint32_t)__builtin_bit_cast(uint16_t, lo) << 16);
+}
+__device__ inline float unpack_hi(uint32_t p) { return __builtin_bit_cast(float, p << 16); }
+__device__ inline float unpack_lo(uint32_t p) { return __builtin_bit_cast(float, p & 0xffff0000u); }
+
+// The hi and lo operands of a row of packed pairs, elements in accumulator
+// order (as lds_op_perm): two runs of 4 consecutive entries.
+__device__ inline void lds_pair_op(const uint32_t* row, int ks, int hh, bf16x8& hi,
+                                   bf16x8& lo) {
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 a = *reinterpret_cast<const u32x4*>(row + 16 * ks + 4 * hh);
+  const u32x4 b = *reinterpret_cast<const u32x4*>(row + 16 * ks + 8 + 4 * hh);
+  typedef unsigned u32x4v __attribute__((ext_vector_type(4)));
+  u32x4v h, l;
+  // low halves of consecutive dwords -> hi pieces, high halves -> lo pieces
+  h[0] = __builtin_amdgcn_perm(a[1], a[0], 0x05040100u);
+  h[1] = __builtin_amdgcn_perm(a[3], a[2], 0x05040100u);
+  h[2] = __builtin_amdgcn_perm(b[1], b[0], 0x05040100u);
+  h[3] = __builtin_amdgcn_perm(b[3], b[2], 0x05040100u);
+  l[0] = __builtin_amdgcn_perm(a[1], a[0], 0x07060302u);
+  l[1] = __builtin_amdgcn_perm(a[3], a[2], 0x07060302u);
+  l[2] = __builtin_amdgcn_perm(b[1], b[0], 0x07060302u);
+  l[3] = __builtin_amdgcn_perm(b[3], b[2], 0x07060302u);
+  hi = __builtin_bit_cast(bf16x8, h);
+  lo = __builtin_bit_cast(bf16x8, l);
+}
+
 template <typename T>
 __device__ inline void store_out1(void* out, size_t idx, float v, bool f32) {
   if (sizeof(T) == 4 || f32)

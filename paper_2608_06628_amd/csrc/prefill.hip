@@ -328,6 +328,363 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_prefill_kernel(
   for (int r = tid; r < f; r += blockDim.x) dstz[r] = sh.z[r];
 }
 
+
+// ---------------------------------------------------------------------------
+// Pipelined walk (bf16, F <= 64, outputs wanted): one workgroup per (request,
+// head, segment) with producer and state waves working on consecutive blocks.
+//   producer waves (NP = 2 + D/64), block c+1:
+//     wave 0: phi(Q) of the block, the whole feature map in one wave;
+//     wave 1: phi(K), likewise, written transposed (the commit's A operand);
+//     waves 2..: the in-block softmax branch for 64 columns each: scores,
+//                row max and sum, P V relative to the row max;
+//   state waves (D/32), block c: the readout against the state of the blocks
+//     before c, the merge, the output store, the commit of c into S
+//     (columns 32w..32w+31 in fp32 accumulators) and z.
+// The two groups meet at one barrier per block; everything they exchange is
+// double-buffered in LDS, and z too (the state waves read z_c while writing
+// z_{c+1}).  Within a group no barrier is needed: the feature map's row
+// maximum and sum stay inside the wave.  Arithmetic and operand precision
+// are those of the single-group walk above.
+// ---------------------------------------------------------------------------
+template <typename T, int D, int F>
+struct PrefillPipeCfg {
+  typedef Mma<T> M;
+  typedef typename M::op_t op_t;
+  static constexpr int NC = D / kTile;              // state waves
+  static constexpr int NSM = D / 64 > 0 ? D / 64 : 1;  // softmax waves
+  static constexpr int CT = NC / NSM;               // column tiles per softmax wave
+  static constexpr int NP = 2 + NSM;                // producer waves
+  static constexpr int NWAVE = NP + NC;
+  static constexpr int f = 2 * F;
+  static constexpr int NRT = f / kTile;
+  static constexpr int KD = D / M::KW;
+  static constexpr int KL = kTile / M::KW;
+  static constexpr int KF = f / M::KW;
+  static constexpr int PAD = 16 / (int)sizeof(T);
+  typedef WaveFeatMap<T, D, F> WFM;
+  struct alignas(16) Buf {
+    T phiQ[kTile][f + PAD];          // phi(q_i)[r] at [i][r]
+    uint32_t phiKT[f][kTile + 4];    // phi(k_t)[r] at [r][t]: bf16 hi | lo << 16
+    float sm[kTile][D + 4];          // P V relative to the row max, [i][c];
+                                     // then the state waves' outputs
+    float m[kTile], den[kTile];
+    op_t vop[NC][KL][kWave];         // V operands (column tile, k-step, lane)
+  };
+  struct alignas(16) Smem {
+    Buf buf[2];
+    float z[2][f];
+  };
+};
+
+template <int D>
+constexpr int pipe_threads() {
+  return kWave * (2 + (D / 64 > 0 ? D / 64 : 1) + D / kTile);
+}
+
+template <typename T, int D, int F>
+__global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
+    PrefillArgs a, int nseg, int seg_blocks) {
+  typedef PrefillPipeCfg<T, D, F> C;
+  typedef typename C::M M;
+  typedef typename C::op_t op_t;
+  typedef typename C::WFM WFM;
+  constexpr int f = C::f, E = M::E, KW = M::KW, NP = C::NP, NC = C::NC;
+  static_assert(pipe_threads<D>() == kWave * C::NWAVE, "launch bounds match the waves");
+  __shared__ typename C::Smem sh;
+
+  // The wave index through readfirstlane: the compiler then knows it is
+  // uniform, and the role branches below are scalar jumps, not exec masks.
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int w = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int li = lane & 31, hh = lane >> 5;
+  const int Hq = a.s.Hq, Hkv = a.s.Hkv, L = a.s.L, T_ = a.T;
+  const int units = a.s.B * Hq;
+  const int vix = xcd_unit(blockIdx.x, units * nseg);
+  const int u = vix % units, seg = vix / units;
+  const int b = u / Hq, h = u % Hq, g = h / (Hq / Hkv);
+  const int slot = a.slots ? a.slots[b] : b;
+  const bool last = seg == nseg - 1;
+  const size_t qstride = (size_t)Hq * D, kstride = (size_t)Hkv * D;
+  const int nblk = T_ / L;
+  const int blk0 = seg * seg_blocks, blk1 = min(nblk, blk0 + seg_blocks);
+  if (slot < 0 || slot >= a.s.n_slots) {  // uniform per workgroup
+    const size_t ob = ((size_t)b * T_ * Hq + h) * D;
+    for (int t = blk0 * L; t < blk1 * L; ++t)
+      for (int c = tid; c < D; c += blockDim.x)
+        store_out1<T>(a.out, ob + (size_t)t * qstride + c, __builtin_nanf(""), a.s.out_f32);
+    return;
+  }
+  const bool producer = w < NP;
+  const int cw = w - NP;                    // state wave index (columns 32cw..)
+  const int col = cw * kTile + li;
+  const size_t sbase = (size_t)slot * Hq + h;
+  float* __restrict__ Sh = a.S + sbase * f * D;
+  float* __restrict__ zh = a.z + sbase * f;
+  float* __restrict__ wsS = a.ws + (size_t)u * (nseg - 1) * D * f;
+  float* __restrict__ wsz = a.ws + (size_t)units * (nseg - 1) * D * f + (size_t)u * (nseg - 1) * f;
+  const bool row_ok = li < L;
+  const int lrow = min(li, L - 1);
+
+  // State waves: S columns col of all f rows, S + the earlier segments'
+  // increments; z likewise into z[0].
+  f32x16 sacc[C::NRT];
+  if (!producer) {
+#pragma unroll
+    for (int rt = 0; rt < C::NRT; ++rt)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        f32x4 x = *reinterpret_cast<const f32x4*>(Sh + (size_t)col * f + rt * kTile + row_of(4 * j, hh));
+        for (int s = 0; s < seg; ++s) {
+          const f32x4 y = *reinterpret_cast<const f32x4*>(
+              wsS + (size_t)s * D * f + (size_t)col * f + rt * kTile + row_of(4 * j, hh));
+#pragma unroll
+          for (int r = 0; r < 4; ++r) x[r] += y[r];
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sacc[rt][4 * j + r] = x[r];
+      }
+    for (int r = tid - NP * kWave; r < f; r += NC * kWave) {
+      float zr = zh[r];
+      for (int s = 0; s < seg; ++s) zr += wsz[(size_t)s * f + r];
+      sh.z[0][r] = zr;
+    }
+  }
+
+  const float scale = 1.0f / sqrtf((float)D);
+  const float lw = log_sigmoid(a.alpha[h]);
+  auto qbase = [&](int blk) {
+    return (const T*)a.q + (((size_t)b * T_ + (size_t)blk * L) * Hq + h) * D;
+  };
+  auto kbase = [&](int blk) {
+    return (const T*)a.k + (((size_t)b * T_ + (size_t)blk * L) * Hkv + g) * D;
+  };
+  auto vbase = [&](int blk) {
+    return (const T*)a.v + (((size_t)b * T_ + (size_t)blk * L) * Hkv + g) * D;
+  };
+  // Rows of a block tile as operands (rows past the block length read row
+  // L-1; the roles mask them).
+  auto load_rows = [&](const T* base, size_t stride, op_t (&o)[C::KD]) {
+    const T* row = base + (size_t)lrow * stride + hh * E;
+#pragma unroll
+    for (int ks = 0; ks < C::KD; ++ks) o[ks] = load_op<T>(row + ks * KW);
+  };
+  lds_barrier();  // z[0] ready
+
+  // Each role runs its own loop over the iterations blk0 .. blk1 (producers
+  // work on block it, the state waves on block it - 1) with one barrier per
+  // iteration, so that every role keeps only its own operands in registers.
+  if (w < 2) {
+    // ---- feature map of Q (wave 0) or K (wave 1) ----
+    const T* __restrict__ Wt_h = (const T*)a.W + (size_t)h * F * D;
+    op_t wop[WFM::NT][C::KD];
+    WFM::load_w(Wt_h, li, hh, wop);
+    op_t x[C::KD];
+    auto load = [&](int blk) {
+      if (w == 0) load_rows(qbase(blk), qstride, x);
+      else load_rows(kbase(blk), kstride, x);
+    };
+    if (blk0 < blk1) load(blk0);
+    for (int it = blk0; it <= blk1; ++it) {
+      if (it < blk1) {
+        typename C::Buf& B = sh.buf[(it - blk0) & 1];
+        op_t xm[C::KD];
+#pragma unroll
+        for (int ks = 0; ks < C::KD; ++ks) xm[ks] = keep_if<T>(row_ok, x[ks]);
+        if (it + 1 < blk1) load(it + 1);  // next block in flight
+        float phi[WFM::NPAIR][16];
+        WFM::compute(wop, xm, phi);
+        if (w == 0) {
+#pragma unroll
+          for (int p = 0; p < WFM::NPAIR; ++p)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) B.phiQ[li][WFM::feature(16 * p + i, hh)] = from_f32<T>(phi[p][i]);
+        } else {
+#pragma unroll
+          for (int p = 0; p < WFM::NPAIR; ++p)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+              const int r = WFM::feature(16 * p + i, hh);
+              const float xk = row_ok ? phi[p][i] : 0.0f;
+              B.phiKT[r][li] = pack_hi_lo(xk);
+            }
+        }
+      }
+      lds_barrier();
+    }
+  } else if (producer) {
+    // ---- in-block softmax branch for column tiles c0 .. c0+CT-1 ----
+    const int c0 = (w - 2) * C::CT;
+    op_t ko[C::KD], qo[C::KD], vo[C::CT][C::KL];
+    auto load = [&](int blk) {
+      load_rows(kbase(blk), kstride, ko);
+      load_rows(qbase(blk), qstride, qo);
+#pragma unroll
+      for (int ct = 0; ct < C::CT; ++ct)
+#pragma unroll
+        for (int ks = 0; ks < C::KL; ++ks)
+          vo[ct][ks] = load_rows_op<T>(vbase(blk) + (c0 + ct) * kTile + li, kstride, ks, hh, L, false);
+    };
+    if (blk0 < blk1) load(blk0);
+    for (int it = blk0; it <= blk1; ++it) {
+      if (it < blk1) {
+        typename C::Buf& B = sh.buf[(it - blk0) & 1];
+        // keys in rows, queries in columns
+        f32x16 sc = {};
+#pragma unroll
+        for (int ks = 0; ks < C::KD; ++ks)
+          sc = M::mma(keep_if<T>(row_ok, ko[ks]), keep_if<T>(row_ok, qo[ks]), sc);
+        op_t vc[C::CT][C::KL];
+#pragma unroll
+        for (int ct = 0; ct < C::CT; ++ct)
+#pragma unroll
+          for (int ks = 0; ks < C::KL; ++ks) vc[ct][ks] = vo[ct][ks];
+        if (it + 1 < blk1) load(it + 1);  // next block in flight
+        float pr[16];
+        float m = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          pr[i] = row_of(i, hh) < L ? sc[i] * scale : -INFINITY;
+          m = fmaxf(m, pr[i]);
+        }
+        m = fmaxf(m, xor32(m));
+        float den = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          pr[i] = row_of(i, hh) < L ? fast_exp(pr[i] - m) : 0.0f;
+          den += pr[i];
+        }
+        den += xor32(den);
+#pragma unroll
+        for (int ct = 0; ct < C::CT; ++ct) {
+          f32x16 acc = {};
+#pragma unroll
+          for (int ks = 0; ks < C::KL; ++ks) acc = mma_split_b<T>(vc[ct][ks], &pr[ks * E], acc);
+#pragma unroll
+          for (int i = 0; i < 16; i += 4)
+            *reinterpret_cast<f32x4*>(&B.sm[li][(c0 + ct) * kTile + row_of(i, hh)]) =
+                f32x4{acc[i], acc[i + 1], acc[i + 2], acc[i + 3]};
+        }
+        if (w == 2 && hh == 0) {
+          B.m[li] = m;
+          B.den[li] = den;
+        }
+        // the same V operands serve the state waves' commit of this block
+#pragma unroll
+        for (int ct = 0; ct < C::CT; ++ct)
+#pragma unroll
+          for (int ks = 0; ks < C::KL; ++ks) B.vop[c0 + ct][ks][lane] = vc[ct][ks];
+      }
+      lds_barrier();
+    }
+  } else {
+    // ---- state waves: readout, merge, store and commit of block it - 1 ----
+    for (int it = blk0; it <= blk1; ++it) {
+      const int cblk = it - 1;
+      if (cblk >= blk0) {
+        typename C::Buf& B = sh.buf[(cblk - blk0) & 1];
+        const float* zr = sh.z[(cblk - blk0) & 1];
+        float* zw = sh.z[(cblk - blk0 + 1) & 1];
+        // lin_den = phi(q_li) . z, each lane half over half the features
+        float lden = 0.0f;
+#pragma unroll
+        for (int r = hh * (f / 2); r < (hh + 1) * (f / 2); r += 8) {
+          const uint4 xq = *reinterpret_cast<const uint4*>(&B.phiQ[li][r]);
+          const T* xt = reinterpret_cast<const T*>(&xq);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) lden += to_f32(xt[e]) * zr[r + e];
+        }
+        lden += xor32(lden);
+        // readout against the state of the blocks before cblk
+        f32x16 acc_lin = {};
+#pragma unroll
+        for (int ks = 0; ks < C::KF; ++ks) {
+          const op_t pb = lds_op_perm<T>(&B.phiQ[li][0], ks, hh, 0);
+          op_t sa;
+#pragma unroll
+          for (int e = 0; e < E; ++e) {
+            const int j = ks * E + e;
+            sa[e] = (T)sacc[j / 16][j % 16];
+          }
+          acc_lin = M::mma(sa, pb, acc_lin);
+        }
+        if (row_ok) {
+          const float m = B.m[li], den = B.den[li];
+          float ca = 1.0f, cz = 0.0f, rz = 0.0f;
+          if (lden > 0.0f) {
+            const float la = lw + m, lb = logf(lden);
+            const float c = fmaxf(la, lb);
+            ca = expf(la - c);
+            cz = expf(lb - c);
+            rz = 1.0f / lden;
+          }
+          const float inv = 1.0f / (ca * den + cz);
+          // outputs over the numerators just read (this lane's own slots)
+#pragma unroll
+          for (int i = 0; i < 16; i += 4) {
+            float* sp = &B.sm[li][cw * kTile + row_of(i, hh)];
+            const f32x4 smv = *reinterpret_cast<const f32x4*>(sp);
+            f32x4 o;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) o[e] = (ca * smv[e] + cz * (acc_lin[i + e] * rz)) * inv;
+            *reinterpret_cast<f32x4*>(sp) = o;
+          }
+        }
+        // This wave's 32 columns of the block's rows, 8 columns (16 bytes of
+        // bf16) per lane: 64 contiguous bytes per token.  The staging slots
+        // were written by other lanes of this wave just above; LDS operations
+        // of one wave complete in order, and the wait keeps the compiler from
+        // moving the reads up.
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+        for (int pass = 0; pass < 2; ++pass) {
+          const int t = pass * 16 + lane / 4, c8 = (lane & 3) * 8;
+          if (t < L) {
+            const float* sp = &B.sm[t][cw * kTile + c8];
+            const f32x4 x0 = *reinterpret_cast<const f32x4*>(sp);
+            const f32x4 x1 = *reinterpret_cast<const f32x4*>(sp + 4);
+            const float o8[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+            const size_t oidx = (((size_t)b * T_ + (size_t)cblk * L + t) * Hq + h) * D + cw * kTile + c8;
+            store_out8<T>(a.out, oidx, o8, a.s.out_f32);
+          }
+        }
+        // commit: S += phi(K)^T V (this wave's columns); z_{c+1} = z_c + sum phi(k)
+#pragma unroll
+        for (int rt = 0; rt < C::NRT; ++rt)
+#pragma unroll
+          for (int ks = 0; ks < C::KL; ++ks) {
+            op_t khi, klo;
+            lds_pair_op(&B.phiKT[rt * kTile + li][0], ks, hh, khi, klo);
+            const op_t vk = B.vop[cw][ks][lane];
+            sacc[rt] = M::mma(khi, vk, sacc[rt]);
+            sacc[rt] = M::mma(klo, vk, sacc[rt]);
+          }
+        for (int r = tid - NP * kWave; r < f; r += NC * kWave) {
+          float s = zr[r];
+#pragma unroll
+          for (int t0 = 0; t0 < kTile; t0 += 4) {
+            const uint4 xk = *reinterpret_cast<const uint4*>(&B.phiKT[r][t0]);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) s += unpack_hi(xk[e]) + unpack_lo(xk[e]);
+          }
+          zw[r] = s;
+        }
+      }
+      lds_barrier();
+    }
+  }
+
+  if (!producer && last) {
+#pragma unroll
+    for (int rt = 0; rt < C::NRT; ++rt)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        *reinterpret_cast<f32x4*>(Sh + (size_t)col * f + rt * kTile + row_of(4 * j, hh)) =
+            f32x4{sacc[rt][4 * j], sacc[rt][4 * j + 1], sacc[rt][4 * j + 2], sacc[rt][4 * j + 3]};
+    const float* zf = sh.z[(blk1 - blk0) & 1];
+    for (int r = tid - NP * kWave; r < f; r += NC * kWave) zh[r] = zf[r];
+  }
+}
+
 template <typename T, int D, int F>
 static hipError_t prefill_go(const PrefillArgs& a, hipStream_t st) {
   const int units = a.s.B * a.s.Hq, nblk = a.T / a.s.L;
@@ -339,6 +696,16 @@ static hipError_t prefill_go(const PrefillArgs& a, hipStream_t st) {
                        a, nseg, seg_blocks, 1);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
+  }
+  // The pipelined walk serves bf16 with F <= 64 when outputs are wanted;
+  // the single-group walk serves the rest.
+  if constexpr (sizeof(T) == 2 && F <= 64) {
+    if (a.out != nullptr) {
+      typedef PrefillPipeCfg<T, D, F> P;
+      hipLaunchKernelGGL((hyb_prefill_pipe_kernel<T, D, F>), dim3(units * nseg),
+                         dim3(kWave * P::NWAVE), 0, st, a, nseg, seg_blocks);
+      return hipGetLastError();
+    }
   }
   hipLaunchKernelGGL((hyb_prefill_kernel<T, D, F>), dim3(units * nseg), block, 0, st, a, nseg,
                      seg_blocks, 0);
