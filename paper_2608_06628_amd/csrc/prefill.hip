@@ -685,6 +685,185 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
   }
 }
 
+
+// ---------------------------------------------------------------------------
+// Pipelined delta (bf16, F <= 64): a segment's own increment
+// dS = sum_c phi(K_c)^T V_c, dz = sum_c sum_t phi(k_t), two blocks per
+// iteration.  Waves 0 and 1 compute phi(K) of the pair's two blocks (the
+// whole feature map in one wave), waves 2 and 3 load their V operands, and
+// the D/32 state waves commit the previous pair into S columns 32w..32w+31
+// in fp32 accumulators; one barrier per pair, buffers double-buffered.
+// ---------------------------------------------------------------------------
+template <typename T, int D, int F>
+struct DeltaPipeCfg {
+  typedef Mma<T> M;
+  typedef typename M::op_t op_t;
+  static constexpr int NC = D / kTile;   // state waves
+  static constexpr int NP = 4;           // 2 feature-map + 2 V waves
+  static constexpr int NWAVE = NP + NC;
+  static constexpr int f = 2 * F;
+  static constexpr int NRT = f / kTile;
+  static constexpr int KD = D / M::KW;
+  static constexpr int KL = kTile / M::KW;
+  typedef WaveFeatMap<T, D, F> WFM;
+  struct alignas(16) Buf {
+    uint32_t phiKT[2][f][kTile + 4];     // per block of the pair: bf16 hi | lo << 16
+    op_t vop[2][NC][KL][kWave];          // per block of the pair: V operands
+  };
+  struct alignas(16) Smem {
+    Buf buf[2];
+    float z[f];
+  };
+};
+
+template <int D>
+constexpr int delta_pipe_threads() {
+  return kWave * (4 + D / kTile);
+}
+
+template <typename T, int D, int F>
+__global__ __launch_bounds__(delta_pipe_threads<D>()) void hyb_prefill_delta_pipe_kernel(
+    PrefillArgs a, int nseg, int seg_blocks) {
+  typedef DeltaPipeCfg<T, D, F> C;
+  typedef typename C::M M;
+  typedef typename C::op_t op_t;
+  typedef typename C::WFM WFM;
+  constexpr int f = C::f, E = M::E, KW = M::KW, NP = C::NP, NC = C::NC;
+  static_assert(delta_pipe_threads<D>() == kWave * C::NWAVE, "launch bounds match the waves");
+  __shared__ typename C::Smem sh;
+
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int w = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int li = lane & 31, hh = lane >> 5;
+  const int Hq = a.s.Hq, Hkv = a.s.Hkv, L = a.s.L, T_ = a.T;
+  const int units = a.s.B * Hq;
+  // segments 0 .. nseg-2 (the last segment's increment is never needed)
+  const int vix = xcd_unit(blockIdx.x, units * (nseg - 1));
+  const int u = vix % units, seg = vix / units;
+  const int b = u / Hq, h = u % Hq, g = h / (Hq / Hkv);
+  const int slot = a.slots ? a.slots[b] : b;
+  if (slot < 0 || slot >= a.s.n_slots) return;  // uniform: no increment needed
+  const size_t kstride = (size_t)Hkv * D;
+  const int nblk = T_ / L;
+  const int blk0 = seg * seg_blocks, blk1 = min(nblk, blk0 + seg_blocks);
+  const int npair = (blk1 - blk0 + 1) / 2;
+  const bool row_ok = li < L;
+  const int lrow = min(li, L - 1);
+  float* __restrict__ wsS = a.ws + ((size_t)u * (nseg - 1) + seg) * D * f;
+  float* __restrict__ wsz = a.ws + (size_t)units * (nseg - 1) * D * f + ((size_t)u * (nseg - 1) + seg) * f;
+  auto kbase = [&](int blk) {
+    return (const T*)a.k + (((size_t)b * T_ + (size_t)blk * L) * Hkv + g) * D;
+  };
+  auto vbase = [&](int blk) {
+    return (const T*)a.v + (((size_t)b * T_ + (size_t)blk * L) * Hkv + g) * D;
+  };
+  for (int r = tid; r < f; r += blockDim.x) sh.z[r] = 0.0f;
+  lds_barrier();
+
+  if (w < 2) {
+    // ---- phi(K) of block blk0 + 2j + w ----
+    const T* __restrict__ Wt_h = (const T*)a.W + (size_t)h * F * D;
+    op_t wop[WFM::NT][C::KD];
+    WFM::load_w(Wt_h, li, hh, wop);
+    op_t x[C::KD];
+    auto load = [&](int blk) {
+      const T* row = kbase(blk) + (size_t)lrow * kstride + hh * E;
+#pragma unroll
+      for (int ks = 0; ks < C::KD; ++ks) x[ks] = load_op<T>(row + ks * KW);
+    };
+    if (blk0 + w < blk1) load(blk0 + w);
+    for (int j = 0; j <= npair; ++j) {
+      const int blk = blk0 + 2 * j + w;
+      if (j < npair && blk < blk1) {
+        typename C::Buf& B = sh.buf[j & 1];
+        op_t xm[C::KD];
+#pragma unroll
+        for (int ks = 0; ks < C::KD; ++ks) xm[ks] = keep_if<T>(row_ok, x[ks]);
+        if (blk + 2 < blk1) load(blk + 2);  // next pair's block in flight
+        float phi[WFM::NPAIR][16];
+        WFM::compute(wop, xm, phi);
+#pragma unroll
+        for (int p = 0; p < WFM::NPAIR; ++p)
+#pragma unroll
+          for (int i = 0; i < 16; ++i)
+            B.phiKT[w][WFM::feature(16 * p + i, hh)][li] = pack_hi_lo(row_ok ? phi[p][i] : 0.0f);
+      }
+      lds_barrier();
+    }
+  } else if (w < NP) {
+    // ---- V operands of block blk0 + 2j + (w - 2), every column tile ----
+    const int q = w - 2;
+    op_t vo[NC][C::KL];
+    auto load = [&](int blk) {
+#pragma unroll
+      for (int ct = 0; ct < NC; ++ct)
+#pragma unroll
+        for (int ks = 0; ks < C::KL; ++ks)
+          vo[ct][ks] = load_rows_op<T>(vbase(blk) + ct * kTile + li, kstride, ks, hh, L, false);
+    };
+    if (blk0 + q < blk1) load(blk0 + q);
+    for (int j = 0; j <= npair; ++j) {
+      const int blk = blk0 + 2 * j + q;
+      if (j < npair && blk < blk1) {
+        typename C::Buf& B = sh.buf[j & 1];
+#pragma unroll
+        for (int ct = 0; ct < NC; ++ct)
+#pragma unroll
+          for (int ks = 0; ks < C::KL; ++ks) B.vop[q][ct][ks][lane] = vo[ct][ks];
+        if (blk + 2 < blk1) load(blk + 2);
+      }
+      lds_barrier();
+    }
+  } else {
+    // ---- state waves: commit the previous pair ----
+    const int cw = w - NP, col = cw * kTile + li;
+    f32x16 sacc[C::NRT];
+#pragma unroll
+    for (int rt = 0; rt < C::NRT; ++rt) sacc[rt] = f32x16{};
+    for (int j = 0; j <= npair; ++j) {
+      const int pj = j - 1;
+      if (pj >= 0) {
+        typename C::Buf& B = sh.buf[pj & 1];
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          if (blk0 + 2 * pj + q >= blk1) continue;  // uniform
+#pragma unroll
+          for (int rt = 0; rt < C::NRT; ++rt)
+#pragma unroll
+            for (int ks = 0; ks < C::KL; ++ks) {
+              op_t khi, klo;
+              lds_pair_op(&B.phiKT[q][rt * kTile + li][0], ks, hh, khi, klo);
+              const op_t vk = B.vop[q][cw][ks][lane];
+              sacc[rt] = M::mma(khi, vk, sacc[rt]);
+              sacc[rt] = M::mma(klo, vk, sacc[rt]);
+            }
+          for (int r = tid - NP * kWave; r < f; r += NC * kWave) {
+            float s = 0.0f;
+#pragma unroll
+            for (int t0 = 0; t0 < kTile; t0 += 4) {
+              const uint4 xk = *reinterpret_cast<const uint4*>(&B.phiKT[q][r][t0]);
+#pragma unroll
+              for (int e = 0; e < 4; ++e) s += unpack_hi(xk[e]) + unpack_lo(xk[e]);
+            }
+            sh.z[r] += s;
+          }
+        }
+      }
+      lds_barrier();
+    }
+#pragma unroll
+    for (int rt = 0; rt < C::NRT; ++rt)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        *reinterpret_cast<f32x4*>(wsS + (size_t)col * f + rt * kTile + row_of(4 * j, hh)) =
+            f32x4{sacc[rt][4 * j], sacc[rt][4 * j + 1], sacc[rt][4 * j + 2], sacc[rt][4 * j + 3]};
+    for (int r = tid - NP * kWave; r < f; r += NC * kWave) wsz[r] = sh.z[r];
+  }
+}
+
+template <typename T, int D, int F>
+static hipError_t prefill_delta_go(const PrefillArgs& a, hipStream_t st);
+
 template <typename T, int D, int F>
 static hipError_t prefill_go(const PrefillArgs& a, hipStream_t st) {
   const int units = a.s.B * a.s.Hq, nblk = a.T / a.s.L;
@@ -692,9 +871,7 @@ static hipError_t prefill_go(const PrefillArgs& a, hipStream_t st) {
   const int seg_blocks = (nblk + nseg - 1) / nseg;
   const dim3 block(kWave * (D / kTile));
   if (nseg > 1) {
-    hipLaunchKernelGGL((hyb_prefill_kernel<T, D, F>), dim3(units * (nseg - 1)), block, 0, st,
-                       a, nseg, seg_blocks, 1);
-    const hipError_t e = hipGetLastError();
+    const hipError_t e = prefill_delta_go<T, D, F>(a, st);
     if (e != hipSuccess) return e;
   }
   // The pipelined walk serves bf16 with F <= 64 when outputs are wanted;
@@ -718,6 +895,11 @@ static hipError_t prefill_delta_go(const PrefillArgs& a, hipStream_t st) {
   const int nseg = prefill_segments(a.s, a.T);
   const int seg_blocks = (nblk + nseg - 1) / nseg;
   if (nseg <= 1) return hipSuccess;
+  if constexpr (sizeof(T) == 2 && F <= 64) {
+    hipLaunchKernelGGL((hyb_prefill_delta_pipe_kernel<T, D, F>), dim3(units * (nseg - 1)),
+                       dim3(delta_pipe_threads<D>()), 0, st, a, nseg, seg_blocks);
+    return hipGetLastError();
+  }
   hipLaunchKernelGGL((hyb_prefill_kernel<T, D, F>), dim3(units * (nseg - 1)),
                      dim3(kWave * (D / kTile)), 0, st, a, nseg, seg_blocks, 1);
   return hipGetLastError();
