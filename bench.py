@@ -623,6 +623,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--only-table3", action="store_true",
                     help="run only the prefix-length x batch latency sweep and print it")
+    ap.add_argument("--only-mix", action="store_true",
+                    help="run only the mix128 softmax-prefix vs hybrid timing and print it")
     ap.add_argument("--only-prefill", action="store_true",
                     help="run only the prefill8 timing and print it")
     ap.add_argument("--only-backward", action="store_true",
@@ -638,6 +640,11 @@ def main():
         sys.exit(2)
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.only_mix:
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(5)
+        print(json.dumps(bench_mix(gen, "cuda")), flush=True)
         return
     if args.only_prefill:
         gen = torch.Generator(device="cuda")

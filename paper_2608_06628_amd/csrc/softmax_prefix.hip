@@ -16,33 +16,41 @@
 
 namespace hyb {
 
-template <typename T, int D>
+template <typename T, int D, int NG>
 struct SpCfg {
   typedef Mma<T> M;
   typedef typename M::op_t op_t;
   static constexpr int KD = D / M::KW;
   static constexpr int KL = kTile / M::KW;
   static constexpr int NCT = D / kTile;
-  static constexpr int LD = D + 16 / (int)sizeof(T);
   static constexpr int EPC = 16 / (int)sizeof(T);  // elements per 16 bytes
+  static constexpr int KLD = D + EPC;              // K rows: 16-byte pad
+  static constexpr int VLD = D + 2 * EPC;          // V rows: 32-byte pad
+  static constexpr int CPR = D / EPC;              // 16-byte chunks per row
+  static constexpr int NCH = (kTile * CPR + kWave * NG - 1) / (kWave * NG);  // per thread
   struct alignas(16) Smem {
-    T k[kTile][LD];
-    T v[kTile][LD];
+    T k[2][kTile][KLD];
+    T v[2][kTile][VLD];
   };
 };
 
 constexpr int kMaxGroup = 8;  // query heads per KV head handled by one WG
 
-template <typename T, int D>
-__global__ __launch_bounds__(kWave* kMaxGroup) void hyb_sp_partial_kernel(
+// One wave per query head of the KV group; 32-key tiles double-buffered in
+// LDS: the tile after next is loaded into registers while the current one is
+// computed, and the next one is moved from registers into the free buffer at
+// the end of the step, so one barrier per tile orders everything.
+template <typename T, int D, int NG>
+__global__ __launch_bounds__(kWave* NG) void hyb_sp_partial_kernel(
     SoftmaxPrefixArgs a, int chunk) {
-  typedef SpCfg<T, D> C;
+  typedef SpCfg<T, D, NG> C;
   typedef typename C::M M;
   typedef typename C::op_t op_t;
-  constexpr int E = M::E, KW = M::KW;
+  constexpr int E = M::E, KW = M::KW, EPC = C::EPC, CPR = C::CPR, NCH = C::NCH;
   __shared__ typename C::Smem sh;
 
-  const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int w = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int li = lane & 31, hh = lane >> 5;
   const int Hq = a.s.Hq, Hkv = a.s.Hkv, L = a.s.L, G = Hq / Hkv;
   const int ns = a.n_split, Pmax = a.max_prefix;
@@ -69,69 +77,123 @@ __global__ __launch_bounds__(kWave* kMaxGroup) void hyb_sp_partial_kernel(
   const T* kbk = (const T*)a.k + ((size_t)b * L * Hkv + g) * D;
   const T* vbk = (const T*)a.v + ((size_t)b * L * Hkv + g) * D;
 
+  // Tile loads: keys past the range read the range's last key (in bounds)
+  // and are masked out of the scores below.
+  // A tile's share of this thread, held in registers between its load and
+  // its move into LDS: nx is the next tile, af the one after it.
+  struct TileRegs {
+    uint4 k[NCH], v[NCH];
+  };
+  auto fetch = [&](int j0) __attribute__((always_inline)) {
+    TileRegs r;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int idx = tid + c * kWave * NG, key = idx / CPR, part = idx % CPR;
+      if (idx < kTile * CPR) {  // (NG not a power of two: a partial last set)
+        const int j = min(j0 + key, hi - 1);
+        const size_t o = (size_t)part * EPC;
+        const T* ks = j < P ? kc + (size_t)j * kstride : kbk + (size_t)(j - P) * kstride;
+        const T* vs = j < P ? vc + (size_t)j * kstride : vbk + (size_t)(j - P) * kstride;
+        r.k[c] = *reinterpret_cast<const uint4*>(ks + o);
+        r.v[c] = *reinterpret_cast<const uint4*>(vs + o);
+      }
+    }
+    return r;
+  };
+  auto put = [&](const TileRegs& r, int buf) __attribute__((always_inline)) {
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+      const int idx = tid + c * kWave * NG, key = idx / CPR, part = idx % CPR;
+      if (idx < kTile * CPR) {
+        *reinterpret_cast<uint4*>(&sh.k[buf][key][part * EPC]) = r.k[c];
+        *reinterpret_cast<uint4*>(&sh.v[buf][key][part * EPC]) = r.v[c];
+      }
+    }
+  };
+  // V^T operand of column tile ct, k-step ks: lane (li, hh) holds column
+  // ct*32 + li at keys row_of(ks*E + e, hh).  bf16: in each 16-lane quarter
+  // the transposing read gives lane i element i%4 of the 8-byte pieces
+  // addressed by lanes i/4 + 4j (j = 0..3); lane i addresses key
+  // kb + i/4 at columns cb + 4*(i%4) .. +3, so it receives keys kb .. kb+3
+  // of column cb + i.
+  auto vt_op = [&](int buf, int ct, int ks) __attribute__((always_inline)) -> op_t {
+    if constexpr (E == 1) {
+      return to_f32(sh.v[buf][row_of(ks, hh)][ct * kTile + li]);
+    } else {
+      typedef short s16x4 __attribute__((ext_vector_type(4)));
+      const int i = lane & 15;
+      const int cb = ct * kTile + 16 * ((lane >> 4) & 1);
+      const int kb = 16 * ks + 4 * hh;
+      auto piece = [&](int key) {
+        const T* src = &sh.v[buf][key][cb + 4 * (i & 3)];
+        return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) s16x4*)src);
+      };
+      const s16x4 x0 = piece(kb + i / 4), x1 = piece(kb + 8 + i / 4);
+      return __builtin_bit_cast(op_t, __builtin_shufflevector(x0, x1, 0, 1, 2, 3, 4, 5, 6, 7));
+    }
+  };
+
   const float scale = 1.0f / sqrtf((float)D);
   float m = -INFINITY, l = 0.0f;
   f32x16 acc[C::NCT];
 #pragma unroll
   for (int ct = 0; ct < C::NCT; ++ct) acc[ct] = f32x16{};
 
-  constexpr int CPR = D / C::EPC;  // 16-byte chunks per key row
-  for (int j0 = lo; j0 < hi; j0 += kTile) {
-    __syncthreads();
-    // Keys past the range read the range's last key (in bounds) and are
-    // masked out of the scores below.
-    for (int c = tid; c < kTile * CPR; c += blockDim.x) {
-      const int key = c / CPR, part = c % CPR, j = min(j0 + key, hi - 1);
-      const size_t o = (size_t)part * C::EPC;
-      const T* ks = j < P ? kc + (size_t)j * kstride : kbk + (size_t)(j - P) * kstride;
-      const T* vs = j < P ? vc + (size_t)j * kstride : vbk + (size_t)(j - P) * kstride;
-      *reinterpret_cast<uint4*>(&sh.k[key][part * C::EPC]) =
-          *reinterpret_cast<const uint4*>(ks + o);
-      *reinterpret_cast<uint4*>(&sh.v[key][part * C::EPC]) =
-          *reinterpret_cast<const uint4*>(vs + o);
-    }
-    __syncthreads();
+  TileRegs nx = {}, af = {};
+  if (lo < hi) {
+    put(fetch(lo), 0);
+    if (lo + kTile < hi) nx = fetch(lo + kTile);
+  }
+  __syncthreads();
+  int n = 0;
+  for (int j0 = lo; j0 < hi; j0 += kTile, ++n) {
+    const int buf = n & 1;
+    if (j0 + 2 * kTile < hi) af = fetch(j0 + 2 * kTile);  // tile after next
 
     f32x16 sc = {};
 #pragma unroll
     for (int ks = 0; ks < C::KD; ++ks)
-      sc = M::mma(load_op<T>(&sh.k[li][ks * KW + hh * E]), qop[ks], sc);
+      sc = M::mma(load_op<T>(&sh.k[buf][li][ks * KW + hh * E]), qop[ks], sc);
+    // Scaled scores; keys past the range only in the range's last tile
+    // (a wave-uniform test, so full tiles carry no masks).
+    const bool full = j0 + kTile <= hi;
     float p[16];
     float mt = -INFINITY;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      p[i] = j0 + row_of(i, hh) < hi ? sc[i] * scale : -INFINITY;
+      p[i] = (full || j0 + row_of(i, hh) < hi) ? sc[i] * scale : -INFINITY;
       mt = fmaxf(mt, p[i]);
     }
     mt = fmaxf(mt, xor32(mt));
     const float mn = fmaxf(m, mt);
-    const float corr = fast_exp(m - mn);
     float ps = 0.0f;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      p[i] = j0 + row_of(i, hh) < hi ? as_operand<T>(fast_exp(p[i] - mn)) : 0.0f;
+      p[i] = as_operand<T>(fast_exp(p[i] - mn));  // exp(-inf) = 0 past the range
       ps += p[i];
     }
     ps += xor32(ps);
-    l = l * corr + ps;
+    // The accumulators are rescaled only when some query's running maximum
+    // rose: once the maximum settles most tiles skip the 64 multiplies.
+    if (__any(mn > m)) {
+      const float corr = fast_exp(m - mn);
+      l *= corr;
+#pragma unroll
+      for (int ct = 0; ct < C::NCT; ++ct)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[ct][i] *= corr;
+    }
+    l += ps;
     m = mn;
 #pragma unroll
-    for (int ct = 0; ct < C::NCT; ++ct) {
+    for (int ct = 0; ct < C::NCT; ++ct)
 #pragma unroll
-      for (int i = 0; i < 16; ++i) acc[ct][i] *= corr;
-#pragma unroll
-      for (int ks = 0; ks < C::KL; ++ks) {
-        op_t va;
-        if constexpr (E == 1) {
-          va = to_f32(sh.v[row_of(ks, hh)][ct * kTile + li]);
-        } else {
-#pragma unroll
-          for (int e = 0; e < E; ++e)
-            va[e] = sh.v[row_of(ks * E + e, hh)][ct * kTile + li];
-        }
-        acc[ct] = M::mma(va, cvt_op<T>(&p[ks * E]), acc[ct]);
-      }
-    }
+      for (int ks = 0; ks < C::KL; ++ks)
+        acc[ct] = M::mma(vt_op(buf, ct, ks), cvt_op<T>(&p[ks * E]), acc[ct]);
+    if (j0 + kTile < hi) put(nx, buf ^ 1);  // next tile into the free buffer
+    nx = af;
+    __syncthreads();
   }
 
   // Partial result of this range: unnormalised O, running max and sum.
@@ -195,9 +257,24 @@ static hipError_t sp_go(const SoftmaxPrefixArgs& a, hipStream_t st) {
   int chunk = (a.max_prefix + a.s.L + ns - 1) / ns;
   chunk = (chunk + kTile - 1) / kTile * kTile;
   const int G = a.s.Hq / a.s.Hkv;
-  hipLaunchKernelGGL((hyb_sp_partial_kernel<T, D>),
-                     dim3(a.s.B * a.s.Hkv * ns), dim3(kWave * G), 0, st, a,
-                     chunk);
+  const dim3 grid(a.s.B * a.s.Hkv * ns);
+#define HYB_SP_CASE(NG)                                                               \
+  case NG:                                                                            \
+    hipLaunchKernelGGL((hyb_sp_partial_kernel<T, D, NG>), grid, dim3(kWave * NG), 0, st, a, \
+                       chunk);                                                        \
+    break;
+  switch (G) {
+    HYB_SP_CASE(1)
+    HYB_SP_CASE(2)
+    HYB_SP_CASE(3)
+    HYB_SP_CASE(4)
+    HYB_SP_CASE(5)
+    HYB_SP_CASE(6)
+    HYB_SP_CASE(7)
+    HYB_SP_CASE(8)
+    default: return hipErrorInvalidValue;
+  }
+#undef HYB_SP_CASE
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL((hyb_sp_combine_kernel<T, D>), dim3(a.s.B * a.s.Hq * a.s.L),
