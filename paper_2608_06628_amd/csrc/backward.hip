@@ -198,7 +198,8 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_fwd_kernel(BwdKArgs
   __shared__ typename C::SmemF sh;
   const BackwardArgs& a = ka.a;
 
-  const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int w = __builtin_amdgcn_readfirstlane(tid / kWave);  // wave-uniform
   const int li = lane & 31, hh = lane >> 5;
   const int Hq = a.s.Hq, Hkv = a.s.Hkv, L = a.s.L, T_ = a.T;
   const int units = a.s.B * Hq, nseg = ka.nseg;
@@ -551,7 +552,8 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_rev_kernel(BwdKArgs
   __shared__ typename C::SmemB sh;
   const BackwardArgs& a = ka.a;
 
-  const int tid = threadIdx.x, lane = tid & (kWave - 1), w = tid / kWave;
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int w = __builtin_amdgcn_readfirstlane(tid / kWave);  // wave-uniform
   const int li = lane & 31, hh = lane >> 5;
   const int Hq = a.s.Hq, Hkv = a.s.Hkv, L = a.s.L, T_ = a.T;
   const int units = a.s.B * Hq, nseg = ka.nseg;

@@ -146,3 +146,27 @@ def test_mix128_softmax_prefix_sampled():
     ref = oracle.softmax_prefix(_bf16_host(q[s]), _bf16_host(k[s]), _bf16_host(v[s]),
                                 _bf16_host(kc[s]), _bf16_host(vc[s]), plen[s])
     assert_close(host(o32[s]), ref, "bf16", "mix128 softmax prefix, requests [0, 127]")
+
+
+def test_train8_backward_full():
+    """The Stage-1 backward at the benchmark's training size (8 sequences of
+    2048 tokens, 16q/4kv, d=128, f=128, blocks of 32, attention-transfer
+    mode) in the bench's launch configuration, against the oracle on the
+    whole batch: dW, dalpha and the loss (every element)."""
+    dims = synth.TRAIN8
+    T = synth.TRAIN8_T
+    q, k, v = synth.sequence_qkv(dims, T, 61, 1.0)
+    Wt, alpha = synth.feature_weights(dims, 62, 63, 1.0 / math.sqrt(dims.d))
+    tgt = synth.upstream(dims, T, 64, 0.05)
+    announce("train8: backward B=8 x 2048 tokens")
+    dW, da, loss = hb.hybrid_attn_backward(act(q, "bf16"), act(k, "bf16"), act(v, "bf16"),
+                                           act(Wt, "bf16"), f32(alpha), dims.L,
+                                           target=act(tgt, "bf16"))
+    torch.cuda.synchronize()
+    ref_W, ref_a, ref_l = oracle.backward(q, k, v, Wt, alpha, dims.L, target=tgt)
+    for got, ref, what in ((host(dW), ref_W, "dW"), (host(da), ref_a, "dalpha"),
+                           (host(loss), ref_l, "loss")):
+        err = float(np.abs(got - ref).max())
+        tol = 2e-2 * float(np.sqrt(np.mean(ref ** 2)))
+        print(f"[parity] train8 backward {what}: max abs err {err:.3e} (tol {tol:.3e})")
+        assert np.isfinite(got).all() and err <= tol, what
