@@ -11,6 +11,8 @@
 // lane column), an online-softmax update, and O^T += V^T P^T, with P rounded
 // once to the operand type and the running sum taken over the rounded
 // weights.  A second kernel merges the ranges with their log-sum-exp weights.
+#include <type_traits>
+
 #include "device.h"
 #include "launch.h"
 
@@ -213,6 +215,204 @@ __global__ __launch_bounds__(kWave* NG) void hyb_sp_partial_kernel(
   }
 }
 
+
+// bf16 with 1, 2, 4 or 8 query heads per KV head: the K/V tiles reach LDS by
+// direct global->LDS copies into a ring of R = 4 tile slots, three tiles in
+// flight while one is computed, with no registers held for them.  Each copy
+// instruction reads whole rows, 16 bytes per lane; chunk c of a staged row t
+// sits at position c ^ swz(t), so the rows one operand read touches fall in
+// distinct LDS banks.  The slots are distinct arrays and the tile loop is
+// unrolled over them, so every copy and every read names its slot at
+// compile time.  A wave waits only for its own copies of the tile it is
+// about to read (vmcnt counts the later tiles' copies still in flight), then
+// one barrier per tile makes all of them visible and frees the slot the
+// next copy reuses.
+template <int D>
+struct SpRing {
+  static constexpr int EPC = 8;                      // bf16 per 16 bytes
+  static constexpr int CPR = D / EPC;                // chunks per row
+  static constexpr int RPI = kWave / CPR;            // rows per copy instruction
+  static constexpr int RP256 = 256 / (D * 2) > 0 ? 256 / (D * 2) : 1;
+  static constexpr int IK = kTile / RPI;             // copies per 32-row tile
+  static constexpr int R = 4;                        // ring slots
+  __device__ static constexpr int swz(int t) { return (t / RP256) % CPR; }
+};
+
+template <int D>
+struct alignas(16) SpSlot {
+  bf16 k[kTile * D];
+  bf16 v[kTile * D];
+};
+
+template <int D, int NG>
+__global__ __launch_bounds__(kWave* NG, 2) void hyb_sp_ring_kernel(SoftmaxPrefixArgs a, int chunk) {
+  typedef Mma<bf16> M;
+  typedef typename M::op_t op_t;
+  typedef SpRing<D> RG;
+  constexpr int E = M::E, KW = M::KW, KD = D / KW, KL = kTile / KW, NCT = D / kTile;
+  constexpr int EPC = RG::EPC, CPR = RG::CPR, RPI = RG::RPI, IK = RG::IK, R = RG::R;
+  constexpr int IPW = 2 * IK / NG;  // copies per wave per tile
+  static_assert(IPW * NG == 2 * IK, "copies split evenly over the waves");
+  __shared__ SpSlot<D> s0, s1, s2, s3;
+
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int w = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int li = lane & 31, hh = lane >> 5;
+  const int Hq = a.s.Hq, Hkv = a.s.Hkv, L = a.s.L, G = Hq / Hkv;
+  const int ns = a.n_split, Pmax = a.max_prefix;
+  // The KV head varies fastest: the Hkv workgroups that read the same
+  // token rows of the cache (each its 1/Hkv share of every row) start
+  // together.
+  const int g = blockIdx.x % Hkv;
+  const int s = (blockIdx.x / Hkv) % ns;
+  const int b = blockIdx.x / (Hkv * ns), h = g * G + w;
+  int P = a.prefix_len[b];
+  P = P < 0 ? 0 : (P > Pmax ? Pmax : P);
+  const int N = P + L;
+  const int lo = s * chunk;
+  const int hi = min(lo + chunk, N);
+  const int ntiles = hi > lo ? (hi - lo + kTile - 1) / kTile : 0;
+  const size_t qstride = (size_t)Hq * D, kstride = (size_t)Hkv * D;
+
+  op_t qop[KD];
+  {
+    const bf16* qrow = (const bf16*)a.q + ((size_t)b * L * Hq + h) * D + (size_t)li * qstride + hh * E;
+#pragma unroll
+    for (int ks = 0; ks < KD; ++ks) qop[ks] = li < L ? load_op<bf16>(qrow + ks * KW) : M::zero();
+  }
+  const bf16* kc = (const bf16*)a.k_cache + ((size_t)b * Pmax * Hkv + g) * D;
+  const bf16* vc = (const bf16*)a.v_cache + ((size_t)b * Pmax * Hkv + g) * D;
+  const bf16* kbk = (const bf16*)a.k + ((size_t)b * L * Hkv + g) * D;
+  const bf16* vbk = (const bf16*)a.v + ((size_t)b * L * Hkv + g) * D;
+
+  // This wave's copies of tile n (keys past the range read the range's last
+  // key, in bounds, and are masked below).
+  auto issue = [&](int n, SpSlot<D>& sl) __attribute__((always_inline)) {
+    const int j0 = lo + n * kTile;
+#pragma unroll
+    for (int u = 0; u < IPW; ++u) {
+      const int ins = w * IPW + u, kv = ins / IK, i = ins % IK;
+      const int t = i * RPI + lane / CPR, pos = lane % CPR;
+      const int j = min(j0 + t, hi - 1);
+      const bf16* row = kv == 0 ? (j < P ? kc + (size_t)j * kstride : kbk + (size_t)(j - P) * kstride)
+                                : (j < P ? vc + (size_t)j * kstride : vbk + (size_t)(j - P) * kstride);
+      bf16* dst = (kv == 0 ? sl.k : sl.v) + i * RPI * D;
+      __builtin_amdgcn_global_load_lds(
+          (const __attribute__((address_space(1))) void*)(row + (pos ^ RG::swz(t)) * EPC),
+          (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
+    }
+  };
+
+  const float scale = 1.0f / sqrtf((float)D);
+  float m = -INFINITY, l = 0.0f;
+  f32x16 acc[NCT];
+#pragma unroll
+  for (int ct = 0; ct < NCT; ++ct) acc[ct] = f32x16{};
+
+  auto compute = [&](int n, const SpSlot<D>& sl) __attribute__((always_inline)) {
+    const int j0 = lo + n * kTile;
+    f32x16 sc = {};
+#pragma unroll
+    for (int ks = 0; ks < KD; ++ks) {
+      const int c = 2 * ks + hh;  // 16-byte chunk of elements ks*KW + hh*E
+      sc = M::mma(load_op<bf16>(&sl.k[li * D + (c ^ RG::swz(li)) * EPC]), qop[ks], sc);
+    }
+    const bool full = j0 + kTile <= hi;
+    float p[16];
+    float mt = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      p[i] = (full || j0 + row_of(i, hh) < hi) ? sc[i] * scale : -INFINITY;
+      mt = fmaxf(mt, p[i]);
+    }
+    mt = fmaxf(mt, xor32(mt));
+    const float mn = fmaxf(m, mt);
+    float ps = 0.0f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      p[i] = as_operand<bf16>(fast_exp(p[i] - mn));
+      ps += p[i];
+    }
+    ps += xor32(ps);
+    if (__any(mn > m)) {
+      const float corr = fast_exp(m - mn);
+      l *= corr;
+#pragma unroll
+      for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[ct][i] *= corr;
+    }
+    l += ps;
+    m = mn;
+    // V^T operands by transposing reads: in each 16-lane quarter lane i
+    // addresses key kb + i/4 at columns cb + 4*(i%4) .. +3 and receives
+    // keys kb .. kb+3 of column cb + i.
+    typedef short s16x4 __attribute__((ext_vector_type(4)));
+    const int qi = lane & 15;
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct) {
+      const int col = ct * kTile + 16 * ((lane >> 4) & 1) + 4 * (qi & 3);
+#pragma unroll
+      for (int ks = 0; ks < KL; ++ks) {
+        auto piece = [&](int t) {
+          const bf16* src = &sl.v[t * D + ((col / EPC) ^ RG::swz(t)) * EPC + col % EPC];
+          return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)src);
+        };
+        const int kb = 16 * ks + 4 * hh + qi / 4;
+        const s16x4 x0 = piece(kb), x1 = piece(kb + 8);
+        const op_t va = __builtin_bit_cast(op_t, __builtin_shufflevector(x0, x1, 0, 1, 2, 3, 4, 5, 6, 7));
+        acc[ct] = M::mma(va, cvt_op<bf16>(&p[ks * E]), acc[ct]);
+      }
+    }
+  };
+
+  // Wait for this wave's copies of tile n, with `later` tiles issued after
+  // it still in flight.
+  auto wait_tile = [&](int later) __attribute__((always_inline)) {
+    if (later >= 2) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * IPW) : "memory");
+    else if (later == 1) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(IPW) : "memory");
+    else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  };
+  auto slot = [&](auto S) -> SpSlot<D>& {
+    if constexpr (decltype(S)::value == 0) return s0;
+    else if constexpr (decltype(S)::value == 1) return s1;
+    else if constexpr (decltype(S)::value == 2) return s2;
+    else return s3;
+  };
+  auto step = [&](int n, auto S) __attribute__((always_inline)) {
+    constexpr int SV = decltype(S)::value;
+    wait_tile(min(R - 2, ntiles - 1 - n));
+    lds_barrier_nodrain();  // tile n visible everywhere; slot of tile n-1 free
+    if (n + R - 1 < ntiles) issue(n + R - 1, slot(std::integral_constant<int, (SV + R - 1) % R>{}));
+    compute(n, slot(S));
+  };
+
+  if (0 < ntiles) issue(0, s0);
+  if (1 < ntiles) issue(1, s1);
+  if (2 < ntiles) issue(2, s2);
+  for (int n = 0; n < ntiles; n += R) {
+    step(n, std::integral_constant<int, 0>{});
+    if (n + 1 < ntiles) step(n + 1, std::integral_constant<int, 1>{});
+    if (n + 2 < ntiles) step(n + 2, std::integral_constant<int, 2>{});
+    if (n + 3 < ntiles) step(n + 3, std::integral_constant<int, 3>{});
+  }
+
+  if (li >= L) return;
+  const size_t row = (((size_t)b * Hq + h) * ns + s) * L + li;
+  float* wacc = (float*)a.ws + row * D;
+  float* wml = (float*)a.ws + (size_t)a.s.B * Hq * ns * L * D + row * 2;
+#pragma unroll
+  for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+    for (int i = 0; i < 16; i += 4)
+      *reinterpret_cast<f32x4*>(wacc + ct * kTile + row_of(i, hh)) =
+          f32x4{acc[ct][i], acc[ct][i + 1], acc[ct][i + 2], acc[ct][i + 3]};
+  if (hh == 0) {
+    wml[0] = m;
+    wml[1] = l;
+  }
+}
+
 // Merge of the n_split partial results of one (request, head, query).
 template <typename T, int D>
 __global__ __launch_bounds__(D) void hyb_sp_combine_kernel(
@@ -258,21 +458,34 @@ static hipError_t sp_go(const SoftmaxPrefixArgs& a, hipStream_t st) {
   chunk = (chunk + kTile - 1) / kTile * kTile;
   const int G = a.s.Hq / a.s.Hkv;
   const dim3 grid(a.s.B * a.s.Hkv * ns);
+  bool launched_ring = false;
+  if constexpr (sizeof(T) == 2) {
+    launched_ring = true;
+    switch (G) {
+      case 1: hipLaunchKernelGGL((hyb_sp_ring_kernel<D, 1>), grid, dim3(kWave), 0, st, a, chunk); break;
+      case 2: hipLaunchKernelGGL((hyb_sp_ring_kernel<D, 2>), grid, dim3(kWave * 2), 0, st, a, chunk); break;
+      case 4: hipLaunchKernelGGL((hyb_sp_ring_kernel<D, 4>), grid, dim3(kWave * 4), 0, st, a, chunk); break;
+      case 8: hipLaunchKernelGGL((hyb_sp_ring_kernel<D, 8>), grid, dim3(kWave * 8), 0, st, a, chunk); break;
+      default: launched_ring = false;  // the register-staged kernel below
+    }
+  }
 #define HYB_SP_CASE(NG)                                                               \
   case NG:                                                                            \
     hipLaunchKernelGGL((hyb_sp_partial_kernel<T, D, NG>), grid, dim3(kWave * NG), 0, st, a, \
                        chunk);                                                        \
     break;
-  switch (G) {
-    HYB_SP_CASE(1)
-    HYB_SP_CASE(2)
-    HYB_SP_CASE(3)
-    HYB_SP_CASE(4)
-    HYB_SP_CASE(5)
-    HYB_SP_CASE(6)
-    HYB_SP_CASE(7)
-    HYB_SP_CASE(8)
-    default: return hipErrorInvalidValue;
+  if (!launched_ring) {
+    switch (G) {
+      HYB_SP_CASE(1)
+      HYB_SP_CASE(2)
+      HYB_SP_CASE(3)
+      HYB_SP_CASE(4)
+      HYB_SP_CASE(5)
+      HYB_SP_CASE(6)
+      HYB_SP_CASE(7)
+      HYB_SP_CASE(8)
+      default: return hipErrorInvalidValue;
+    }
   }
 #undef HYB_SP_CASE
   hipError_t e = hipGetLastError();
