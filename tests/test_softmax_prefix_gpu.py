@@ -20,6 +20,11 @@ CASES = [
     (3, 4, 4, 128, 16, "bf16", 777, [0, 777, 5]),
     (2, 8, 1, 64, 32, "bf16", 2048, [2048, 1536]),
     (2, 4, 2, 128, 7, "bf16", 96, [96, 200]),   # prefix_len above max is clamped
+    # the copy-ring kernel at d=64 with 4 heads per KV head, and at d=128 with 8;
+    # 3 heads per KV head take the register-staged kernel
+    (2, 8, 2, 64, 16, "bf16", 500, [500, 260]),
+    (1, 8, 1, 128, 32, "bf16", 5000, [4900]),
+    (2, 6, 2, 64, 32, "bf16", 1000, [1000, 33]),
 ]
 
 
