@@ -70,6 +70,10 @@ PREFILL_SHAPES = [
     (2, 4, 1, 64, 16, 128, "bf16", 96),
     (1, 8, 8, 128, 32, 128, "bf16", 96),
     (2, 4, 2, 128, 5, 64, "bf16", 35),
+    # the pipelined walk and delta at d=64 with F=64, and at d=128 with F=32
+    # (two segments of 5 blocks: an odd count for the delta's block pairs)
+    (2, 8, 2, 64, 32, 64, "bf16", 256),
+    (2, 8, 4, 128, 16, 32, "bf16", 160),
 ]
 
 
