@@ -413,29 +413,40 @@ __global__ __launch_bounds__(kWave* NG, 2) void hyb_sp_ring_kernel(SoftmaxPrefix
   }
 }
 
-// Merge of the n_split partial results of one (request, head, query).
+// Merge of the n_split partial results.  A thread handles 4 columns of one
+// (request, head, query) row (16-byte loads); a workgroup of 256 threads
+// covers 256 / (D/4) rows.
 template <typename T, int D>
-__global__ __launch_bounds__(D) void hyb_sp_combine_kernel(
-    SoftmaxPrefixArgs a) {
+__global__ __launch_bounds__(256) void hyb_sp_combine_kernel(SoftmaxPrefixArgs a) {
+  constexpr int TPR = D / 4;              // threads per row
+  constexpr int RPB = 256 / TPR;          // rows per workgroup
   const int Hq = a.s.Hq, L = a.s.L, ns = a.n_split;
-  const int i = blockIdx.x % L, bh = blockIdx.x / L;
-  const int b = bh / Hq, h = bh % Hq, c = threadIdx.x;
-  const size_t row0 = ((size_t)bh * ns) * L + i;
+  const size_t nrows = (size_t)a.s.B * Hq * L;
+  const size_t r = (size_t)blockIdx.x * RPB + threadIdx.x / TPR;
+  if (r >= nrows) return;
+  const int c = (threadIdx.x % TPR) * 4;
+  const int i = (int)(r % L);
+  const size_t bh = r / L;
+  const int b = (int)(bh / Hq), h = (int)(bh % Hq);
+  const size_t row0 = (bh * ns) * L + i;
   const float* wacc = (const float*)a.ws;
   const float* wml = wacc + (size_t)a.s.B * Hq * ns * L * D;
   float M = -INFINITY;
   for (int s = 0; s < ns; ++s) M = fmaxf(M, wml[(row0 + (size_t)s * L) * 2]);
-  float num = 0.0f, den = 0.0f;
+  f32x4 num = {0.0f, 0.0f, 0.0f, 0.0f};
+  float den = 0.0f;
   for (int s = 0; s < ns; ++s) {
-    const size_t r = row0 + (size_t)s * L;
-    const float ms = wml[r * 2];
+    const size_t rr = row0 + (size_t)s * L;
+    const float ms = wml[rr * 2];
     if (ms == -INFINITY) continue;
     const float wgt = expf(ms - M);
-    num += wgt * wacc[r * D + c];
-    den += wgt * wml[r * 2 + 1];
+    const f32x4 x = *reinterpret_cast<const f32x4*>(wacc + rr * D + c);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) num[e] += wgt * x[e];
+    den += wgt * wml[rr * 2 + 1];
   }
-  store_out1<T>(a.out, (((size_t)b * L + i) * Hq + h) * D + c, num / den,
-                a.s.out_f32);
+  const float o[4] = {num[0] / den, num[1] / den, num[2] / den, num[3] / den};
+  store_out4<T>(a.out, (((size_t)b * L + i) * Hq + h) * D + c, o, a.s.out_f32);
 }
 
 int softmax_prefix_splits(const Shape& s, int max_prefix) {
@@ -490,8 +501,12 @@ static hipError_t sp_go(const SoftmaxPrefixArgs& a, hipStream_t st) {
 #undef HYB_SP_CASE
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((hyb_sp_combine_kernel<T, D>), dim3(a.s.B * a.s.Hq * a.s.L),
-                     dim3(D), 0, st, a);
+  {
+    const size_t rows = (size_t)a.s.B * a.s.Hq * a.s.L;
+    constexpr int RPB = 256 / (D / 4);
+    hipLaunchKernelGGL((hyb_sp_combine_kernel<T, D>), dim3((unsigned)((rows + RPB - 1) / RPB)),
+                       dim3(256), 0, st, a);
+  }
   return hipGetLastError();
 }
 
