@@ -10,7 +10,8 @@
 // LDS).  Each 32-key tile gives Sc^T = K Q^T (keys in rows, one query per
 // lane column), an online-softmax update, and O^T += V^T P^T, with P rounded
 // once to the operand type and the running sum taken over the rounded
-// weights.  A second kernel merges the ranges with their log-sum-exp weights.
+// weights.  A second kernel merges the ranges with their log-sum-exp weights;
+// with a single range the first kernel writes the normalised output itself.
 #include <type_traits>
 
 #include "device.h"
@@ -200,6 +201,20 @@ __global__ __launch_bounds__(kWave* NG) void hyb_sp_partial_kernel(
 
   // Partial result of this range: unnormalised O, running max and sum.
   if (li >= L) return;
+  if (ns == 1) {
+    // one range: the result is final, normalised here (no combine launch)
+    const float inv = 1.0f / l;
+    const size_t ob = (((size_t)b * L + li) * Hq + h) * D;
+#pragma unroll
+    for (int ct = 0; ct < C::NCT; ++ct)
+#pragma unroll
+      for (int i = 0; i < 16; i += 4) {
+        const float o[4] = {acc[ct][i] * inv, acc[ct][i + 1] * inv, acc[ct][i + 2] * inv,
+                            acc[ct][i + 3] * inv};
+        store_out4<T>(a.out, ob + ct * kTile + row_of(i, hh), o, a.s.out_f32);
+      }
+    return;
+  }
   const size_t row = (((size_t)b * Hq + h) * ns + s) * L + li;
   float* wacc = (float*)a.ws + row * D;
   float* wml = (float*)a.ws + (size_t)a.s.B * Hq * ns * L * D + row * 2;
@@ -398,6 +413,20 @@ __global__ __launch_bounds__(kWave* NG, 2) void hyb_sp_ring_kernel(SoftmaxPrefix
   }
 
   if (li >= L) return;
+  if (ns == 1) {
+    // one range: the result is final, normalised here (no combine launch)
+    const float inv = 1.0f / l;
+    const size_t ob = (((size_t)b * L + li) * Hq + h) * D;
+#pragma unroll
+    for (int ct = 0; ct < NCT; ++ct)
+#pragma unroll
+      for (int i = 0; i < 16; i += 4) {
+        const float o[4] = {acc[ct][i] * inv, acc[ct][i + 1] * inv, acc[ct][i + 2] * inv,
+                            acc[ct][i + 3] * inv};
+        store_out4<bf16>(a.out, ob + ct * kTile + row_of(i, hh), o, a.s.out_f32);
+      }
+    return;
+  }
   const size_t row = (((size_t)b * Hq + h) * ns + s) * L + li;
   float* wacc = (float*)a.ws + row * D;
   float* wml = (float*)a.ws + (size_t)a.s.B * Hq * ns * L * D + row * 2;
@@ -500,7 +529,7 @@ static hipError_t sp_go(const SoftmaxPrefixArgs& a, hipStream_t st) {
   }
 #undef HYB_SP_CASE
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
+  if (e != hipSuccess || ns == 1) return e;  // one range: already written out
   {
     const size_t rows = (size_t)a.s.B * a.s.Hq * a.s.L;
     constexpr int RPB = 256 / (D / 4);
