@@ -25,8 +25,9 @@
 //      dL/dphi(Q), which contracts over the head dimension.  Per block it
 //      forms out, dL/dN, dL/dD, dL/dphi(Q) and the query part of dL/dW and
 //      dL/dalpha, and hands dL/dN^T and dL/dD to the workspace;
-//   3. hyb_bwd_rev_kernel, delta mode: each segment's sum of
-//      phi(Q)^T dL/dN (and phi(Q)^T dL/dD);
+//   3. each segment's sum of phi(Q)^T dL/dN (and phi(Q)^T dL/dD):
+//      hyb_bwd_gdelta_kernel on the bf16 path (pipelined, below),
+//      hyb_bwd_rev_kernel in delta mode on fp32;
 //   4. hyb_bwd_rev_kernel, walk mode: reverse walk with Gbar^T in the
 //      accumulators, the key part of dL/dW;
 //   5. hyb_bwd_reduce_kernel: sums the per-(request, segment) partials in a
@@ -769,6 +770,189 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_rev_kernel(BwdKArgs
   }
 }
 
+
+// ---------------------------------------------------------------------------
+// 3'. Pipelined reverse delta (bf16, F <= 64): the sum over a segment's
+// blocks of phi(Q)^T dL/dN (and phi(Q)^T dL/dD), two blocks per step.
+// Waves 0 and 1 compute phi(Q) of the pair's blocks (the whole feature map in
+// one wave) and store it transposed as packed hi/lo pairs; waves 2 and 3 turn
+// the blocks' dL/dN^T rows (fp32, from the forward walk) into hi/lo
+// operands; the state waves accumulate Gbar (rows: features, columns
+// 32w..32w+31) with three products per pair of operand pairs.  One barrier
+// per block pair; buffers double-buffered.
+// ---------------------------------------------------------------------------
+template <int D, int F>
+struct GDeltaCfg {
+  typedef Mma<bf16> M;
+  typedef typename M::op_t op_t;
+  static constexpr int NC = D / kTile;   // state waves
+  static constexpr int NP = 4;           // 2 feature-map + 2 operand waves
+  static constexpr int NWAVE = NP + NC;
+  static constexpr int f = 2 * F;
+  static constexpr int NRT = f / kTile;
+  static constexpr int KD = D / M::KW;
+  static constexpr int KL = kTile / M::KW;
+  typedef WaveFeatMap<bf16, D, F> WFM;
+  struct alignas(16) Buf {
+    uint32_t phiQT[2][f][kTile + 4];     // per block of the pair: bf16 hi | lo << 16
+    op_t gn[2][2][NC][KL][kWave];        // per block: hi/lo, column tile, k-step, lane
+    float gd[2][kTile];
+  };
+  struct alignas(16) Smem {
+    Buf buf[2];
+    float gz[f];
+  };
+};
+
+template <int D>
+constexpr int gdelta_threads() {
+  return kWave * (4 + D / kTile);
+}
+
+template <int D, int F>
+__global__ __launch_bounds__(gdelta_threads<D>()) void hyb_bwd_gdelta_kernel(BwdKArgs ka) {
+  typedef GDeltaCfg<D, F> C;
+  typedef typename C::M M;
+  typedef typename C::op_t op_t;
+  typedef typename C::WFM WFM;
+  constexpr int f = C::f, E = M::E, KW = M::KW, NP = C::NP, NC = C::NC;
+  static_assert(gdelta_threads<D>() == kWave * C::NWAVE, "launch bounds match the waves");
+  __shared__ typename C::Smem sh;
+  const BackwardArgs& a = ka.a;
+
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int w = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int li = lane & 31, hh = lane >> 5;
+  const int Hq = a.s.Hq, L = a.s.L, T_ = a.T;
+  const int units = a.s.B * Hq, nseg = ka.nseg;
+  // segments 1 .. nseg-1 (segment 0's sum is never needed)
+  const int vix = xcd_unit(blockIdx.x, units * (nseg - 1));
+  const int u = vix % units, seg = vix / units + 1;
+  const int b = u / Hq, h = u % Hq;
+  const size_t qstride = (size_t)Hq * D;
+  const int blk0 = seg * ka.seg_blocks, blk1 = min(ka.nblk, blk0 + ka.seg_blocks);
+  const int npair = (blk1 - blk0 + 1) / 2;
+  const bool row_ok = li < L;
+  const int lrow = min(li, L - 1);
+  for (int r = tid; r < f; r += blockDim.x) sh.gz[r] = 0.0f;
+  lds_barrier();
+
+  if (w < 2) {
+    // ---- phi(Q) of block blk0 + 2j + w ----
+    const bf16* __restrict__ Wt_h = (const bf16*)a.W + (size_t)h * F * D;
+    op_t wop[WFM::NT][C::KD];
+    WFM::load_w(Wt_h, li, hh, wop);
+    op_t x[C::KD];
+    auto load = [&](int blk) {
+      const bf16* row = (const bf16*)a.q + (((size_t)b * T_ + (size_t)blk * L) * Hq + h) * D +
+                        (size_t)lrow * qstride + hh * E;
+#pragma unroll
+      for (int ks = 0; ks < C::KD; ++ks) x[ks] = load_op<bf16>(row + ks * KW);
+    };
+    if (blk0 + w < blk1) load(blk0 + w);
+    for (int j = 0; j <= npair; ++j) {
+      const int blk = blk0 + 2 * j + w;
+      if (j < npair && blk < blk1) {
+        typename C::Buf& B = sh.buf[j & 1];
+        op_t xm[C::KD];
+#pragma unroll
+        for (int ks = 0; ks < C::KD; ++ks) xm[ks] = keep_if<bf16>(row_ok, x[ks]);
+        if (blk + 2 < blk1) load(blk + 2);  // next pair's block in flight
+        float phi[WFM::NPAIR][16];
+        WFM::compute(wop, xm, phi);
+#pragma unroll
+        for (int p = 0; p < WFM::NPAIR; ++p)
+#pragma unroll
+          for (int i = 0; i < 16; ++i)
+            B.phiQT[w][WFM::feature(16 * p + i, hh)][li] = pack_hi_lo(row_ok ? phi[p][i] : 0.0f);
+      }
+      lds_barrier();
+    }
+  } else if (w < NP) {
+    // ---- dL/dN^T operands (and dL/dD) of block blk0 + 2j + (w - 2) ----
+    // Operand of column tile ct, k-step ks: lane (li, hh) holds column
+    // 32ct + li at the block's tokens row_of(ks*E + e, hh) (two runs of 4).
+    const int q = w - 2;
+    for (int j = 0; j <= npair; ++j) {
+      const int blk = blk0 + 2 * j + q;
+      if (j < npair && blk < blk1) {
+        typename C::Buf& B = sh.buf[j & 1];
+        const float* gnT = ka.gnT + ((size_t)u * ka.nblk + blk) * D * kTile;
+#pragma unroll
+        for (int ct = 0; ct < NC; ++ct)
+#pragma unroll
+          for (int ks = 0; ks < C::KL; ++ks) {
+            const float* src = gnT + (size_t)(ct * kTile + li) * kTile + 16 * ks + 4 * hh;
+            const f32x4 x0 = *reinterpret_cast<const f32x4*>(src);
+            const f32x4 x1 = *reinterpret_cast<const f32x4*>(src + 8);
+            const float xv[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+            op_t hi, lo;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              hi[e] = (bf16)xv[e];
+              lo[e] = (bf16)(xv[e] - (float)hi[e]);
+            }
+            B.gn[q][0][ct][ks][lane] = hi;
+            B.gn[q][1][ct][ks][lane] = lo;
+          }
+        if (lane < kTile) B.gd[q][lane] = ka.gd[((size_t)u * ka.nblk + blk) * kTile + lane];
+      }
+      lds_barrier();
+    }
+  } else {
+    // ---- state waves: Gbar (features x columns 32cw..) += phi(Q)^T dL/dN ----
+    const int cw = w - NP, col = cw * kTile + li;
+    f32x16 gacc[C::NRT];
+#pragma unroll
+    for (int rt = 0; rt < C::NRT; ++rt) gacc[rt] = f32x16{};
+    for (int j = 0; j <= npair; ++j) {
+      const int pj = j - 1;
+      if (pj >= 0) {
+        typename C::Buf& B = sh.buf[pj & 1];
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          if (blk0 + 2 * pj + q >= blk1) continue;  // uniform
+#pragma unroll
+          for (int ks = 0; ks < C::KL; ++ks) {
+            const op_t gh = B.gn[q][0][cw][ks][lane], gl = B.gn[q][1][cw][ks][lane];
+#pragma unroll
+            for (int rt = 0; rt < C::NRT; ++rt) {
+              op_t ph, pl;
+              lds_pair_op(&B.phiQT[q][rt * kTile + li][0], ks, hh, ph, pl);
+              gacc[rt] = M::mma(ph, gh, gacc[rt]);
+              gacc[rt] = M::mma(pl, gh, gacc[rt]);
+              gacc[rt] = M::mma(ph, gl, gacc[rt]);
+            }
+          }
+          // gz += sum_i phi(q_i) dL/dD_i
+          for (int r = tid - NP * kWave; r < f; r += NC * kWave) {
+            float s = 0.0f;
+#pragma unroll
+            for (int t0 = 0; t0 < kTile; t0 += 4) {
+              const uint4 xq = *reinterpret_cast<const uint4*>(&B.phiQT[q][r][t0]);
+#pragma unroll
+              for (int e = 0; e < 4; ++e)
+                s += (unpack_hi(xq[e]) + unpack_lo(xq[e])) * B.gd[q][t0 + e];
+            }
+            sh.gz[r] += s;
+          }
+        }
+      }
+      lds_barrier();
+    }
+    // Gbar^T tiles as the reverse walk reads them: element (c, r) at c*f + r
+    float* dst = ka.dG + ((size_t)u * nseg + seg) * D * f;
+#pragma unroll
+    for (int rt = 0; rt < C::NRT; ++rt)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj)
+        *reinterpret_cast<f32x4*>(dst + (size_t)col * f + rt * kTile + row_of(4 * jj, hh)) =
+            f32x4{gacc[rt][4 * jj], gacc[rt][4 * jj + 1], gacc[rt][4 * jj + 2], gacc[rt][4 * jj + 3]};
+    float* zd = ka.dgz + ((size_t)u * nseg + seg) * f;
+    for (int r = tid - NP * kWave; r < f; r += NC * kWave) zd[r] = sh.gz[r];
+  }
+}
+
 // ---------------------------------------------------------------------------
 // 5. Sum of the partials over requests and segments, in a fixed order.
 // ---------------------------------------------------------------------------
@@ -839,8 +1023,13 @@ static hipError_t bwd_go(const BackwardArgs& a, hipStream_t st) {
   hipLaunchKernelGGL((hyb_bwd_fwd_kernel<T, D, F>), dim3(units * nseg), block, 0, st, ka);
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (nseg > 1) {
-    hipLaunchKernelGGL((hyb_bwd_rev_kernel<T, D, F>), dim3(units * (nseg - 1)), block, 0, st,
-                       ka, 1);
+    if constexpr (sizeof(T) == 2) {
+      hipLaunchKernelGGL((hyb_bwd_gdelta_kernel<D, F>), dim3(units * (nseg - 1)),
+                         dim3(gdelta_threads<D>()), 0, st, ka);
+    } else {
+      hipLaunchKernelGGL((hyb_bwd_rev_kernel<T, D, F>), dim3(units * (nseg - 1)), block, 0, st,
+                         ka, 1);
+    }
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
   hipLaunchKernelGGL((hyb_bwd_rev_kernel<T, D, F>), dim3(units * nseg), block, 0, st, ka, 0);
