@@ -28,8 +28,9 @@
 //   3. each segment's sum of phi(Q)^T dL/dN (and phi(Q)^T dL/dD):
 //      hyb_bwd_gdelta_kernel on the bf16 path (pipelined, below),
 //      hyb_bwd_rev_kernel in delta mode on fp32;
-//   4. hyb_bwd_rev_kernel, walk mode: reverse walk with Gbar^T in the
-//      accumulators, the key part of dL/dW;
+//   4. reverse walk with Gbar^T in the accumulators, the key part of dL/dW:
+//      hyb_bwd_rwalk_kernel on the bf16 path (pipelined, below),
+//      hyb_bwd_rev_kernel in walk mode on fp32;
 //   5. hyb_bwd_reduce_kernel: sums the per-(request, segment) partials in a
 //      fixed order (bitwise reproducible, no atomics).
 // On the bf16 path phi(K), phi(Q) (as an update operand) and dL/du enter the
@@ -175,6 +176,16 @@ __device__ inline void load_split_op(const float* p, typename Mma<T>::op_t& hi,
       hi[e] = (T)x[e];
       lo[e] = (T)(x[e] - as_operand<T>(x[e]));
     }
+  }
+}
+
+// Eight fp32 values (a, then b) as a bf16 operand pair hi + lo.
+__device__ inline void split_op(const f32x4& a, const f32x4& b, bf16x8& hi, bf16x8& lo) {
+  const float x[8] = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+#pragma unroll
+  for (int e = 0; e < 8; ++e) {
+    hi[e] = (bf16)x[e];
+    lo[e] = (bf16)(x[e] - as_operand<bf16>(x[e]));
   }
 }
 
@@ -953,6 +964,342 @@ __global__ __launch_bounds__(gdelta_threads<D>()) void hyb_bwd_gdelta_kernel(Bwd
   }
 }
 
+
+// ---------------------------------------------------------------------------
+// 4'. Pipelined reverse walk (bf16, F <= 64).  Blocks are taken last to
+// first; producers prepare block c-1 while the state waves finish block c:
+//   wave 0: phi(Q) of the block, stored transposed as packed hi/lo pairs
+//           (the operand of the Gbar update);
+//   wave 1: phi(K), fp32 [token][feature] (the feature-map Jacobian);
+//   wave 2: the V rows as operands of dL/dphi(K) and the K^T operands of dW;
+//   wave 3: the dL/dN^T hi/lo operands and dL/dD of the block;
+//   state waves (D/32): dL/dphi(K) = Gbar v + gz for the feature tiles they
+//           own, the per-sign sums, dL/du (packed hi/lo, transposed), then
+//           the Gbar and gz updates, then dW += dL/du^T K for columns
+//           32w..32w+31.  Gbar^T and the partial dW stay in registers.
+// Three barriers per block (all waves take part): after the per-sign
+// partial sums, after dL/du, and at the end of the step.
+// ---------------------------------------------------------------------------
+template <int D, int F>
+struct RWalkCfg {
+  typedef Mma<bf16> M;
+  typedef typename M::op_t op_t;
+  static constexpr int NC = D / kTile;       // state waves / column slices
+  static constexpr int NP = 4;
+  static constexpr int NWAVE = NP + NC;
+  static constexpr int f = 2 * F;
+  static constexpr int NRT = f / kTile;      // feature tiles
+  static constexpr int NT = F / kTile;       // tiles per sign
+  static constexpr int RPW = (NRT + NC - 1) / NC;
+  static constexpr int KD = D / M::KW;
+  static constexpr int KL = kTile / M::KW;
+  typedef WaveFeatMap<bf16, D, F> WFM;
+  struct alignas(16) Buf {
+    uint32_t phiQT[f][kTile + 4];    // phi(q_i)[r] at [r][i], bf16 hi | lo << 16
+    float phiK[kTile][f + 4];        // phi(k_t)[r] at [t][r]
+    op_t vrow[NC][KL][kWave];        // V rows: lane (t, hh), columns 32s + row_of
+    op_t ktop[NC][KL][kWave];        // K^T: lane (c, hh), tokens in row_of order
+    op_t gn[2][NC][KL][kWave];       // dL/dN^T hi, lo: lane (c, hh), tokens natural
+    float gd[kTile];
+  };
+  struct alignas(16) Smem {
+    Buf buf[2];
+    uint32_t duT[2][F][kTile + 4];   // +-dL/du of each sign at [j][t], packed hi/lo
+    float gz[f];
+    float jsum[NRT][kTile];
+  };
+};
+
+template <int D>
+constexpr int rwalk_threads() {
+  return kWave * (4 + D / kTile);
+}
+
+template <int D, int F>
+__global__ __launch_bounds__(rwalk_threads<D>()) void hyb_bwd_rwalk_kernel(BwdKArgs ka) {
+  typedef RWalkCfg<D, F> C;
+  typedef typename C::M M;
+  typedef typename C::op_t op_t;
+  typedef typename C::WFM WFM;
+  constexpr int f = C::f, E = M::E, KW = M::KW, NP = C::NP, NC = C::NC;
+  constexpr int NRT = C::NRT, NT = C::NT, RPW = C::RPW;
+  static_assert(rwalk_threads<D>() == kWave * C::NWAVE, "launch bounds match the waves");
+  __shared__ typename C::Smem sh;
+  const BackwardArgs& a = ka.a;
+
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int w = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int li = lane & 31, hh = lane >> 5;
+  const int Hq = a.s.Hq, Hkv = a.s.Hkv, L = a.s.L, T_ = a.T;
+  const int units = a.s.B * Hq, nseg = ka.nseg;
+  const int vix = xcd_unit(blockIdx.x, units * nseg);
+  const int u = vix % units, seg = vix / units;
+  const int b = u / Hq, h = u % Hq, g = h / (Hq / Hkv);
+  const size_t qstride = (size_t)Hq * D, kstride = (size_t)Hkv * D;
+  const int blk0 = seg * ka.seg_blocks, blk1 = min(ka.nblk, blk0 + ka.seg_blocks);
+  const int nb = blk1 - blk0;
+  const bool row_ok = li < L;
+  const int lrow = min(li, L - 1);
+  auto blk_of = [&](int n) { return blk1 - 1 - n; };  // step n handles block blk_of(n)
+  auto qrow = [&](int blk) {
+    return (const bf16*)a.q + (((size_t)b * T_ + (size_t)blk * L) * Hq + h) * D;
+  };
+  auto krow = [&](int blk) {
+    return (const bf16*)a.k + (((size_t)b * T_ + (size_t)blk * L) * Hkv + g) * D;
+  };
+  auto vrowp = [&](int blk) {
+    return (const bf16*)a.v + (((size_t)b * T_ + (size_t)blk * L) * Hkv + g) * D;
+  };
+
+  // gz: the later segments' sums (Gbar likewise, in the state waves below)
+  for (int r = tid; r < f; r += blockDim.x) {
+    float zr = 0.0f;
+    for (int sp = seg + 1; sp < nseg; ++sp) zr += ka.dgz[((size_t)u * nseg + sp) * f + r];
+    sh.gz[r] = zr;
+  }
+  lds_barrier();
+
+  if (w < 2) {
+    // ---- feature map of Q (wave 0) or K (wave 1) ----
+    const bf16* __restrict__ Wt_h = (const bf16*)a.W + (size_t)h * F * D;
+    op_t wop[WFM::NT][C::KD];
+    WFM::load_w(Wt_h, li, hh, wop);
+    op_t x[C::KD];
+    auto load = [&](int blk) {
+      const bf16* row = (w == 0 ? qrow(blk) + (size_t)lrow * qstride : krow(blk) + (size_t)lrow * kstride) + hh * E;
+#pragma unroll
+      for (int ks = 0; ks < C::KD; ++ks) x[ks] = load_op<bf16>(row + ks * KW);
+    };
+    if (nb > 0) load(blk_of(0));
+    for (int n = 0; n <= nb; ++n) {
+      if (n < nb) {
+        typename C::Buf& B = sh.buf[n & 1];
+        op_t xm[C::KD];
+#pragma unroll
+        for (int ks = 0; ks < C::KD; ++ks) xm[ks] = keep_if<bf16>(row_ok, x[ks]);
+        if (n + 1 < nb) load(blk_of(n + 1));
+        float phi[WFM::NPAIR][16];
+        WFM::compute(wop, xm, phi);
+        if (w == 0) {
+#pragma unroll
+          for (int p = 0; p < WFM::NPAIR; ++p)
+#pragma unroll
+            for (int i = 0; i < 16; ++i)
+              B.phiQT[WFM::feature(16 * p + i, hh)][li] = pack_hi_lo(row_ok ? phi[p][i] : 0.0f);
+        } else {
+#pragma unroll
+          for (int p = 0; p < WFM::NPAIR; ++p)
+#pragma unroll
+            for (int i = 0; i < 16; ++i)
+              B.phiK[li][WFM::feature(16 * p + i, hh)] = row_ok ? phi[p][i] : 0.0f;
+        }
+      }
+      lds_barrier();
+      lds_barrier();
+      lds_barrier();
+    }
+  } else if (w == 2) {
+    // ---- V rows (operands of dL/dphi(K)) and K^T (operands of dW) ----
+    op_t vr[NC][C::KL], kt[NC][C::KL];
+    auto load = [&](int blk) {
+      const bf16* vb = vrowp(blk) + (size_t)lrow * kstride;
+#pragma unroll
+      for (int s = 0; s < NC; ++s)
+#pragma unroll
+        for (int ks = 0; ks < C::KL; ++ks) {
+          vr[s][ks] = keep_if<bf16>(row_ok, lds_op_perm<bf16>(vb, ks, hh, s * kTile));
+          kt[s][ks] = load_rows_op<bf16>(krow(blk) + s * kTile + li, kstride, ks, hh, L, false);
+        }
+    };
+    if (nb > 0) load(blk_of(0));
+    for (int n = 0; n <= nb; ++n) {
+      if (n < nb) {
+        typename C::Buf& B = sh.buf[n & 1];
+#pragma unroll
+        for (int s = 0; s < NC; ++s)
+#pragma unroll
+          for (int ks = 0; ks < C::KL; ++ks) {
+            B.vrow[s][ks][lane] = vr[s][ks];
+            B.ktop[s][ks][lane] = kt[s][ks];
+          }
+        if (n + 1 < nb) load(blk_of(n + 1));
+      }
+      lds_barrier();
+      lds_barrier();
+      lds_barrier();
+    }
+  } else if (w == 3) {
+    // ---- dL/dN^T hi/lo operands (tokens natural) and dL/dD ----
+    f32x4 graw[NC][C::KL][2];
+    float gdv = 0.0f;
+    auto load = [&](int blk) {
+      const float* gnT = ka.gnT + ((size_t)u * ka.nblk + blk) * D * kTile;
+#pragma unroll
+      for (int s = 0; s < NC; ++s)
+#pragma unroll
+        for (int ks = 0; ks < C::KL; ++ks) {
+          const float* src = gnT + (size_t)(s * kTile + li) * kTile + ks * KW + hh * E;
+          graw[s][ks][0] = *reinterpret_cast<const f32x4*>(src);
+          graw[s][ks][1] = *reinterpret_cast<const f32x4*>(src + 4);
+        }
+      if (lane < kTile) gdv = ka.gd[((size_t)u * ka.nblk + blk) * kTile + lane];
+    };
+    if (nb > 0) load(blk_of(0));
+    for (int n = 0; n <= nb; ++n) {
+      if (n < nb) {
+        typename C::Buf& B = sh.buf[n & 1];
+#pragma unroll
+        for (int s = 0; s < NC; ++s)
+#pragma unroll
+          for (int ks = 0; ks < C::KL; ++ks) {
+            op_t gh, gl;
+            split_op(graw[s][ks][0], graw[s][ks][1], gh, gl);
+            B.gn[0][s][ks][lane] = gh;
+            B.gn[1][s][ks][lane] = gl;
+          }
+        if (lane < kTile) B.gd[lane] = gdv;
+        if (n + 1 < nb) load(blk_of(n + 1));
+      }
+      lds_barrier();
+      lds_barrier();
+      lds_barrier();
+    }
+  } else {
+    // ---- state waves ----
+    const int cw = w - NP, col = cw * kTile + li;
+    // Gbar^T tiles (rows c of slice s, columns of feature tile p): the sums
+    // over the later segments
+    f32x16 gacc[RPW][NC];
+#pragma unroll
+    for (int j = 0; j < RPW; ++j)
+#pragma unroll
+      for (int s = 0; s < NC; ++s) gacc[j][s] = f32x16{};
+    for (int sp = seg + 1; sp < nseg; ++sp) {
+      const float* src = ka.dG + ((size_t)u * nseg + sp) * D * f;
+#pragma unroll
+      for (int j = 0; j < RPW; ++j) {
+        const int p = cw + j * NC;
+        if (p >= NRT) continue;
+#pragma unroll
+        for (int s = 0; s < NC; ++s)
+#pragma unroll
+          for (int i = 0; i < 16; ++i)
+            gacc[j][s][i] += src[(size_t)(s * kTile + row_of(i, hh)) * f + p * kTile + li];
+      }
+    }
+    f32x16 dwacc[NT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) dwacc[t] = f32x16{};
+    // step 0: the producers fill the first buffer
+    lds_barrier();
+    lds_barrier();
+    lds_barrier();
+    for (int n = 1; n <= nb; ++n) {
+      {
+        typename C::Buf& B = sh.buf[(n - 1) & 1];
+        // dL/dphi(k_t) = Gbar v_t + gz (Gbar over the later blocks only)
+        float dphi[RPW][16], pk[RPW][16];
+#pragma unroll
+        for (int j = 0; j < RPW; ++j) {
+          const int p = cw + j * NC;
+          if (p >= NRT) continue;
+          f32x16 dk = {};
+#pragma unroll
+          for (int s = 0; s < NC; ++s)
+#pragma unroll
+            for (int ks = 0; ks < C::KL; ++ks) {
+              const op_t vb = B.vrow[s][ks][lane];
+              dk = M::mma(acc_op<bf16>(gacc[j][s], ks), vb, dk);
+              dk = M::mma(acc_op_lo<bf16>(gacc[j][s], ks), vb, dk);
+            }
+          float js = 0.0f;
+#pragma unroll
+          for (int i4 = 0; i4 < 16; i4 += 4) {
+            const int r = p * kTile + row_of(i4, hh);
+            const f32x4 pk4 = *reinterpret_cast<const f32x4*>(&B.phiK[li][r]);
+            const f32x4 gz4 = *reinterpret_cast<const f32x4*>(&sh.gz[r]);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              pk[j][i4 + e] = pk4[e];
+              dphi[j][i4 + e] = dk[i4 + e] + gz4[e];
+              js += dphi[j][i4 + e] * pk4[e];
+            }
+          }
+          js += xor32(js);
+          if (hh == 0) sh.jsum[p][li] = js;
+        }
+        lds_barrier();
+        // dL/du for each sign, transposed and packed (phi(k) of a padding
+        // token is stored as zero, so is its dL/du)
+#pragma unroll
+        for (int j = 0; j < RPW; ++j) {
+          const int p = cw + j * NC;
+          if (p >= NRT) continue;
+          const int sg = p / NT, t = p % NT;
+          float ssum = 0.0f;
+#pragma unroll
+          for (int tt = 0; tt < NT; ++tt) ssum += sh.jsum[sg * NT + tt][li];
+          const float sgn = sg ? -1.0f : 1.0f;
+#pragma unroll
+          for (int i = 0; i < 16; ++i)
+            sh.duT[sg][t * kTile + row_of(i, hh)][li] = pack_hi_lo(sgn * pk[j][i] * (dphi[j][i] - ssum));
+        }
+        // gz += sum_i phi(q_i) dL/dD_i (every read of gz this step is above)
+        for (int r = tid - NP * kWave; r < f; r += NC * kWave) {
+          float acc = 0.0f;
+#pragma unroll
+          for (int t0 = 0; t0 < kTile; t0 += 4) {
+            const uint4 xq = *reinterpret_cast<const uint4*>(&B.phiQT[r][t0]);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) acc += (unpack_hi(xq[e]) + unpack_lo(xq[e])) * B.gd[t0 + e];
+          }
+          sh.gz[r] += acc;
+        }
+        // Gbar^T += dL/dN^T phi(Q) (rows c of slice s, columns of tile p)
+#pragma unroll
+        for (int j = 0; j < RPW; ++j) {
+          const int p = cw + j * NC;
+          if (p >= NRT) continue;
+#pragma unroll
+          for (int ks = 0; ks < C::KL; ++ks) {
+            op_t ph, pl;
+            lds_pair_op_nat(&B.phiQT[p * kTile + li][0], ks, hh, ph, pl);
+#pragma unroll
+            for (int s = 0; s < NC; ++s) {
+              const op_t gh = B.gn[0][s][ks][lane], gl = B.gn[1][s][ks][lane];
+              gacc[j][s] = M::mma(gh, ph, gacc[j][s]);
+              gacc[j][s] = M::mma(gl, ph, gacc[j][s]);
+              gacc[j][s] = M::mma(gh, pl, gacc[j][s]);
+              __builtin_amdgcn_sched_barrier(0);  // keep operand reads near their use
+            }
+          }
+        }
+        lds_barrier();
+        // dW^T tiles (rows j of tile t, columns 32cw..) += dL/du^T K
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+#pragma unroll
+          for (int sg = 0; sg < 2; ++sg)
+#pragma unroll
+            for (int ks = 0; ks < C::KL; ++ks) {
+              op_t uh, ul;
+              lds_pair_op(&sh.duT[sg][t * kTile + li][0], ks, hh, uh, ul);
+              const op_t kb = B.ktop[cw][ks][lane];
+              dwacc[t] = M::mma(uh, kb, dwacc[t]);
+              dwacc[t] = M::mma(ul, kb, dwacc[t]);
+              __builtin_amdgcn_sched_barrier(0);
+            }
+      }
+      lds_barrier();
+    }
+    float* dwk = ka.dwk + ((size_t)u * nseg + seg) * F * D;
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) dwk[(size_t)(t * kTile + row_of(i, hh)) * D + col] = dwacc[t][i];
+  }
+}
+
 // ---------------------------------------------------------------------------
 // 5. Sum of the partials over requests and segments, in a fixed order.
 // ---------------------------------------------------------------------------
@@ -1032,7 +1379,12 @@ static hipError_t bwd_go(const BackwardArgs& a, hipStream_t st) {
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  hipLaunchKernelGGL((hyb_bwd_rev_kernel<T, D, F>), dim3(units * nseg), block, 0, st, ka, 0);
+  if constexpr (sizeof(T) == 2) {
+    hipLaunchKernelGGL((hyb_bwd_rwalk_kernel<D, F>), dim3(units * nseg), dim3(rwalk_threads<D>()),
+                       0, st, ka);
+  } else {
+    hipLaunchKernelGGL((hyb_bwd_rev_kernel<T, D, F>), dim3(units * nseg), block, 0, st, ka, 0);
+  }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   const size_t n = (size_t)s.Hq * s.F * s.D;
   hipLaunchKernelGGL(hyb_bwd_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,

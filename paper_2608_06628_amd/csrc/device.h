@@ -292,6 +292,26 @@ __device__ inline void lds_pair_op(const uint32_t* row, int ks, int hh, bf16x8& 
   lo = __builtin_bit_cast(bf16x8, l);
 }
 
+// The same for 8 consecutive packed entries (natural order): row + 16*ks +
+// 8*hh .. +7.
+__device__ inline void lds_pair_op_nat(const uint32_t* row, int ks, int hh, bf16x8& hi,
+                                       bf16x8& lo) {
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  const u32x4 a = *reinterpret_cast<const u32x4*>(row + 16 * ks + 8 * hh);
+  const u32x4 b = *reinterpret_cast<const u32x4*>(row + 16 * ks + 8 * hh + 4);
+  u32x4 h, l;
+  h[0] = __builtin_amdgcn_perm(a[1], a[0], 0x05040100u);
+  h[1] = __builtin_amdgcn_perm(a[3], a[2], 0x05040100u);
+  h[2] = __builtin_amdgcn_perm(b[1], b[0], 0x05040100u);
+  h[3] = __builtin_amdgcn_perm(b[3], b[2], 0x05040100u);
+  l[0] = __builtin_amdgcn_perm(a[1], a[0], 0x07060302u);
+  l[1] = __builtin_amdgcn_perm(a[3], a[2], 0x07060302u);
+  l[2] = __builtin_amdgcn_perm(b[1], b[0], 0x07060302u);
+  l[3] = __builtin_amdgcn_perm(b[3], b[2], 0x07060302u);
+  hi = __builtin_bit_cast(bf16x8, h);
+  lo = __builtin_bit_cast(bf16x8, l);
+}
+
 template <typename T>
 __device__ inline void store_out1(void* out, size_t idx, float v, bool f32) {
   if (sizeof(T) == 4 || f32)
