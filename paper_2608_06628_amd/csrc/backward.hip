@@ -19,12 +19,13 @@
 // Kernels (one workgroup per (request, head, sequence segment), NW = D/32
 // waves; segments as in the prefill, so the grid fills the chip):
 //   1. the prefill's delta launch: each segment's state increment;
-//   2. hyb_bwd_fwd_kernel: forward walk.  Wave w keeps S columns 32w..+31
-//      in fp32 accumulators (the readout operand, as in the prefill).  Each
-//      block also copies S_{c-1} to LDS as [feature][column] operands, for
-//      dL/dphi(Q), which contracts over the head dimension.  Per block it
-//      forms out, dL/dN, dL/dD, dL/dphi(Q) and the query part of dL/dW and
-//      dL/dalpha, and hands dL/dN^T and dL/dD to the workspace;
+//   2. forward walk: per block out, dL/dN, dL/dD, dL/dphi(Q) and the query
+//      part of dL/dW and dL/dalpha; dL/dN^T and dL/dD go to the workspace.
+//      On the bf16 path hyb_bwd_fpipe_kernel (pipelined, below) keeps S and
+//      S^T both in fp32 accumulators; on fp32 hyb_bwd_fwd_kernel keeps S
+//      columns 32w..+31 in accumulators (the readout operand, as in the
+//      prefill) and copies S_{c-1} to LDS each block as [feature][column]
+//      operands for dL/dphi(Q), which contracts over the head dimension;
 //   3. each segment's sum of phi(Q)^T dL/dN (and phi(Q)^T dL/dD):
 //      hyb_bwd_gdelta_kernel on the bf16 path (pipelined, below),
 //      hyb_bwd_rev_kernel in delta mode on fp32;
@@ -542,6 +543,544 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_fwd_kernel(BwdKArgs
   if (tid == 0) {
     float x0 = 0.0f, x1 = 0.0f;
     for (int ww = 0; ww < NW; ++ww) {
+      x0 += sh.fin[ww][0];
+      x1 += sh.fin[ww][1];
+    }
+    ka.red[((size_t)u * nseg + seg) * 2] = x0;
+    ka.red[((size_t)u * nseg + seg) * 2 + 1] = x1;
+  }
+}
+
+
+// ---------------------------------------------------------------------------
+// 2'. Pipelined forward walk (bf16, F <= 64).  Producers prepare block c+1
+// while the state waves finish block c:
+//   wave 0: phi(Q) as packed hi/lo pairs [query][feature] (the readout's
+//           operand, and phi(Q) itself for the feature-map Jacobian);
+//   wave 1: phi(K) transposed and packed (the commit's operand);
+//   waves 2 .. NP-1: the in-block softmax numerators P V (relative to the
+//           row maximum) for 64 columns each, the row maxima and sums, and
+//           the V^T operands of the commit; then, once the state waves have
+//           posted dL/du of their block, the query part of dW for the same
+//           64 columns;
+//   state waves (D/32): S columns 32w..32w+31 (the readout) and S^T for the
+//           feature tiles w, w + D/32, ... (dL/dphi(Q), which contracts over
+//           the head dimension) both in fp32 accumulators; the merge, dL/dN,
+//           dL/dD, dL/dphi(Q) and dL/du; then the commit of the block into
+//           both copies.
+// Five barriers per block, all waves: after the merge's partial sums, after
+// dL/dN, after the per-sign sums, after dL/du, and at the end of the step.
+// ---------------------------------------------------------------------------
+template <int D, int F>
+struct FPipeCfg {
+  typedef Mma<bf16> M;
+  typedef typename M::op_t op_t;
+  static constexpr int NC = D / kTile;                 // state waves
+  static constexpr int NSM = D / 64 > 0 ? D / 64 : 1;  // softmax waves
+  static constexpr int CT = NC / NSM;                  // column tiles per softmax wave
+  static constexpr int NP = 2 + NSM;
+  static constexpr int NWAVE = NP + NC;
+  static constexpr int f = 2 * F;
+  static constexpr int NRT = f / kTile;
+  static constexpr int NT = F / kTile;
+  static constexpr int RPW = (NRT + NC - 1) / NC;      // S^T feature tiles per state wave
+  static constexpr int KD = D / M::KW;
+  static constexpr int KL = kTile / M::KW;
+  static constexpr int KF = f / M::KW;
+  typedef WaveFeatMap<bf16, D, F> WFM;
+  struct alignas(16) Buf {
+    uint32_t phiQ[kTile][f + 4];     // phi(q_i)[r] at [i][r], bf16 hi | lo << 16
+    uint32_t phiKT[f][kTile + 4];    // phi(k_t)[r] at [r][t], packed likewise
+    float sm[kTile][D + 4];          // P V relative to the row maximum, [i][c]
+    float m[kTile], den[kTile];
+    op_t vop[NC][KL][kWave];         // V^T: lane (c, hh), tokens in row_of order
+    op_t qtop[NC][KL][kWave];        // Q^T likewise
+  };
+  struct alignas(16) Smem {
+    Buf buf[2];
+    union {
+      uint32_t gn[kTile][D + 4];     // dL/dN_i[c] at [i][c], packed
+      uint32_t duT[2][F][kTile + 4]; // +-dL/du of each sign at [j][t], packed
+    } x;
+    float z[2][f];
+    float red[NC][kTile][2];
+    float jsum[NRT][kTile];
+    float fin[NC][2];
+  };
+};
+
+template <int D>
+constexpr int fpipe_threads() {
+  return kWave * (2 + (D / 64 > 0 ? D / 64 : 1) + D / kTile);
+}
+
+template <int D, int F>
+__global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKArgs ka) {
+  typedef FPipeCfg<D, F> C;
+  typedef typename C::M M;
+  typedef typename C::op_t op_t;
+  typedef typename C::WFM WFM;
+  typedef typename C::Buf Buf;
+  constexpr int f = C::f, E = M::E, KW = M::KW, NP = C::NP, NC = C::NC;
+  constexpr int NRT = C::NRT, NT = C::NT, RPW = C::RPW, KD = C::KD, KL = C::KL;
+  constexpr int NBAR = 5;  // barriers per block step
+  static_assert(fpipe_threads<D>() == kWave * C::NWAVE, "launch bounds match the waves");
+  __shared__ typename C::Smem sh;
+  const BackwardArgs& a = ka.a;
+
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int w = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int li = lane & 31, hh = lane >> 5;
+  const int Hq = a.s.Hq, Hkv = a.s.Hkv, L = a.s.L, T_ = a.T;
+  const int units = a.s.B * Hq, nseg = ka.nseg;
+  const int vix = xcd_unit(blockIdx.x, units * nseg);
+  const int u = vix % units, seg = vix / units;
+  const int b = u / Hq, h = u % Hq, g = h / (Hq / Hkv);
+  const size_t qstride = (size_t)Hq * D, kstride = (size_t)Hkv * D;
+  const int blk0 = seg * ka.seg_blocks, blk1 = min(ka.nblk, blk0 + ka.seg_blocks);
+  const int nb = blk1 - blk0;
+  const bool row_ok = li < L;
+  const int lrow = min(li, L - 1);
+  auto qbase = [&](int blk) {
+    return (const bf16*)a.q + (((size_t)b * T_ + (size_t)blk * L) * Hq + h) * D;
+  };
+  auto kbase = [&](int blk) {
+    return (const bf16*)a.k + (((size_t)b * T_ + (size_t)blk * L) * Hkv + g) * D;
+  };
+  auto vbase = [&](int blk) {
+    return (const bf16*)a.v + (((size_t)b * T_ + (size_t)blk * L) * Hkv + g) * D;
+  };
+  auto load_rows = [&](const bf16* base, size_t stride, op_t (&o)[KD]) {
+    const bf16* row = base + (size_t)lrow * stride + hh * E;
+#pragma unroll
+    for (int ks = 0; ks < KD; ++ks) o[ks] = load_op<bf16>(row + ks * KW);
+  };
+
+  // z at the segment's start: the earlier segments' sums
+  for (int r = tid; r < f; r += blockDim.x) {
+    float zr = 0.0f;
+    for (int sp = 0; sp < seg; ++sp) zr += ka.dz[((size_t)u * (nseg - 1) + sp) * f + r];
+    sh.z[0][r] = zr;
+  }
+  lds_barrier();
+
+  if (w < 2) {
+    // ---- feature map of Q (wave 0) or K (wave 1) ----
+    const bf16* __restrict__ Wt_h = (const bf16*)a.W + (size_t)h * F * D;
+    op_t wop[WFM::NT][KD];
+    WFM::load_w(Wt_h, li, hh, wop);
+    op_t x[KD];
+    auto load = [&](int blk) {
+      if (w == 0) load_rows(qbase(blk), qstride, x);
+      else load_rows(kbase(blk), kstride, x);
+    };
+    if (nb > 0) load(blk0);
+    for (int n = 0; n <= nb; ++n) {
+      if (n < nb) {
+        Buf& B = sh.buf[n & 1];
+        op_t xm[KD];
+#pragma unroll
+        for (int ks = 0; ks < KD; ++ks) xm[ks] = keep_if<bf16>(row_ok, x[ks]);
+        if (n + 1 < nb) load(blk0 + n + 1);
+        float phi[WFM::NPAIR][16];
+        WFM::compute(wop, xm, phi);
+        if (w == 0) {
+#pragma unroll
+          for (int p = 0; p < WFM::NPAIR; ++p)
+#pragma unroll
+            for (int i = 0; i < 16; i += 4) {
+              uint4 pk;
+#pragma unroll
+              for (int e = 0; e < 4; ++e) pk[e] = pack_hi_lo(row_ok ? phi[p][i + e] : 0.0f);
+              *reinterpret_cast<uint4*>(&B.phiQ[li][WFM::feature(16 * p + i, hh)]) = pk;
+            }
+        } else {
+#pragma unroll
+          for (int p = 0; p < WFM::NPAIR; ++p)
+#pragma unroll
+            for (int i = 0; i < 16; ++i)
+              B.phiKT[WFM::feature(16 * p + i, hh)][li] = pack_hi_lo(row_ok ? phi[p][i] : 0.0f);
+        }
+      }
+#pragma unroll
+      for (int k = 0; k < NBAR; ++k) lds_barrier();
+    }
+  } else if (w < NP) {
+    // ---- in-block softmax branch for column tiles c0 .. c0+CT-1 ----
+    const int c0 = (w - 2) * C::CT;
+    const float scale = 1.0f / sqrtf((float)D);
+    op_t ko[KD], qo[KD], vo[C::CT][KL];
+    auto load = [&](int blk) {
+      load_rows(kbase(blk), kstride, ko);
+      load_rows(qbase(blk), qstride, qo);
+#pragma unroll
+      for (int ct = 0; ct < C::CT; ++ct)
+#pragma unroll
+        for (int ks = 0; ks < KL; ++ks)
+          vo[ct][ks] = load_rows_op<bf16>(vbase(blk) + (c0 + ct) * kTile + li, kstride, ks, hh, L, false);
+    };
+    // the query part of dW^T for columns 32(c0+ct)..: rows j of tile t
+    f32x16 dwacc[NT][C::CT];
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int ct = 0; ct < C::CT; ++ct) dwacc[t][ct] = f32x16{};
+    if (nb > 0) load(blk0);
+    for (int n = 0; n <= nb; ++n) {
+      if (n < nb) {
+        Buf& B = sh.buf[n & 1];
+        // keys in rows, queries in columns
+        f32x16 sc = {};
+#pragma unroll
+        for (int ks = 0; ks < KD; ++ks)
+          sc = M::mma(keep_if<bf16>(row_ok, ko[ks]), keep_if<bf16>(row_ok, qo[ks]), sc);
+        // Q^T operands (lane: column, elements: tokens in row_of order) from
+        // the Q rows times the identity: Q_c = Q_c I holds the tokens in its
+        // accumulator rows (exact: one nonzero bf16 product per entry)
+        // (this wave's column tiles picked with constant indices: the wave
+        // index is uniform but not a compile-time constant)
+        op_t qsel[C::CT][KL];
+#pragma unroll
+        for (int sw = 0; sw < C::NSM; ++sw)
+          if (w - 2 == sw) {
+#pragma unroll
+            for (int ct = 0; ct < C::CT; ++ct)
+#pragma unroll
+              for (int kk = 0; kk < KL; ++kk) qsel[ct][kk] = qo[(sw * C::CT + ct) * KL + kk];
+          }
+#pragma unroll
+        for (int ct = 0; ct < C::CT; ++ct) {
+          f32x16 qa = {};
+#pragma unroll
+          for (int kk = 0; kk < KL; ++kk) {
+            op_t id;
+#pragma unroll
+            for (int e = 0; e < E; ++e) id[e] = (bf16)(kk * KW + hh * E + e == li ? 1.0f : 0.0f);
+            qa = M::mma(keep_if<bf16>(row_ok, qsel[ct][kk]), id, qa);
+          }
+#pragma unroll
+          for (int kk = 0; kk < KL; ++kk) B.qtop[c0 + ct][kk][lane] = acc_op<bf16>(qa, kk);
+        }
+        float pr[16];
+        float m = -INFINITY;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          pr[i] = row_of(i, hh) < L ? sc[i] * scale : -INFINITY;
+          m = fmaxf(m, pr[i]);
+        }
+        m = fmaxf(m, xor32(m));
+        float den = 0.0f;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          pr[i] = row_of(i, hh) < L ? fast_exp(pr[i] - m) : 0.0f;
+          den += pr[i];
+        }
+        den += xor32(den);
+#pragma unroll
+        for (int ct = 0; ct < C::CT; ++ct) {
+          f32x16 acc = {};
+#pragma unroll
+          for (int ks = 0; ks < KL; ++ks) acc = mma_split_b<bf16>(vo[ct][ks], &pr[ks * E], acc);
+#pragma unroll
+          for (int i = 0; i < 16; i += 4)
+            *reinterpret_cast<f32x4*>(&B.sm[li][(c0 + ct) * kTile + row_of(i, hh)]) =
+                f32x4{acc[i], acc[i + 1], acc[i + 2], acc[i + 3]};
+        }
+        if (w == 2 && hh == 0) {
+          B.m[li] = m;
+          B.den[li] = den;
+        }
+#pragma unroll
+        for (int ct = 0; ct < C::CT; ++ct)
+#pragma unroll
+          for (int ks = 0; ks < KL; ++ks) B.vop[c0 + ct][ks][lane] = vo[ct][ks];
+        if (n + 1 < nb) load(blk0 + n + 1);  // next block in flight
+      }
+#pragma unroll
+      for (int k = 0; k < NBAR - 1; ++k) lds_barrier();
+      if (n > 0) {
+        // dW^T += dL/du^T Q for the block the state waves are finishing
+        // (its dL/du is in LDS between their fourth and fifth barrier)
+        const Buf& Bp = sh.buf[(n - 1) & 1];
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+#pragma unroll
+          for (int sg = 0; sg < 2; ++sg)
+#pragma unroll
+            for (int ks = 0; ks < KL; ++ks) {
+              op_t uh, ul;
+              lds_pair_op(&sh.x.duT[sg][t * kTile + li][0], ks, hh, uh, ul);
+#pragma unroll
+              for (int ct = 0; ct < C::CT; ++ct) {
+                const op_t qt = Bp.qtop[c0 + ct][ks][lane];
+                dwacc[t][ct] = M::mma(uh, qt, dwacc[t][ct]);
+                dwacc[t][ct] = M::mma(ul, qt, dwacc[t][ct]);
+              }
+            }
+      }
+      lds_barrier();
+    }
+    float* dwq = ka.dwq + ((size_t)u * nseg + seg) * F * D;
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int ct = 0; ct < C::CT; ++ct)
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          dwq[(size_t)(t * kTile + row_of(i, hh)) * D + (c0 + ct) * kTile + li] = dwacc[t][ct][i];
+  } else {
+    // ---- state waves ----
+    const int cw = w - NP, col = cw * kTile + li;
+    const bool tmode = a.target != nullptr;
+    const float lw = log_sigmoid(a.alpha[h]);
+    const float one_minus_w = expf(log_sigmoid(-a.alpha[h]));
+    // S (columns col) and S^T (feature tiles cw + j*NC): the earlier
+    // segments' increments
+    f32x16 sacc[NRT], sT[RPW][NC];
+#pragma unroll
+    for (int rt = 0; rt < NRT; ++rt) sacc[rt] = f32x16{};
+#pragma unroll
+    for (int j = 0; j < RPW; ++j)
+#pragma unroll
+      for (int s = 0; s < NC; ++s) sT[j][s] = f32x16{};
+    for (int sp = 0; sp < seg; ++sp) {
+      const float* src = ka.dS + ((size_t)u * (nseg - 1) + sp) * D * f;
+#pragma unroll
+      for (int rt = 0; rt < NRT; ++rt)
+#pragma unroll
+        for (int i = 0; i < 16; i += 4) {
+          const f32x4 y = *reinterpret_cast<const f32x4*>(src + (size_t)col * f + rt * kTile + row_of(i, hh));
+#pragma unroll
+          for (int e = 0; e < 4; ++e) sacc[rt][i + e] += y[e];
+        }
+#pragma unroll
+      for (int j = 0; j < RPW; ++j) {
+        const int p = cw + j * NC;
+        if (p >= NRT) continue;
+#pragma unroll
+        for (int s = 0; s < NC; ++s)
+#pragma unroll
+          for (int i = 0; i < 16; ++i)
+            sT[j][s][i] += src[(size_t)(s * kTile + row_of(i, hh)) * f + p * kTile + li];
+      }
+    }
+    float dal = 0.0f, lss = 0.0f;
+    // the block's upstream rows (dout, or the teacher's output) at columns
+    // 32cw + row_of(i, hh): prefetched a block ahead
+    const bf16* gsrc = (const bf16*)(tmode ? a.target : a.dout);
+    bf16x4 gin4[4];
+    auto load_g = [&](int blk) {
+      const bf16* row = gsrc + (((size_t)b * T_ + (size_t)blk * L + lrow) * Hq + h) * D + cw * kTile;
+#pragma unroll
+      for (int i4 = 0; i4 < 4; ++i4) gin4[i4] = *reinterpret_cast<const bf16x4*>(row + row_of(4 * i4, hh));
+    };
+    if (nb > 0) load_g(blk0);
+    // step 0: the producers fill the first buffer
+#pragma unroll
+    for (int k = 0; k < NBAR; ++k) lds_barrier();
+    for (int n = 1; n <= nb; ++n) {
+      const int blk = blk0 + n - 1;
+      Buf& B = sh.buf[(n - 1) & 1];
+      const float* zc = sh.z[(n - 1) & 1];
+      float* zn = sh.z[n & 1];
+      // -- lin_den = phi(q_li) . z (each lane half over half the features)
+      float lden = 0.0f;
+#pragma unroll
+      for (int r = hh * (f / 2); r < (hh + 1) * (f / 2); r += 4) {
+        const uint4 xq = *reinterpret_cast<const uint4*>(&B.phiQ[li][r]);
+        const f32x4 z4 = *reinterpret_cast<const f32x4*>(&zc[r]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) lden += (unpack_hi(xq[e]) + unpack_lo(xq[e])) * z4[e];
+      }
+      lden += xor32(lden);
+      // -- readout against S_{c-1}: both operands as hi + lo pairs
+      f32x16 acc_lin = {};
+#pragma unroll
+      for (int ks = 0; ks < C::KF; ++ks) {
+        op_t ph, pl;
+        lds_pair_op(&B.phiQ[li][0], ks, hh, ph, pl);
+        const int rt = ks / KL, kk = ks % KL;
+        const op_t sa = acc_op<bf16>(sacc[rt], kk);
+        acc_lin = M::mma(sa, ph, acc_lin);
+        acc_lin = M::mma(acc_op_lo<bf16>(sacc[rt], kk), ph, acc_lin);
+        acc_lin = M::mma(sa, pl, acc_lin);
+      }
+      // -- merge (scaled by exp(-c) so nothing overflows): out = N / D with
+      // w sm_den = exp(la) den, lin_den = exp(lb), c = max(la, lb)
+      const float m = B.m[li], den = B.den[li];
+      float ca = 1.0f, cz = 0.0f, rz = 0.0f, cmax = lw + m;
+      if (lden > 0.0f) {
+        const float la = lw + m, lb = logf(lden);
+        cmax = fmaxf(la, lb);
+        ca = expf(la - cmax);
+        cz = expf(lb - cmax);
+        rz = 1.0f / lden;
+      }
+      const float inv = 1.0f / (ca * den + cz);
+      float gq[16];
+      float go_p = 0.0f, gs_p = 0.0f;
+#pragma unroll
+      for (int i4 = 0; i4 < 16; i4 += 4) {
+        const f32x4 smv = *reinterpret_cast<const f32x4*>(&B.sm[li][col - li + row_of(i4, hh)]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int i = i4 + e;
+          const float gin = row_ok ? (float)gin4[i4 / 4][e] : 0.0f;
+          const float o = (ca * smv[e] + cz * (acc_lin[i] * rz)) * inv;
+          if (tmode) {
+            const float er = row_ok ? o - gin : 0.0f;
+            lss += er * er;
+            gq[i] = 2.0f * er;
+          } else {
+            gq[i] = gin;
+          }
+          go_p += gq[i] * o;
+          gs_p += gq[i] * smv[e];
+        }
+      }
+      if (n < nb) load_g(blk + 1);
+      go_p += xor32(go_p);
+      gs_p += xor32(gs_p);
+      if (hh == 0) {
+        sh.red[cw][li][0] = go_p;
+        sh.red[cw][li][1] = gs_p;
+      }
+      lds_barrier();  // 1
+      // -- dL/dN (packed, and fp32 for the reverse pass), dL/dD, dL/dalpha
+      float go = 0.0f, gs = 0.0f;
+#pragma unroll
+      for (int ww = 0; ww < NC; ++ww) {
+        go += sh.red[ww][li][0];
+        gs += sh.red[ww][li][1];
+      }
+      // 1/D = inv exp(-c); dL/dalpha = dL/dw w(1-w), and
+      // dL/dw = exp(m - c) inv (g.acc_sm - (g.out) den) with exp(m - c) w = ca.
+      const float rD = inv * expf(-cmax);
+      const float gD = row_ok ? -rD * go : 0.0f;
+      if (cw == 0 && hh == 0 && row_ok) dal += ca * one_minus_w * inv * (gs - go * den);
+      {
+        // dL/dN^T: column 32cw + row_of(i, hh) = 32cw + 4hh + 8(i/4) + i%4,
+        // query li; one base address, the rest immediate offsets
+        float* gnT = ka.gnT + ((size_t)u * ka.nblk + blk) * D * kTile +
+                     (size_t)(cw * kTile + 4 * hh) * kTile + li;
+#pragma unroll
+        for (int i4 = 0; i4 < 16; i4 += 4) {
+          uint4 pk;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            const float x = rD * gq[i4 + e];
+            pk[e] = pack_hi_lo(x);
+            gnT[(2 * i4 + e) * kTile] = x;
+          }
+          *reinterpret_cast<uint4*>(&sh.x.gn[li][col - li + row_of(i4, hh)]) = pk;
+        }
+        if (cw == 0 && hh == 0) ka.gd[((size_t)u * ka.nblk + blk) * kTile + li] = gD;
+      }
+      lds_barrier();  // 2
+      // -- dL/dphi(q_i) = S_{c-1} dL/dN_i + z_{c-1} dL/dD_i for the feature
+      // tiles this wave owns (rows r, columns i), and the per-tile sums
+      float dphi[RPW][16], pq[RPW][16];
+#pragma unroll
+      for (int j = 0; j < RPW; ++j) {
+        const int p = cw + j * NC;
+        if (p >= NRT) continue;
+        f32x16 dq = {};
+#pragma unroll
+        for (int s = 0; s < NC; ++s)
+#pragma unroll
+          for (int ks = 0; ks < KL; ++ks) {
+            op_t gh, gl;
+            lds_pair_op(&sh.x.gn[li][s * kTile], ks, hh, gh, gl);
+            const op_t ah = acc_op<bf16>(sT[j][s], ks);
+            dq = M::mma(ah, gh, dq);
+            dq = M::mma(acc_op_lo<bf16>(sT[j][s], ks), gh, dq);
+            dq = M::mma(ah, gl, dq);
+          }
+        float js = 0.0f;
+#pragma unroll
+        for (int i4 = 0; i4 < 16; i4 += 4) {
+          const int r = p * kTile + row_of(i4, hh);
+          const uint4 xq = *reinterpret_cast<const uint4*>(&B.phiQ[li][r]);
+          const f32x4 z4 = *reinterpret_cast<const f32x4*>(&zc[r]);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            pq[j][i4 + e] = unpack_hi(xq[e]) + unpack_lo(xq[e]);
+            dphi[j][i4 + e] = dq[i4 + e] + gD * z4[e];
+            js += dphi[j][i4 + e] * pq[j][i4 + e];
+          }
+        }
+        js += xor32(js);
+        if (hh == 0) sh.jsum[p][li] = js;
+      }
+      lds_barrier();  // 3
+      // -- feature-map backward: dL/du of each sign, transposed and packed
+      // (phi(q) of a padding query is stored as zero, so is its dL/du)
+#pragma unroll
+      for (int j = 0; j < RPW; ++j) {
+        const int p = cw + j * NC;
+        if (p >= NRT) continue;
+        const int sg = p / NT, t = p % NT;
+        float ssum = 0.0f;
+#pragma unroll
+        for (int tt = 0; tt < NT; ++tt) ssum += sh.jsum[sg * NT + tt][li];
+        const float sgn = sg ? -1.0f : 1.0f;
+#pragma unroll
+        for (int i = 0; i < 16; ++i)
+          sh.x.duT[sg][t * kTile + row_of(i, hh)][li] = pack_hi_lo(sgn * pq[j][i] * (dphi[j][i] - ssum));
+      }
+      lds_barrier();  // 4
+      // -- commit the block: S += phi(K)^T V (columns col), S^T += V^T phi(K)
+      // (feature tiles of this wave), z_{c+1} = z_c + sum_t phi(k_t)
+#pragma unroll
+      for (int rt = 0; rt < NRT; ++rt)
+#pragma unroll
+        for (int ks = 0; ks < KL; ++ks) {
+          op_t khi, klo;
+          lds_pair_op(&B.phiKT[rt * kTile + li][0], ks, hh, khi, klo);
+          const op_t vk = B.vop[cw][ks][lane];
+          sacc[rt] = M::mma(khi, vk, sacc[rt]);
+          sacc[rt] = M::mma(klo, vk, sacc[rt]);
+        }
+#pragma unroll
+      for (int j = 0; j < RPW; ++j) {
+        const int p = cw + j * NC;
+        if (p >= NRT) continue;
+#pragma unroll
+        for (int ks = 0; ks < KL; ++ks) {
+          op_t khi, klo;
+          lds_pair_op(&B.phiKT[p * kTile + li][0], ks, hh, khi, klo);
+#pragma unroll
+          for (int s = 0; s < NC; ++s) {
+            const op_t vs = B.vop[s][ks][lane];
+            sT[j][s] = M::mma(vs, khi, sT[j][s]);
+            sT[j][s] = M::mma(vs, klo, sT[j][s]);
+          }
+        }
+      }
+      for (int r = tid - NP * kWave; r < f; r += NC * kWave) {
+        float zs = zc[r];
+#pragma unroll
+        for (int t0 = 0; t0 < kTile; t0 += 4) {
+          const uint4 xk = *reinterpret_cast<const uint4*>(&B.phiKT[r][t0]);
+#pragma unroll
+          for (int e = 0; e < 4; ++e) zs += unpack_hi(xk[e]) + unpack_lo(xk[e]);
+        }
+        zn[r] = zs;
+      }
+      lds_barrier();  // 5
+    }
+    // partials of this (request, head, segment)
+    dal = wave_sum(dal);
+    lss = wave_sum(lss);
+    if (lane == 0) {
+      sh.fin[cw][0] = dal;
+      sh.fin[cw][1] = lss;
+    }
+  }
+  lds_barrier();
+  if (tid == NP * kWave) {
+    float x0 = 0.0f, x1 = 0.0f;
+    for (int ww = 0; ww < NC; ++ww) {
       x0 += sh.fin[ww][0];
       x1 += sh.fin[ww][1];
     }
@@ -1367,7 +1906,12 @@ static hipError_t bwd_go(const BackwardArgs& a, hipStream_t st) {
     pa.s.n_slots = s.B;
     if ((e = launch_prefill_delta(pa, st)) != hipSuccess) return e;
   }
-  hipLaunchKernelGGL((hyb_bwd_fwd_kernel<T, D, F>), dim3(units * nseg), block, 0, st, ka);
+  if constexpr (sizeof(T) == 2) {
+    hipLaunchKernelGGL((hyb_bwd_fpipe_kernel<D, F>), dim3(units * nseg), dim3(fpipe_threads<D>()),
+                       0, st, ka);
+  } else {
+    hipLaunchKernelGGL((hyb_bwd_fwd_kernel<T, D, F>), dim3(units * nseg), block, 0, st, ka);
+  }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (nseg > 1) {
     if constexpr (sizeof(T) == 2) {
