@@ -678,28 +678,28 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
     for (int n = 0; n <= nb; ++n) {
       if (n < nb) {
         Buf& B = sh.buf[n & 1];
-        op_t xm[KD];
-#pragma unroll
-        for (int ks = 0; ks < KD; ++ks) xm[ks] = keep_if<bf16>(row_ok, x[ks]);
-        if (n + 1 < nb) load(blk0 + n + 1);
+        // a padding row reads row L-1 (finite); keep = row_ok zeroes its phi
         float phi[WFM::NPAIR][16];
-        WFM::compute(wop, xm, phi);
+        WFM::logits(wop, x, phi);
+        if (n + 1 < nb) load(blk0 + n + 1);
+        WFM::softmax(phi, row_ok);
         if (w == 0) {
 #pragma unroll
           for (int p = 0; p < WFM::NPAIR; ++p)
 #pragma unroll
             for (int i = 0; i < 16; i += 4) {
               uint4 pk;
-#pragma unroll
-              for (int e = 0; e < 4; ++e) pk[e] = pack_hi_lo(row_ok ? phi[p][i + e] : 0.0f);
+              pack_hi_lo2(phi[p][i], phi[p][i + 1], pk[0], pk[1]);
+              pack_hi_lo2(phi[p][i + 2], phi[p][i + 3], pk[2], pk[3]);
               *reinterpret_cast<uint4*>(&B.phiQ[li][WFM::feature(16 * p + i, hh)]) = pk;
             }
         } else {
 #pragma unroll
           for (int p = 0; p < WFM::NPAIR; ++p)
 #pragma unroll
-            for (int i = 0; i < 16; ++i)
-              B.phiKT[WFM::feature(16 * p + i, hh)][li] = pack_hi_lo(row_ok ? phi[p][i] : 0.0f);
+            for (int i = 0; i < 16; i += 2)
+              pack_hi_lo2(phi[p][i], phi[p][i + 1], B.phiKT[WFM::feature(16 * p + i, hh)][li],
+                          B.phiKT[WFM::feature(16 * p + i + 1, hh)][li]);
         }
       }
 #pragma unroll
@@ -966,12 +966,14 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
 #pragma unroll
         for (int i4 = 0; i4 < 16; i4 += 4) {
           uint4 pk;
+          float x[4];
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
-            const float x = rD * gq[i4 + e];
-            pk[e] = pack_hi_lo(x);
-            gnT[(2 * i4 + e) * kTile] = x;
+            x[e] = rD * gq[i4 + e];
+            gnT[(2 * i4 + e) * kTile] = x[e];
           }
+          pack_hi_lo2(x[0], x[1], pk[0], pk[1]);
+          pack_hi_lo2(x[2], x[3], pk[2], pk[3]);
           *reinterpret_cast<uint4*>(&sh.x.gn[li][col - li + row_of(i4, hh)]) = pk;
         }
         if (cw == 0 && hh == 0) ka.gd[((size_t)u * ka.nblk + blk) * kTile + li] = gD;
@@ -1025,8 +1027,10 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
         for (int tt = 0; tt < NT; ++tt) ssum += sh.jsum[sg * NT + tt][li];
         const float sgn = sg ? -1.0f : 1.0f;
 #pragma unroll
-        for (int i = 0; i < 16; ++i)
-          sh.x.duT[sg][t * kTile + row_of(i, hh)][li] = pack_hi_lo(sgn * pq[j][i] * (dphi[j][i] - ssum));
+        for (int i = 0; i < 16; i += 2)
+          pack_hi_lo2(sgn * pq[j][i] * (dphi[j][i] - ssum), sgn * pq[j][i + 1] * (dphi[j][i + 1] - ssum),
+                      sh.x.duT[sg][t * kTile + row_of(i, hh)][li],
+                      sh.x.duT[sg][t * kTile + row_of(i + 1, hh)][li]);
       }
       lds_barrier();  // 4
       // -- commit the block: S += phi(K)^T V (columns col), S^T += V^T phi(K)
@@ -1404,17 +1408,17 @@ __global__ __launch_bounds__(gdelta_threads<D>()) void hyb_bwd_gdelta_kernel(Bwd
       const int blk = blk0 + 2 * j + w;
       if (j < npair && blk < blk1) {
         typename C::Buf& B = sh.buf[j & 1];
-        op_t xm[C::KD];
-#pragma unroll
-        for (int ks = 0; ks < C::KD; ++ks) xm[ks] = keep_if<bf16>(row_ok, x[ks]);
-        if (blk + 2 < blk1) load(blk + 2);  // next pair's block in flight
+        // a padding row reads row L-1 (finite); keep = row_ok zeroes its phi
         float phi[WFM::NPAIR][16];
-        WFM::compute(wop, xm, phi);
+        WFM::logits(wop, x, phi);
+        if (blk + 2 < blk1) load(blk + 2);  // next pair's block in flight
+        WFM::softmax(phi, row_ok);
 #pragma unroll
         for (int p = 0; p < WFM::NPAIR; ++p)
 #pragma unroll
-          for (int i = 0; i < 16; ++i)
-            B.phiQT[w][WFM::feature(16 * p + i, hh)][li] = pack_hi_lo(row_ok ? phi[p][i] : 0.0f);
+          for (int i = 0; i < 16; i += 2)
+            pack_hi_lo2(phi[p][i], phi[p][i + 1], B.phiQT[w][WFM::feature(16 * p + i, hh)][li],
+                        B.phiQT[w][WFM::feature(16 * p + i + 1, hh)][li]);
       }
       lds_barrier();
     }
@@ -1613,24 +1617,25 @@ __global__ __launch_bounds__(rwalk_threads<D>()) void hyb_bwd_rwalk_kernel(BwdKA
     for (int n = 0; n <= nb; ++n) {
       if (n < nb) {
         typename C::Buf& B = sh.buf[n & 1];
-        op_t xm[C::KD];
-#pragma unroll
-        for (int ks = 0; ks < C::KD; ++ks) xm[ks] = keep_if<bf16>(row_ok, x[ks]);
-        if (n + 1 < nb) load(blk_of(n + 1));
+        // a padding row reads row L-1 (finite); keep = row_ok zeroes its phi
         float phi[WFM::NPAIR][16];
-        WFM::compute(wop, xm, phi);
+        WFM::logits(wop, x, phi);
+        if (n + 1 < nb) load(blk_of(n + 1));
+        WFM::softmax(phi, row_ok);
         if (w == 0) {
 #pragma unroll
           for (int p = 0; p < WFM::NPAIR; ++p)
 #pragma unroll
-            for (int i = 0; i < 16; ++i)
-              B.phiQT[WFM::feature(16 * p + i, hh)][li] = pack_hi_lo(row_ok ? phi[p][i] : 0.0f);
+            for (int i = 0; i < 16; i += 2)
+              pack_hi_lo2(phi[p][i], phi[p][i + 1], B.phiQT[WFM::feature(16 * p + i, hh)][li],
+                          B.phiQT[WFM::feature(16 * p + i + 1, hh)][li]);
         } else {
 #pragma unroll
           for (int p = 0; p < WFM::NPAIR; ++p)
 #pragma unroll
-            for (int i = 0; i < 16; ++i)
-              B.phiK[li][WFM::feature(16 * p + i, hh)] = row_ok ? phi[p][i] : 0.0f;
+            for (int i = 0; i < 16; i += 4)
+              *reinterpret_cast<f32x4*>(&B.phiK[li][WFM::feature(16 * p + i, hh)]) =
+                  f32x4{phi[p][i], phi[p][i + 1], phi[p][i + 2], phi[p][i + 3]};
         }
       }
       lds_barrier();
@@ -1780,8 +1785,10 @@ __global__ __launch_bounds__(rwalk_threads<D>()) void hyb_bwd_rwalk_kernel(BwdKA
           for (int tt = 0; tt < NT; ++tt) ssum += sh.jsum[sg * NT + tt][li];
           const float sgn = sg ? -1.0f : 1.0f;
 #pragma unroll
-          for (int i = 0; i < 16; ++i)
-            sh.duT[sg][t * kTile + row_of(i, hh)][li] = pack_hi_lo(sgn * pk[j][i] * (dphi[j][i] - ssum));
+          for (int i = 0; i < 16; i += 2)
+            pack_hi_lo2(sgn * pk[j][i] * (dphi[j][i] - ssum), sgn * pk[j][i + 1] * (dphi[j][i + 1] - ssum),
+                        sh.duT[sg][t * kTile + row_of(i, hh)][li],
+                        sh.duT[sg][t * kTile + row_of(i + 1, hh)][li]);
         }
         // gz += sum_i phi(q_i) dL/dD_i (every read of gz this step is above)
         for (int r = tid - NP * kWave; r < f; r += NC * kWave) {

@@ -267,6 +267,18 @@ __device__ inline uint32_t pack_hi_lo(float x) {
   return (uint32_t)__builtin_bit_cast(uint16_t, hi) |
          ((uint32_t)__builtin_bit_cast(uint16_t, lo) << 16);
 }
+// pack_hi_lo of two values at once: one paired rounding for the two hi parts
+// and one for the two lo parts, then one byte permute per result (the same
+// bits as two pack_hi_lo calls).
+__device__ inline void pack_hi_lo2(float x0, float x1, uint32_t& p0, uint32_t& p1) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const uint32_t h = __builtin_bit_cast(uint32_t, bf16x2{(__bf16)x0, (__bf16)x1});
+  const float h0 = __builtin_bit_cast(float, h << 16);
+  const float h1 = __builtin_bit_cast(float, h & 0xffff0000u);
+  const uint32_t l = __builtin_bit_cast(uint32_t, bf16x2{(__bf16)(x0 - h0), (__bf16)(x1 - h1)});
+  p0 = __builtin_amdgcn_perm(l, h, 0x05040100u);  // h bits 0..15 | l bits 0..15 << 16
+  p1 = __builtin_amdgcn_perm(l, h, 0x07060302u);  // h bits 16..31 | l bits 16..31 << 16
+}
 __device__ inline float unpack_hi(uint32_t p) { return __builtin_bit_cast(float, p << 16); }
 __device__ inline float unpack_lo(uint32_t p) { return __builtin_bit_cast(float, p & 0xffff0000u); }
 

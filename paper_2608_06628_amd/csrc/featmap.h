@@ -173,38 +173,52 @@ struct WaveFeatMap {
     }
   }
 
-  __device__ static inline void compute(const op_t (&wop)[NT][KD],
-                                        const op_t (&xop)[KD],
-                                        float (&phi)[NPAIR][16]) {
-    float mx = -INFINITY, mn = INFINITY;
+  // The logits U^T = W^T X^T into phi[0 .. NT-1] (the operands of X are
+  // free again afterwards).
+  __device__ static inline void logits(const op_t (&wop)[NT][KD],
+                                       const op_t (&xop)[KD],
+                                       float (&phi)[NPAIR][16]) {
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
       f32x16 acc = {};
 #pragma unroll
       for (int ks = 0; ks < KD; ++ks) acc = M::mma(wop[t][ks], xop[ks], acc);
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        phi[t][i] = acc[i];
-        mx = fmaxf(mx, acc[i]);
-        mn = fminf(mn, acc[i]);
-      }
+      for (int i = 0; i < 16; ++i) phi[t][i] = acc[i];
     }
+  }
+
+  // Both softmaxes over the logits.  keep = false gives phi = 0 (a padding
+  // row) at no extra cost: it folds into the normalising factors.
+  __device__ static inline void softmax(float (&phi)[NPAIR][16], bool keep) {
+    float mx = -INFINITY, mn = INFINITY;
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        mx = fmaxf(mx, phi[t][i]);
+        mn = fminf(mn, phi[t][i]);
+      }
     mx = fmaxf(mx, xor32(mx));
     mn = fminf(mn, xor32(mn));
+    // e^(u - mx) = 2^(u log2 e - mx log2 e): one fma per exponent; the
+    // rounding of mx log2 e is common to the row and cancels in the ratio
+    constexpr float kLog2e = 1.4426950408889634f;
+    const float mxl = mx * kLog2e, mnl = mn * kLog2e;
     float sp = 0.0f, sn = 0.0f;
 #pragma unroll
     for (int t = 0; t < NT; ++t)
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
         const float u = phi[t][i];
-        phi[t][i] = fast_exp(u - mx);        // softmax(+U): shift by max U
-        phi[NT + t][i] = fast_exp(mn - u);   // softmax(-U): shift by max -U
+        phi[t][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(u, kLog2e, -mxl));       // softmax(+U)
+        phi[NT + t][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(-u, kLog2e, mnl));  // softmax(-U)
         sp += phi[t][i];
         sn += phi[NT + t][i];
       }
     sp += xor32(sp);
     sn += xor32(sn);
-    const float ip = 1.0f / sp, in = 1.0f / sn;
+    const float ip = keep ? 1.0f / sp : 0.0f, in = keep ? 1.0f / sn : 0.0f;
 #pragma unroll
     for (int t = 0; t < NT; ++t)
 #pragma unroll
@@ -212,6 +226,14 @@ struct WaveFeatMap {
         phi[t][i] *= ip;
         phi[NT + t][i] *= in;
       }
+  }
+
+  __device__ static inline void compute(const op_t (&wop)[NT][KD],
+                                        const op_t (&xop)[KD],
+                                        float (&phi)[NPAIR][16],
+                                        bool keep = true) {
+    logits(wop, xop, phi);
+    softmax(phi, keep);
   }
 };
 

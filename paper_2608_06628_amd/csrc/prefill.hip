@@ -487,12 +487,11 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
     for (int it = blk0; it <= blk1; ++it) {
       if (it < blk1) {
         typename C::Buf& B = sh.buf[(it - blk0) & 1];
-        op_t xm[C::KD];
-#pragma unroll
-        for (int ks = 0; ks < C::KD; ++ks) xm[ks] = keep_if<T>(row_ok, x[ks]);
-        if (it + 1 < blk1) load(it + 1);  // next block in flight
+        // a padding row reads row L-1 (finite); keep = row_ok zeroes its phi
         float phi[WFM::NPAIR][16];
-        WFM::compute(wop, xm, phi);
+        WFM::logits(wop, x, phi);
+        if (it + 1 < blk1) load(it + 1);  // next block in flight
+        WFM::softmax(phi, row_ok);
         if (w == 0) {
 #pragma unroll
           for (int p = 0; p < WFM::NPAIR; ++p)
@@ -502,11 +501,7 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
 #pragma unroll
           for (int p = 0; p < WFM::NPAIR; ++p)
 #pragma unroll
-            for (int i = 0; i < 16; ++i) {
-              const int r = WFM::feature(16 * p + i, hh);
-              const float xk = row_ok ? phi[p][i] : 0.0f;
-              B.phiKT[r][li] = pack_hi_lo(xk);
-            }
+            for (int i = 0; i < 16; ++i) B.phiKT[WFM::feature(16 * p + i, hh)][li] = pack_hi_lo(phi[p][i]);
         }
       }
       lds_barrier();
@@ -776,17 +771,17 @@ __global__ __launch_bounds__(delta_pipe_threads<D>()) void hyb_prefill_delta_pip
       const int blk = blk0 + 2 * j + w;
       if (j < npair && blk < blk1) {
         typename C::Buf& B = sh.buf[j & 1];
-        op_t xm[C::KD];
-#pragma unroll
-        for (int ks = 0; ks < C::KD; ++ks) xm[ks] = keep_if<T>(row_ok, x[ks]);
-        if (blk + 2 < blk1) load(blk + 2);  // next pair's block in flight
+        // a padding row reads row L-1 (finite); keep = row_ok zeroes its phi
         float phi[WFM::NPAIR][16];
-        WFM::compute(wop, xm, phi);
+        WFM::logits(wop, x, phi);
+        if (blk + 2 < blk1) load(blk + 2);  // next pair's block in flight
+        WFM::softmax(phi, row_ok);
 #pragma unroll
         for (int p = 0; p < WFM::NPAIR; ++p)
 #pragma unroll
-          for (int i = 0; i < 16; ++i)
-            B.phiKT[w][WFM::feature(16 * p + i, hh)][li] = pack_hi_lo(row_ok ? phi[p][i] : 0.0f);
+          for (int i = 0; i < 16; i += 2)
+            pack_hi_lo2(phi[p][i], phi[p][i + 1], B.phiKT[w][WFM::feature(16 * p + i, hh)][li],
+                        B.phiKT[w][WFM::feature(16 * p + i + 1, hh)][li]);
       }
       lds_barrier();
     }
