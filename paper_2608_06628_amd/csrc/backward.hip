@@ -160,6 +160,25 @@ __device__ inline typename Mma<T>::op_t acc_op_lo(const f32x16& x, int ks) {
   return r;
 }
 
+// acc_op and acc_op_lo of the same registers in one pass on the bf16 path:
+// one paired rounding for two hi parts and one for two lo parts.
+__device__ inline void acc_op_pair(const f32x16& x, int ks, bf16x8& hi, bf16x8& lo) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+  u32x4 h4, l4;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const float x0 = x[ks * 8 + 2 * e], x1 = x[ks * 8 + 2 * e + 1];
+    const uint32_t h = __builtin_bit_cast(uint32_t, bf16x2{(__bf16)x0, (__bf16)x1});
+    const float h0 = __builtin_bit_cast(float, h << 16);
+    const float h1 = __builtin_bit_cast(float, h & 0xffff0000u);
+    h4[e] = h;
+    l4[e] = __builtin_bit_cast(uint32_t, bf16x2{(__bf16)(x0 - h0), (__bf16)(x1 - h1)});
+  }
+  hi = __builtin_bit_cast(bf16x8, h4);
+  lo = __builtin_bit_cast(bf16x8, l4);
+}
+
 // E fp32 values from p as an operand pair hi + lo (lo is zero on fp32).
 template <typename T>
 __device__ inline void load_split_op(const float* p, typename Mma<T>::op_t& hi,
@@ -603,6 +622,7 @@ struct FPipeCfg {
       uint32_t duT[2][F][kTile + 4]; // +-dL/du of each sign at [j][t], packed
     } x;
     float z[2][f];
+    bf16 zh[2][f], zl[2][f];         // z as a bf16 pair hi + lo
     float red[NC][kTile][2];
     float jsum[NRT][kTile];
     float fin[NC][2];
@@ -656,11 +676,14 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
     for (int ks = 0; ks < KD; ++ks) o[ks] = load_op<bf16>(row + ks * KW);
   };
 
-  // z at the segment's start: the earlier segments' sums
+  // z at the segment's start: the earlier segments' sums (fp32, and as a
+  // bf16 pair hi + lo for the products that form lin_den)
   for (int r = tid; r < f; r += blockDim.x) {
     float zr = 0.0f;
     for (int sp = 0; sp < seg; ++sp) zr += ka.dz[((size_t)u * (nseg - 1) + sp) * f + r];
     sh.z[0][r] = zr;
+    sh.zh[0][r] = (bf16)zr;
+    sh.zl[0][r] = (bf16)(zr - as_operand<bf16>(zr));
   }
   lds_barrier();
 
@@ -881,30 +904,28 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
     for (int n = 1; n <= nb; ++n) {
       const int blk = blk0 + n - 1;
       Buf& B = sh.buf[(n - 1) & 1];
-      const float* zc = sh.z[(n - 1) & 1];
-      float* zn = sh.z[n & 1];
-      // -- lin_den = phi(q_li) . z (each lane half over half the features)
-      float lden = 0.0f;
-#pragma unroll
-      for (int r = hh * (f / 2); r < (hh + 1) * (f / 2); r += 4) {
-        const uint4 xq = *reinterpret_cast<const uint4*>(&B.phiQ[li][r]);
-        const f32x4 z4 = *reinterpret_cast<const f32x4*>(&zc[r]);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) lden += (unpack_hi(xq[e]) + unpack_lo(xq[e])) * z4[e];
-      }
-      lden += xor32(lden);
-      // -- readout against S_{c-1}: both operands as hi + lo pairs
-      f32x16 acc_lin = {};
+      const int zb = (n - 1) & 1;
+      const float* zc = sh.z[zb];
+      // -- readout against S_{c-1} and lin_den = phi(q) . z_{c-1}, all
+      // operands as hi + lo pairs.  lin_den is the product of a tile whose
+      // rows all equal z with phi(Q)^T: every row of the result holds it.
+      f32x16 acc_lin = {}, acc_den = {};
 #pragma unroll
       for (int ks = 0; ks < C::KF; ++ks) {
         op_t ph, pl;
         lds_pair_op(&B.phiQ[li][0], ks, hh, ph, pl);
         const int rt = ks / KL, kk = ks % KL;
-        const op_t sa = acc_op<bf16>(sacc[rt], kk);
+        op_t sa, sl;
+        acc_op_pair(sacc[rt], kk, sa, sl);
         acc_lin = M::mma(sa, ph, acc_lin);
-        acc_lin = M::mma(acc_op_lo<bf16>(sacc[rt], kk), ph, acc_lin);
+        acc_lin = M::mma(sl, ph, acc_lin);
         acc_lin = M::mma(sa, pl, acc_lin);
+        const op_t zh = lds_op_perm<bf16>(&sh.zh[zb][0], ks, hh, 0);
+        acc_den = M::mma(zh, ph, acc_den);
+        acc_den = M::mma(lds_op_perm<bf16>(&sh.zl[zb][0], ks, hh, 0), ph, acc_den);
+        acc_den = M::mma(zh, pl, acc_den);
       }
+      const float lden = acc_den[0];
       // -- merge (scaled by exp(-c) so nothing overflows): out = N / D with
       // w sm_den = exp(la) den, lin_den = exp(lb), c = max(la, lb)
       const float m = B.m[li], den = B.den[li];
@@ -993,9 +1014,10 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
           for (int ks = 0; ks < KL; ++ks) {
             op_t gh, gl;
             lds_pair_op(&sh.x.gn[li][s * kTile], ks, hh, gh, gl);
-            const op_t ah = acc_op<bf16>(sT[j][s], ks);
+            op_t ah, al;
+            acc_op_pair(sT[j][s], ks, ah, al);
             dq = M::mma(ah, gh, dq);
-            dq = M::mma(acc_op_lo<bf16>(sT[j][s], ks), gh, dq);
+            dq = M::mma(al, gh, dq);
             dq = M::mma(ah, gl, dq);
           }
         float js = 0.0f;
@@ -1069,7 +1091,9 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
 #pragma unroll
           for (int e = 0; e < 4; ++e) zs += unpack_hi(xk[e]) + unpack_lo(xk[e]);
         }
-        zn[r] = zs;
+        sh.z[zb ^ 1][r] = zs;
+        sh.zh[zb ^ 1][r] = (bf16)zs;
+        sh.zl[zb ^ 1][r] = (bf16)(zs - as_operand<bf16>(zs));
       }
       lds_barrier();  // 5
     }
@@ -1753,8 +1777,10 @@ __global__ __launch_bounds__(rwalk_threads<D>()) void hyb_bwd_rwalk_kernel(BwdKA
 #pragma unroll
             for (int ks = 0; ks < C::KL; ++ks) {
               const op_t vb = B.vrow[s][ks][lane];
-              dk = M::mma(acc_op<bf16>(gacc[j][s], ks), vb, dk);
-              dk = M::mma(acc_op_lo<bf16>(gacc[j][s], ks), vb, dk);
+              op_t gh, gl;
+              acc_op_pair(gacc[j][s], ks, gh, gl);
+              dk = M::mma(gh, vb, dk);
+              dk = M::mma(gl, vb, dk);
             }
           float js = 0.0f;
 #pragma unroll
