@@ -685,6 +685,12 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
     sh.zh[0][r] = (bf16)zr;
     sh.zl[0][r] = (bf16)(zr - as_operand<bf16>(zr));
   }
+  // dL/du and the second buffer's Q^T operands start at zero: the softmax
+  // waves' first dW update then adds exact zeros, and their loop needs no
+  // branch (which would make the compiler keep a second copy of dW)
+  for (int i = tid; i < (int)(sizeof(sh.x) / 4); i += blockDim.x) reinterpret_cast<uint32_t*>(&sh.x)[i] = 0u;
+  for (int i = tid; i < (int)(sizeof(sh.buf[1].qtop) / 4); i += blockDim.x)
+    reinterpret_cast<uint32_t*>(&sh.buf[1].qtop)[i] = 0u;
   lds_barrier();
 
   if (w < 2) {
@@ -821,9 +827,10 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
       }
 #pragma unroll
       for (int k = 0; k < NBAR - 1; ++k) lds_barrier();
-      if (n > 0) {
+      {
         // dW^T += dL/du^T Q for the block the state waves are finishing
-        // (its dL/du is in LDS between their fourth and fifth barrier)
+        // (its dL/du is in LDS between their fourth and fifth barrier; zeros
+        // at n = 0)
         const Buf& Bp = sh.buf[(n - 1) & 1];
 #pragma unroll
         for (int t = 0; t < NT; ++t)
@@ -1483,9 +1490,10 @@ __global__ __launch_bounds__(gdelta_threads<D>()) void hyb_bwd_gdelta_kernel(Bwd
     f32x16 gacc[C::NRT];
 #pragma unroll
     for (int rt = 0; rt < C::NRT; ++rt) gacc[rt] = f32x16{};
-    for (int j = 0; j <= npair; ++j) {
+    lds_barrier();  // step 0 (peeled: the producers fill the first buffer)
+    for (int j = 1; j <= npair; ++j) {
       const int pj = j - 1;
-      if (pj >= 0) {
+      {
         typename C::Buf& B = sh.buf[pj & 1];
 #pragma unroll
         for (int q = 0; q < 2; ++q) {

@@ -425,24 +425,9 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
   const bool row_ok = li < L;
   const int lrow = min(li, L - 1);
 
-  // State waves: S columns col of all f rows, S + the earlier segments'
-  // increments; z likewise into z[0].
-  f32x16 sacc[C::NRT];
+  // z + the earlier segments' increments into z[0] (the state waves' S
+  // likewise, in their own branch below).
   if (!producer) {
-#pragma unroll
-    for (int rt = 0; rt < C::NRT; ++rt)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        f32x4 x = *reinterpret_cast<const f32x4*>(Sh + (size_t)col * f + rt * kTile + row_of(4 * j, hh));
-        for (int s = 0; s < seg; ++s) {
-          const f32x4 y = *reinterpret_cast<const f32x4*>(
-              wsS + (size_t)s * D * f + (size_t)col * f + rt * kTile + row_of(4 * j, hh));
-#pragma unroll
-          for (int r = 0; r < 4; ++r) x[r] += y[r];
-        }
-#pragma unroll
-        for (int r = 0; r < 4; ++r) sacc[rt][4 * j + r] = x[r];
-      }
     for (int r = tid - NP * kWave; r < f; r += NC * kWave) {
       float zr = zh[r];
       for (int s = 0; s < seg; ++s) zr += wsz[(size_t)s * f + r];
@@ -501,7 +486,9 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
 #pragma unroll
           for (int p = 0; p < WFM::NPAIR; ++p)
 #pragma unroll
-            for (int i = 0; i < 16; ++i) B.phiKT[WFM::feature(16 * p + i, hh)][li] = pack_hi_lo(phi[p][i]);
+            for (int i = 0; i < 16; i += 2)
+              pack_hi_lo2(phi[p][i], phi[p][i + 1], B.phiKT[WFM::feature(16 * p + i, hh)][li],
+                          B.phiKT[WFM::feature(16 * p + i + 1, hh)][li]);
         }
       }
       lds_barrier();
@@ -573,9 +560,31 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
     }
   } else {
     // ---- state waves: readout, merge, store and commit of block it - 1 ----
-    for (int it = blk0; it <= blk1; ++it) {
+    // S columns col of all f rows: S + the earlier segments' increments.
+    // (Declared here, not before the role branches: a value live across the
+    // other roles' code takes registers there too.)
+    f32x16 sacc[C::NRT];
+#pragma unroll
+    for (int rt = 0; rt < C::NRT; ++rt)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        f32x4 x = *reinterpret_cast<const f32x4*>(Sh + (size_t)col * f + rt * kTile + row_of(4 * j, hh));
+        for (int s = 0; s < seg; ++s) {
+          const f32x4 y = *reinterpret_cast<const f32x4*>(
+              wsS + (size_t)s * D * f + (size_t)col * f + rt * kTile + row_of(4 * j, hh));
+#pragma unroll
+          for (int r = 0; r < 4; ++r) x[r] += y[r];
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r) sacc[rt][4 * j + r] = x[r];
+      }
+    // (iteration blk0, where the producers fill the first buffer, is peeled:
+    // a branch inside the loop would make the compiler keep a second copy of
+    // the accumulators)
+    lds_barrier();
+    for (int it = blk0 + 1; it <= blk1; ++it) {
       const int cblk = it - 1;
-      if (cblk >= blk0) {
+      {
         typename C::Buf& B = sh.buf[(cblk - blk0) & 1];
         const float* zr = sh.z[(cblk - blk0) & 1];
         float* zw = sh.z[(cblk - blk0 + 1) & 1];
@@ -666,17 +675,16 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
       }
       lds_barrier();
     }
-  }
-
-  if (!producer && last) {
+    if (last) {
 #pragma unroll
-    for (int rt = 0; rt < C::NRT; ++rt)
+      for (int rt = 0; rt < C::NRT; ++rt)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        *reinterpret_cast<f32x4*>(Sh + (size_t)col * f + rt * kTile + row_of(4 * j, hh)) =
-            f32x4{sacc[rt][4 * j], sacc[rt][4 * j + 1], sacc[rt][4 * j + 2], sacc[rt][4 * j + 3]};
-    const float* zf = sh.z[(blk1 - blk0) & 1];
-    for (int r = tid - NP * kWave; r < f; r += NC * kWave) zh[r] = zf[r];
+        for (int j = 0; j < 4; ++j)
+          *reinterpret_cast<f32x4*>(Sh + (size_t)col * f + rt * kTile + row_of(4 * j, hh)) =
+              f32x4{sacc[rt][4 * j], sacc[rt][4 * j + 1], sacc[rt][4 * j + 2], sacc[rt][4 * j + 3]};
+      const float* zf = sh.z[(blk1 - blk0) & 1];
+      for (int r = tid - NP * kWave; r < f; r += NC * kWave) zh[r] = zf[r];
+    }
   }
 }
 
@@ -815,9 +823,10 @@ __global__ __launch_bounds__(delta_pipe_threads<D>()) void hyb_prefill_delta_pip
     f32x16 sacc[C::NRT];
 #pragma unroll
     for (int rt = 0; rt < C::NRT; ++rt) sacc[rt] = f32x16{};
-    for (int j = 0; j <= npair; ++j) {
+    lds_barrier();  // step 0 (peeled: the producers fill the first buffer)
+    for (int j = 1; j <= npair; ++j) {
       const int pj = j - 1;
-      if (pj >= 0) {
+      {
         typename C::Buf& B = sh.buf[pj & 1];
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
