@@ -128,6 +128,21 @@ __device__ inline float cvt_op<float>(const float* x) {
 }
 
 // x, or a zero operand when ok is false (a select, not a branch).
+// Accumulator registers ks*E .. ks*E+E-1 as a T operand; the tile's rows
+// become the contraction index (row_of order).  For values that a T holds
+// exactly (a transpose through the identity).
+template <typename T>
+__device__ inline typename Mma<T>::op_t acc_op_exact(const f32x16& x, int ks) {
+  typename Mma<T>::op_t r;
+  if constexpr (Mma<T>::E == 1) {
+    r = x[ks];
+  } else {
+#pragma unroll
+    for (int e = 0; e < Mma<T>::E; ++e) r[e] = (T)x[ks * Mma<T>::E + e];
+  }
+  return r;
+}
+
 template <typename T>
 __device__ inline typename Mma<T>::op_t keep_if(bool ok,
                                                typename Mma<T>::op_t x) {

@@ -496,16 +496,23 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
   } else if (producer) {
     // ---- in-block softmax branch for column tiles c0 .. c0+CT-1 ----
     const int c0 = (w - 2) * C::CT;
-    op_t ko[C::KD], qo[C::KD], vo[C::CT][C::KL];
+    // V rows of this wave's column tiles (lane: token, 16 contiguous bytes
+    // per load), turned into V^T operands by a product with the identity
+    op_t ko[C::KD], qo[C::KD], vx[C::CT][C::KL];
     auto load = [&](int blk) {
       load_rows(kbase(blk), kstride, ko);
       load_rows(qbase(blk), qstride, qo);
+      const T* vrow = vbase(blk) + (size_t)lrow * kstride + hh * E;
 #pragma unroll
       for (int ct = 0; ct < C::CT; ++ct)
 #pragma unroll
-        for (int ks = 0; ks < C::KL; ++ks)
-          vo[ct][ks] = load_rows_op<T>(vbase(blk) + (c0 + ct) * kTile + li, kstride, ks, hh, L, false);
+        for (int ks = 0; ks < C::KL; ++ks) vx[ct][ks] = load_op<T>(vrow + (c0 + ct) * kTile + ks * KW);
     };
+    op_t ident[C::KL];
+#pragma unroll
+    for (int ks = 0; ks < C::KL; ++ks)
+#pragma unroll
+      for (int e = 0; e < E; ++e) ident[ks][e] = (T)(ks * KW + hh * E + e == li ? 1.0f : 0.0f);
     if (blk0 < blk1) load(blk0);
     for (int it = blk0; it <= blk1; ++it) {
       if (it < blk1) {
@@ -515,11 +522,17 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
 #pragma unroll
         for (int ks = 0; ks < C::KD; ++ks)
           sc = M::mma(keep_if<T>(row_ok, ko[ks]), keep_if<T>(row_ok, qo[ks]), sc);
+        // V^T (lane: column, elements: tokens in row_of order; padding
+        // tokens zero) from V_c = V_c I, exact: one nonzero product per entry
         op_t vc[C::CT][C::KL];
 #pragma unroll
-        for (int ct = 0; ct < C::CT; ++ct)
+        for (int ct = 0; ct < C::CT; ++ct) {
+          f32x16 va = {};
 #pragma unroll
-          for (int ks = 0; ks < C::KL; ++ks) vc[ct][ks] = vo[ct][ks];
+          for (int ks = 0; ks < C::KL; ++ks) va = M::mma(keep_if<T>(row_ok, vx[ct][ks]), ident[ks], va);
+#pragma unroll
+          for (int ks = 0; ks < C::KL; ++ks) vc[ct][ks] = acc_op_exact<T>(va, ks);
+        }
         if (it + 1 < blk1) load(it + 1);  // next block in flight
         float pr[16];
         float m = -INFINITY;
@@ -578,6 +591,19 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
 #pragma unroll
         for (int r = 0; r < 4; ++r) sacc[rt][4 * j + r] = x[r];
       }
+    // z of the feature tiles cw, cw + NC, ... as accumulator tiles whose
+    // columns are all equal: the commit adds phi(K)^T 1 on the MFMAs
+    constexpr int ZPW = (C::NRT + NC - 1) / NC;
+    f32x16 zt[ZPW];
+#pragma unroll
+    for (int j = 0; j < ZPW; ++j) {
+      const int p = cw + j * NC;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) zt[j][i] = p < C::NRT ? sh.z[0][p * kTile + row_of(i, hh)] : 0.0f;
+    }
+    op_t ones;
+#pragma unroll
+    for (int e = 0; e < E; ++e) ones[e] = (T)1.0f;
     // (iteration blk0, where the producers fill the first buffer, is peeled:
     // a branch inside the loop would make the compiler keep a second copy of
     // the accumulators)
@@ -662,15 +688,23 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
             sacc[rt] = M::mma(khi, vk, sacc[rt]);
             sacc[rt] = M::mma(klo, vk, sacc[rt]);
           }
-        for (int r = tid - NP * kWave; r < f; r += NC * kWave) {
-          float s = zr[r];
 #pragma unroll
-          for (int t0 = 0; t0 < kTile; t0 += 4) {
-            const uint4 xk = *reinterpret_cast<const uint4*>(&B.phiKT[r][t0]);
+        for (int j = 0; j < ZPW; ++j) {
+          const int p = cw + j * NC;
+          if (p >= C::NRT) continue;  // uniform
 #pragma unroll
-            for (int e = 0; e < 4; ++e) s += unpack_hi(xk[e]) + unpack_lo(xk[e]);
+          for (int ks = 0; ks < C::KL; ++ks) {
+            op_t khi, klo;
+            lds_pair_op(&B.phiKT[p * kTile + li][0], ks, hh, khi, klo);
+            zt[j] = M::mma(khi, ones, zt[j]);
+            zt[j] = M::mma(klo, ones, zt[j]);
           }
-          zw[r] = s;
+          if (li == 0) {
+#pragma unroll
+            for (int i = 0; i < 16; i += 4)
+              *reinterpret_cast<f32x4*>(&zw[p * kTile + row_of(i, hh)]) =
+                  f32x4{zt[j][i], zt[j][i + 1], zt[j][i + 2], zt[j][i + 3]};
+          }
         }
       }
       lds_barrier();
