@@ -1891,13 +1891,23 @@ __global__ void hyb_bwd_reduce_kernel(BwdKArgs ka) {
   if (idx < (size_t)Hq * per) {
     const int h = (int)(idx / per);
     const size_t e = idx % per;
+    // terms t = b * nseg + sg in increasing order; each batch's loads are
+    // issued before its additions, which keep that order
+    const int nterm = a.s.B * nseg;
+    constexpr int CH = 8;
     float s = 0.0f;
-    for (int b = 0; b < a.s.B; ++b) {
-      const size_t u = (size_t)b * Hq + h;
-      for (int sg = 0; sg < nseg; ++sg) {
-        const size_t o = (u * nseg + sg) * per + e;
-        s += ka.dwq[o] + ka.dwk[o];
+    for (int t0 = 0; t0 < nterm; t0 += CH) {
+      float q[CH], k[CH];
+#pragma unroll
+      for (int j = 0; j < CH; ++j) {
+        const int t = min(t0 + j, nterm - 1);  // in bounds; unused past nterm
+        const size_t o = (((size_t)(t / nseg) * Hq + h) * nseg + t % nseg) * per + e;
+        q[j] = ka.dwq[o];
+        k[j] = ka.dwk[o];
       }
+#pragma unroll
+      for (int j = 0; j < CH; ++j)
+        if (t0 + j < nterm) s += q[j] + k[j];
     }
     a.dW[idx] = s;
   }
