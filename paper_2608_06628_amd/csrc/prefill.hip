@@ -727,9 +727,10 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
 // Pipelined delta (bf16, F <= 64): a segment's own increment
 // dS = sum_c phi(K_c)^T V_c, dz = sum_c sum_t phi(k_t), two blocks per
 // iteration.  Waves 0 and 1 compute phi(K) of the pair's two blocks (the
-// whole feature map in one wave), waves 2 and 3 load their V operands, and
-// the D/32 state waves commit the previous pair into S columns 32w..32w+31
-// in fp32 accumulators; one barrier per pair, buffers double-buffered.
+// whole feature map in one wave), waves 2 and 3 load their V rows and turn
+// them into V^T operands, and the D/32 state waves commit the previous pair
+// into S columns 32w..32w+31 and dz (as phi(K)^T 1) in fp32 accumulators; one
+// barrier per pair, buffers double-buffered.
 // ---------------------------------------------------------------------------
 template <typename T, int D, int F>
 struct DeltaPipeCfg {
@@ -749,7 +750,6 @@ struct DeltaPipeCfg {
   };
   struct alignas(16) Smem {
     Buf buf[2];
-    float z[f];
   };
 };
 
@@ -794,9 +794,6 @@ __global__ __launch_bounds__(delta_pipe_threads<D>()) void hyb_prefill_delta_pip
   auto vbase = [&](int blk) {
     return (const T*)a.v + (((size_t)b * T_ + (size_t)blk * L) * Hkv + g) * D;
   };
-  for (int r = tid; r < f; r += blockDim.x) sh.z[r] = 0.0f;
-  lds_barrier();
-
   if (w < 2) {
     // ---- phi(K) of block blk0 + 2j + w ----
     const T* __restrict__ Wt_h = (const T*)a.W + (size_t)h * F * D;
@@ -828,25 +825,36 @@ __global__ __launch_bounds__(delta_pipe_threads<D>()) void hyb_prefill_delta_pip
       lds_barrier();
     }
   } else if (w < NP) {
-    // ---- V operands of block blk0 + 2j + (w - 2), every column tile ----
+    // ---- V operands of block blk0 + 2j + (w - 2), every column tile: V
+    // rows (lane: token, 16 contiguous bytes per load) turned into V^T by a
+    // product with the identity (exact: one nonzero product per entry) ----
     const int q = w - 2;
-    op_t vo[NC][C::KL];
+    op_t vx[NC][C::KL];
     auto load = [&](int blk) {
+      const T* vrow = vbase(blk) + (size_t)lrow * kstride + hh * E;
 #pragma unroll
       for (int ct = 0; ct < NC; ++ct)
 #pragma unroll
-        for (int ks = 0; ks < C::KL; ++ks)
-          vo[ct][ks] = load_rows_op<T>(vbase(blk) + ct * kTile + li, kstride, ks, hh, L, false);
+        for (int ks = 0; ks < C::KL; ++ks) vx[ct][ks] = load_op<T>(vrow + ct * kTile + ks * KW);
     };
+    op_t ident[C::KL];
+#pragma unroll
+    for (int ks = 0; ks < C::KL; ++ks)
+#pragma unroll
+      for (int e = 0; e < E; ++e) ident[ks][e] = (T)(ks * KW + hh * E + e == li ? 1.0f : 0.0f);
     if (blk0 + q < blk1) load(blk0 + q);
     for (int j = 0; j <= npair; ++j) {
       const int blk = blk0 + 2 * j + q;
       if (j < npair && blk < blk1) {
         typename C::Buf& B = sh.buf[j & 1];
 #pragma unroll
-        for (int ct = 0; ct < NC; ++ct)
+        for (int ct = 0; ct < NC; ++ct) {
+          f32x16 va = {};
 #pragma unroll
-          for (int ks = 0; ks < C::KL; ++ks) B.vop[q][ct][ks][lane] = vo[ct][ks];
+          for (int ks = 0; ks < C::KL; ++ks) va = M::mma(keep_if<T>(row_ok, vx[ct][ks]), ident[ks], va);
+#pragma unroll
+          for (int ks = 0; ks < C::KL; ++ks) B.vop[q][ct][ks][lane] = acc_op_exact<T>(va, ks);
+        }
         if (blk + 2 < blk1) load(blk + 2);
       }
       lds_barrier();
@@ -857,6 +865,15 @@ __global__ __launch_bounds__(delta_pipe_threads<D>()) void hyb_prefill_delta_pip
     f32x16 sacc[C::NRT];
 #pragma unroll
     for (int rt = 0; rt < C::NRT; ++rt) sacc[rt] = f32x16{};
+    // dz of the feature tiles cw, cw + NC, ... as accumulator tiles whose
+    // columns are all equal: phi(K)^T 1 on the MFMAs
+    constexpr int ZPW = (C::NRT + NC - 1) / NC;
+    f32x16 zt[ZPW];
+#pragma unroll
+    for (int j = 0; j < ZPW; ++j) zt[j] = f32x16{};
+    op_t ones;
+#pragma unroll
+    for (int e = 0; e < E; ++e) ones[e] = (T)1.0f;
     lds_barrier();  // step 0 (peeled: the producers fill the first buffer)
     for (int j = 1; j <= npair; ++j) {
       const int pj = j - 1;
@@ -875,15 +892,17 @@ __global__ __launch_bounds__(delta_pipe_threads<D>()) void hyb_prefill_delta_pip
               sacc[rt] = M::mma(khi, vk, sacc[rt]);
               sacc[rt] = M::mma(klo, vk, sacc[rt]);
             }
-          for (int r = tid - NP * kWave; r < f; r += NC * kWave) {
-            float s = 0.0f;
 #pragma unroll
-            for (int t0 = 0; t0 < kTile; t0 += 4) {
-              const uint4 xk = *reinterpret_cast<const uint4*>(&B.phiKT[q][r][t0]);
+          for (int j = 0; j < ZPW; ++j) {
+            const int p = cw + j * NC;
+            if (p >= C::NRT) continue;  // uniform
 #pragma unroll
-              for (int e = 0; e < 4; ++e) s += unpack_hi(xk[e]) + unpack_lo(xk[e]);
+            for (int ks = 0; ks < C::KL; ++ks) {
+              op_t khi, klo;
+              lds_pair_op(&B.phiKT[q][p * kTile + li][0], ks, hh, khi, klo);
+              zt[j] = M::mma(khi, ones, zt[j]);
+              zt[j] = M::mma(klo, ones, zt[j]);
             }
-            sh.z[r] += s;
           }
         }
       }
@@ -895,7 +914,16 @@ __global__ __launch_bounds__(delta_pipe_threads<D>()) void hyb_prefill_delta_pip
       for (int j = 0; j < 4; ++j)
         *reinterpret_cast<f32x4*>(wsS + (size_t)col * f + rt * kTile + row_of(4 * j, hh)) =
             f32x4{sacc[rt][4 * j], sacc[rt][4 * j + 1], sacc[rt][4 * j + 2], sacc[rt][4 * j + 3]};
-    for (int r = tid - NP * kWave; r < f; r += NC * kWave) wsz[r] = sh.z[r];
+#pragma unroll
+    for (int j = 0; j < ZPW; ++j) {
+      const int p = cw + j * NC;
+      if (p < C::NRT && li == 0) {
+#pragma unroll
+        for (int i = 0; i < 16; i += 4)
+          *reinterpret_cast<f32x4*>(wsz + p * kTile + row_of(i, hh)) =
+              f32x4{zt[j][i], zt[j][i + 1], zt[j][i + 2], zt[j][i + 3]};
+      }
+    }
   }
 }
 
