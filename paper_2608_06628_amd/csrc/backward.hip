@@ -1580,7 +1580,6 @@ struct RWalkCfg {
   struct alignas(16) Smem {
     Buf buf[2];
     uint32_t duT[2][F][kTile + 4];   // +-dL/du of each sign at [j][t], packed hi/lo
-    float gz[f];
     float jsum[NRT][kTile];
   };
 };
@@ -1626,12 +1625,6 @@ __global__ __launch_bounds__(rwalk_threads<D>()) void hyb_bwd_rwalk_kernel(BwdKA
     return (const bf16*)a.v + (((size_t)b * T_ + (size_t)blk * L) * Hkv + g) * D;
   };
 
-  // gz: the later segments' sums (Gbar likewise, in the state waves below)
-  for (int r = tid; r < f; r += blockDim.x) {
-    float zr = 0.0f;
-    for (int sp = seg + 1; sp < nseg; ++sp) zr += ka.dgz[((size_t)u * nseg + sp) * f + r];
-    sh.gz[r] = zr;
-  }
   lds_barrier();
 
   if (w < 2) {
@@ -1763,6 +1756,19 @@ __global__ __launch_bounds__(rwalk_threads<D>()) void hyb_bwd_rwalk_kernel(BwdKA
             gacc[j][s][i] += src[(size_t)(s * kTile + row_of(i, hh)) * f + p * kTile + li];
       }
     }
+    // gz for the same feature tiles, as accumulator tiles whose columns are
+    // all equal (register i: feature 32p + row_of(i, hh)); its update
+    // phi(Q)^T dL/dD runs on the MFMAs against a broadcast dL/dD operand
+    f32x16 gzt[RPW];
+#pragma unroll
+    for (int j = 0; j < RPW; ++j) {
+      gzt[j] = f32x16{};
+      const int p = cw + j * NC;
+      if (p >= NRT) continue;
+      for (int sp = seg + 1; sp < nseg; ++sp)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) gzt[j][i] += ka.dgz[((size_t)u * nseg + sp) * f + p * kTile + row_of(i, hh)];
+    }
     f32x16 dwacc[NT];
 #pragma unroll
     for (int t = 0; t < NT; ++t) dwacc[t] = f32x16{};
@@ -1795,11 +1801,10 @@ __global__ __launch_bounds__(rwalk_threads<D>()) void hyb_bwd_rwalk_kernel(BwdKA
           for (int i4 = 0; i4 < 16; i4 += 4) {
             const int r = p * kTile + row_of(i4, hh);
             const f32x4 pk4 = *reinterpret_cast<const f32x4*>(&B.phiK[li][r]);
-            const f32x4 gz4 = *reinterpret_cast<const f32x4*>(&sh.gz[r]);
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
               pk[j][i4 + e] = pk4[e];
-              dphi[j][i4 + e] = dk[i4 + e] + gz4[e];
+              dphi[j][i4 + e] = dk[i4 + e] + gzt[j][i4 + e];
               js += dphi[j][i4 + e] * pk4[e];
             }
           }
@@ -1824,17 +1829,13 @@ __global__ __launch_bounds__(rwalk_threads<D>()) void hyb_bwd_rwalk_kernel(BwdKA
                         sh.duT[sg][t * kTile + row_of(i, hh)][li],
                         sh.duT[sg][t * kTile + row_of(i + 1, hh)][li]);
         }
-        // gz += sum_i phi(q_i) dL/dD_i (every read of gz this step is above)
-        for (int r = tid - NP * kWave; r < f; r += NC * kWave) {
-          float acc = 0.0f;
+        // dL/dD of the block's queries (natural order) as a broadcast operand
+        // pair: gz += phi(Q)^T dL/dD below (every read of gz this step is above)
+        op_t gdh[C::KL], gdl[C::KL];
 #pragma unroll
-          for (int t0 = 0; t0 < kTile; t0 += 4) {
-            const uint4 xq = *reinterpret_cast<const uint4*>(&B.phiQT[r][t0]);
-#pragma unroll
-            for (int e = 0; e < 4; ++e) acc += (unpack_hi(xq[e]) + unpack_lo(xq[e])) * B.gd[t0 + e];
-          }
-          sh.gz[r] += acc;
-        }
+        for (int ks = 0; ks < C::KL; ++ks)
+          split_op(*reinterpret_cast<const f32x4*>(&B.gd[ks * KW + hh * E]),
+                   *reinterpret_cast<const f32x4*>(&B.gd[ks * KW + hh * E + 4]), gdh[ks], gdl[ks]);
         // Gbar^T += dL/dN^T phi(Q) (rows c of slice s, columns of tile p)
 #pragma unroll
         for (int j = 0; j < RPW; ++j) {
@@ -1844,6 +1845,9 @@ __global__ __launch_bounds__(rwalk_threads<D>()) void hyb_bwd_rwalk_kernel(BwdKA
           for (int ks = 0; ks < C::KL; ++ks) {
             op_t ph, pl;
             lds_pair_op_nat(&B.phiQT[p * kTile + li][0], ks, hh, ph, pl);
+            gzt[j] = M::mma(ph, gdh[ks], gzt[j]);
+            gzt[j] = M::mma(pl, gdh[ks], gzt[j]);
+            gzt[j] = M::mma(ph, gdl[ks], gzt[j]);
 #pragma unroll
             for (int s = 0; s < NC; ++s) {
               const op_t gh = B.gn[0][s][ks][lane], gl = B.gn[1][s][ks][lane];
