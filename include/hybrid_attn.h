@@ -162,8 +162,9 @@ int hybrid_state_commit(const hyb_dims_t* dims, const void* k, const void* v,
  * is then ignored and may be NULL).  ws/ws_bytes: workspace of at least
  * hybrid_workspace_bytes(dims, HYB_OP_PREFILL, seq_len) bytes (may be NULL
  * when that is 0); the prompt is processed in sequence segments whose state
- * increments pass through it, so results equal the block-by-block ones up to
- * the order of fp32 additions.  It must not overlap any other argument.  Two
+ * increments (and a snapshot of the incoming state, which the segments start
+ * from) pass through it, so results equal the block-by-block ones up to the
+ * order of fp32 additions.  It must not overlap any other argument.  Two
  * requests of one call must not share a slot. */
 int hybrid_state_prefill(const hyb_dims_t* dims, int32_t seq_len,
                          const void* q, const void* k, const void* v,
@@ -175,7 +176,9 @@ int hybrid_state_prefill(const hyb_dims_t* dims, int32_t seq_len,
  * cached prefix plus the block itself (the softmax teacher the hybrid layer
  * replaces; Section 2.2, without a mask inside the block).  prefix_len is a
  * device array [B]; values are clamped to [0, max_prefix].  ws/ws_bytes: at
- * least hybrid_workspace_bytes(dims, HYB_OP_SOFTMAX_PREFIX, max_prefix). */
+ * least hybrid_workspace_bytes(dims, HYB_OP_SOFTMAX_PREFIX, max_prefix)
+ * bytes, not overlapping any argument; when that is 0 (the prefix is not
+ * split across workgroups) ws may be NULL. */
 int softmax_prefix_step(const hyb_dims_t* dims, const void* q, const void* k,
                         const void* v, const void* k_cache,
                         const void* v_cache, const int32_t* prefix_len,

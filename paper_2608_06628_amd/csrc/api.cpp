@@ -291,6 +291,12 @@ int softmax_prefix_step(const hyb_dims_t* dims, const void* q, const void* k,
       overlap(out, no, v, nkv) || overlap(out, no, k_cache, nc) ||
       overlap(out, no, v_cache, nc) || overlap(out, no, ws, need))
     return fail(HYB_EINVAL, "out overlaps an input or the workspace");
+  // the split kernels write the workspace while they read the inputs
+  if (need > 0 && (overlap(ws, need, q, nq) || overlap(ws, need, k, nkv) ||
+                   overlap(ws, need, v, nkv) || overlap(ws, need, k_cache, nc) ||
+                   overlap(ws, need, v_cache, nc) ||
+                   overlap(ws, need, prefix_len, (size_t)s.B * 4)))
+    return fail(HYB_EINVAL, "the workspace overlaps an input");
   hyb::SoftmaxPrefixArgs a{s,         q,   k,  v,
                            k_cache,   v_cache, prefix_len, max_prefix,
                            out,       ws,  hyb::softmax_prefix_splits(s, max_prefix)};

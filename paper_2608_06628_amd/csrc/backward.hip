@@ -100,7 +100,7 @@ static BwdLayout bwd_layout(const Shape& s, int T) {
   BwdLayout l;
   size_t o = 0;
   l.dS = o;
-  o = align256(o + prefill_ws_bytes(s, T));
+  o = align256(o + prefill_delta_ws_bytes(s, T));
   l.dG = o;
   o = align256(o + units * nseg * s.D * f * 4);
   l.dgz = o;

@@ -80,6 +80,8 @@ hipError_t launch_softmax_prefix(const SoftmaxPrefixArgs& a, hipStream_t st);
 // Prefill: number of sequence segments and the workspace they need.
 int prefill_segments(const Shape& s, int T);
 size_t prefill_ws_bytes(const Shape& s, int T);
+// The part of it that the delta launch writes (the segment increments).
+size_t prefill_delta_ws_bytes(const Shape& s, int T);
 // The prefill's first launch alone: each segment's state increment (all
 // segments but the last) into a.ws; a.S, a.z, a.q, a.alpha are not used.
 hipError_t launch_prefill_delta(const PrefillArgs& a, hipStream_t st);

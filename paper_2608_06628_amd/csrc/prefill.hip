@@ -12,6 +12,10 @@
 // its blocks as below; the last segment writes the final state.  Only the
 // associativity of the sum is used, so the result is the sequential one up to
 // rounding order.  Without outputs, only the last segment walks.
+// Ordering: with nseg > 1 the walk segments start from a snapshot of the
+// incoming S, z that a launch before the walk copies into the workspace, never
+// from S, z themselves, which the last segment overwrites in the same launch
+// (workgroups of one launch are not ordered).
 //
 // Within a segment, one workgroup per (request b, query head h) walks the
 // blocks in order, with the next block's Q, K and V in flight while the
@@ -54,6 +58,35 @@ struct PrefillCfg {
     typename FM::Smem fq, fk;
   };
 };
+
+// Workspace layout (nseg > 1): the segment increments dS [units][nseg-1][D][f]
+// and dz [units][nseg-1][f], then the snapshot of the incoming state,
+// S0 [units][D][f] and z0 [units][f].
+__device__ inline const float* prefill_snapshot_S(const PrefillArgs& a, int nseg, int u) {
+  const size_t f = 2 * (size_t)a.s.F, units = (size_t)a.s.B * a.s.Hq;
+  return a.ws + units * (nseg - 1) * (a.s.D * f + f) + (size_t)u * a.s.D * f;
+}
+__device__ inline const float* prefill_snapshot_z(const PrefillArgs& a, int nseg, int u) {
+  const size_t f = 2 * (size_t)a.s.F, units = (size_t)a.s.B * a.s.Hq;
+  return a.ws + units * (nseg - 1) * (a.s.D * f + f) + units * a.s.D * f + (size_t)u * f;
+}
+
+// Snapshot of the incoming state of every (request, head) unit into the
+// workspace, one workgroup per unit, 16-byte copies.  A unit whose slot is
+// out of range is skipped (its walk never reads the snapshot).
+__global__ __launch_bounds__(256) void hyb_prefill_snapshot_kernel(PrefillArgs a, int nseg) {
+  const int u = blockIdx.x, Hq = a.s.Hq;
+  const int b = u / Hq, h = u % Hq;
+  const int slot = a.slots ? a.slots[b] : b;
+  if (slot < 0 || slot >= a.s.n_slots) return;
+  const size_t f = 2 * (size_t)a.s.F, n = (size_t)a.s.D * f;
+  const size_t sbase = (size_t)slot * Hq + h;
+  const f32x4* src = reinterpret_cast<const f32x4*>(a.S + sbase * n);
+  f32x4* dst = reinterpret_cast<f32x4*>(const_cast<float*>(prefill_snapshot_S(a, nseg, u)));
+  for (size_t i = threadIdx.x; i < n / 4; i += blockDim.x) dst[i] = src[i];
+  float* dz = const_cast<float*>(prefill_snapshot_z(a, nseg, u));
+  for (size_t i = threadIdx.x; i < f; i += blockDim.x) dz[i] = a.z[sbase * f + i];
+}
 
 template <typename T, int D, int F>
 __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_prefill_kernel(
@@ -99,6 +132,10 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_prefill_kernel(
   // [units][nseg-1][f].
   float* __restrict__ wsS = a.ws + (size_t)u * (nseg - 1) * D * f;
   float* __restrict__ wsz = a.ws + (size_t)units * (nseg - 1) * D * f + (size_t)u * (nseg - 1) * f;
+  // (without outputs only the last segment walks, and no snapshot is taken)
+  const bool snap = nseg > 1 && a.out != nullptr;
+  const float* __restrict__ S0 = snap ? prefill_snapshot_S(a, nseg, u) : Sh;
+  const float* __restrict__ z0 = snap ? prefill_snapshot_z(a, nseg, u) : zh;
 
   // Starting state: zero for a delta, else S plus the earlier segments'
   // increments, all in the accumulator layout.
@@ -119,10 +156,10 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_prefill_kernel(
     for (int rt = 0; rt < C::NRT; ++rt) sacc[rt] = f32x16{};
     for (int r = tid; r < f; r += blockDim.x) sh.z[r] = 0.0f;
   } else {
-    add_state(Sh, true);
+    add_state(S0, true);
     for (int s = 0; s < seg; ++s) add_state(wsS + (size_t)s * D * f, false);
     for (int r = tid; r < f; r += blockDim.x) {
-      float zr = zh[r];
+      float zr = z0[r];
       for (int s = 0; s < seg; ++s) zr += wsz[(size_t)s * f + r];
       sh.z[r] = zr;
     }
@@ -422,6 +459,8 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
   float* __restrict__ zh = a.z + sbase * f;
   float* __restrict__ wsS = a.ws + (size_t)u * (nseg - 1) * D * f;
   float* __restrict__ wsz = a.ws + (size_t)units * (nseg - 1) * D * f + (size_t)u * (nseg - 1) * f;
+  const float* __restrict__ S0 = nseg > 1 ? prefill_snapshot_S(a, nseg, u) : Sh;
+  const float* __restrict__ z0 = nseg > 1 ? prefill_snapshot_z(a, nseg, u) : zh;
   const bool row_ok = li < L;
   const int lrow = min(li, L - 1);
 
@@ -429,7 +468,7 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
   // likewise, in their own branch below).
   if (!producer) {
     for (int r = tid - NP * kWave; r < f; r += NC * kWave) {
-      float zr = zh[r];
+      float zr = z0[r];
       for (int s = 0; s < seg; ++s) zr += wsz[(size_t)s * f + r];
       sh.z[0][r] = zr;
     }
@@ -581,7 +620,7 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
     for (int rt = 0; rt < C::NRT; ++rt)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        f32x4 x = *reinterpret_cast<const f32x4*>(Sh + (size_t)col * f + rt * kTile + row_of(4 * j, hh));
+        f32x4 x = *reinterpret_cast<const f32x4*>(S0 + (size_t)col * f + rt * kTile + row_of(4 * j, hh));
         for (int s = 0; s < seg; ++s) {
           const f32x4 y = *reinterpret_cast<const f32x4*>(
               wsS + (size_t)s * D * f + (size_t)col * f + rt * kTile + row_of(4 * j, hh));
@@ -937,6 +976,13 @@ static hipError_t prefill_go(const PrefillArgs& a, hipStream_t st) {
   const int seg_blocks = (nblk + nseg - 1) / nseg;
   const dim3 block(kWave * (D / kTile));
   if (nseg > 1) {
+    // only the last segment walks when no outputs are wanted, and it alone
+    // writes the state: no snapshot is needed then
+    if (a.out != nullptr) {
+      hipLaunchKernelGGL(hyb_prefill_snapshot_kernel, dim3(units), dim3(256), 0, st, a, nseg);
+      const hipError_t e0 = hipGetLastError();
+      if (e0 != hipSuccess) return e0;
+    }
     const hipError_t e = prefill_delta_go<T, D, F>(a, st);
     if (e != hipSuccess) return e;
   }
@@ -1002,11 +1048,19 @@ int prefill_segments(const Shape& s, int T) {
   return nseg;
 }
 
-size_t prefill_ws_bytes(const Shape& s, int T) {
+size_t prefill_delta_ws_bytes(const Shape& s, int T) {
   const int nseg = prefill_segments(s, T);
   if (nseg <= 1) return 0;
   const size_t f = 2 * (size_t)s.F;
   return (size_t)s.B * s.Hq * (nseg - 1) * ((size_t)s.D * f + f) * 4;
+}
+
+size_t prefill_ws_bytes(const Shape& s, int T) {
+  const int nseg = prefill_segments(s, T);
+  if (nseg <= 1) return 0;
+  const size_t f = 2 * (size_t)s.F;
+  // the increments, then the snapshot of the incoming state
+  return prefill_delta_ws_bytes(s, T) + (size_t)s.B * s.Hq * ((size_t)s.D * f + f) * 4;
 }
 
 template <typename T, int D>

@@ -487,7 +487,10 @@ int softmax_prefix_splits(const Shape& s, int max_prefix) {
   return (int)want;
 }
 
+// A single KV range per (request, KV head) writes the normalised output
+// directly and needs no workspace.
 size_t softmax_prefix_ws_bytes(const Shape& s, int n_split) {
+  if (n_split <= 1) return 0;
   return (size_t)s.B * s.Hq * n_split * s.L * (s.D + 2) * sizeof(float);
 }
 

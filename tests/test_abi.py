@@ -181,6 +181,36 @@ def test_workspace_query():
     assert ws % (128 * 16 * 32 * 130 * 4) == 0 and ws > 0
     assert lib.hybrid_workspace_bytes(ctypes.byref(_dims(head_dim=5)), hb.OP_STEP, 0) == 0
     assert lib.hybrid_workspace_bytes(None, hb.OP_STEP, 0) == 0
+    # a short prefix is not split: the kernel writes out directly, no workspace
+    assert lib.hybrid_workspace_bytes(ctypes.byref(d), hb.OP_SOFTMAX_PREFIX, 64) == 0
+
+
+def test_softmax_prefix_workspace_overlap():
+    lib = hb.load()
+    d = _dims(batch=2)
+    need = lib.hybrid_workspace_bytes(ctypes.byref(d), hb.OP_SOFTMAX_PREFIX, 4096)
+    assert need > 0
+    # q k v k_cache v_cache prefix_len | out ws
+    ptrs = [_addr(i) for i in range(8)]
+    call = lambda p: lib.softmax_prefix_step(ctypes.byref(d), *p[:6], 4096, p[6], p[7], need, None)
+    for r_i in range(6):
+        p = list(ptrs)
+        p[7] = p[r_i]
+        assert call(p) == 2, r_i
+        assert "overlap" in hb.last_error()
+
+
+def test_prefill_workspace_holds_the_snapshot():
+    # the segment increments, then a snapshot of the incoming state
+    lib = hb.load()
+    d = _dims(batch=1, n_q_heads=4, n_kv_heads=1, n_slots=1)
+    T = 32 * 64
+    need = lib.hybrid_workspace_bytes(ctypes.byref(d), hb.OP_PREFILL, T)
+    f, D, units = 128, 128, 4
+    per = (D * f + f) * 4
+    assert need % (units * per) == 0
+    nseg = need // (units * per)
+    assert 2 <= nseg <= 8
 
 
 def test_backward_validation():
@@ -227,3 +257,4 @@ def test_backward_validation():
             assert "overlap" in hb.last_error()
     assert lib.hybrid_attn_backward(ctypes.byref(_dims(batch=0, feat_dim=128)), T,
                                     *([None] * 11), 0, None) == 0
+

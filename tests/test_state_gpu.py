@@ -182,8 +182,11 @@ def test_prefill_segments(shape):
     def call(out_f32):
         S, z = state_dev(c0["S"]), f32(c0["z"])
         states.append((S, z))
+        # a workspace full of NaN bytes: every part the walk reads (the
+        # increments and the snapshot of the incoming state) is written first
+        ws = torch.full((ws_need,), 0xFF, dtype=torch.uint8, device="cuda")
         return hb.hybrid_state_prefill(act(q, dt), act(k, dt), act(v, dt), act(Wt, dt),
-                                       f32(alpha), S, z, L, out_f32=out_f32)
+                                       f32(alpha), S, z, L, out_f32=out_f32, ws=ws)
 
     check_outputs(call, o_r, dt, f"prefill segments out {shape}")
     S, z = states[-1]
