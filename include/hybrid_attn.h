@@ -172,6 +172,28 @@ int hybrid_state_prefill(const hyb_dims_t* dims, int32_t seq_len,
                          const int32_t* slots, void* out, void* ws,
                          size_t ws_bytes, void* stream);
 
+/* Bytes of the library-held scratch buffer of hybrid_state_prefill_noalloc,
+ * per GPU. */
+#define HYB_NOALLOC_SCRATCH_BYTES (64u << 20)
+
+/* hybrid_state_prefill for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): the same computation and results, bit for bit, with the
+ * workspace taken from a scratch buffer the library holds on each GPU
+ * (HYB_NOALLOC_SCRATCH_BYTES, kept from the first call on a device until
+ * the process ends).  The call itself allocates nothing; the caller still
+ * passes inputs, outputs and the state.  A call whose workspace
+ * (hybrid_workspace_bytes(dims, HYB_OP_PREFILL, seq_len)) exceeds the
+ * scratch size returns HYB_EWORKSPACE and enqueues nothing.  Every call on
+ * one GPU shares that GPU's buffer, which keeps the last call's contents
+ * (nothing in it needs to start at zero): calls whose executions overlap on
+ * one GPU, e.g. on two streams, race and must not be issued. */
+int hybrid_state_prefill_noalloc(const hyb_dims_t* dims, int32_t seq_len,
+                                 const void* q, const void* k, const void* v,
+                                 const void* W, const float* alpha, float* S,
+                                 float* z, const int32_t* slots, void* out,
+                                 void* stream);
+
 /* Exact softmax attention of the active block's queries over each request's
  * cached prefix plus the block itself (the softmax teacher the hybrid layer
  * replaces; Section 2.2, without a mask inside the block).  prefix_len is a

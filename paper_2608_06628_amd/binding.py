@@ -23,8 +23,9 @@ STATUS = {0: "HYB_OK", 1: "HYB_ENULL", 2: "HYB_EINVAL", 3: "HYB_EALIGN",
           4: "HYB_EDTYPE", 5: "HYB_EUNSUPPORTED", 6: "HYB_EWORKSPACE",
           7: "HYB_ELAUNCH"}
 EXPORTS = ("hybrid_attn_step", "hybrid_attn_step_commit", "hybrid_state_commit",
-           "hybrid_state_prefill", "softmax_prefix_step", "hybrid_attn_backward",
-           "hybrid_workspace_bytes", "hybrid_last_error")
+           "hybrid_state_prefill", "hybrid_state_prefill_noalloc", "softmax_prefix_step",
+           "hybrid_attn_backward", "hybrid_workspace_bytes", "hybrid_last_error")
+NOALLOC_SCRATCH_BYTES = 64 << 20
 
 
 class HybError(RuntimeError):
@@ -58,6 +59,7 @@ def load():
     lib.hybrid_attn_step_commit.argtypes = [P] + [vp] * 11
     lib.hybrid_state_commit.argtypes = [P] + [vp] * 8
     lib.hybrid_state_prefill.argtypes = [P, i32] + [vp] * 10 + [sz, vp]
+    lib.hybrid_state_prefill_noalloc.argtypes = [P, i32] + [vp] * 10
     lib.softmax_prefix_step.argtypes = [P] + [vp] * 6 + [i32, vp, vp, sz, vp]
     lib.hybrid_attn_backward.argtypes = [P, i32] + [vp] * 11 + [sz, vp]
     lib.hybrid_workspace_bytes.argtypes = [P, i32, i32]
@@ -65,7 +67,7 @@ def load():
     lib.hybrid_last_error.argtypes = []
     lib.hybrid_last_error.restype = ctypes.c_char_p
     for n in ("hybrid_attn_step", "hybrid_attn_step_commit", "hybrid_state_commit", "hybrid_state_prefill",
-              "softmax_prefix_step"):
+              "hybrid_state_prefill_noalloc", "softmax_prefix_step"):
         getattr(lib, n).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -202,6 +204,31 @@ def hybrid_state_prefill(q, k, v, W, alpha, S, z, block, slots=None, out=None,
         _ptr(slots, "slots", torch.int32), _ptr(out, "out", odt) if want_out else None,
         _ptr(ws, "ws") if ws is not None else None,
         ws.numel() * ws.element_size() if ws is not None else 0, _stream(stream)))
+    return out
+
+
+def hybrid_state_prefill_noalloc(q, k, v, W, alpha, S, z, block, slots=None, out=None,
+                                 want_out=True, out_f32=False, stream=None):
+    """hybrid_state_prefill with the library-held scratch buffer as its
+    workspace: the call allocates no device memory (out is allocated here
+    only when the caller passes none)."""
+    lib = load()
+    B, T, Hkv, d = k.shape
+    Hq = W.shape[0]
+    act = k.dtype
+    flags, odt = _out_flags(out, act, out_f32)
+    dims = make_dims(B, Hq, Hkv, d, block, z.shape[2], _dt(k), S.shape[0], flags)
+    if want_out and out is None:
+        out = torch.empty((B, T, Hq, d), dtype=odt, device=k.device)
+    if not want_out:
+        out = None
+    _check(lib.hybrid_state_prefill_noalloc(
+        ctypes.byref(dims), T, _ptr(q, "q", act) if want_out else None,
+        _ptr(k, "k"), _ptr(v, "v", act), _ptr(W, "W", act),
+        _ptr(alpha, "alpha", torch.float32) if want_out else None,
+        _ptr(S, "S", torch.float32), _ptr(z, "z", torch.float32),
+        _ptr(slots, "slots", torch.int32), _ptr(out, "out", odt) if want_out else None,
+        _stream(stream)))
     return out
 
 

@@ -206,11 +206,17 @@ int hybrid_state_commit(const hyb_dims_t* dims, const void* k, const void* v,
   return launched(hyb::launch_commit(a, (hipStream_t)stream), "commit");
 }
 
-int hybrid_state_prefill(const hyb_dims_t* dims, int32_t seq_len,
-                         const void* q, const void* k, const void* v,
-                         const void* W, const float* alpha, float* S, float* z,
-                         const int32_t* slots, void* out, void* ws,
-                         size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Validation and dispatch of the prefill.  ws == nullptr with use_scratch:
+// the workspace is the library-held scratch buffer.
+int prefill_impl(const hyb_dims_t* dims, int32_t seq_len, const void* q,
+                 const void* k, const void* v, const void* W,
+                 const float* alpha, float* S, float* z, const int32_t* slots,
+                 void* out, void* ws, size_t ws_bytes, bool use_scratch,
+                 void* stream) {
   hyb::Shape s;
   TRY(check_dims(dims, true, &s));
   if (seq_len <= 0 || seq_len % s.L != 0)
@@ -229,10 +235,19 @@ int hybrid_state_prefill(const hyb_dims_t* dims, int32_t seq_len,
     TRY(check_ptr(alpha, "alpha"));
   }
   const size_t need = hybrid_workspace_bytes(dims, HYB_OP_PREFILL, seq_len);
-  if (need > 0 && (!ws || ws_bytes < need))
-    return fail(HYB_EWORKSPACE, "prefill needs %zu workspace bytes, got %zu",
-                need, ws ? ws_bytes : (size_t)0);
-  TRY(check_ptr(ws, "ws", false));
+  if (use_scratch) {
+    if (need > hyb::kScratchBytes)
+      return fail(HYB_EWORKSPACE,
+                  "prefill needs %zu scratch bytes, more than the %zu "
+                  "(HYB_NOALLOC_SCRATCH_BYTES) the library holds; use "
+                  "hybrid_state_prefill with a workspace",
+                  need, hyb::kScratchBytes);
+  } else {
+    if (need > 0 && (!ws || ws_bytes < need))
+      return fail(HYB_EWORKSPACE, "prefill needs %zu workspace bytes, got %zu",
+                  need, ws ? ws_bytes : (size_t)0);
+    TRY(check_ptr(ws, "ws", false));
+  }
   const size_t es = elem_bytes(s.dtype), f = 2 * (size_t)s.F;
   const size_t nq = (size_t)s.B * seq_len * s.Hq * s.D * es;
   const size_t no = (size_t)s.B * seq_len * s.Hq * s.D * out_bytes(s);
@@ -248,9 +263,39 @@ int hybrid_state_prefill(const hyb_dims_t* dims, int32_t seq_len,
                    overlap(ws, need, k, nkv) || overlap(ws, need, v, nkv) ||
                    (out && (overlap(ws, need, out, no) || overlap(ws, need, q, nq)))))
     return fail(HYB_EINVAL, "the workspace overlaps an argument");
-  hyb::PrefillArgs a{s, seq_len, q, k, v, W, alpha, S, z, slots, out, (float*)ws};
   (void)hipGetLastError();
+  if (use_scratch && need > 0) {
+    void* p = nullptr;
+    const hipError_t e = hyb::scratch_device_ptr(&p);
+    if (e != hipSuccess)
+      return fail(HYB_ELAUNCH, "scratch buffer lookup failed: %s",
+                  hipGetErrorString(e));
+    ws = p;
+  }
+  hyb::PrefillArgs a{s, seq_len, q, k, v, W, alpha, S, z, slots, out, (float*)ws};
   return launched(hyb::launch_prefill(a, (hipStream_t)stream), "prefill");
+}
+
+}  // namespace
+
+extern "C" {
+
+int hybrid_state_prefill(const hyb_dims_t* dims, int32_t seq_len,
+                         const void* q, const void* k, const void* v,
+                         const void* W, const float* alpha, float* S, float* z,
+                         const int32_t* slots, void* out, void* ws,
+                         size_t ws_bytes, void* stream) {
+  return prefill_impl(dims, seq_len, q, k, v, W, alpha, S, z, slots, out, ws,
+                      ws_bytes, false, stream);
+}
+
+int hybrid_state_prefill_noalloc(const hyb_dims_t* dims, int32_t seq_len,
+                                 const void* q, const void* k, const void* v,
+                                 const void* W, const float* alpha, float* S,
+                                 float* z, const int32_t* slots, void* out,
+                                 void* stream) {
+  return prefill_impl(dims, seq_len, q, k, v, W, alpha, S, z, slots, out,
+                      nullptr, 0, true, stream);
 }
 
 int softmax_prefix_step(const hyb_dims_t* dims, const void* q, const void* k,

@@ -86,6 +86,12 @@ size_t prefill_delta_ws_bytes(const Shape& s, int T);
 // segments but the last) into a.ws; a.S, a.z, a.q, a.alpha are not used.
 hipError_t launch_prefill_delta(const PrefillArgs& a, hipStream_t st);
 
+// The library-held scratch buffer (scratch.hip) of the entry point that
+// allocates nothing: its size, and its device address on the current device
+// (looked up on the first call on each device).
+constexpr size_t kScratchBytes = (size_t)64 << 20;
+hipError_t scratch_device_ptr(void** ptr);
+
 hipError_t launch_backward(const BackwardArgs& a, hipStream_t st);
 bool backward_supported(const Shape& s);
 size_t backward_ws_bytes(const Shape& s, int T);

@@ -258,3 +258,23 @@ def test_backward_validation():
     assert lib.hybrid_attn_backward(ctypes.byref(_dims(batch=0, feat_dim=128)), T,
                                     *([None] * 11), 0, None) == 0
 
+
+def test_prefill_noalloc_rejects_beyond_scratch():
+    """The entry point that allocates nothing refuses a call whose workspace
+    exceeds the library-held scratch buffer, before any HIP call."""
+    lib = hb.load()
+    d = _dims(batch=4, n_q_heads=32, n_kv_heads=8, feat_dim=256, n_slots=4)
+    T = 32 * 64
+    need = lib.hybrid_workspace_bytes(ctypes.byref(d), hb.OP_PREFILL, T)
+    assert need > hb.NOALLOC_SCRATCH_BYTES
+    p = [_addr(i) for i in range(10)]
+    rc = lib.hybrid_state_prefill_noalloc(ctypes.byref(d), T, p[0], p[1], p[2], p[3], p[4],
+                                          p[5], p[6], None, p[7], None)
+    assert rc == 6
+    assert "scratch" in hb.last_error() and str(hb.NOALLOC_SCRATCH_BYTES) in hb.last_error()
+    # the same validation as hybrid_state_prefill
+    assert lib.hybrid_state_prefill_noalloc(ctypes.byref(d), 40, *p[:7], None, p[7], None) == 2
+    assert lib.hybrid_state_prefill_noalloc(ctypes.byref(d), T, None, p[1], *p[2:7], None,
+                                            p[7], None) == 1
+    assert lib.hybrid_state_prefill_noalloc(ctypes.byref(_dims(batch=0)), T,
+                                            *([None] * 10)) == 0
