@@ -319,6 +319,7 @@ def run(args):
     del lanes
     torch.cuda.empty_cache()
 
+    result["table4"] = table4()
     if not args.no_extras:
         result["prefill"] = bench_prefill(gen, dev)
         result["softmax_prefix"] = bench_mix(gen, dev)
@@ -464,6 +465,24 @@ def bench_prefill(gen, dev):
             "note": "includes two zero-fills of the 8 MiB state"}
 
 
+PAGE_SIZE = 64  # tokens per page of the paged KV cache legs
+
+
+def paged_pool(kc, vc, ps, gen, dev):
+    """A contiguous cache [B][P][Hkv][d] as page pools [B*P/ps][ps][Hkv][d]
+    with the pages in a random order, and the page table [B][P/ps] that finds
+    them (the same bytes, laid out as a serving engine's paged cache)."""
+    B, P = kc.shape[0], kc.shape[1]
+    npg = B * (P // ps)
+    perm = torch.randperm(npg, generator=gen, device=dev)      # pool slot of logical page i
+    kp = torch.empty((npg, ps) + tuple(kc.shape[2:]), dtype=kc.dtype, device=dev)
+    vp = torch.empty_like(kp)
+    kp[perm] = kc.reshape(npg, ps, *kc.shape[2:])
+    vp[perm] = vc.reshape(npg, ps, *vc.shape[2:])
+    table = perm.to(torch.int32).reshape(B, P // ps).contiguous()
+    return kp, vp, table
+
+
 def bench_mix(gen, dev):
     dims = synth.MIX128
     B, Hq, Hkv, d, L, f, P = dims.B, dims.Hq, dims.Hkv, dims.d, dims.L, dims.f, synth.MIX128_PREFIX
@@ -480,7 +499,18 @@ def bench_mix(gen, dev):
     sm = lambda: hb.softmax_prefix_step(q, k, v, kc, vc, plen, out=out, ws=ws)
     sm()
     ms_sm = time_region(sm, 5)
+    ref_out = out.clone()
+    # The same cache as a paged pool (pages of PAGE_SIZE tokens in a random
+    # order, a page table per request): the same bytes, read page by page.
+    kp, vp, table = paged_pool(kc, vc, PAGE_SIZE, gen, dev)
     del kc, vc
+    torch.cuda.empty_cache()
+    smp = lambda: hb.softmax_prefix_step_paged(q, k, v, kp, vp, table, plen, out=out, ws=ws)
+    smp()
+    ms_smp = time_region(smp, 5)
+    torch.cuda.synchronize()
+    assert torch.equal(out, ref_out), "paged and contiguous softmax-prefix outputs differ"
+    del kp, vp, table
     torch.cuda.empty_cache()
     # hybrid step at the same batch; 4 rotating state sets keep it cache-cold
     Wt, alpha = synth.feature_weights(dims, 1, 2)
@@ -500,11 +530,16 @@ def bench_mix(gen, dev):
     sm_bytes = 2 * B * P * Hkv * d * 2 + (2 * B * L * Hq * d + 2 * B * L * Hkv * d) * 2
     sm_flops = 4 * B * Hq * L * (P + L) * d
     hy_bytes = step_bytes(B, Hq, Hkv, d, L, f)
-    log(f"mix128: softmax {ms_sm:.3f} ms, hybrid {ms_hy * 1e3:.1f} us")
+    log(f"mix128: softmax {ms_sm:.3f} ms (paged {ms_smp:.3f} ms), hybrid {ms_hy * 1e3:.1f} us")
+    sm_roof_ms = sm_bytes / (HBM_PEAK_GBPS * 1e9) * 1e3
     return {"workload": "mix128: B=128, 16q/4kv, d=128, block 32, prefix 32768, bf16 KV cache",
             "softmax_ms": ms_sm, "softmax_gbps": sm_bytes / (ms_sm * 1e-3) / 1e9,
             "softmax_hbm_frac": sm_bytes / (ms_sm * 1e-3) / 1e9 / HBM_PEAK_GBPS,
             "softmax_tflops": sm_flops / (ms_sm * 1e-3) / 1e12,
+            "softmax_roofline_ms": sm_roof_ms,
+            "softmax_paged_ms": ms_smp, "page_size": PAGE_SIZE,
+            "softmax_paged_hbm_frac": sm_bytes / (ms_smp * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+            "speedup_vs_softmax_roofline": sm_roof_ms / ms_hy,
             "hybrid_us": ms_hy * 1e3, "hybrid_gbps": hy_bytes / (ms_hy * 1e-3) / 1e9,
             "speedup": ms_sm / ms_hy,
             "mix_6h14s_vs_20s": (20 * ms_sm) / (6 * ms_hy + 14 * ms_sm)}
@@ -580,10 +615,25 @@ def bench_table3(gen, dev):
                 hb.hybrid_attn_step(*qkv, W, al, S, z, out=out)
 
             ms_sm, ms_hy = median_ms(sm), median_ms(hy)
-            del caches
+            ms_smp = None
+            if P >= PAGE_SIZE:
+                pools = [paged_pool(kc, vc, PAGE_SIZE, gen, dev) for kc, vc in caches]
+                del caches
+                torch.cuda.empty_cache()
+
+                def smp():
+                    kp, vp, table = pools[it[0] % n_kv]
+                    it[0] += 1
+                    hb.softmax_prefix_step_paged(*qkv, kp, vp, table, plen, out=out, ws=ws)
+
+                ms_smp = median_ms(smp)
+                del pools
+            else:
+                del caches
             torch.cuda.empty_cache()
             pt, ph = PAPER_TABLE3_MS[(B, P)]
             rows.append({"B": B, "P": P, "softmax_ms": ms_sm, "hybrid_ms": ms_hy,
+                         "softmax_paged_ms": ms_smp,
                          "speedup": ms_sm / ms_hy,
                          # attention time of a 20-layer model with n hybrid layers
                          "mix_6of20_vs_softmax": 20 * ms_sm / (6 * ms_hy + 14 * ms_sm),
@@ -595,8 +645,55 @@ def bench_table3(gen, dev):
         del states
         torch.cuda.empty_cache()
     return {"workload": "Table 3 analogue: one 32-token block, 16q/4kv, d=128, f=128, bf16; "
-                        "median of 20 calls on cold inputs",
+                        "median of 20 calls on cold inputs; softmax_paged_ms: the same cache as "
+                        f"{PAGE_SIZE}-token pages in a random order",
             "rows": rows}
+
+
+# Resident-request capacity after the paper's Table 4 (one H200, 4096-token
+# footprint per request: B* = 544 for the softmax teacher vs 704 for the
+# hybrid model).  Computed from the bytes this library keeps per request and
+# layer; the model's attention shape is not given in the paper, so the
+# benchmark's 16q/4kv, d=128 shape stands in for it.
+TABLE4_TOKENS = 4096
+MODEL_LAYERS, HYBRID_LAYERS = 20, 6
+MODEL_PARAMS = 16e9  # "16B" (Section 4), bf16 weights
+
+
+def table4_capacity(mem_bytes=288e9, frac_static=0.85):
+    dims = synth.SERVE64
+    Hq, Hkv, d, L, f = dims.Hq, dims.Hkv, dims.d, dims.L, dims.f
+    T = TABLE4_TOKENS
+    softmax_layer = 2 * T * Hkv * d * 2                        # K and V cache, bf16
+    state_layer = Hq * (d * f + f) * 4                         # S and z, fp32, as the library stores them
+    block_kv = 2 * L * Hkv * d * 2                             # the active block's K and V
+    hybrid_layer = state_layer + block_kv
+    teacher = MODEL_LAYERS * softmax_layer
+    hybrid = (MODEL_LAYERS - HYBRID_LAYERS) * softmax_layer + HYBRID_LAYERS * hybrid_layer
+    pool = mem_bytes * frac_static - MODEL_PARAMS * 2
+    bt, bh = int(pool // teacher), int(pool // hybrid)
+    return {"workload": f"{T}-token footprint per request; {MODEL_LAYERS} attention layers, "
+                        f"{HYBRID_LAYERS} hybrid; 16q/4kv, d=128, f=128 per layer (stand-in shape); "
+                        f"{mem_bytes / 1e9:.0f} GB, {frac_static} of it for weights "
+                        f"({MODEL_PARAMS * 2 / 1e9:.0f} GB bf16) and the cache/state pool",
+            "softmax_layer_bytes_per_request": softmax_layer,
+            "hybrid_layer_bytes_per_request": hybrid_layer,
+            "hybrid_state_bytes_per_request_layer": state_layer,
+            "teacher_bytes_per_request": teacher, "hybrid_model_bytes_per_request": hybrid,
+            "pool_bytes": pool, "teacher_max_batch": bt, "hybrid_max_batch": bh,
+            "ratio": bh / bt,
+            "paper_h200": {"teacher_max_batch": 544, "hybrid_max_batch": 704, "ratio": 704 / 544}}
+
+
+def table4(mem_bytes=288e9, frac_static=0.85):
+    """The capacity calculation for one MI355X, and the same calculation for
+    the paper's H200 (141 GB) beside its measured B*."""
+    r = table4_capacity(mem_bytes, frac_static)
+    h = table4_capacity(141e9, frac_static)
+    r["same_calculation_h200_141gb"] = {"teacher_max_batch": h["teacher_max_batch"],
+                                        "hybrid_max_batch": h["hybrid_max_batch"],
+                                        "ratio": h["ratio"]}
+    return r
 
 
 def copy_calibration():

@@ -207,6 +207,31 @@ int softmax_prefix_step(const hyb_dims_t* dims, const void* q, const void* k,
                         int32_t max_prefix, void* out, void* ws,
                         size_t ws_bytes, void* stream);
 
+/* softmax_prefix_step over a paged KV cache, as a serving engine keeps it
+ * (Section 3.3 keeps the hybrid state beside such a cache; the softmax
+ * layers it replaces read it).  k_pages, v_pages: page pools
+ * [n_pages][page_size][Hkv][d] in dims->dtype; page_table: device
+ * [B][max_pages] int32, entry i of request b naming the page that holds its
+ * cached tokens i*page_size .. (i+1)*page_size - 1 (token j at row
+ * j % page_size).  prefix_len (device [B]) is clamped to
+ * [0, max_pages * page_size]; only the first ceil(prefix_len[b] / page_size)
+ * entries of a row are read, and a page number outside [0, n_pages) is
+ * clamped into it (device values cannot be checked on the host).  page_size
+ * is a power of two from 32 to 65536 (HYB_EUNSUPPORTED otherwise); n_pages
+ * >= 1 and the page table are required when max_pages > 0.  Pages may be
+ * shared by requests and appear in any order.  The result equals
+ * softmax_prefix_step on the gathered contiguous cache, bit for bit.
+ * ws/ws_bytes: at least hybrid_workspace_bytes(dims, HYB_OP_SOFTMAX_PREFIX,
+ * max_pages * page_size) bytes (NULL when that is 0), not overlapping any
+ * argument.  out must not overlap an input. */
+int softmax_prefix_step_paged(const hyb_dims_t* dims, const void* q,
+                              const void* k, const void* v,
+                              const void* k_pages, const void* v_pages,
+                              int32_t n_pages, int32_t page_size,
+                              const int32_t* page_table, int32_t max_pages,
+                              const int32_t* prefix_len, void* out, void* ws,
+                              size_t ws_bytes, void* stream);
+
 /* Gradient of the block-hybrid layer over a training sequence with respect
  * to its feature-map weights W and gate logits alpha: the attention transfer
  * of Section 3.2 (Stage 1), which trains only {W, alpha} with the backbone

@@ -24,6 +24,7 @@ STATUS = {0: "HYB_OK", 1: "HYB_ENULL", 2: "HYB_EINVAL", 3: "HYB_EALIGN",
           7: "HYB_ELAUNCH"}
 EXPORTS = ("hybrid_attn_step", "hybrid_attn_step_commit", "hybrid_state_commit",
            "hybrid_state_prefill", "hybrid_state_prefill_noalloc", "softmax_prefix_step",
+           "softmax_prefix_step_paged",
            "hybrid_attn_backward", "hybrid_workspace_bytes", "hybrid_last_error")
 NOALLOC_SCRATCH_BYTES = 64 << 20
 
@@ -61,13 +62,15 @@ def load():
     lib.hybrid_state_prefill.argtypes = [P, i32] + [vp] * 10 + [sz, vp]
     lib.hybrid_state_prefill_noalloc.argtypes = [P, i32] + [vp] * 10
     lib.softmax_prefix_step.argtypes = [P] + [vp] * 6 + [i32, vp, vp, sz, vp]
+    lib.softmax_prefix_step_paged.argtypes = [P] + [vp] * 5 + [i32, i32, vp, i32, vp, vp, vp,
+                                                                sz, vp]
     lib.hybrid_attn_backward.argtypes = [P, i32] + [vp] * 11 + [sz, vp]
     lib.hybrid_workspace_bytes.argtypes = [P, i32, i32]
     lib.hybrid_workspace_bytes.restype = sz
     lib.hybrid_last_error.argtypes = []
     lib.hybrid_last_error.restype = ctypes.c_char_p
     for n in ("hybrid_attn_step", "hybrid_attn_step_commit", "hybrid_state_commit", "hybrid_state_prefill",
-              "hybrid_state_prefill_noalloc", "softmax_prefix_step"):
+              "hybrid_state_prefill_noalloc", "softmax_prefix_step", "softmax_prefix_step_paged"):
         getattr(lib, n).restype = ctypes.c_int
     _lib = lib
     return lib
@@ -252,6 +255,34 @@ def softmax_prefix_step(q, k, v, k_cache, v_cache, prefix_len, out=None, ws=None
         ctypes.byref(dims), _ptr(q, "q"), _ptr(k, "k", act), _ptr(v, "v", act),
         _ptr(k_cache, "k_cache", act), _ptr(v_cache, "v_cache", act),
         _ptr(prefix_len, "prefix_len", torch.int32), Pmax, _ptr(out, "out", odt),
+        _ptr(ws, "ws") if ws is not None else None,
+        ws.numel() * ws.element_size() if ws is not None else 0, _stream(stream)))
+    return out
+
+
+def softmax_prefix_step_paged(q, k, v, k_pages, v_pages, page_table, prefix_len, out=None,
+                              ws=None, out_f32=False, stream=None):
+    """softmax_prefix_step over a paged cache: k_pages/v_pages
+    [n_pages][page_size][Hkv][d], page_table [B][max_pages] int32 and
+    prefix_len [B] int32 on the device."""
+    lib = load()
+    B, L, Hq, d = q.shape
+    Hkv = k.shape[2]
+    n_pages, page_size = k_pages.shape[0], k_pages.shape[1]
+    max_pages = page_table.shape[1]
+    act = q.dtype
+    flags, odt = _out_flags(out, act, out_f32)
+    dims = make_dims(B, Hq, Hkv, d, L, 64, _dt(q), 1, flags)
+    if out is None:
+        out = torch.empty(q.shape, dtype=odt, device=q.device)
+    need = workspace_bytes(dims, OP_SOFTMAX_PREFIX, max_pages * page_size)
+    if need and ws is None:
+        ws = torch.empty(need, dtype=torch.uint8, device=q.device)
+    _check(lib.softmax_prefix_step_paged(
+        ctypes.byref(dims), _ptr(q, "q"), _ptr(k, "k", act), _ptr(v, "v", act),
+        _ptr(k_pages, "k_pages", act), _ptr(v_pages, "v_pages", act), n_pages, page_size,
+        _ptr(page_table, "page_table", torch.int32), max_pages,
+        _ptr(prefix_len, "prefix_len", torch.int32), _ptr(out, "out", odt),
         _ptr(ws, "ws") if ws is not None else None,
         ws.numel() * ws.element_size() if ws is not None else 0, _stream(stream)))
     return out

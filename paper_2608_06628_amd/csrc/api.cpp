@@ -298,13 +298,36 @@ int hybrid_state_prefill_noalloc(const hyb_dims_t* dims, int32_t seq_len,
                       nullptr, 0, true, stream);
 }
 
-int softmax_prefix_step(const hyb_dims_t* dims, const void* q, const void* k,
+}  // extern "C"
+
+namespace {
+
+// Validation and dispatch of the softmax-prefix step; !paged:
+// contiguous cache [B][max_prefix][Hkv][d]; otherwise page pools
+// [n_pages][page_size][Hkv][d] and a [B][max_pages] page table.
+int softmax_prefix_impl(const hyb_dims_t* dims, const void* q, const void* k,
                         const void* v, const void* k_cache,
                         const void* v_cache, const int32_t* prefix_len,
-                        int32_t max_prefix, void* out, void* ws,
-                        size_t ws_bytes, void* stream) {
+                        int32_t max_prefix, bool paged,
+                        const int32_t* page_table, int32_t n_pages,
+                        int32_t page_size, int32_t max_pages, void* out,
+                        void* ws, size_t ws_bytes, void* stream) {
   hyb::Shape s;
   TRY(check_dims(dims, false, &s));
+  int page_shift = 0;
+  if (paged) {
+    if (max_pages < 0) return fail(HYB_EINVAL, "max_pages %d < 0", max_pages);
+    if (page_size < 32 || page_size > (1 << 16) || (page_size & (page_size - 1)))
+      return fail(HYB_EUNSUPPORTED,
+                  "page_size %d not supported (a power of two, 32 .. 65536)",
+                  page_size);
+    while ((1 << page_shift) < page_size) ++page_shift;
+    if ((long long)max_pages * page_size > 0x7fffffffLL - 64)
+      return fail(HYB_EINVAL, "max_pages * page_size exceeds the index range");
+    if (max_pages > 0 && n_pages < 1)
+      return fail(HYB_EINVAL, "n_pages %d < 1", n_pages);
+    max_prefix = max_pages * page_size;
+  }
   if (max_prefix < 0)
     return fail(HYB_EINVAL, "max_prefix %d < 0", max_prefix);
   if (s.Hq / s.Hkv > 8)
@@ -317,8 +340,9 @@ int softmax_prefix_step(const hyb_dims_t* dims, const void* q, const void* k,
   TRY(check_ptr(out, "out"));
   TRY(check_ptr(prefix_len, "prefix_len"));
   if (max_prefix > 0) {
-    TRY(check_ptr(k_cache, "k_cache"));
-    TRY(check_ptr(v_cache, "v_cache"));
+    TRY(check_ptr(k_cache, paged ? "k_pages" : "k_cache"));
+    TRY(check_ptr(v_cache, paged ? "v_pages" : "v_cache"));
+    if (paged) TRY(check_ptr(page_table, "page_table"));
   }
   const size_t need =
       hybrid_workspace_bytes(dims, HYB_OP_SOFTMAX_PREFIX, max_prefix);
@@ -331,23 +355,56 @@ int softmax_prefix_step(const hyb_dims_t* dims, const void* q, const void* k,
   const size_t nq = (size_t)s.B * s.L * s.Hq * s.D * es;
   const size_t no = (size_t)s.B * s.L * s.Hq * s.D * out_bytes(s);
   const size_t nkv = (size_t)s.B * s.L * s.Hkv * s.D * es;
-  const size_t nc = (size_t)s.B * max_prefix * s.Hkv * s.D * es;
+  const size_t nc = paged ? (size_t)n_pages * page_size * s.Hkv * s.D * es
+                          : (size_t)s.B * max_prefix * s.Hkv * s.D * es;
+  const size_t nt = paged ? (size_t)s.B * max_pages * 4 : 0;
   if (overlap(out, no, q, nq) || overlap(out, no, k, nkv) ||
       overlap(out, no, v, nkv) || overlap(out, no, k_cache, nc) ||
-      overlap(out, no, v_cache, nc) || overlap(out, no, ws, need))
+      overlap(out, no, v_cache, nc) || overlap(out, no, ws, need) ||
+      overlap(out, no, prefix_len, (size_t)s.B * 4) ||
+      overlap(out, no, page_table, nt))
     return fail(HYB_EINVAL, "out overlaps an input or the workspace");
   // the split kernels write the workspace while they read the inputs
   if (need > 0 && (overlap(ws, need, q, nq) || overlap(ws, need, k, nkv) ||
                    overlap(ws, need, v, nkv) || overlap(ws, need, k_cache, nc) ||
                    overlap(ws, need, v_cache, nc) ||
-                   overlap(ws, need, prefix_len, (size_t)s.B * 4)))
+                   overlap(ws, need, prefix_len, (size_t)s.B * 4) ||
+                   overlap(ws, need, page_table, nt)))
     return fail(HYB_EINVAL, "the workspace overlaps an input");
   hyb::SoftmaxPrefixArgs a{s,         q,   k,  v,
                            k_cache,   v_cache, prefix_len, max_prefix,
-                           out,       ws,  hyb::softmax_prefix_splits(s, max_prefix)};
+                           out,       ws,  hyb::softmax_prefix_splits(s, max_prefix),
+                           paged && max_prefix > 0 ? page_table : nullptr,
+                           page_shift, max_pages, n_pages};
   (void)hipGetLastError();
   return launched(hyb::launch_softmax_prefix(a, (hipStream_t)stream),
                   "softmax_prefix_step");
+}
+
+}  // namespace
+
+extern "C" {
+
+int softmax_prefix_step(const hyb_dims_t* dims, const void* q, const void* k,
+                        const void* v, const void* k_cache,
+                        const void* v_cache, const int32_t* prefix_len,
+                        int32_t max_prefix, void* out, void* ws,
+                        size_t ws_bytes, void* stream) {
+  return softmax_prefix_impl(dims, q, k, v, k_cache, v_cache, prefix_len,
+                             max_prefix, false, nullptr, 0, 0, 0, out, ws,
+                             ws_bytes, stream);
+}
+
+int softmax_prefix_step_paged(const hyb_dims_t* dims, const void* q,
+                              const void* k, const void* v,
+                              const void* k_pages, const void* v_pages,
+                              int32_t n_pages, int32_t page_size,
+                              const int32_t* page_table, int32_t max_pages,
+                              const int32_t* prefix_len, void* out, void* ws,
+                              size_t ws_bytes, void* stream) {
+  return softmax_prefix_impl(dims, q, k, v, k_pages, v_pages, prefix_len, 0,
+                             true, page_table, n_pages, page_size, max_pages,
+                             out, ws, ws_bytes, stream);
 }
 
 int hybrid_attn_backward(const hyb_dims_t* dims, int32_t seq_len,

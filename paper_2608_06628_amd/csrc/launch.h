@@ -66,6 +66,12 @@ struct SoftmaxPrefixArgs {
   void* out;
   void* ws;
   int n_split;  // KV splits per (request, KV head)
+  // Paged cache (page_table non-null): k_cache, v_cache are page pools
+  // [n_pages][1 << page_shift][Hkv][d]; cached token j of request b is row
+  // j & (page size - 1) of page page_table[b * max_pages + (j >> page_shift)]
+  // (clamped to the pool); max_prefix = max_pages << page_shift.
+  const int32_t* page_table;
+  int page_shift, max_pages, n_pages;
 };
 
 hipError_t launch_step(const StepArgs& a, hipStream_t st);

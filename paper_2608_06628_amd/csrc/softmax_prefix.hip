@@ -12,6 +12,15 @@
 // once to the operand type and the running sum taken over the rounded
 // weights.  A second kernel merges the ranges with their log-sum-exp weights;
 // with a single range the first kernel writes the normalised output itself.
+//
+// The cache is either contiguous per request ([B][max_prefix][Hkv][d]) or
+// paged: a pool of fixed-size pages ([n_pages][page][Hkv][d]) and a page table
+// per request, as a serving engine's paged KV cache keeps it (Section 3.3).
+// The page size is a power of two of at least 32 rows, so a 32-key tile lies
+// in one page.  The ring kernel stages its range's page numbers in LDS when
+// it starts (a range holds at most kMaxRange keys), so the copies of a tile
+// take their page from LDS and no vector load of the page table sits among
+// the copies whose counts the ring waits on.
 #include <type_traits>
 
 #include "device.h"
@@ -38,12 +47,22 @@ struct SpCfg {
 };
 
 constexpr int kMaxGroup = 8;  // query heads per KV head handled by one WG
+constexpr int kMaxRange = 32768;  // keys of one split range at most
+// pages of one range at the smallest page size (32), unaligned ends included
+constexpr int kMaxRangePages = kMaxRange / 32 + 2;
+
+// Page of cached token j of a request (page table row ptab), clamped to the
+// pool.
+__device__ inline int sp_page(const SoftmaxPrefixArgs& a, const int32_t* ptab, int j) {
+  const int pg = ptab[j >> a.page_shift];
+  return min(max(pg, 0), a.n_pages - 1);
+}
 
 // One wave per query head of the KV group; 32-key tiles double-buffered in
 // LDS: the tile after next is loaded into registers while the current one is
 // computed, and the next one is moved from registers into the free buffer at
 // the end of the step, so one barrier per tile orders everything.
-template <typename T, int D, int NG>
+template <typename T, int D, int NG, bool PAGED>
 __global__ __launch_bounds__(kWave* NG) void hyb_sp_partial_kernel(
     SoftmaxPrefixArgs a, int chunk) {
   typedef SpCfg<T, D, NG> C;
@@ -75,10 +94,20 @@ __global__ __launch_bounds__(kWave* NG) void hyb_sp_partial_kernel(
     for (int ks = 0; ks < C::KD; ++ks)
       qop[ks] = li < L ? load_op<T>(qrow + ks * KW) : M::zero();
   }
-  const T* kc = (const T*)a.k_cache + ((size_t)b * Pmax * Hkv + g) * D;
-  const T* vc = (const T*)a.v_cache + ((size_t)b * Pmax * Hkv + g) * D;
+  // contiguous: this request's rows; paged: the pool, at KV head g
+  const T* kc = (const T*)a.k_cache + ((PAGED ? 0 : (size_t)b * Pmax * Hkv) + g) * D;
+  const T* vc = (const T*)a.v_cache + ((PAGED ? 0 : (size_t)b * Pmax * Hkv) + g) * D;
   const T* kbk = (const T*)a.k + ((size_t)b * L * Hkv + g) * D;
   const T* vbk = (const T*)a.v + ((size_t)b * L * Hkv + g) * D;
+  const int32_t* ptab = PAGED ? a.page_table + (size_t)b * a.max_pages : nullptr;
+  // row offset of cached token j (j < P)
+  auto crow = [&](int j) __attribute__((always_inline)) -> size_t {
+    if constexpr (PAGED)
+      return (((size_t)sp_page(a, ptab, j) << a.page_shift) + (j & ((1 << a.page_shift) - 1))) *
+             kstride;
+    else
+      return (size_t)j * kstride;
+  };
 
   // Tile loads: keys past the range read the range's last key (in bounds)
   // and are masked out of the scores below.
@@ -95,8 +124,9 @@ __global__ __launch_bounds__(kWave* NG) void hyb_sp_partial_kernel(
       if (idx < kTile * CPR) {  // (NG not a power of two: a partial last set)
         const int j = min(j0 + key, hi - 1);
         const size_t o = (size_t)part * EPC;
-        const T* ks = j < P ? kc + (size_t)j * kstride : kbk + (size_t)(j - P) * kstride;
-        const T* vs = j < P ? vc + (size_t)j * kstride : vbk + (size_t)(j - P) * kstride;
+        const size_t cr = j < P ? crow(j) : 0;
+        const T* ks = j < P ? kc + cr : kbk + (size_t)(j - P) * kstride;
+        const T* vs = j < P ? vc + cr : vbk + (size_t)(j - P) * kstride;
         r.k[c] = *reinterpret_cast<const uint4*>(ks + o);
         r.v[c] = *reinterpret_cast<const uint4*>(vs + o);
       }
@@ -259,7 +289,7 @@ struct alignas(16) SpSlot {
   bf16 v[kTile * D];
 };
 
-template <int D, int NG>
+template <int D, int NG, bool PAGED>
 __global__ __launch_bounds__(kWave* NG, 2) void hyb_sp_ring_kernel(SoftmaxPrefixArgs a, int chunk) {
   typedef Mma<bf16> M;
   typedef typename M::op_t op_t;
@@ -295,22 +325,47 @@ __global__ __launch_bounds__(kWave* NG, 2) void hyb_sp_ring_kernel(SoftmaxPrefix
 #pragma unroll
     for (int ks = 0; ks < KD; ++ks) qop[ks] = li < L ? load_op<bf16>(qrow + ks * KW) : M::zero();
   }
-  const bf16* kc = (const bf16*)a.k_cache + ((size_t)b * Pmax * Hkv + g) * D;
-  const bf16* vc = (const bf16*)a.v_cache + ((size_t)b * Pmax * Hkv + g) * D;
+  // contiguous: this request's rows; paged: the pool, at KV head g
+  const bf16* kc = (const bf16*)a.k_cache + ((PAGED ? 0 : (size_t)b * Pmax * Hkv) + g) * D;
+  const bf16* vc = (const bf16*)a.v_cache + ((PAGED ? 0 : (size_t)b * Pmax * Hkv) + g) * D;
   const bf16* kbk = (const bf16*)a.k + ((size_t)b * L * Hkv + g) * D;
   const bf16* vbk = (const bf16*)a.v + ((size_t)b * L * Hkv + g) * D;
+  // Paged: the pages of the cached keys of this range, lo .. min(hi, P) - 1,
+  // staged in LDS (page index p0 + e at e), clamped to the pool.
+  __shared__ int pages[PAGED ? kMaxRangePages : 1];
+  const int p0 = lo >> a.page_shift;
+  if constexpr (PAGED) {
+    const int32_t* ptab = a.page_table + (size_t)b * a.max_pages;
+    const int chi = min(hi, P);
+    const int np = chi > lo ? ((chi - 1) >> a.page_shift) - p0 + 1 : 0;
+    for (int e = tid; e < np; e += kWave * NG) pages[e] = sp_page(a, ptab, (p0 + e) << a.page_shift);
+    __syncthreads();
+  }
 
   // This wave's copies of tile n (keys past the range read the range's last
   // key, in bounds, and are masked below).
   auto issue = [&](int n, SpSlot<D>& sl) __attribute__((always_inline)) {
     const int j0 = lo + n * kTile;
+    const bf16* kcb = kc;
+    const bf16* vcb = vc;
+    if constexpr (PAGED) {
+      // the tile's rows (clamped to the range, all >= j0) lie in the page of
+      // row j0: that page's base, shifted so that base + j * kstride is row j
+      if (j0 < P) {
+        const int pi = j0 >> a.page_shift;
+        const ptrdiff_t sh = ((ptrdiff_t)pages[pi - p0] - pi) * ((ptrdiff_t)kstride << a.page_shift);
+        kcb += sh;
+        vcb += sh;
+      }
+    }
 #pragma unroll
     for (int u = 0; u < IPW; ++u) {
       const int ins = w * IPW + u, kv = ins / IK, i = ins % IK;
       const int t = i * RPI + lane / CPR, pos = lane % CPR;
       const int j = min(j0 + t, hi - 1);
-      const bf16* row = kv == 0 ? (j < P ? kc + (size_t)j * kstride : kbk + (size_t)(j - P) * kstride)
-                                : (j < P ? vc + (size_t)j * kstride : vbk + (size_t)(j - P) * kstride);
+      const bf16* cb = kv == 0 ? kcb : vcb;
+      const bf16* row = kv == 0 ? (j < P ? cb + (size_t)j * kstride : kbk + (size_t)(j - P) * kstride)
+                                : (j < P ? cb + (size_t)j * kstride : vbk + (size_t)(j - P) * kstride);
       bf16* dst = (kv == 0 ? sl.k : sl.v) + i * RPI * D;
       __builtin_amdgcn_global_load_lds(
           (const __attribute__((address_space(1))) void*)(row + (pos ^ RG::swz(t)) * EPC),
@@ -483,6 +538,10 @@ int softmax_prefix_splits(const Shape& s, int max_prefix) {
   long want = units > 0 ? (2048 + units - 1) / units : 1;
   const long cap = ((long)max_prefix + s.L + 511) / 512;
   if (want > cap) want = cap;
+  // no range longer than kMaxRange keys (the paged kernel stages a range's
+  // page numbers in LDS)
+  const long least = ((long)max_prefix + s.L + kMaxRange - 1) / kMaxRange;
+  if (want < least) want = least;
   if (want < 1) want = 1;
   return (int)want;
 }
@@ -494,7 +553,7 @@ size_t softmax_prefix_ws_bytes(const Shape& s, int n_split) {
   return (size_t)s.B * s.Hq * n_split * s.L * (s.D + 2) * sizeof(float);
 }
 
-template <typename T, int D>
+template <typename T, int D, bool PAGED>
 static hipError_t sp_go(const SoftmaxPrefixArgs& a, hipStream_t st) {
   const int ns = a.n_split;
   int chunk = (a.max_prefix + a.s.L + ns - 1) / ns;
@@ -505,16 +564,16 @@ static hipError_t sp_go(const SoftmaxPrefixArgs& a, hipStream_t st) {
   if constexpr (sizeof(T) == 2) {
     launched_ring = true;
     switch (G) {
-      case 1: hipLaunchKernelGGL((hyb_sp_ring_kernel<D, 1>), grid, dim3(kWave), 0, st, a, chunk); break;
-      case 2: hipLaunchKernelGGL((hyb_sp_ring_kernel<D, 2>), grid, dim3(kWave * 2), 0, st, a, chunk); break;
-      case 4: hipLaunchKernelGGL((hyb_sp_ring_kernel<D, 4>), grid, dim3(kWave * 4), 0, st, a, chunk); break;
-      case 8: hipLaunchKernelGGL((hyb_sp_ring_kernel<D, 8>), grid, dim3(kWave * 8), 0, st, a, chunk); break;
+      case 1: hipLaunchKernelGGL((hyb_sp_ring_kernel<D, 1, PAGED>), grid, dim3(kWave), 0, st, a, chunk); break;
+      case 2: hipLaunchKernelGGL((hyb_sp_ring_kernel<D, 2, PAGED>), grid, dim3(kWave * 2), 0, st, a, chunk); break;
+      case 4: hipLaunchKernelGGL((hyb_sp_ring_kernel<D, 4, PAGED>), grid, dim3(kWave * 4), 0, st, a, chunk); break;
+      case 8: hipLaunchKernelGGL((hyb_sp_ring_kernel<D, 8, PAGED>), grid, dim3(kWave * 8), 0, st, a, chunk); break;
       default: launched_ring = false;  // the register-staged kernel below
     }
   }
 #define HYB_SP_CASE(NG)                                                               \
   case NG:                                                                            \
-    hipLaunchKernelGGL((hyb_sp_partial_kernel<T, D, NG>), grid, dim3(kWave * NG), 0, st, a, \
+    hipLaunchKernelGGL((hyb_sp_partial_kernel<T, D, NG, PAGED>), grid, dim3(kWave * NG), 0, st, a, \
                        chunk);                                                        \
     break;
   if (!launched_ring) {
@@ -542,11 +601,20 @@ static hipError_t sp_go(const SoftmaxPrefixArgs& a, hipStream_t st) {
   return hipGetLastError();
 }
 
+template <bool PAGED>
+static hipError_t sp_dispatch(const SoftmaxPrefixArgs& a, hipStream_t st) {
+  if (a.s.dtype == 1)
+    return a.s.D == 64 ? sp_go<bf16, 64, PAGED>(a, st) : sp_go<bf16, 128, PAGED>(a, st);
+  return a.s.D == 64 ? sp_go<float, 64, PAGED>(a, st) : sp_go<float, 128, PAGED>(a, st);
+}
+
 hipError_t launch_softmax_prefix(const SoftmaxPrefixArgs& a, hipStream_t st) {
   if (a.s.Hq / a.s.Hkv > kMaxGroup) return hipErrorInvalidValue;
-  if (a.s.dtype == 1)
-    return a.s.D == 64 ? sp_go<bf16, 64>(a, st) : sp_go<bf16, 128>(a, st);
-  return a.s.D == 64 ? sp_go<float, 64>(a, st) : sp_go<float, 128>(a, st);
+  if (a.page_table) {
+    if (a.page_shift < 5 || a.n_pages < 1) return hipErrorInvalidValue;
+    return sp_dispatch<true>(a, st);
+  }
+  return sp_dispatch<false>(a, st);
 }
 
 }  // namespace hyb

@@ -278,3 +278,39 @@ def test_prefill_noalloc_rejects_beyond_scratch():
                                             p[7], None) == 1
     assert lib.hybrid_state_prefill_noalloc(ctypes.byref(_dims(batch=0)), T,
                                             *([None] * 10)) == 0
+
+
+def test_softmax_prefix_paged_validation():
+    lib = hb.load()
+    d = _dims(batch=2)
+    # q k v k_pages v_pages | page_table prefix_len out ws
+    p = [_addr(i) for i in range(9)]
+    need = lib.hybrid_workspace_bytes(ctypes.byref(d), hb.OP_SOFTMAX_PREFIX, 64 * 32)
+
+    def call(n_pages=10, ps=32, max_pages=64, ptrs=p, ws_bytes=None, dims=d):
+        return lib.softmax_prefix_step_paged(
+            ctypes.byref(dims), *ptrs[:5], n_pages, ps, ptrs[5], max_pages, ptrs[6], ptrs[7],
+            ptrs[8], need if ws_bytes is None else ws_bytes, None)
+
+    for ps in (0, 16, 48, 1 << 17):
+        assert call(ps=ps) == 5, ps
+        assert "page_size" in hb.last_error()
+    assert call(max_pages=-1) == 2
+    assert call(n_pages=0) == 2
+    for i in (0, 1, 2, 3, 4, 5, 6, 7):
+        q = list(p)
+        q[i] = None
+        assert call(ptrs=q) == 1, i
+        q[i] = MISALIGNED
+        assert call(ptrs=q) == 3, i
+    assert call(ws_bytes=need - 1) == 6
+    # out and the workspace against every input
+    for w_i in (7, 8):
+        for r_i in range(7):
+            q = list(p)
+            q[w_i] = q[r_i]
+            assert call(ptrs=q) == 2, (w_i, r_i)
+            assert "overlap" in hb.last_error()
+    assert call(dims=_dims(batch=0)) == 0
+    # the workspace is sized by max_pages * page_size
+    assert need == lib.hybrid_workspace_bytes(ctypes.byref(d), hb.OP_SOFTMAX_PREFIX, 2048)
