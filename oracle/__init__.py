@@ -56,7 +56,7 @@ def _load():
     lib.oracle_prefill.argtypes = [i] * 7 + [_dp] * 7 + [_ip, _dp]
     lib.oracle_softmax_prefix.argtypes = [i] * 6 + [_dp] * 5 + [_ip, _dp]
     lib.oracle_feature_map.argtypes = [i] * 3 + [_dp] * 3
-    lib.oracle_backward.argtypes = [i] * 7 + [_dp] * 10
+    lib.oracle_backward.argtypes = [i] * 7 + [_dp] * 13
     for fn in (lib.oracle_step, lib.oracle_commit, lib.oracle_prefill,
                lib.oracle_softmax_prefix, lib.oracle_feature_map, lib.oracle_backward):
         fn.restype = ctypes.c_int
@@ -199,15 +199,19 @@ def softmax_prefix(q, k, v, k_cache, v_cache, plen):
     return out
 
 
-def backward(q, k, v, Wt, alpha, L, dout=None, target=None):
+def backward(q, k, v, Wt, alpha, L, dout=None, target=None, inputs=False):
     """Gradient of the block-causal hybrid layer over a training sequence
     (empty starting state, blocks of L) with respect to W and alpha, the
-    parameters Stage 1 of Section 3.2 trains.
+    parameters Stage 1 of Section 3.2 trains, and (inputs=True) with respect
+    to the layer's inputs q, k, v, which end-to-end training through the
+    layer (Stage 2) needs.
 
     Exactly one of dout (upstream gradient, objective sum <dout, out>) and
     target (the softmax teacher's output; objective sum |out - target|^2,
     the attention-transfer loss) is given.  Returns (dWt [Hq][F][d],
-    dalpha [Hq], loss [Hq] or None); gradients are summed over the batch.
+    dalpha [Hq], loss [Hq] or None), then with inputs=True also (dq, dk, dv)
+    in the layouts of q, k, v; dW and dalpha are summed over the batch, dk
+    and dv over the query heads that share a KV head.
     """
     assert (dout is None) != (target is None)
     lib = _load()
@@ -230,10 +234,15 @@ def backward(q, k, v, Wt, alpha, L, dout=None, target=None):
     dW = np.zeros((Hq, F, d))
     da = np.zeros(Hq)
     loss = np.zeros(Hq) if target is not None else None
+    dq = np.zeros(q.shape) if inputs else None
+    dk = np.zeros(k.shape) if inputs else None
+    dv = np.zeros(v.shape) if inputs else None
+    ptr = lambda a: a.ctypes.data_as(_dp) if a is not None else None
     _check(lib.oracle_backward(B, T, Hq, Hkv, d, L, F, pq, pk, pv, pW, pa, pg, pt,
-                               dW.ctypes.data_as(_dp), da.ctypes.data_as(_dp),
-                               loss.ctypes.data_as(_dp) if loss is not None else None),
+                               ptr(dW), ptr(da), ptr(loss), ptr(dq), ptr(dk), ptr(dv)),
            "backward")
+    if inputs:
+        return dW, da, loss, dq, dk, dv
     return dW, da, loss
 
 

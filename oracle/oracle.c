@@ -293,13 +293,28 @@ int oracle_feature_map(int n, int d, int F, const double *X, const double *Wt,
  *   dL/dalpha = dL/dw * w (1 - w).
  * Outputs are sums over the batch: dWt [Hq][F][d] (same layout as Wt),
  * dalpha [Hq], loss [Hq] (may be NULL without a target).
+ *
+ * Gradients with respect to the layer's inputs q, k, v (what end-to-end
+ * training through the hybrid layers needs, Stage 2 of Section 3.2), written
+ * from the same definitions; a_ij = exp(s_ij), s_ij = q_i . k_j / sqrt(d) for
+ * i, j in one block:
+ *   softmax branch (d sm_num_i = w dL/dN_i, d sm_den_i = w dL/dD_i):
+ *     dL/da_ij = w (dL/dN_i . v_j + dL/dD_i),   dL/ds_ij = a_ij dL/da_ij
+ *     dL/dq_i += sum_j dL/ds_ij k_j / sqrt(d)
+ *     dL/dk_j += sum_i dL/ds_ij q_i / sqrt(d)
+ *     dL/dv_j += sum_i a_ij w dL/dN_i
+ *   feature maps: dL/dx += W_h dL/du (x = q_i or k_t, as above)
+ *   state: dL/dv_t += G_c^T phi(k_t)                           (t in block c)
+ * dq [B][T][Hq][d]; dk, dv [B][T][Hkv][d], each summed over the query heads
+ * that share the KV head (in head order).  Any of them may be NULL.
  * --------------------------------------------------------------------------- */
 
 /* dL/du of the feature map at x (phi already evaluated there), added into
- * dWt as x dL/du_j. */
+ * dWt as x dL/du_j, and (dx not NULL) into dx as W dL/du, i.e.
+ * dx_i += sum_j W[i][j] dL/du_j with W[i][j] = Wt[j][i]. */
 static void feature_map_backward(const double *x, const double *phi,
                                  const double *dphi, int d, int F,
-                                 double *dWt) {
+                                 const double *Wt, double *dWt, double *dx) {
   const double *p = phi, *n = phi + F, *dp = dphi, *dn = dphi + F;
   double sp = 0.0, sn = 0.0;
   for (int j = 0; j < F; ++j) {
@@ -309,6 +324,8 @@ static void feature_map_backward(const double *x, const double *phi,
   for (int j = 0; j < F; ++j) {
     const double du = p[j] * (dp[j] - sp) - n[j] * (dn[j] - sn);
     for (int i = 0; i < d; ++i) dWt[(size_t)j * d + i] += du * x[i];
+    if (dx)
+      for (int i = 0; i < d; ++i) dx[i] += Wt[(size_t)j * d + i] * du;
   }
 }
 
@@ -316,16 +333,21 @@ int oracle_backward(int B, int T, int Hq, int Hkv, int d, int L, int F,
                     const double *q, const double *k, const double *v,
                     const double *Wt, const double *alpha, const double *dout,
                     const double *target, double *dWt, double *dalpha,
-                    double *loss) {
+                    double *loss, double *dq, double *dk, double *dv) {
   const int G = Hq / Hkv, f = 2 * F;
   if (L <= 0 || T % L != 0) return 2;
   if ((dout == NULL) == (target == NULL)) return 2;
   const int nblk = T / L;
   const long units = (long)B * Hq;
+  const double rs = 1.0 / sqrt((double)d);
   /* per-unit results, summed over the batch in a fixed order afterwards */
   double *u_dW = (double *)calloc((size_t)units * F * d, sizeof(double));
   double *u_dw = (double *)calloc((size_t)units, sizeof(double));
   double *u_loss = (double *)calloc((size_t)units, sizeof(double));
+  /* per-unit dk, dv [units][T][d], summed over the heads of a group after */
+  double *u_dk = dk ? (double *)calloc((size_t)units * T * d, sizeof(double)) : NULL;
+  double *u_dv = dv ? (double *)calloc((size_t)units * T * d, sizeof(double)) : NULL;
+  if (dq) memset(dq, 0, sizeof(double) * (size_t)B * T * Hq * d);
   int err = 0;
 #pragma omp parallel for schedule(dynamic) reduction(| : err)
   for (long u = 0; u < units; ++u) {
@@ -344,6 +366,8 @@ int oracle_backward(int B, int T, int Hq, int Hkv, int d, int L, int F,
     double *sm_num = (double *)malloc(sizeof(double) * d);
     double *o = (double *)malloc(sizeof(double) * d);
     double *gi = (double *)malloc(sizeof(double) * d);
+    double *dku = u_dk ? u_dk + (size_t)u * T * d : NULL;
+    double *dvu = u_dv ? u_dv + (size_t)u * T * d : NULL;
     double dw = 0.0, ls = 0.0;
     for (int c = 0; c < nblk && !err; ++c) {
       const size_t t0 = (size_t)c * L;
@@ -397,7 +421,30 @@ int oracle_backward(int B, int T, int Hq, int Hkv, int d, int L, int F,
           for (int cc = 0; cc < d; ++cc) s += S[(size_t)r * d + cc] * dNi[cc];
           dphi[r] = s;
         }
-        feature_map_backward(qi, ph, dphi, d, F, dWu);
+        double *dqi = dq ? dq + qo : NULL;
+        feature_map_backward(qi, ph, dphi, d, F, Wh, dWu, dqi);
+        /* the block softmax branch: scores against every key of the block */
+        if (dq || dku || dvu) {
+          for (int j = 0; j < L; ++j) {
+            const size_t ko = (((size_t)b * T + t0 + j) * Hkv + g) * d;
+            double s = 0.0;
+            for (int x = 0; x < d; ++x) s += qi[x] * k[ko + x];
+            const double a = exp(s * rs);
+            double da = dDi;
+            for (int cc = 0; cc < d; ++cc) da += dNi[cc] * v[ko + cc];
+            const double ds = a * w * da;
+            if (dqi)
+              for (int x = 0; x < d; ++x) dqi[x] += ds * k[ko + x] * rs;
+            if (dku) {
+              double *dkj = dku + (size_t)(t0 + j) * d;
+              for (int x = 0; x < d; ++x) dkj[x] += ds * qi[x] * rs;
+            }
+            if (dvu) {
+              double *dvj = dvu + (size_t)(t0 + j) * d;
+              for (int cc = 0; cc < d; ++cc) dvj[cc] += a * w * dNi[cc];
+            }
+          }
+        }
       }
       for (int t = 0; t < L; ++t) {
         const size_t ko = (((size_t)b * T + t0 + t) * Hkv + g) * d;
@@ -418,7 +465,17 @@ int oracle_backward(int B, int T, int Hq, int Hkv, int d, int L, int F,
           for (int cc = 0; cc < d; ++cc) s += Gs[(size_t)r * d + cc] * v[ko + cc];
           dphi[r] = s;
         }
-        feature_map_backward(k + ko, phi, dphi, d, F, dWu);
+        feature_map_backward(k + ko, phi, dphi, d, F, Wh,
+                             dWu, dku ? dku + (size_t)(t0 + t) * d : NULL);
+        if (dvu) {
+          /* the state read by the later blocks: G_c^T phi(k_t) */
+          double *dvt = dvu + (size_t)(t0 + t) * d;
+          for (int cc = 0; cc < d; ++cc) {
+            double s = 0.0;
+            for (int r = 0; r < f; ++r) s += Gs[(size_t)r * d + cc] * phi[r];
+            dvt[cc] += s;
+          }
+        }
       }
       for (int i = 0; i < L; ++i) {
         const double *ph = phiq + (size_t)(t0 + i) * f;
@@ -446,6 +503,22 @@ int oracle_backward(int B, int T, int Hq, int Hkv, int d, int L, int F,
       if (loss) loss[h] += u_loss[u];
     }
   }
-  free(u_dW); free(u_dw); free(u_loss);
+  /* dk, dv: sum over the G query heads of each KV head, in head order */
+  for (int pass = 0; pass < 2; ++pass) {
+    double *dst = pass == 0 ? dk : dv;
+    const double *src = pass == 0 ? u_dk : u_dv;
+    if (!dst) continue;
+    for (int b = 0; b < B; ++b)
+      for (int t = 0; t < T; ++t)
+        for (int g = 0; g < Hkv; ++g) {
+          double *o = dst + (((size_t)b * T + t) * Hkv + g) * d;
+          for (int x = 0; x < d; ++x) o[x] = 0.0;
+          for (int h = g * G; h < (g + 1) * G; ++h) {
+            const double *p = src + (((size_t)b * Hq + h) * T + t) * d;
+            for (int x = 0; x < d; ++x) o[x] += p[x];
+          }
+        }
+  }
+  free(u_dW); free(u_dw); free(u_loss); free(u_dk); free(u_dv);
   return err;
 }

@@ -182,3 +182,87 @@ def test_backward_rejects_bad_arguments():
         oracle.backward(q, k, v, Wt, alpha, L)
     with pytest.raises(ValueError):
         oracle.backward(q, k, v, Wt, alpha, 5, dout=g)
+
+
+# ---------------------------------------------------------------------------
+# Gradients with respect to the inputs q, k, v (end-to-end training through
+# the hybrid layers, Stage 2 of Section 3.2).
+# ---------------------------------------------------------------------------
+
+
+def test_input_gradients_match_finite_differences():
+    """Central differences of the oracle's forward for every entry of q, k
+    and v; two query heads share one KV head, so dk and dv sum over them."""
+    q, k, v, Wt, alpha, g, L = _case(B=1, T=12, Hq=2, Hkv=1, d=6, F=4, L=4, seed=11)
+    _, _, _, dq, dk, dv = oracle.backward(q, k, v, Wt, alpha, L, dout=g, inputs=True)
+    eps = 1e-6
+    obj = lambda q_, k_, v_: float((_forward(q_, k_, v_, Wt, alpha, L) * g).sum())
+    for name, x, grad in (("q", q, dq), ("k", k, dk), ("v", v, dv)):
+        fd = np.zeros_like(x)
+        for idx in np.ndindex(*x.shape):
+            xp, xm = x.copy(), x.copy()
+            xp[idx] += eps
+            xm[idx] -= eps
+            args_p = {"q": q, "k": k, "v": v}
+            args_m = dict(args_p)
+            args_p[name], args_m[name] = xp, xm
+            fd[idx] = (obj(**{n + "_": a for n, a in args_p.items()}) -
+                       obj(**{n + "_": a for n, a in args_m.items()})) / (2 * eps)
+        scale = np.abs(fd).max()
+        assert scale > 1e-2, name
+        np.testing.assert_allclose(grad, fd, rtol=0, atol=1e-7 * max(1.0, scale), err_msg=name)
+
+
+@pytest.mark.parametrize("seed,Hq,Hkv", [(12, 2, 1), (13, 4, 2)])
+def test_input_gradients_match_autograd_of_dense_form(seed, Hq, Hkv):
+    q, k, v, Wt, alpha, g, L = _case(B=2, T=16, Hq=Hq, Hkv=Hkv, d=8, F=4, L=4, seed=seed)
+    for mode in ("dout", "target"):
+        tq = [torch.tensor(x, requires_grad=True) for x in (q, k, v)]
+        out = _dense_torch(*tq, torch.tensor(Wt), torch.tensor(alpha), L)
+        if mode == "dout":
+            obj = (out * torch.tensor(g)).sum()
+            res = oracle.backward(q, k, v, Wt, alpha, L, dout=g, inputs=True)
+        else:
+            tgt = g * 0.3
+            obj = ((out - torch.tensor(tgt)) ** 2).sum()
+            res = oracle.backward(q, k, v, Wt, alpha, L, target=tgt, inputs=True)
+        obj.backward()
+        for got, t in zip(res[3:], tq):
+            np.testing.assert_allclose(got, t.grad.numpy(), rtol=0, atol=1e-10)
+
+
+def test_single_block_input_gradients_are_softmax_attention_gradients():
+    """T = L: the layer is plain bidirectional softmax attention over the
+    block (the state is empty), so its input gradients are those of torch's
+    scaled_dot_product_attention, with each KV head repeated for its query
+    heads."""
+    q, k, v, Wt, alpha, g, L = _case(B=2, T=8, Hq=4, Hkv=2, d=8, F=4, L=8, seed=14)
+    _, _, _, dq, dk, dv = oracle.backward(q, k, v, Wt, alpha, L, dout=g, inputs=True)
+    tq, tk, tv = (torch.tensor(x, requires_grad=True) for x in (q, k, v))
+    G = q.shape[2] // k.shape[2]
+    out = torch.nn.functional.scaled_dot_product_attention(
+        tq.transpose(1, 2), tk.repeat_interleave(G, 2).transpose(1, 2),
+        tv.repeat_interleave(G, 2).transpose(1, 2)).transpose(1, 2)
+    (out * torch.tensor(g)).sum().backward()
+    np.testing.assert_allclose(dq, tq.grad.numpy(), rtol=0, atol=1e-12)
+    np.testing.assert_allclose(dk, tk.grad.numpy(), rtol=0, atol=1e-12)
+    np.testing.assert_allclose(dv, tv.grad.numpy(), rtol=0, atol=1e-12)
+
+
+def test_input_gradient_invariants():
+    """Every output is a convex combination of values, so with v_t = v for
+    all t the output is v whatever q and k are (dq = dk = 0); and with a
+    constant upstream gradient c, the value gradients of a KV head sum to
+    (queries reading it) x c."""
+    q, k, v, Wt, alpha, g, L = _case(B=2, T=12, Hq=4, Hkv=2, seed=15)
+    ve = v.copy()
+    ve[:] = ve[:, :1]
+    _, _, _, dq, dk, _ = oracle.backward(q, k, ve, Wt, alpha, L, dout=g, inputs=True)
+    assert np.abs(dq).max() < 1e-12 and np.abs(dk).max() < 1e-12
+    c = np.random.default_rng(16).normal(size=q.shape[3])
+    gc = np.broadcast_to(c, g.shape).copy()
+    _, _, _, _, _, dv = oracle.backward(q, k, v, Wt, alpha, L, dout=gc, inputs=True)
+    B, T, Hq, d = q.shape
+    G = Hq // k.shape[2]
+    np.testing.assert_allclose(dv.sum(axis=1), np.broadcast_to(T * G * c, dv.sum(axis=1).shape),
+                               atol=1e-10)
