@@ -422,7 +422,14 @@ def bench_backward(gen, dev):
     ms = time_region(once, 5)
     fl = backward_flops(B, T, Hq, d, L, f)
     byts = (q.numel() + k.numel() + v.numel() + tgt.numel()) * 2
-    log(f"backward train8 {ms:.3f} ms")
+    # the same gradient plus dq, dk, dv (hybrid_attn_backward_full)
+    wsf = torch.empty(hb.workspace_bytes(hb.make_dims(B, Hq, Hkv, d, L, f, hb.HYB_BF16, 1),
+                                         hb.OP_BACKWARD_FULL, T), dtype=torch.uint8, device=dev)
+    full = lambda: hb.hybrid_attn_backward_full(q, k, v, W, al, L, target=tgt, ws=wsf)
+    full()
+    ms_full = time_region(full, 5)
+    del wsf
+    log(f"backward train8 {ms:.3f} ms (with dq, dk, dv: {ms_full:.3f} ms)")
     return {"workload": "train8: attention transfer of one layer, B=8 x 2048 tokens, 16q/4kv, "
                         "d=128, f=128, blocks of 32, bf16, teacher-output target",
             "ms": ms, "training_tokens_per_s": B * T / (ms * 1e-3),
@@ -430,7 +437,9 @@ def bench_backward(gen, dev):
             "mfma_frac": fl / (ms * 1e-3) / 1e12 / BF16_MFMA_PEAK_TFLOPS,
             "flops_per_call": fl, "input_bytes": byts,
             "gbps_inputs": byts / (ms * 1e-3) / 1e9,
-            "ws_bytes": ws.numel()}
+            "ws_bytes": ws.numel(),
+            "full_ms": ms_full,
+            "full_note": "hybrid_attn_backward_full: dW, dalpha, the loss and dq, dk, dv"}
 
 
 def bench_prefill(gen, dev):

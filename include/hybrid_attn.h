@@ -99,7 +99,8 @@ typedef enum {
   HYB_OP_COMMIT = 1,
   HYB_OP_PREFILL = 2,
   HYB_OP_SOFTMAX_PREFIX = 3,
-  HYB_OP_BACKWARD = 4
+  HYB_OP_BACKWARD = 4,
+  HYB_OP_BACKWARD_FULL = 5
 } hyb_op_t;
 
 typedef struct {
@@ -258,9 +259,29 @@ int hybrid_attn_backward(const hyb_dims_t* dims, int32_t seq_len,
                          const void* target, float* dW, float* dalpha,
                          float* loss, void* ws, size_t ws_bytes, void* stream);
 
+/* hybrid_attn_backward that also returns the gradients with respect to the
+ * layer's inputs q, k and v, which end-to-end training through the hybrid
+ * layers needs (Stage 2 of Section 3.2 adapts the attention projections
+ * around them).  Arguments and the objective as for hybrid_attn_backward;
+ * dq [B][T][Hq][d], dk and dv [B][T][Hkv][d] are fp32 whatever dims->dtype
+ * is (dk and dv sum over the query heads that share each KV head), all
+ * three required and overwritten.  ws/ws_bytes: at least
+ * hybrid_workspace_bytes(dims, HYB_OP_BACKWARD_FULL, seq_len) bytes.  No
+ * output may overlap another output, an input or the workspace.  The
+ * in-block softmax weights are formed as exp(log w + q.k/sqrt(d)), so the
+ * scaled scores must stay well below 80 (the W, alpha gradients share this
+ * range through 1/D).  Deterministic. */
+int hybrid_attn_backward_full(const hyb_dims_t* dims, int32_t seq_len,
+                              const void* q, const void* k, const void* v,
+                              const void* W, const float* alpha,
+                              const void* dout, const void* target, float* dq,
+                              float* dk, float* dv, float* dW, float* dalpha,
+                              float* loss, void* ws, size_t ws_bytes,
+                              void* stream);
+
 /* Workspace bytes the given op needs for these dims; `extent` is seq_len for
- * HYB_OP_PREFILL and HYB_OP_BACKWARD, max_prefix for HYB_OP_SOFTMAX_PREFIX,
- * ignored otherwise.  Returns 0 for invalid dims. */
+ * HYB_OP_PREFILL, HYB_OP_BACKWARD and HYB_OP_BACKWARD_FULL, max_prefix for
+ * HYB_OP_SOFTMAX_PREFIX, ignored otherwise.  Returns 0 for invalid dims. */
 size_t hybrid_workspace_bytes(const hyb_dims_t* dims, int32_t op,
                               int32_t extent);
 

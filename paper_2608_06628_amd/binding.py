@@ -18,14 +18,15 @@ LIB_PATH = os.path.join(_PKG, "libhybattn.so")
 
 HYB_F32, HYB_BF16 = 0, 1
 HYB_OUT_F32 = 1
-OP_STEP, OP_COMMIT, OP_PREFILL, OP_SOFTMAX_PREFIX, OP_BACKWARD = 0, 1, 2, 3, 4
+OP_STEP, OP_COMMIT, OP_PREFILL, OP_SOFTMAX_PREFIX, OP_BACKWARD, OP_BACKWARD_FULL = 0, 1, 2, 3, 4, 5
 STATUS = {0: "HYB_OK", 1: "HYB_ENULL", 2: "HYB_EINVAL", 3: "HYB_EALIGN",
           4: "HYB_EDTYPE", 5: "HYB_EUNSUPPORTED", 6: "HYB_EWORKSPACE",
           7: "HYB_ELAUNCH"}
 EXPORTS = ("hybrid_attn_step", "hybrid_attn_step_commit", "hybrid_state_commit",
            "hybrid_state_prefill", "hybrid_state_prefill_noalloc", "softmax_prefix_step",
            "softmax_prefix_step_paged",
-           "hybrid_attn_backward", "hybrid_workspace_bytes", "hybrid_last_error")
+           "hybrid_attn_backward", "hybrid_attn_backward_full", "hybrid_workspace_bytes",
+           "hybrid_last_error")
 NOALLOC_SCRATCH_BYTES = 64 << 20
 
 
@@ -65,11 +66,13 @@ def load():
     lib.softmax_prefix_step_paged.argtypes = [P] + [vp] * 5 + [i32, i32, vp, i32, vp, vp, vp,
                                                                 sz, vp]
     lib.hybrid_attn_backward.argtypes = [P, i32] + [vp] * 11 + [sz, vp]
+    lib.hybrid_attn_backward_full.argtypes = [P, i32] + [vp] * 14 + [sz, vp]
     lib.hybrid_workspace_bytes.argtypes = [P, i32, i32]
     lib.hybrid_workspace_bytes.restype = sz
     lib.hybrid_last_error.argtypes = []
     lib.hybrid_last_error.restype = ctypes.c_char_p
     for n in ("hybrid_attn_step", "hybrid_attn_step_commit", "hybrid_state_commit", "hybrid_state_prefill",
+              "hybrid_attn_backward", "hybrid_attn_backward_full",
               "hybrid_state_prefill_noalloc", "softmax_prefix_step", "softmax_prefix_step_paged"):
         getattr(lib, n).restype = ctypes.c_int
     _lib = lib
@@ -320,3 +323,36 @@ def hybrid_attn_backward(q, k, v, W, alpha, block, dout=None, target=None, dW=No
         _ptr(ws, "ws") if ws is not None else None,
         ws.numel() * ws.element_size() if ws is not None else 0, _stream(stream)))
     return dW, dalpha, loss
+
+
+def hybrid_attn_backward_full(q, k, v, W, alpha, block, dout=None, target=None, ws=None,
+                              stream=None):
+    """hybrid_attn_backward plus the gradients with respect to the inputs.
+    Returns (dq fp32 [B][T][Hq][d], dk, dv fp32 [B][T][Hkv][d], dW, dalpha,
+    loss or None)."""
+    lib = load()
+    B, T, Hq, d = q.shape
+    Hkv = k.shape[2]
+    F = W.shape[1]
+    act = q.dtype
+    dims = make_dims(B, Hq, Hkv, d, block, 2 * F, _dt(q), 1, 0)
+    dev = q.device
+    f32 = torch.float32
+    dq = torch.empty((B, T, Hq, d), dtype=f32, device=dev)
+    dk = torch.empty((B, T, Hkv, d), dtype=f32, device=dev)
+    dv = torch.empty((B, T, Hkv, d), dtype=f32, device=dev)
+    dW = torch.empty((Hq, F, d), dtype=f32, device=dev)
+    dalpha = torch.empty(Hq, dtype=f32, device=dev)
+    loss = torch.empty(Hq, dtype=f32, device=dev) if target is not None else None
+    need = workspace_bytes(dims, OP_BACKWARD_FULL, T)
+    if ws is None and need:
+        ws = torch.empty(need, dtype=torch.uint8, device=dev)
+    _check(lib.hybrid_attn_backward_full(
+        ctypes.byref(dims), T, _ptr(q, "q"), _ptr(k, "k", act), _ptr(v, "v", act),
+        _ptr(W, "W", act), _ptr(alpha, "alpha", f32),
+        _ptr(dout, "dout", act), _ptr(target, "target", act),
+        _ptr(dq, "dq", f32), _ptr(dk, "dk", f32), _ptr(dv, "dv", f32),
+        _ptr(dW, "dW", f32), _ptr(dalpha, "dalpha", f32), _ptr(loss, "loss", f32),
+        _ptr(ws, "ws") if ws is not None else None,
+        ws.numel() * ws.element_size() if ws is not None else 0, _stream(stream)))
+    return dq, dk, dv, dW, dalpha, loss

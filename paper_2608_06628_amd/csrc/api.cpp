@@ -407,11 +407,18 @@ int softmax_prefix_step_paged(const hyb_dims_t* dims, const void* q,
                              out, ws, ws_bytes, stream);
 }
 
-int hybrid_attn_backward(const hyb_dims_t* dims, int32_t seq_len,
-                         const void* q, const void* k, const void* v,
-                         const void* W, const float* alpha, const void* dout,
-                         const void* target, float* dW, float* dalpha,
-                         float* loss, void* ws, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Validation and dispatch of the backward; dq, dk, dv all null (the Stage-1
+// gradient only) or all set (the input gradients as well).
+int backward_impl(const hyb_dims_t* dims, int32_t seq_len, const void* q,
+                  const void* k, const void* v, const void* W,
+                  const float* alpha, const void* dout, const void* target,
+                  float* dq, float* dk, float* dv, bool inputs, float* dW,
+                  float* dalpha, float* loss, void* ws, size_t ws_bytes,
+                  void* stream) {
   hyb::Shape s;
   TRY(check_dims(dims, false, &s));
   if (dims->flags != 0) return fail(HYB_EINVAL, "flags must be 0 for the backward");
@@ -432,10 +439,16 @@ int hybrid_attn_backward(const hyb_dims_t* dims, int32_t seq_len,
   if ((dout == nullptr) == (target == nullptr))
     return fail(HYB_EINVAL, "exactly one of dout and target must be given");
   if (dout && loss) return fail(HYB_EINVAL, "loss needs a target");
+  if (inputs) {
+    TRY(check_ptr(dq, "dq"));
+    TRY(check_ptr(dk, "dk"));
+    TRY(check_ptr(dv, "dv"));
+  }
   TRY(check_ptr(dW, "dW"));
   TRY(check_ptr(dalpha, "dalpha"));
   TRY(check_ptr(loss, "loss", false));
-  const size_t need = hybrid_workspace_bytes(dims, HYB_OP_BACKWARD, seq_len);
+  const size_t need = hybrid_workspace_bytes(
+      dims, inputs ? HYB_OP_BACKWARD_FULL : HYB_OP_BACKWARD, seq_len);
   if (!ws || ws_bytes < need)
     return fail(HYB_EWORKSPACE, "backward needs %zu workspace bytes, got %zu",
                 need, ws ? ws_bytes : (size_t)0);
@@ -444,19 +457,24 @@ int hybrid_attn_backward(const hyb_dims_t* dims, int32_t seq_len,
   const size_t nq = (size_t)s.B * seq_len * s.Hq * s.D * es;
   const size_t nkv = (size_t)s.B * seq_len * s.Hkv * s.D * es;
   const size_t nW = (size_t)s.Hq * s.F * s.D * es;
+  const size_t nq4 = (size_t)s.B * seq_len * s.Hq * s.D * 4;
+  const size_t nkv4 = (size_t)s.B * seq_len * s.Hkv * s.D * 4;
   struct Buf {
     const void* p;
     size_t n;
   };
-  const Buf written[4] = {{dW, (size_t)s.Hq * s.F * s.D * 4},
+  const Buf written[7] = {{dW, (size_t)s.Hq * s.F * s.D * 4},
                           {dalpha, (size_t)s.Hq * 4},
                           {loss, (size_t)s.Hq * 4},
-                          {ws, need}};
+                          {ws, need},
+                          {dq, nq4},
+                          {dk, nkv4},
+                          {dv, nkv4}};
   const Buf read_only[6] = {{q, nq},  {k, nkv}, {v, nkv}, {W, nW},
                             {alpha, (size_t)s.Hq * 4},
                             {dout ? dout : target, nq}};
-  for (int i = 0; i < 4; ++i) {
-    for (int j = i + 1; j < 4; ++j)
+  for (int i = 0; i < 7; ++i) {
+    for (int j = i + 1; j < 7; ++j)
       if (overlap(written[i].p, written[i].n, written[j].p, written[j].n))
         return fail(HYB_EINVAL, "outputs or the workspace overlap each other");
     for (int j = 0; j < 6; ++j)
@@ -465,8 +483,38 @@ int hybrid_attn_backward(const hyb_dims_t* dims, int32_t seq_len,
   }
   hyb::BackwardArgs a{s, seq_len, q, k, v, W, alpha, dout, target,
                       dW, dalpha, loss, ws};
+  if (inputs) {
+    a.dq = dq;
+    a.dk = dk;
+    a.dv = dv;
+  }
   (void)hipGetLastError();
   return launched(hyb::launch_backward(a, (hipStream_t)stream), "backward");
+}
+
+}  // namespace
+
+extern "C" {
+
+int hybrid_attn_backward(const hyb_dims_t* dims, int32_t seq_len,
+                         const void* q, const void* k, const void* v,
+                         const void* W, const float* alpha, const void* dout,
+                         const void* target, float* dW, float* dalpha,
+                         float* loss, void* ws, size_t ws_bytes, void* stream) {
+  return backward_impl(dims, seq_len, q, k, v, W, alpha, dout, target, nullptr,
+                       nullptr, nullptr, false, dW, dalpha, loss, ws, ws_bytes,
+                       stream);
+}
+
+int hybrid_attn_backward_full(const hyb_dims_t* dims, int32_t seq_len,
+                              const void* q, const void* k, const void* v,
+                              const void* W, const float* alpha,
+                              const void* dout, const void* target, float* dq,
+                              float* dk, float* dv, float* dW, float* dalpha,
+                              float* loss, void* ws, size_t ws_bytes,
+                              void* stream) {
+  return backward_impl(dims, seq_len, q, k, v, W, alpha, dout, target, dq, dk,
+                       dv, true, dW, dalpha, loss, ws, ws_bytes, stream);
 }
 
 size_t hybrid_workspace_bytes(const hyb_dims_t* dims, int32_t op,
@@ -487,8 +535,9 @@ size_t hybrid_workspace_bytes(const hyb_dims_t* dims, int32_t op,
       return hyb::softmax_prefix_ws_bytes(
           s, hyb::softmax_prefix_splits(s, extent));
     case HYB_OP_BACKWARD:
+    case HYB_OP_BACKWARD_FULL:
       if (extent == 0 || extent % s.L != 0 || !hyb::backward_supported(s)) return 0;
-      return hyb::backward_ws_bytes(s, extent);
+      return hyb::backward_ws_bytes(s, extent, op == HYB_OP_BACKWARD_FULL);
   }
   return 0;
 }

@@ -36,6 +36,8 @@
 //      fixed order (bitwise reproducible, no atomics).
 // On the bf16 path phi(K), phi(Q) (as an update operand) and dL/du enter the
 // matrix products as bf16 pairs hi + lo; the state, Gbar and dL/dN as bf16.
+#include <type_traits>
+
 #include "device.h"
 #include "featmap.h"
 #include "launch.h"
@@ -88,13 +90,17 @@ struct BwdCfg {
 //   dL/dD          gd  [units][nblk][32]
 //   partial dW     dwq, dwk [units][nseg][F][D]
 //   partial scalars red [units][nseg][2]  (dL/dalpha, loss)
+// and, when the input gradients are formed:
+//   dL/du of the queries   duq [units][T][F]
+//   dL/du of the keys      duk [units][T][F]
+//   Gbar_c^T phi(k_t)       dvl [units][T][D]  (the state part of dL/dv_t)
 struct BwdLayout {
-  size_t dS, dG, dgz, gnT, gd, dwq, dwk, red, total;
+  size_t dS, dG, dgz, gnT, gd, dwq, dwk, red, duq, duk, dvl, total;
 };
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-static BwdLayout bwd_layout(const Shape& s, int T) {
+static BwdLayout bwd_layout(const Shape& s, int T, bool inputs) {
   const size_t units = (size_t)s.B * s.Hq, f = 2 * (size_t)s.F;
   const int nseg = prefill_segments(s, T), nblk = T / s.L;
   BwdLayout l;
@@ -115,16 +121,41 @@ static BwdLayout bwd_layout(const Shape& s, int T) {
   o = align256(o + units * nseg * s.F * s.D * 4);
   l.red = o;
   o = align256(o + units * nseg * 2 * 4);
+  l.duq = l.duk = l.dvl = o;
+  if (inputs) {
+    l.duq = o;
+    o = align256(o + units * T * s.F * 4);
+    l.duk = o;
+    o = align256(o + units * T * s.F * 4);
+    l.dvl = o;
+    o = align256(o + units * T * s.D * 4);
+  }
   l.total = o;
   return l;
 }
 
-size_t backward_ws_bytes(const Shape& s, int T) { return bwd_layout(s, T).total; }
+size_t backward_ws_bytes(const Shape& s, int T, bool inputs) {
+  return bwd_layout(s, T, inputs).total;
+}
 
 struct BwdKArgs {
   BackwardArgs a;
   int nseg, seg_blocks, nblk;
   float *dS, *dz, *dG, *dgz, *gd, *dwq, *dwk, *red, *gnT;
+  float *duq, *duk, *dvl;  // input-gradient intermediates (null otherwise)
+};
+
+// LDS of the reverse walk's extra work when the input gradients are formed:
+// Gbar^T of the blocks after this one and phi(K), as operands.
+template <typename T, int D, int F>
+struct RevInSmem {
+  static constexpr int NPART = sizeof(T) == 2 ? 2 : 1;
+  static constexpr int PAD = 16 / (int)sizeof(T);
+  T gT[NPART][D][2 * F + PAD];      // Gbar^T[c][r]
+  T phiK[NPART][kTile][2 * F + PAD];  // phi(k_t)[r] at [t][r]
+};
+struct NoSmem {
+  char unused;
 };
 
 // Accumulator registers ks*E .. ks*E+E-1 of a tile as a T operand (the tile's
@@ -219,7 +250,7 @@ __device__ inline float wave_sum(float x) {
 // ---------------------------------------------------------------------------
 // 2. Forward walk.
 // ---------------------------------------------------------------------------
-template <typename T, int D, int F>
+template <typename T, int D, int F, bool IN>
 __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_fwd_kernel(BwdKArgs ka) {
   typedef BwdCfg<T, D, F> C;
   typedef typename C::M M;
@@ -515,6 +546,24 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_fwd_kernel(BwdKArgs
     for (int ks = 0; ks < C::KL; ++ks)
       qtop[ks] = load_rows_op<T>(qb + col, qstride, ks, hh, L, false);
     lds_barrier();
+    if constexpr (IN) {
+      // dL/du of the block's queries, both signs summed, for dL/dq = W dL/du
+      float* dst = ka.duq + ((size_t)u * T_ + t0) * F;
+      for (int it = tid; it < L * (F / 4); it += blockDim.x) {
+        const int t = it / (F / 4), j4 = (it % (F / 4)) * 4;
+        f32x4 x;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          float acc = 0.0f;
+#pragma unroll
+          for (int sg = 0; sg < 2; ++sg)
+#pragma unroll
+            for (int part = 0; part < C::NPART; ++part) acc += to_f32(sh.duT[sg][part][j4 + e][t]);
+          x[e] = acc;
+        }
+        *reinterpret_cast<f32x4*>(dst + (size_t)t * F + j4) = x;
+      }
+    }
     // dW^T tiles (rows j of tile t, columns 32w..): += dL/du^T Q.
 #pragma unroll
     for (int t = 0; t < NT; ++t)
@@ -1127,7 +1176,7 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
 // ---------------------------------------------------------------------------
 // 3./4. Reverse walk (delta: only the segment's Gbar sum).
 // ---------------------------------------------------------------------------
-template <typename T, int D, int F>
+template <typename T, int D, int F, bool IN>
 __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_rev_kernel(BwdKArgs ka, int delta) {
   typedef BwdCfg<T, D, F> C;
   typedef typename C::M M;
@@ -1136,6 +1185,7 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_rev_kernel(BwdKArgs
   constexpr int f = C::f, E = M::E, KW = M::KW, NW = C::NW, RPW = C::RPW;
   constexpr int NT = C::NT, NRT = C::NRT;
   __shared__ typename C::SmemB sh;
+  __shared__ typename std::conditional<IN, RevInSmem<T, D, F>, NoSmem>::type shi;
   const BackwardArgs& a = ka.a;
 
   const int tid = threadIdx.x, lane = tid & (kWave - 1);
@@ -1265,8 +1315,57 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_rev_kernel(BwdKArgs
         js += xor32(js);
         if (hh == 0) sh.jsum[p][li] = js;
       }
+      if constexpr (IN) {
+        // Gbar^T (before this block's queries join it) and phi(K) to LDS as
+        // operand pairs, for dL/dv_t += Gbar^T phi(k_t) below
+#pragma unroll
+        for (int j = 0; j < RPW; ++j) {
+          const int p = w + j * NW;
+          if (p >= NRT) continue;
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            const int r = p * kTile + row_of(i, hh);
+            const float x = row_ok ? vk[j][i] : 0.0f;
+            const T xh = from_f32<T>(x);
+            shi.phiK[0][li][r] = xh;
+            if constexpr (C::NPART == 2) shi.phiK[1][li][r] = from_f32<T>(x - to_f32(xh));
+#pragma unroll
+            for (int s = 0; s < NW; ++s) {
+              const float gv = gacc[j][s][i];
+              const T gh = from_f32<T>(gv);
+              shi.gT[0][s * kTile + row_of(i, hh)][p * kTile + li] = gh;
+              if constexpr (C::NPART == 2)
+                shi.gT[1][s * kTile + row_of(i, hh)][p * kTile + li] = from_f32<T>(gv - to_f32(gh));
+            }
+          }
+        }
+      }
     }
     lds_barrier();
+    if constexpr (IN) {
+      if (!delta) {
+        // dL/dv_t (state part) = Gbar^T phi(k_t): rows c of slice w,
+        // columns t; both operands as hi + lo pairs on the bf16 path
+        f32x16 dvacc = {};
+#pragma unroll
+        for (int ks = 0; ks < f / KW; ++ks) {
+          const op_t ah = load_op<T>(&shi.gT[0][w * kTile + li][ks * KW + hh * E]);
+          const op_t bh = load_op<T>(&shi.phiK[0][li][ks * KW + hh * E]);
+          dvacc = M::mma(ah, bh, dvacc);
+          if constexpr (C::NPART == 2) {
+            dvacc = M::mma(load_op<T>(&shi.gT[1][w * kTile + li][ks * KW + hh * E]), bh, dvacc);
+            dvacc = M::mma(ah, load_op<T>(&shi.phiK[1][li][ks * KW + hh * E]), dvacc);
+          }
+        }
+        if (row_ok) {
+          float* dst = ka.dvl + ((size_t)u * T_ + t0 + li) * D + w * kTile;
+#pragma unroll
+          for (int i = 0; i < 16; i += 4)
+            *reinterpret_cast<f32x4*>(dst + row_of(i, hh)) =
+                f32x4{dvacc[i], dvacc[i + 1], dvacc[i + 2], dvacc[i + 3]};
+        }
+      }
+    }
     if (!delta) {
 #pragma unroll
       for (int j = 0; j < RPW; ++j) {
@@ -1318,6 +1417,24 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_rev_kernel(BwdKArgs
     }
     if (!delta) {
       lds_barrier();
+      if constexpr (IN) {
+        // dL/du of the block's keys, both signs summed, for dL/dk = W dL/du
+        float* dst = ka.duk + ((size_t)u * T_ + t0) * F;
+        for (int it = tid; it < L * (F / 4); it += blockDim.x) {
+          const int t = it / (F / 4), j4 = (it % (F / 4)) * 4;
+          f32x4 x;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            float acc = 0.0f;
+#pragma unroll
+            for (int sg = 0; sg < 2; ++sg)
+#pragma unroll
+              for (int part = 0; part < C::NPART; ++part) acc += to_f32(sh.duT[sg][part][j4 + e][t]);
+            x[e] = acc;
+          }
+          *reinterpret_cast<f32x4*>(dst + (size_t)t * F + j4) = x;
+        }
+      }
 #pragma unroll
       for (int t = 0; t < NT; ++t)
 #pragma unroll
@@ -1885,6 +2002,242 @@ __global__ __launch_bounds__(rwalk_threads<D>()) void hyb_bwd_rwalk_kernel(BwdKA
 }
 
 // ---------------------------------------------------------------------------
+// 6. Gradients with respect to the inputs q, k, v.  With a_ij = exp(s_ij),
+// s_ij = q_i . k_j / sqrt(d) for i, j in one block, and dL/dN, dL/dD from the
+// forward walk:
+//   dL/ds_ij = w a_ij (dL/dN_i . v_j + dL/dD_i)
+//   dL/dq_i  = sum_j dL/ds_ij k_j / sqrt(d) + W_h dL/du(q_i)
+//   dL/dk_j  = sum_h [ sum_i dL/ds_ij q_i / sqrt(d) + W_h dL/du(k_j) ]
+//   dL/dv_j  = sum_h [ sum_i w a_ij dL/dN_i + Gbar_c^T phi(k_j) ]
+// where dL/du(q), dL/du(k) and Gbar^T phi(k) come from the walks.  Blocks are
+// independent: one workgroup per (request, KV head, block), NW = D/32 waves,
+// wave w forming columns 32w .. 32w+31 of every output; the G query heads of
+// the KV head run in turn and dk, dv sum over them in registers.  The 32x32
+// score and dL/dP tiles are formed in both orientations (queries in lanes for
+// dq, keys in lanes for dk and dv), so each feeds its product straight from
+// the accumulators.  w a_ij is evaluated as exp(log w + s_ij): scores must
+// stay well inside the fp32 exponent range (the forward walk's 1/D has the
+// same limit).
+// ---------------------------------------------------------------------------
+template <typename T, int D, int F>
+struct InCfg {
+  typedef Mma<T> M;
+  typedef typename M::op_t op_t;
+  static constexpr int NW = D / kTile;
+  static constexpr int NPART = sizeof(T) == 2 ? 2 : 1;
+  static constexpr int PAD = 16 / (int)sizeof(T);
+  static constexpr int EPC = 16 / (int)sizeof(T);  // elements per 16 bytes
+  static constexpr int KD = D / M::KW;
+  static constexpr int KL = kTile / M::KW;
+  static constexpr int KF = F / M::KW;
+  struct alignas(16) Smem {
+    T k[kTile][D + PAD];
+    T v[kTile][D + PAD];
+    T q[kTile][D + PAD];
+    T dn[NPART][kTile][D + PAD];  // dL/dN_i[c] at [part][i][c]
+    T wt[F][D + PAD];             // W_h[c][j] at [j][c] (the layout of W)
+    float gd[kTile];
+  };
+};
+
+// An operand whose element e is col[idx(e) * ld]: idx(e) = row_of(ks*E + e,
+// hh) (accumulator-row order) or, natural, ks*KW + hh*E + e.
+template <typename T>
+__device__ inline typename Mma<T>::op_t lds_col_op(const T* col, int ld, int ks, int hh,
+                                                   bool natural) {
+  typedef Mma<T> M;
+  typename M::op_t x;
+  if constexpr (M::E == 1) {
+    x = col[(size_t)(natural ? ks * M::KW + hh : row_of(ks, hh)) * ld];
+  } else {
+#pragma unroll
+    for (int e = 0; e < M::E; ++e)
+      x[e] = col[(size_t)(natural ? ks * M::KW + hh * M::E + e : row_of(ks * M::E + e, hh)) * ld];
+  }
+  return x;
+}
+
+// Accumulator registers ks*E .. as an operand pair hi + lo (lo zero on fp32).
+template <typename T>
+__device__ inline void acc_split(const f32x16& x, int ks, typename Mma<T>::op_t& hi,
+                                 typename Mma<T>::op_t& lo) {
+  if constexpr (Mma<T>::E == 1) {
+    hi = x[ks];
+    lo = 0.0f;
+  } else {
+    acc_op_pair(x, ks, hi, lo);
+  }
+}
+
+template <typename T, int D, int F>
+__global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_inputs_kernel(BwdKArgs ka) {
+  typedef InCfg<T, D, F> C;
+  typedef typename C::M M;
+  typedef typename C::op_t op_t;
+  constexpr int E = M::E, KW = M::KW, EPC = C::EPC, LD = D + C::PAD;
+  __shared__ typename C::Smem sh;
+  const BackwardArgs& a = ka.a;
+
+  const int tid = threadIdx.x, lane = tid & (kWave - 1);
+  const int w = __builtin_amdgcn_readfirstlane(tid / kWave);
+  const int li = lane & 31, hh = lane >> 5;
+  const int Hq = a.s.Hq, Hkv = a.s.Hkv, L = a.s.L, T_ = a.T, G = Hq / Hkv;
+  const int nblk = ka.nblk;
+  const int blk = blockIdx.x % nblk, bg = blockIdx.x / nblk;
+  const int b = bg / Hkv, g = bg % Hkv;
+  const size_t t0 = (size_t)blk * L;
+  const size_t qstride = (size_t)Hq * D, kstride = (size_t)Hkv * D;
+  const float scale = 1.0f / sqrtf((float)D);
+  const int cc = w * kTile + li;  // this lane's output column
+  const bool lrow = li < L;
+
+  // rows of a [.][stride] tensor into a [32][LD] LDS tile, rows past L zero
+  auto stage_rows = [&](T (*dst)[LD], const T* src, size_t stride) {
+    for (int it = tid; it < kTile * (D / EPC); it += blockDim.x) {
+      const int r = it / (D / EPC), c = (it % (D / EPC)) * EPC;
+      uint4 x = {0u, 0u, 0u, 0u};
+      if (r < L) x = *reinterpret_cast<const uint4*>(src + (size_t)r * stride + c);
+      *reinterpret_cast<uint4*>(&dst[r][c]) = x;
+    }
+  };
+  stage_rows(sh.k, (const T*)a.k + (((size_t)b * T_ + t0) * Hkv + g) * D, kstride);
+  stage_rows(sh.v, (const T*)a.v + (((size_t)b * T_ + t0) * Hkv + g) * D, kstride);
+
+  f32x16 dks = {}, dkl = {}, dva = {};
+  for (int hq = 0; hq < G; ++hq) {
+    const int h = g * G + hq;
+    const size_t u = (size_t)b * Hq + h;
+    const float lw = log_sigmoid(a.alpha[h]);
+    lds_barrier();  // the previous head's readers are done
+    stage_rows(sh.q, (const T*)a.q + (((size_t)b * T_ + t0) * Hq + h) * D, qstride);
+    {
+      const float* gn = ka.gnT + (u * nblk + blk) * D * kTile;  // dL/dN^T [c][i]
+      for (int it = tid; it < D * kTile; it += blockDim.x) {
+        const int c = it / kTile, i = it % kTile;
+        const float x = i < L ? gn[it] : 0.0f;
+        const T xh = from_f32<T>(x);
+        sh.dn[0][i][c] = xh;
+        if constexpr (C::NPART == 2) sh.dn[1][i][c] = from_f32<T>(x - to_f32(xh));
+      }
+      if (tid < kTile) sh.gd[tid] = tid < L ? ka.gd[(u * nblk + blk) * kTile + tid] : 0.0f;
+      const T* wsrc = (const T*)a.W + (size_t)h * F * D;
+      for (int it = tid; it < F * (D / EPC); it += blockDim.x) {
+        const int j = it / (D / EPC), c = (it % (D / EPC)) * EPC;
+        *reinterpret_cast<uint4*>(&sh.wt[j][c]) =
+            *reinterpret_cast<const uint4*>(wsrc + (size_t)j * D + c);
+      }
+    }
+    lds_barrier();
+
+    // Scores and dL/dP = dL/dN_i . v_j: queries in lanes (sq, pq: rows j,
+    // columns i) and keys in lanes (sk, pk: rows i, columns j).
+    f32x16 sq = {}, sk = {}, pq = {}, pk = {};
+#pragma unroll
+    for (int ks = 0; ks < C::KD; ++ks) {
+      const op_t ko = load_op<T>(&sh.k[li][ks * KW + hh * E]);
+      const op_t qo = load_op<T>(&sh.q[li][ks * KW + hh * E]);
+      const op_t vo = load_op<T>(&sh.v[li][ks * KW + hh * E]);
+      const op_t nh = load_op<T>(&sh.dn[0][li][ks * KW + hh * E]);
+      sq = M::mma(ko, qo, sq);
+      sk = M::mma(qo, ko, sk);
+      pq = M::mma(vo, nh, pq);
+      pk = M::mma(nh, vo, pk);
+      if constexpr (C::NPART == 2) {
+        const op_t nl = load_op<T>(&sh.dn[1][li][ks * KW + hh * E]);
+        pq = M::mma(vo, nl, pq);
+        pk = M::mma(nl, vo, pk);
+      }
+    }
+    // w a_ij and dL/ds_ij in both orientations (zero outside the block)
+    f32x16 dsq, ak, dsk;
+    {
+      const float gdi = sh.gd[li];
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int o = row_of(r, hh);
+        const float aq = (lrow && o < L) ? expf(lw + sq[r] * scale) : 0.0f;
+        dsq[r] = aq * (pq[r] + gdi);
+        ak[r] = (lrow && o < L) ? expf(lw + sk[r] * scale) : 0.0f;
+        dsk[r] = ak[r] * (pk[r] + sh.gd[o]);
+      }
+    }
+
+    // dq: sum_j ds_ij k_j (scaled after) + du(q_i) W_h^T
+    f32x16 dqs = {}, dql = {};
+#pragma unroll
+    for (int ks = 0; ks < C::KL; ++ks) {
+      op_t hi, lo;
+      acc_split<T>(dsq, ks, hi, lo);
+      const op_t kc = lds_col_op<T>(&sh.k[0][cc], LD, ks, hh, false);
+      dqs = M::mma(hi, kc, dqs);
+      if constexpr (C::NPART == 2) dqs = M::mma(lo, kc, dqs);
+      // dk (this head): sum_i ds_ij q_i
+      acc_split<T>(dsk, ks, hi, lo);
+      const op_t qc = lds_col_op<T>(&sh.q[0][cc], LD, ks, hh, false);
+      dks = M::mma(hi, qc, dks);
+      if constexpr (C::NPART == 2) dks = M::mma(lo, qc, dks);
+      // dv (this head): sum_i w a_ij dL/dN_i
+      acc_split<T>(ak, ks, hi, lo);
+      const op_t nc = lds_col_op<T>(&sh.dn[0][0][cc], LD, ks, hh, false);
+      dva = M::mma(hi, nc, dva);
+      if constexpr (C::NPART == 2) {
+        dva = M::mma(lo, nc, dva);
+        dva = M::mma(hi, lds_col_op<T>(&sh.dn[1][0][cc], LD, ks, hh, false), dva);
+      }
+    }
+    // feature-map parts: du (rows: tokens, natural F) times W_h^T
+    {
+      const float* duq = ka.duq + (u * T_ + t0 + min(li, L - 1)) * F;
+      const float* duk = ka.duk + (u * T_ + t0 + min(li, L - 1)) * F;
+#pragma unroll
+      for (int ks = 0; ks < C::KF; ++ks) {
+        const op_t wc = lds_col_op<T>(&sh.wt[0][cc], LD, ks, hh, true);
+        op_t hi, lo;
+        load_split_op<T>(duq + ks * KW + hh * E, hi, lo);
+        hi = keep_if<T>(lrow, hi);
+        lo = keep_if<T>(lrow, lo);
+        dql = M::mma(hi, wc, dql);
+        if constexpr (C::NPART == 2) dql = M::mma(lo, wc, dql);
+        load_split_op<T>(duk + ks * KW + hh * E, hi, lo);
+        hi = keep_if<T>(lrow, hi);
+        lo = keep_if<T>(lrow, lo);
+        dkl = M::mma(hi, wc, dkl);
+        if constexpr (C::NPART == 2) dkl = M::mma(lo, wc, dkl);
+      }
+    }
+    // dq of head h: rows i (queries), column cc
+    {
+      float* dst = a.dq + (((size_t)b * T_ + t0) * Hq + h) * D + cc;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int i = row_of(r, hh);
+        if (i < L) dst[(size_t)i * qstride] = dqs[r] * scale + dql[r];
+      }
+    }
+    // the state part of dv: Gbar^T phi(k_j) from the reverse walk
+    {
+      const float* src = ka.dvl + (u * T_ + t0) * D + cc;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int j = row_of(r, hh);
+        if (j < L) dva[r] += src[(size_t)j * D];
+      }
+    }
+  }
+  // dk, dv of the KV head: rows j (keys), column cc
+  float* dkd = a.dk + (((size_t)b * T_ + t0) * Hkv + g) * D + cc;
+  float* dvd = a.dv + (((size_t)b * T_ + t0) * Hkv + g) * D + cc;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int j = row_of(r, hh);
+    if (j < L) {
+      dkd[(size_t)j * kstride] = dks[r] * scale + dkl[r];
+      dvd[(size_t)j * kstride] = dva[r];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // 5. Sum of the partials over requests and segments, in a fixed order.
 // ---------------------------------------------------------------------------
 __global__ void hyb_bwd_reduce_kernel(BwdKArgs ka) {
@@ -1935,7 +2288,8 @@ static hipError_t bwd_go(const BackwardArgs& a, hipStream_t st) {
   const int units = s.B * s.Hq, nblk = a.T / s.L;
   const int nseg = prefill_segments(s, a.T);
   const int seg_blocks = (nblk + nseg - 1) / nseg;
-  const BwdLayout l = bwd_layout(s, a.T);
+  const bool inputs = a.dq != nullptr;
+  const BwdLayout l = bwd_layout(s, a.T, inputs);
   char* ws = (char*)a.ws;
   const size_t f = 2 * (size_t)s.F;
   BwdKArgs ka;
@@ -1952,6 +2306,9 @@ static hipError_t bwd_go(const BackwardArgs& a, hipStream_t st) {
   ka.dwq = (float*)(ws + l.dwq);
   ka.dwk = (float*)(ws + l.dwk);
   ka.red = (float*)(ws + l.red);
+  ka.duq = inputs ? (float*)(ws + l.duq) : nullptr;
+  ka.duk = inputs ? (float*)(ws + l.duk) : nullptr;
+  ka.dvl = inputs ? (float*)(ws + l.dvl) : nullptr;
   const dim3 block(kWave * (D / kTile));
   hipError_t e;
   if (nseg > 1) {
@@ -1961,11 +2318,16 @@ static hipError_t bwd_go(const BackwardArgs& a, hipStream_t st) {
     pa.s.n_slots = s.B;
     if ((e = launch_prefill_delta(pa, st)) != hipSuccess) return e;
   }
-  if constexpr (sizeof(T) == 2) {
+  // With the input gradients the four-wave walks serve both dtypes (they
+  // also write dL/du and Gbar^T phi(K)); otherwise bf16 takes the pipelined
+  // walks.
+  if (inputs) {
+    hipLaunchKernelGGL((hyb_bwd_fwd_kernel<T, D, F, true>), dim3(units * nseg), block, 0, st, ka);
+  } else if constexpr (sizeof(T) == 2) {
     hipLaunchKernelGGL((hyb_bwd_fpipe_kernel<D, F>), dim3(units * nseg), dim3(fpipe_threads<D>()),
                        0, st, ka);
   } else {
-    hipLaunchKernelGGL((hyb_bwd_fwd_kernel<T, D, F>), dim3(units * nseg), block, 0, st, ka);
+    hipLaunchKernelGGL((hyb_bwd_fwd_kernel<T, D, F, false>), dim3(units * nseg), block, 0, st, ka);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (nseg > 1) {
@@ -1973,18 +2335,27 @@ static hipError_t bwd_go(const BackwardArgs& a, hipStream_t st) {
       hipLaunchKernelGGL((hyb_bwd_gdelta_kernel<D, F>), dim3(units * (nseg - 1)),
                          dim3(gdelta_threads<D>()), 0, st, ka);
     } else {
-      hipLaunchKernelGGL((hyb_bwd_rev_kernel<T, D, F>), dim3(units * (nseg - 1)), block, 0, st,
-                         ka, 1);
+      hipLaunchKernelGGL((hyb_bwd_rev_kernel<T, D, F, false>), dim3(units * (nseg - 1)), block, 0,
+                         st, ka, 1);
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
   }
-  if constexpr (sizeof(T) == 2) {
+  if (inputs) {
+    hipLaunchKernelGGL((hyb_bwd_rev_kernel<T, D, F, true>), dim3(units * nseg), block, 0, st, ka,
+                       0);
+  } else if constexpr (sizeof(T) == 2) {
     hipLaunchKernelGGL((hyb_bwd_rwalk_kernel<D, F>), dim3(units * nseg), dim3(rwalk_threads<D>()),
                        0, st, ka);
   } else {
-    hipLaunchKernelGGL((hyb_bwd_rev_kernel<T, D, F>), dim3(units * nseg), block, 0, st, ka, 0);
+    hipLaunchKernelGGL((hyb_bwd_rev_kernel<T, D, F, false>), dim3(units * nseg), block, 0, st, ka,
+                       0);
   }
   if ((e = hipGetLastError()) != hipSuccess) return e;
+  if (inputs) {
+    hipLaunchKernelGGL((hyb_bwd_inputs_kernel<T, D, F>), dim3(s.B * s.Hkv * nblk), block, 0, st,
+                       ka);
+    if ((e = hipGetLastError()) != hipSuccess) return e;
+  }
   const size_t n = (size_t)s.Hq * s.F * s.D;
   hipLaunchKernelGGL(hyb_bwd_reduce_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st,
                      ka);

@@ -56,6 +56,10 @@ struct BackwardArgs {
   const void* target;
   float *dW, *dalpha, *loss;  // loss may be null
   void* ws;
+  // Gradients with respect to the inputs (fp32, layouts of q, k, v), all
+  // three set or all null; dk and dv are summed over the query heads that
+  // share a KV head.
+  float *dq = nullptr, *dk = nullptr, *dv = nullptr;
 };
 
 struct SoftmaxPrefixArgs {
@@ -100,7 +104,8 @@ hipError_t scratch_device_ptr(void** ptr);
 
 hipError_t launch_backward(const BackwardArgs& a, hipStream_t st);
 bool backward_supported(const Shape& s);
-size_t backward_ws_bytes(const Shape& s, int T);
+// inputs: the workspace of a call that also forms dq, dk, dv
+size_t backward_ws_bytes(const Shape& s, int T, bool inputs = false);
 
 // Workspace of softmax_prefix_step for n_split splits.
 size_t softmax_prefix_ws_bytes(const Shape& s, int n_split);

@@ -314,3 +314,33 @@ def test_softmax_prefix_paged_validation():
     assert call(dims=_dims(batch=0)) == 0
     # the workspace is sized by max_pages * page_size
     assert need == lib.hybrid_workspace_bytes(ctypes.byref(d), hb.OP_SOFTMAX_PREFIX, 2048)
+
+
+def test_backward_full_validation():
+    lib = hb.load()
+    d = _dims(feat_dim=128)
+    T = 64
+    need = lib.hybrid_workspace_bytes(ctypes.byref(d), hb.OP_BACKWARD_FULL, T)
+    assert need > lib.hybrid_workspace_bytes(ctypes.byref(d), hb.OP_BACKWARD, T)
+    # q k v W alpha dout target dq dk dv dW dalpha loss ws
+    ok = [_addr(i) for i in range(14)]
+    ok[6] = None   # dout mode
+    ok[12] = None  # no loss without a target
+    call = lambda p, n=need: lib.hybrid_attn_backward_full(ctypes.byref(d), T, *p[:13], p[13], n,
+                                                           None)
+    for i in (7, 8, 9):
+        p = list(ok)
+        p[i] = None
+        assert call(p) == 1, i
+        p[i] = MISALIGNED
+        assert call(p) == 3, i
+    assert call(ok, need - 1) == 6
+    # dq, dk, dv against the inputs, each other and the workspace
+    for w_i in (7, 8, 9):
+        for r_i in (0, 1, 2, 3, 4, 5, 7, 8, 9, 10, 11, 13):
+            if r_i == w_i:
+                continue
+            p = list(ok)
+            p[w_i] = p[r_i]
+            assert call(p) == 2, (w_i, r_i)
+            assert "overlap" in hb.last_error()

@@ -25,11 +25,13 @@ def _close(got, ref, dt, what):
     assert got.shape == ref.shape, (got.shape, ref.shape)
     assert np.isfinite(got).all(), f"{what}: non-finite"
     err = float(np.abs(got - ref).max())
+    amax = float(np.abs(ref).max())
     if dt == "f32":
-        tol = 1e-5 * max(1.0, float(np.abs(ref).max()))
+        tol = 1e-5 * max(1.0, amax)
     else:
         tol = 2e-2 * float(np.sqrt(np.mean(ref ** 2)))
-    print(f"[parity] {what}: max abs err {err:.3e} (tol {tol:.3e})")
+    print(f"[parity] {what}: max abs err {err:.3e} (tol {tol:.3e}, max |ref| {amax:.3e}"
+          f"{', within the absolute 1e-5' if err <= 1e-5 else ''})")
     assert err <= tol, f"{what}: max abs err {err:.3e} > tol {tol:.3e}"
 
 
