@@ -2,12 +2,17 @@
 // state update): S_h += sum_t phi_h(k_t) v_t^T, z_h += sum_t phi_h(k_t).
 //
 // One workgroup per (request b, query head h); wave w of NW = D/32 owns the
-// state columns 32w .. 32w+31 for all f rows.  The state tile is loaded
-// straight into MFMA accumulator layout (row r = 32*rt + row_of(i, hh),
-// column 32w + li), so S += phi(K)^T V is one accumulate-in-place product per
-// 32-row tile, then stored back to the same addresses: every S element is read
-// once and written once.  phi(K) is built with the shared feature-map code
-// and transposed through LDS (feature-major) to serve as the A operand.
+// state columns 32w .. 32w+31 for all f rows, i.e. 32 consecutive rows of
+// the stored S_h^T ([d][f], features contiguous): a contiguous 16 KiB.  The
+// update is formed transposed, S^T += V^T phi(K), so the accumulator tile
+// (w, rt) holds value dim c = 32w + row_of(i, hh) in register i and feature
+// r = 32 rt + li in lane li: the state moves in and out with 4-byte accesses
+// whose 32 lanes cover a whole 128-byte line, two lines per instruction.
+// (With features in registers instead, every 16-byte access of an
+// instruction would land in a different line; that costs a fifth of the
+// bandwidth of a read-modify-write stream on this chip.)  Every S element is
+// read once and written once.  phi(K) is built with the shared feature-map
+// code and stored feature-major in LDS, the B operand of the update.
 // On the bf16 path phi is kept as a bf16 pair hi + lo (two products), so the
 // update carries phi to about 16 bits instead of 8.  Tokens beyond the
 // request's block length get phi = 0 and v = 0 (padding rows are never used
@@ -37,7 +42,7 @@ struct CommitCfg {
 };
 
 template <typename T, int D, int F>
-__global__ __launch_bounds__(kWave*(D / kTile)) void hyb_commit_kernel(
+__global__ __launch_bounds__(kWave*(D / kTile), 2) void hyb_commit_kernel(
     CommitArgs a) {
   typedef CommitCfg<T, D, F> C;
   typedef typename C::M M;
@@ -51,10 +56,13 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_commit_kernel(
   const int Hq = a.s.Hq, Hkv = a.s.Hkv, L = a.s.L;
   const int u = xcd_unit(blockIdx.x, a.s.B * Hq);
   const int b = u / Hq, h = u % Hq, g = h / (Hq / Hkv);
-  const int slot = a.slots ? a.slots[b] : b;
+  // (slot and block length are uniform: through readfirstlane the state's
+  // base address is a scalar, and each state access needs only a 32-bit
+  // lane offset and an immediate, not a 64-bit address of its own)
+  const int slot = __builtin_amdgcn_readfirstlane(a.slots ? a.slots[b] : b);
   if (slot < 0 || slot >= a.s.n_slots) return;  // uniform per workgroup
   // Active tokens of this request's block (padding tokens contribute nothing).
-  const int Lb = a.block_len ? min(max(a.block_len[b], 0), L) : L;
+  const int Lb = __builtin_amdgcn_readfirstlane(a.block_len ? min(max(a.block_len[b], 0), L) : L);
   if (Lb == 0) return;  // nothing to commit (uniform per workgroup)
   const size_t sbase = (size_t)slot * Hq + h;
   float* __restrict__ Sh = a.S + sbase * f * D;
@@ -86,22 +94,29 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_commit_kernel(
   float zreg[ZPT];
 #pragma unroll
   for (int j = 0; j < ZPT; ++j) zreg[j] = zh[min(tid + j * NTH, f - 1)];
-  f32x16 sacc[C::NRT];
-#pragma unroll
-  for (int rt = 0; rt < C::NRT; ++rt)
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {  // rows rt*32 + j*8 + hh*4 .. +3: 16 bytes
-      const f32x4 x = *reinterpret_cast<const f32x4*>(
-          Sh + (size_t)col * f + rt * kTile + row_of(4 * j, hh));
-#pragma unroll
-      for (int r = 0; r < 4; ++r) sacc[rt][4 * j + r] = x[r];
-    }
 #pragma unroll
   for (int ks = 0; ks < C::KD; ++ks) kop[ks] = keep_if<T>(tok_ok, kop[ks]);
 
-  // 2. phi(K), transposed into LDS; padding tokens contribute nothing.
+  // 2. phi(K), transposed into LDS; padding tokens contribute nothing.  The
+  //    state is requested after the logits, when the W_h and K operands are
+  //    no longer live (their loads are not queued behind the state reads).
   float val[FM::PPW][16];
   FM::logits(wop, kop, w, li, hh, val, sh.fm);
+  asm volatile("" ::: "memory");  // the state loads stay after the logits
+  // tile (w, rt): value dim 32w + row_of(i, hh), feature 32 rt + li
+  f32x16 sacc[C::NRT];
+  // Buffer accesses over this head's state: the lane offset in one VGPR,
+  // the 8-row group of register i in the scalar offset, the rest in the
+  // immediate.
+  const __amdgpu_buffer_rsrc_t srs =
+      __builtin_amdgcn_make_buffer_rsrc(Sh, 0, f * D * 4, kBufferWord3);
+  const int soff = ((w * kTile + hh * 4) * f + li) * 4;  // bytes
+#pragma unroll
+  for (int rt = 0; rt < C::NRT; ++rt)
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      sacc[rt][i] = __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(
+          srs, soff + ((i & 3) * f + rt * kTile) * 4, (i >> 2) * 8 * f * 4, 0));
   lds_barrier();
   FM::exps(w, li, hh, val, sh.fm);
   lds_barrier();
@@ -116,20 +131,22 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_commit_kernel(
   });
   lds_barrier();
 
-  // 3. S += phi(K)^T V, one accumulate per 32-row tile, stored in place.
+  // 3. S^T += V^T phi(K), one accumulate per 32-feature tile, stored in place.
+
 #pragma unroll
   for (int rt = 0; rt < C::NRT; ++rt) {
 #pragma unroll
     for (int ks = 0; ks < C::KL; ++ks)
 #pragma unroll
       for (int part = 0; part < C::NPART; ++part)
-        sacc[rt] = M::mma(
-            load_op<T>(&sh.phiT[part][rt * kTile + li][ks * KW + hh * E]),
-            vop[ks], sacc[rt]);
+        sacc[rt] = M::mma(vop[ks],
+                          load_op<T>(&sh.phiT[part][rt * kTile + li][ks * KW + hh * E]),
+                          sacc[rt]);
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-      *reinterpret_cast<f32x4*>(Sh + (size_t)col * f + rt * kTile + row_of(4 * j, hh)) =
-          f32x4{sacc[rt][4 * j], sacc[rt][4 * j + 1], sacc[rt][4 * j + 2], sacc[rt][4 * j + 3]};
+    for (int i = 0; i < 16; ++i)
+      __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, (float)sacc[rt][i]), srs,
+                                            soff + ((i & 3) * f + rt * kTile) * 4,
+                                            (i >> 2) * 8 * f * 4, 0);
   }
 
   // 4. z += sum_t phi(k_t), from the same values that entered S.

@@ -364,6 +364,10 @@ __device__ inline float log_sigmoid(float a) {
 // all of its outstanding global loads before the barrier; restricting the
 // fences to the local address space keeps loads issued before the barrier in
 // flight (LDS writes are still complete and visible after it).
+// Word 3 of a raw buffer resource on gfx9-family chips (32-bit data
+// format; the untyped loads and stores used here take no other field).
+constexpr int kBufferWord3 = 0x00020000;
+
 __device__ inline void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
   __builtin_amdgcn_s_barrier();
