@@ -261,11 +261,13 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
   const int u = xcd_unit(blockIdx.x, a.s.B * ngrp);
   const int hg = u % ngrp, b = u / ngrp;
   const int h = hg * NW + w, g = (hg * NW) / (Hq / Hkv);
-  const int slot = a.slots ? a.slots[b] : b;
+  // (uniform through readfirstlane: the state base is then a scalar and
+  // each state load needs a 32-bit lane offset, not a 64-bit address)
+  const int slot = __builtin_amdgcn_readfirstlane(a.slots ? a.slots[b] : b);
   const bool slot_ok = slot >= 0 && slot < a.s.n_slots;
   // Active tokens of this request's block (the rest are padding: masked as
   // keys, never written as outputs, never committed).
-  const int Lb = a.block_len ? min(max(a.block_len[b], 0), L) : L;
+  const int Lb = __builtin_amdgcn_readfirstlane(a.block_len ? min(max(a.block_len[b], 0), L) : L);
   // Rows past Lb read row Lc instead: in bounds, and an active row, so the
   // padding rows are never read whatever they hold.  A request with Lb = 0
   // writes no output and commits nothing.
@@ -276,11 +278,19 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
   // 16-byte runs of column column(cb, c16) at features feature(4 rn, quad).
   f32x4 buf[NBUF][RUNS];
   const float* __restrict__ St = a.S + sbase * f * D;
+  // Buffer loads over the head's state: the column block's part of the
+  // offset is a scalar, the lane's part one VGPR, the run's part the
+  // immediate, so a load needs no address arithmetic of its own.
+  const __amdgpu_buffer_rsrc_t srs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<float*>(St), 0, f * D * 4, kBufferWord3);
+  const int slane = (C::column(0, c16) * f + C::feature(0, quad)) * 4;  // bytes
   auto issue = [&](int cb) {
 #pragma unroll
     for (int rn = 0; rn < RUNS; ++rn)
-      buf[cb % NBUF][rn] = *reinterpret_cast<const f32x4*>(
-          St + (size_t)C::column(cb, c16) * f + C::feature(rn * 4, quad));
+      buf[cb % NBUF][rn] = __builtin_bit_cast(
+          f32x4, __builtin_amdgcn_raw_buffer_load_b128(
+                     srs, slane + (C::feature(rn * 4, 0) - C::feature(0, 0)) * 4,
+                     (C::column(cb, 0) - C::column(0, 0)) * f * 4, 0));
   };
 
   // Staged V rows (bf16) or V^T (fp32) of this head's KV head.
