@@ -112,13 +112,25 @@ typedef struct {
   int32_t feat_dim;   /* f = 2F, rows of S: 64, 128 or 256                   */
   int32_t dtype;      /* hyb_dtype_t                                         */
   int32_t n_slots;    /* rows of the state pool S, z; >= 1 when batch > 0   */
-  int32_t flags;      /* 0 or HYB_OUT_F32; any other bit is rejected        */
+  int32_t flags;      /* HYB_OUT_F32 and, for the step only, HYB_STEP_SPLIT
+                         or HYB_STEP_WHOLE; any other bit is rejected      */
 } hyb_dims_t;
 
 /* flags: out is fp32 whatever dtype is (default: out has dtype).  The bf16
  * output of a call equals the round-to-nearest-even bf16 of its fp32 output
  * bit for bit. */
 #define HYB_OUT_F32 1
+/* flags of hybrid_attn_step only (any other entry point rejects them): which
+ * of its two kernels runs.  HYB_STEP_SPLIT: one wave per (request, query
+ * head, 32-column slice of d), for batches too small to fill the chip with
+ * HYB_STEP_WHOLE: one workgroup per group of query heads sharing a KV head,
+ * each streaming its heads' whole states.  Neither: the library picks by the
+ * batch (SPLIT while its B * Hq * d/32 waves fit on the chip at once, 1024
+ * of them).  Both: rejected.
+ * Results agree to the same bound against the definition; they need not
+ * agree bit for bit. */
+#define HYB_STEP_SPLIT 2
+#define HYB_STEP_WHOLE 4
 
 /* One denoising step of the active block (Section 3.1: within-block
  * softmax branch, linear readout of the committed state, gated merge with a

@@ -18,6 +18,8 @@ LIB_PATH = os.path.join(_PKG, "libhybattn.so")
 
 HYB_F32, HYB_BF16 = 0, 1
 HYB_OUT_F32 = 1
+HYB_STEP_SPLIT, HYB_STEP_WHOLE = 2, 4
+_STEP_KERNEL = {None: 0, "auto": 0, "split": HYB_STEP_SPLIT, "whole": HYB_STEP_WHOLE}
 OP_STEP, OP_COMMIT, OP_PREFILL, OP_SOFTMAX_PREFIX, OP_BACKWARD, OP_BACKWARD_FULL = 0, 1, 2, 3, 4, 5
 STATUS = {0: "HYB_OK", 1: "HYB_ENULL", 2: "HYB_EINVAL", 3: "HYB_EALIGN",
           4: "HYB_EDTYPE", 5: "HYB_EUNSUPPORTED", 6: "HYB_EWORKSPACE",
@@ -127,15 +129,18 @@ def _out_flags(out, act, out_f32):
 
 
 def hybrid_attn_step(q, k, v, W, alpha, S, z, slots=None, out=None, out_f32=False,
-                     stream=None, block_len=None):
+                     stream=None, block_len=None, kernel=None):
     """q [B][L][Hq][d], k/v [B][L][Hkv][d], W [Hq][F][d], alpha [Hq] f32,
     S [n_slots][Hq][d][f] f32 (S_h transposed), z [n_slots][Hq][f] f32 -> out [B][L][Hq][d]
     in q's dtype (fp32 with out_f32).  block_len [B] int32 (device): active rows
-    per request; rows past it of out are left as they were."""
+    per request; rows past it of out are left as they were.  kernel: None or
+    "auto" (the library picks), "split" or "whole" (HYB_STEP_SPLIT /
+    HYB_STEP_WHOLE)."""
     lib = load()
     B, L, Hq, d = q.shape
     act = q.dtype
     flags, odt = _out_flags(out, act, out_f32)
+    flags |= _STEP_KERNEL[kernel]
     dims = make_dims(B, Hq, k.shape[2], d, L, z.shape[2], _dt(q), S.shape[0], flags)
     if out is None:
         out = torch.empty(q.shape, dtype=odt, device=q.device)

@@ -17,7 +17,7 @@ CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libhybattn.so")
 BUILD = os.path.join(ROOT, "_build")
 SOURCES = ["api.cpp", "step.hip", "commit.hip", "prefill.hip", "softmax_prefix.hip", "backward.hip",
-           "scratch.hip"]
+           "scratch.hip", "step_small.hip"]
 ARCH = "gfx950"
 FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC",

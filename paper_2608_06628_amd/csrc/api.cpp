@@ -60,11 +60,21 @@ int check_dims(const hyb_dims_t* d, bool need_state, hyb::Shape* s) {
     return fail(HYB_EINVAL, "n_slots %d < 1", d->n_slots);
   if ((long long)d->batch * d->n_q_heads > 0x7fffffffLL)
     return fail(HYB_EINVAL, "batch * n_q_heads exceeds the grid limit");
-  if (d->flags & ~HYB_OUT_F32)
+  if (d->flags & ~(HYB_OUT_F32 | HYB_STEP_SPLIT | HYB_STEP_WHOLE))
     return fail(HYB_EINVAL, "unknown flags 0x%x", d->flags);
+  if ((d->flags & HYB_STEP_SPLIT) && (d->flags & HYB_STEP_WHOLE))
+    return fail(HYB_EINVAL, "HYB_STEP_SPLIT and HYB_STEP_WHOLE together");
   *s = hyb::Shape{d->batch,    d->n_q_heads,    d->n_kv_heads,
                   d->head_dim, d->block,        d->feat_dim / 2,
                   d->dtype,    d->n_slots,      (d->flags & HYB_OUT_F32) ? 1 : 0};
+  s->step_kernel = (d->flags & HYB_STEP_SPLIT) ? 1 : (d->flags & HYB_STEP_WHOLE) ? 2 : 0;
+  return HYB_OK;
+}
+
+// The step-kernel flags belong to hybrid_attn_step alone.
+int no_step_flags(const hyb_dims_t* d) {
+  if (d && (d->flags & (HYB_STEP_SPLIT | HYB_STEP_WHOLE)))
+    return fail(HYB_EINVAL, "HYB_STEP_SPLIT / HYB_STEP_WHOLE apply to hybrid_attn_step only");
   return HYB_OK;
 }
 
@@ -141,6 +151,7 @@ int hybrid_attn_step_commit(const hyb_dims_t* dims, const void* q,
                             void* out, void* stream) {
   hyb::Shape s;
   TRY(check_dims(dims, true, &s));
+  TRY(no_step_flags(dims));
   if (s.B == 0) return ok();
   TRY(check_ptr(q, "q"));
   TRY(check_ptr(k, "k"));
@@ -189,6 +200,7 @@ int hybrid_state_commit(const hyb_dims_t* dims, const void* k, const void* v,
                         void* stream) {
   hyb::Shape s;
   TRY(check_dims(dims, true, &s));
+  TRY(no_step_flags(dims));
   if (s.B == 0) return ok();
   TRY(check_ptr(k, "k"));
   TRY(check_ptr(v, "v"));
@@ -219,6 +231,7 @@ int prefill_impl(const hyb_dims_t* dims, int32_t seq_len, const void* q,
                  void* stream) {
   hyb::Shape s;
   TRY(check_dims(dims, true, &s));
+  TRY(no_step_flags(dims));
   if (seq_len <= 0 || seq_len % s.L != 0)
     return fail(HYB_EINVAL, "seq_len %d is not a positive multiple of block %d",
                 seq_len, s.L);
@@ -314,6 +327,7 @@ int softmax_prefix_impl(const hyb_dims_t* dims, const void* q, const void* k,
                         void* ws, size_t ws_bytes, void* stream) {
   hyb::Shape s;
   TRY(check_dims(dims, false, &s));
+  TRY(no_step_flags(dims));
   int page_shift = 0;
   if (paged) {
     if (max_pages < 0) return fail(HYB_EINVAL, "max_pages %d < 0", max_pages);

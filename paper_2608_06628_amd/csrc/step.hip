@@ -910,7 +910,19 @@ static hipError_t step_d(const StepArgs& a, hipStream_t st) {
   return hipErrorInvalidValue;
 }
 
+// The split kernel while its waves (B Hq d/32, one per unit) fit on the
+// chip's 1024 SIMDs at once and the per-head-group grid (B Hq / 4
+// workgroups, one per CU) would leave CUs idle.  Measured (16q/4kv, d = 128,
+// f = 128, bf16, kernel time): B = 1: 6.1 against 11.1 us; B = 8: 8.4 against
+// 12.0; B = 16: 11.7 against 12.6; B = 20 (a second round of waves): 16.8
+// against 12.7.
+bool step_prefers_split(const Shape& s) {
+  return (long)s.B * s.Hq * (s.D / kTile) <= 1024 && (long)s.B * s.Hq / 4 < 256;
+}
+
 hipError_t launch_step(const StepArgs& a, hipStream_t st) {
+  if (a.s.step_kernel == 1 || (a.s.step_kernel == 0 && step_prefers_split(a.s)))
+    return launch_step_small(a, st);
   return a.s.dtype == 1 ? step_d<bf16, false>(a, st) : step_d<float, false>(a, st);
 }
 

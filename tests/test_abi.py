@@ -344,3 +344,18 @@ def test_backward_full_validation():
             p[w_i] = p[r_i]
             assert call(p) == 2, (w_i, r_i)
             assert "overlap" in hb.last_error()
+
+
+def test_step_kernel_flags():
+    lib = hb.load()
+    p = [_addr(i) for i in range(11)]
+    step = lambda dims: lib.hybrid_attn_step(ctypes.byref(dims), *p[:7], None, None, p[10], None)
+    assert step(_dims(flags=hb.HYB_STEP_SPLIT | hb.HYB_STEP_WHOLE)) == 2
+    assert "together" in hb.last_error()
+    assert step(_dims(flags=8)) == 2
+    # the other entry points reject them
+    d = _dims(flags=hb.HYB_STEP_SPLIT)
+    assert lib.hybrid_state_commit(ctypes.byref(d), *p[:5], None, None, None) == 2
+    assert "hybrid_attn_step only" in hb.last_error()
+    assert lib.hybrid_attn_step_commit(ctypes.byref(d), *p[:7], None, None, p[10], None) == 2
+    assert lib.softmax_prefix_step(ctypes.byref(d), *p[:6], 64, p[6], p[7], 1 << 30, None) == 2

@@ -100,12 +100,17 @@ def test_block_len_step_fused_commit(shape):
     q, k, v, W, al = _dev_inputs(c, dt, qkv)
     sd = None if slots is None else i32(slots)
     bld = i32(bl)
-    # the step: reads the state, writes rows < block_len[b] only
+    # the step (both kernels): reads the state, writes rows < block_len[b] only
+    outs_split = _out_buf(q)
+    hb.hybrid_attn_step(q, k, v, W, al, state_dev(c["S"]), f32(c["z"]), slots=sd, out=outs_split,
+                        block_len=bld, kernel="split")
+    torch.cuda.synchronize()
+    _check_out(outs_split, outs, lens, dt, "step [split]")
     out = _out_buf(q)
     hb.hybrid_attn_step(q, k, v, W, al, state_dev(c["S"]), f32(c["z"]), slots=sd, out=out,
-                        block_len=bld)
+                        block_len=bld, kernel="whole")
     torch.cuda.synchronize()
-    _check_out(out, outs, lens, dt, "step")
+    _check_out(out, outs, lens, dt, "step [whole]")
     # the fused step+commit: the same output, and the state as the commits
     S1, z1 = state_dev(c["S"]), f32(c["z"])
     outf = _out_buf(q)
@@ -137,6 +142,13 @@ def test_full_block_len_equals_null(dt):
     a = hb.hybrid_attn_step(q, k, v, W, al, state_dev(c["S"]), f32(c["z"]), out_f32=True)
     b = hb.hybrid_attn_step(q, k, v, W, al, state_dev(c["S"]), f32(c["z"]), out_f32=True,
                             block_len=full)
+    for kern in ("split", "whole"):
+        x = hb.hybrid_attn_step(q, k, v, W, al, state_dev(c["S"]), f32(c["z"]), out_f32=True,
+                                kernel=kern)
+        y = hb.hybrid_attn_step(q, k, v, W, al, state_dev(c["S"]), f32(c["z"]), out_f32=True,
+                                block_len=full, kernel=kern)
+        torch.cuda.synchronize()
+        assert torch.equal(x, y), f"{kern}: block_len = L differs from no block_len"
     Sa, za, Sb, zb = state_dev(c["S"]), f32(c["z"]), state_dev(c["S"]), f32(c["z"])
     fa = hb.hybrid_attn_step_commit(q, k, v, W, al, Sa, za, out_f32=True)
     fb = hb.hybrid_attn_step_commit(q, k, v, W, al, Sb, zb, out_f32=True, block_len=full)

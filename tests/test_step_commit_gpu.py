@@ -36,9 +36,10 @@ def check_fused(c, dims, what):
     assert_close(host(o32), ref_out, dt, what + " out" + (" (fp32 out)" if dt == "bf16" else ""))
     assert_close(state_host(S1) - c["S"], Sr - c["S"], dt, what + " dS")
     assert_close(host(z1) - c["z"], zr - c["z"], dt, what + " dz")
-    # the same output as the library's step on the untouched state
+    # the same output as the library's per-head step kernel (the fused
+    # kernel is that kernel with the commit) on the untouched state
     step = hb.hybrid_attn_step(*_inputs(c, dt), state_dev(c["S"]), f32(c["z"]),
-                               out_f32=(dt == "bf16"))
+                               out_f32=(dt == "bf16"), kernel="whole")
     torch.cuda.synchronize()
     assert torch.equal(o32, step), f"{what}: fused output differs from the step's"
     if dt == "bf16":

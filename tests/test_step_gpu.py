@@ -14,21 +14,28 @@ from _helpers import (act, announce, assert_close, check_outputs, f32, host, i32
 pytestmark = pytest.mark.gpu
 
 
-def step_call(c, dims, slots=None):
+# The step's two kernels: one wave per (request, head, 32-column slice),
+# and one workgroup per group of heads.  Every parity case runs both.
+KERNELS = ["split", "whole"]
+
+
+def step_call(c, dims, slots=None, kernel=None):
     args = (act(c["q"], dims.dtype), act(c["k"], dims.dtype), act(c["v"], dims.dtype),
             act(c["Wt"], dims.dtype), f32(c["alpha"]), state_dev(c["S"]), f32(c["z"]))
     sl = None if slots is None else i32(slots)
-    return lambda out_f32: hb.hybrid_attn_step(*args, slots=sl, out_f32=out_f32)
+    return lambda out_f32: hb.hybrid_attn_step(*args, slots=sl, out_f32=out_f32, kernel=kernel)
 
 
-def run_step(c, dims, slots=None):
-    out = step_call(c, dims, slots)(False)
+def run_step(c, dims, slots=None, kernel=None):
+    out = step_call(c, dims, slots, kernel)(False)
     torch.cuda.synchronize()
     return host(out)
 
 
 def check_step(c, dims, what, slots=None):
-    return check_outputs(step_call(c, dims, slots), ref_step(c, slots), dims.dtype, what)
+    ref = ref_step(c, slots)
+    for kernel in KERNELS:
+        check_outputs(step_call(c, dims, slots, kernel), ref, dims.dtype, f"{what} [{kernel}]")
 
 
 def ref_step(c, slots=None):
@@ -124,17 +131,19 @@ def test_slots_and_bad_slot():
     check_step(c, dims, "step slots", slots)
     announce("step bad slot")
     bad = np.array([4, 7, -1], np.int32)
-    out = host(step_call(c, dims, bad)(True))
-    assert np.isnan(out[1:]).all()
     good = ref_step(c, np.array([4, 0, 0], np.int32))[:1]
-    assert_close(out[:1], good, "bf16", "step valid row next to bad slots")
-    assert np.isnan(run_step(c, dims, bad)[1:]).all()
+    for kernel in KERNELS:
+        out = host(step_call(c, dims, bad, kernel)(True))
+        assert np.isnan(out[1:]).all()
+        assert_close(out[:1], good, "bf16", f"step valid row next to bad slots [{kernel}]")
+        assert np.isnan(run_step(c, dims, bad, kernel)[1:]).all()
 
 
-def test_deterministic_and_guarded():
+@pytest.mark.parametrize("kernel", KERNELS)
+def test_deterministic_and_guarded(kernel):
     """Bitwise identical across runs; bytes around the output stay untouched."""
     dims = synth.DECODE1.with_(B=4)
-    announce("step determinism")
+    announce(f"step determinism [{kernel}]")
     c = make_case(dims, 128, seed=30, peaky=True)
     q, k, v = (act(c[n], "bf16") for n in ("q", "k", "v"))
     W, al, S, z = act(c["Wt"], "bf16"), f32(c["alpha"]), state_dev(c["S"]), f32(c["z"])
@@ -142,9 +151,9 @@ def test_deterministic_and_guarded():
     guard = 4096
     buf = torch.full((n + 2 * guard,), float("nan"), dtype=torch.bfloat16, device="cuda")
     out = buf[guard:guard + n].view(q.shape)
-    first = hb.hybrid_attn_step(q, k, v, W, al, S, z).clone()
+    first = hb.hybrid_attn_step(q, k, v, W, al, S, z, kernel=kernel).clone()
     for _ in range(10):
-        hb.hybrid_attn_step(q, k, v, W, al, S, z, out=out)
+        hb.hybrid_attn_step(q, k, v, W, al, S, z, out=out, kernel=kernel)
         torch.cuda.synchronize()
         assert torch.equal(out.view(torch.int16), first.view(torch.int16))
     assert torch.isnan(buf[:guard].float()).all() and torch.isnan(buf[guard + n:].float()).all()
@@ -159,3 +168,18 @@ def test_matches_commit_free_brute_force():
     ref = brute.hybrid_block_brute(c["q"], c["k"], c["v"], c["kp"], c["vp"],
                                    np.array([synth.TINY_PREFIX]), c["Wt"], c["alpha"])
     check_outputs(step_call(c, dims), ref, "f32", "step tiny vs brute")
+
+
+@pytest.mark.parametrize("B", [1, 8, 16, 32])
+def test_small_batch_kernels(B):
+    """Batch sizes of decode1 and the paper's Table 3 (B = 8, 32), serving
+    shapes, peaky inputs, both kernels; the library's own choice is the split
+    kernel while its B * Hq * d/32 waves fit on the chip (1024), else the
+    per-head kernel."""
+    dims = synth.DECODE1.with_(B=B)
+    announce(f"step small batch B={B}")
+    c = make_case(dims, 96, seed=40 + B, peaky=True)
+    check_step(c, dims, f"step B={B}")
+    auto = run_step(c, dims)
+    want = "split" if B * dims.Hq * (dims.d // 32) <= 1024 else "whole"
+    assert np.array_equal(auto, run_step(c, dims, kernel=want)), f"automatic choice is not {want}"
