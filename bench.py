@@ -127,18 +127,40 @@ class Lane:
         self.qkv = [(q.clone(), k.clone(), v.clone(), torch.empty_like(q)) for q, k, v in qkv_sets]
 
 
-def build_states(dims, plens, W, gen, dev):
-    """Per-request states of synthetic bf16 prefixes, built by the GPU prefill."""
+def build_states(dims, plens, W, gen, dev, keep=()):
+    """Per-request states of synthetic bf16 prefixes, built by the GPU prefill;
+    the prefix K/V of the requests in `keep` are returned for a re-check."""
     S = torch.zeros((dims.B, dims.Hq, dims.d, dims.f), device=dev)   # S_h transposed
     z = torch.zeros((dims.B, dims.Hq, dims.f), device=dev)
     scale = 1.0 / math.sqrt(dims.d)
+    kept = {}
     for b, P in enumerate(plens.tolist()):
         kp = (torch.randn((1, P, dims.Hkv, dims.d), generator=gen, device=dev) * scale).to(torch.bfloat16)
         vp = (torch.randn((1, P, dims.Hkv, dims.d), generator=gen, device=dev) * scale).to(torch.bfloat16)
         hb.hybrid_state_prefill(None, kp, vp, W, None, S[b:b + 1], z[b:b + 1], dims.L,
                                 want_out=False)
+        if b in keep:
+            kept[b] = (kp.float().cpu().numpy(), vp.float().cpu().numpy())
     torch.cuda.synchronize()
-    return S, z
+    return S, z, kept
+
+
+def recheck_states(S, z, kept, Wt_np):
+    """The prefill-built states of the kept requests against the fp64 oracle's
+    state of the same bf16 prefix (2e-2 x rms of the oracle's state)."""
+    import oracle
+    rows = []
+    for b, (kp, vp) in sorted(kept.items()):
+        Sr, zr = oracle.state_from_prefix(kp, vp, Wt_np)
+        Sg = np.swapaxes(S[b:b + 1].double().cpu().numpy(), -1, -2)
+        zg = z[b:b + 1].double().cpu().numpy()
+        for got, ref, what in ((Sg, Sr, "S"), (zg, zr, "z")):
+            err = float(np.abs(got - ref).max())
+            tol = 2e-2 * float(np.sqrt(np.mean(ref ** 2)))
+            rows.append({"request": b, "prefix_tokens": int(kp.shape[1]), "tensor": what,
+                         "max_abs_err": err, "tol": tol})
+            assert err <= tol, f"request {b} {what}: {err:.3e} > {tol:.3e}"
+    return rows
 
 
 def time_region(fn, iters):
@@ -194,8 +216,13 @@ def run(args):
 
     log(f"building {B} states from {int(plens.sum())} prefix tokens by prefill")
     t0 = time.time()
-    S0, z0 = build_states(dims, plens, W, gen, dev)
+    keep = tuple(int(i) for i in np.argsort(plens, kind="stable")[:2])  # two shortest prefixes
+    S0, z0, kept = build_states(dims, plens, W, gen, dev, keep)
     log(f"states built in {time.time() - t0:.1f} s")
+    state_check = None
+    if not args.no_cpu_baseline:
+        state_check = recheck_states(S0, z0, kept, Wt_np)
+        log("prefill-built states of requests " + ", ".join(map(str, keep)) + " match the oracle")
     scale = 1.0 / math.sqrt(d)
     qkv_sets = []
     for s in range(NSTEP):
@@ -271,6 +298,28 @@ def run(args):
     for kind, e0, e1, n in phases:
         if kind == "commit":
             durs[kind].append(e0.elapsed_time(e1) / n)
+    # Per-launch durations over two cycles' step phases (an event pair around
+    # every launch, no host synchronisation between launches; the pairs add a
+    # little to each launch): median, p10 and p90.
+    per = []
+    for _ in range(2):
+        evs = []
+        for s_ in range(NSTEP - 1):
+            for ln in lanes:
+                q, k, v, o = ln.qkv[s_]
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                hb.hybrid_attn_step(q, k, v, W, alpha, ln.S, ln.z, out=o)
+                e1.record()
+                evs.append((e0, e1))
+        for ln in lanes:
+            q, k, v, o = ln.qkv[NSTEP - 1]
+            hb.hybrid_attn_step_commit(q, k, v, W, alpha, ln.S, ln.z, out=o)
+        torch.cuda.synchronize()
+        per += [e0.elapsed_time(e1) * 1e3 for e0, e1 in evs]
+    step_dist = {"median_us": float(np.median(per)), "p10_us": float(np.percentile(per, 10)),
+                 "p90_us": float(np.percentile(per, 90)), "launches": len(per),
+                 "note": "HIP event pair around each launch inside the cycle"}
     t_step = float(np.mean(durs["step"])) * 1e-3
     t_fused = float(np.mean(durs["step_commit"])) * 1e-3
     t_commit = float(np.mean(durs["commit"])) * 1e-3
@@ -300,11 +349,12 @@ def run(args):
                                "with the block's commit",
                    "global_batch": B, "seq_len": L, "lanes": R, "parallelism": "none (1 GPU)",
                    "state_dtype": "fp32", "prefix_tokens": int(plens.sum())},
+        "state_recheck": state_check,
         "roofline": {"bound": "hbm", "achieved": step_gbps, "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": step_gbps / HBM_PEAK_GBPS, "traffic": traffic,
                      "kernel": "hyb_step_kernel<bf16,128,64>",
                      "algorithmic_bytes_per_launch": sb, "mean_launch_us": t_step * 1e6},
-        "step_kernel": {"mean_us": t_step * 1e6,
+        "step_kernel": {"mean_us": t_step * 1e6, "distribution": step_dist,
                         "min_cycle_mean_us": float(np.min(durs["step"])) * 1e3,
                         "max_cycle_mean_us": float(np.max(durs["step"])) * 1e3,
                         "gbps": step_gbps, "tokens_per_s": B * L / t_step,
@@ -321,6 +371,9 @@ def run(args):
 
     result["table4"] = table4()
     if not args.no_extras:
+        result["small_batch"] = bench_small_batch(gen, dev)
+        result["serve64_f256"] = bench_f256(gen, dev)
+        result["copy_ceiling"] = copy_ceiling(dev)
         result["prefill"] = bench_prefill(gen, dev)
         result["softmax_prefix"] = bench_mix(gen, dev)
         result["table3"] = bench_table3(gen, dev)
@@ -328,6 +381,8 @@ def run(args):
     if not args.no_cpu_baseline:
         log("timing the fp64 oracle on the host cores")
         result["cpu_baseline"] = cpu_baseline(dims, args.cpu_requests, plens)
+        log("timing the fp64 oracle on one core")
+        result["cpu_baseline_1core"] = cpu_baseline_1core(dims, plens)
         if not args.no_extras:
             result["prefill"]["cpu_oracle"] = cpu_prefill()
             result["softmax_prefix"]["cpu_oracle"] = cpu_softmax_prefix()
@@ -344,6 +399,118 @@ def run(args):
 
 def _omp_threads():
     return int(os.environ.get("OMP_NUM_THREADS", os.cpu_count() or 1))
+
+
+def cpu_baseline_1core(dims, plens, n_req=4, budget_s=6.0):
+    """The same oracle block cycles on one host thread, over fewer requests."""
+    import oracle
+    before = oracle.max_threads()
+    oracle.set_threads(1)
+    try:
+        r = cpu_baseline(dims, n_req, plens, budget_s)
+    finally:
+        oracle.set_threads(before)
+    r["cores"] = 1
+    return r
+
+
+def bench_small_batch(gen, dev, batches=(1, 8, 16, 32)):
+    """decode1 (B = 1) and the Table 3 batches: one step (16q/4kv, d = 128,
+    f = 128, block 32, bf16) with each of the step's two kernels and with the
+    library's choice; median of 20 individually timed calls on cold states
+    (HIP events around each call, so the launch's own latency is included;
+    the rocprofv3 kernel trace of `--only-small-batch` gives kernel time)."""
+    d0 = synth.SERVE64
+    Hq, Hkv, d, L, f = d0.Hq, d0.Hkv, d0.d, d0.L, d0.f
+    Wt, alpha = synth.feature_weights(d0, 1, 2)
+    W = torch.from_numpy(Wt).to(dev).to(torch.bfloat16)
+    al = torch.from_numpy(alpha).to(dev)
+    sc = 1.0 / math.sqrt(d)
+    rows = []
+    for B in batches:
+        n_st = max(2, -(-COLD_BYTES // (B * Hq * f * d * 4)))
+        states = [(torch.rand((B, Hq, d, f), generator=gen, device=dev) * 0.01,
+                   torch.rand((B, Hq, f), generator=gen, device=dev) + 1.0) for _ in range(n_st)]
+        q = (torch.randn((B, L, Hq, d), generator=gen, device=dev) * sc).to(torch.bfloat16)
+        k = (torch.randn((B, L, Hkv, d), generator=gen, device=dev) * sc).to(torch.bfloat16)
+        v = (torch.randn((B, L, Hkv, d), generator=gen, device=dev) * sc).to(torch.bfloat16)
+        out = torch.empty_like(q)
+        row = {"B": B, "bytes": step_bytes(B, Hq, Hkv, d, L, f)}
+        for kern in ("split", "whole", None):
+            it = [0]
+
+            def fn():
+                S, z = states[it[0] % n_st]
+                it[0] += 1
+                hb.hybrid_attn_step(q, k, v, W, al, S, z, out=out, kernel=kern)
+
+            # one call on every state first: the first touch of each buffer
+            # by a kernel costs extra, which the timed calls must not carry
+            for _ in range(n_st):
+                fn()
+            row[f"{kern or 'auto'}_us"] = median_ms(fn) * 1e3
+        rows.append(row)
+        log(f"small batch B={B:2d}: split {row['split_us']:.1f} us, whole {row['whole_us']:.1f} us, "
+            f"library's choice {row['auto_us']:.1f} us")
+        del states
+        torch.cuda.empty_cache()
+    return {"workload": "one hybrid step, 16q/4kv, d=128, f=128, block 32, bf16, cold states; "
+                        "B=1 is decode1, B=8 and 32 the Table 3 batches", "rows": rows}
+
+
+def bench_f256(gen, dev, lanes=4, reps=10):
+    """The serve64 step at f = 256 (phi in R^{2F} with F = d: the other
+    reading of the feature dimension), 4 cold state lanes: a sensitivity row."""
+    dims = synth.SERVE64
+    B, Hq, Hkv, d, L = dims.B, dims.Hq, dims.Hkv, dims.d, dims.L
+    f = 256
+    Wt, alpha = synth.feature_weights(dims.with_(F=f // 2), 1, 2)
+    W = torch.from_numpy(Wt).to(dev).to(torch.bfloat16)
+    al = torch.from_numpy(alpha).to(dev)
+    sc = 1.0 / math.sqrt(d)
+    q = (torch.randn((B, L, Hq, d), generator=gen, device=dev) * sc).to(torch.bfloat16)
+    k = (torch.randn((B, L, Hkv, d), generator=gen, device=dev) * sc).to(torch.bfloat16)
+    v = (torch.randn((B, L, Hkv, d), generator=gen, device=dev) * sc).to(torch.bfloat16)
+    out = torch.empty_like(q)
+    states = [(torch.rand((B, Hq, d, f), generator=gen, device=dev) * 0.01,
+               torch.rand((B, Hq, f), generator=gen, device=dev) + 1.0) for _ in range(lanes)]
+
+    def cyc():
+        for S, z in states:
+            hb.hybrid_attn_step(q, k, v, W, al, S, z, out=out)
+
+    cyc()
+    us = time_region(cyc, reps) / lanes * 1e3
+    byts = step_bytes(B, Hq, Hkv, d, L, f)
+    log(f"serve64 at f=256: step {us:.2f} us")
+    return {"workload": "serve64 step with f = 256 (W_h 128 x 128, 128 KiB of state per head)",
+            "step_us": us, "bytes_per_launch": byts, "gbps": byts / us / 1e3,
+            "frac": byts / us / 1e3 / HBM_PEAK_GBPS}
+
+
+def copy_ceiling(dev, reps=20):
+    """A plain device-to-device copy (torch's copy kernel) on 8 cold buffer
+    pairs per size: the read+write streaming rate this chip reaches without
+    any of the layer's arithmetic, for context."""
+    res = {}
+    for mib in (64, 256):
+        n = (mib << 20) // 4
+        pairs = [(torch.rand(n, device=dev), torch.empty(n, device=dev)) for _ in range(8)]
+        i = [0]
+
+        def cp():
+            src, dst = pairs[i[0] % 8]
+            i[0] += 1
+            dst.copy_(src)
+
+        cp()
+        us = time_region(cp, reps) * 1e3
+        res[f"copy_{mib}MiB_us"] = us
+        res[f"copy_{mib}MiB_tbps"] = 2 * n * 4 / us / 1e6
+        del pairs
+        torch.cuda.empty_cache()
+    res["note"] = "read + write bytes / time; 8 TB/s is the HBM peak"
+    return res
 
 
 def cpu_prefill():
@@ -735,6 +902,10 @@ def main():
                     help="run only the prefill8 timing and print it")
     ap.add_argument("--only-backward", action="store_true",
                     help="run only the attention-transfer backward timing and print it")
+    ap.add_argument("--only-small-batch", action="store_true",
+                    help="run only the small-batch step timing (B = 1, 8, 16, 32) and print it")
+    ap.add_argument("--stream-ceiling", action="store_true",
+                    help="run only the plain copy timing (the streaming ceiling) and print it")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only copy 256 MiB device to device five times (the reference "
                          "kernel for scaling HBM byte counters), then exit")
@@ -761,6 +932,14 @@ def main():
         gen = torch.Generator(device="cuda")
         gen.manual_seed(5)
         print(json.dumps(bench_backward(gen, "cuda")), flush=True)
+        return
+    if args.only_small_batch:
+        gen = torch.Generator(device="cuda")
+        gen.manual_seed(5)
+        print(json.dumps(bench_small_batch(gen, "cuda", (1, 8, 12, 16, 20, 32))), flush=True)
+        return
+    if args.stream_ceiling:
+        print(json.dumps(copy_ceiling("cuda")), flush=True)
         return
     if args.only_table3:
         gen = torch.Generator(device="cuda")

@@ -57,6 +57,8 @@ def _load():
     lib.oracle_softmax_prefix.argtypes = [i] * 6 + [_dp] * 5 + [_ip, _dp]
     lib.oracle_feature_map.argtypes = [i] * 3 + [_dp] * 3
     lib.oracle_backward.argtypes = [i] * 7 + [_dp] * 13
+    lib.oracle_set_threads.argtypes = [i]
+    lib.oracle_max_threads.restype = i
     for fn in (lib.oracle_step, lib.oracle_commit, lib.oracle_prefill,
                lib.oracle_softmax_prefix, lib.oracle_feature_map, lib.oracle_backward):
         fn.restype = ctypes.c_int
@@ -244,6 +246,15 @@ def backward(q, k, v, Wt, alpha, L, dout=None, target=None, inputs=False):
     if inputs:
         return dW, da, loss, dq, dk, dv
     return dW, da, loss
+
+
+def set_threads(n: int) -> None:
+    """Host threads the oracle's loops use from now on."""
+    _load().oracle_set_threads(int(n))
+
+
+def max_threads() -> int:
+    return int(_load().oracle_max_threads())
 
 
 def empty_state(n_slots, Hq, f, d):
