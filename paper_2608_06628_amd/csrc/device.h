@@ -112,6 +112,19 @@ __device__ inline float load_op<float>(const float* p) {
   return *p;
 }
 
+// E consecutive elements of T at byte offset voff + soff of the raw buffer r
+// (voff per lane, soff wave-uniform): no 64-bit address per lane.
+template <typename T>
+__device__ inline typename Mma<T>::op_t buf_op(__amdgpu_buffer_rsrc_t r, int voff, int soff);
+template <>
+__device__ inline bf16x8 buf_op<bf16>(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+template <>
+__device__ inline float buf_op<float>(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
+}
+
 // E fp32 values converted to an operand (bf16 round-to-nearest-even).
 template <typename T>
 __device__ inline typename Mma<T>::op_t cvt_op(const float* x);
@@ -298,25 +311,34 @@ __device__ inline float unpack_hi(uint32_t p) { return __builtin_bit_cast(float,
 __device__ inline float unpack_lo(uint32_t p) { return __builtin_bit_cast(float, p & 0xffff0000u); }
 
 // The hi and lo operands of a row of packed pairs, elements in accumulator
-// order (as lds_op_perm): two runs of 4 consecutive entries.
-__device__ inline void lds_pair_op(const uint32_t* row, int ks, int hh, bf16x8& hi,
-                                   bf16x8& lo) {
-  typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
-  const u32x4 a = *reinterpret_cast<const u32x4*>(row + 16 * ks + 4 * hh);
-  const u32x4 b = *reinterpret_cast<const u32x4*>(row + 16 * ks + 8 + 4 * hh);
-  typedef unsigned u32x4v __attribute__((ext_vector_type(4)));
-  u32x4v h, l;
+// order (as lds_op_perm): two runs of 4 consecutive entries.  Split into the
+// two reads and the unpacking, for callers that request many operands
+// before using them.
+typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+struct PairRaw {
+  u32x4 a, b;
+};
+__device__ inline PairRaw lds_pair_raw(const uint32_t* row, int ks, int hh) {
+  return PairRaw{*reinterpret_cast<const u32x4*>(row + 16 * ks + 4 * hh),
+                 *reinterpret_cast<const u32x4*>(row + 16 * ks + 8 + 4 * hh)};
+}
+__device__ inline void pair_split(const PairRaw& p, bf16x8& hi, bf16x8& lo) {
+  u32x4 h, l;
   // low halves of consecutive dwords -> hi pieces, high halves -> lo pieces
-  h[0] = __builtin_amdgcn_perm(a[1], a[0], 0x05040100u);
-  h[1] = __builtin_amdgcn_perm(a[3], a[2], 0x05040100u);
-  h[2] = __builtin_amdgcn_perm(b[1], b[0], 0x05040100u);
-  h[3] = __builtin_amdgcn_perm(b[3], b[2], 0x05040100u);
-  l[0] = __builtin_amdgcn_perm(a[1], a[0], 0x07060302u);
-  l[1] = __builtin_amdgcn_perm(a[3], a[2], 0x07060302u);
-  l[2] = __builtin_amdgcn_perm(b[1], b[0], 0x07060302u);
-  l[3] = __builtin_amdgcn_perm(b[3], b[2], 0x07060302u);
+  h[0] = __builtin_amdgcn_perm(p.a[1], p.a[0], 0x05040100u);
+  h[1] = __builtin_amdgcn_perm(p.a[3], p.a[2], 0x05040100u);
+  h[2] = __builtin_amdgcn_perm(p.b[1], p.b[0], 0x05040100u);
+  h[3] = __builtin_amdgcn_perm(p.b[3], p.b[2], 0x05040100u);
+  l[0] = __builtin_amdgcn_perm(p.a[1], p.a[0], 0x07060302u);
+  l[1] = __builtin_amdgcn_perm(p.a[3], p.a[2], 0x07060302u);
+  l[2] = __builtin_amdgcn_perm(p.b[1], p.b[0], 0x07060302u);
+  l[3] = __builtin_amdgcn_perm(p.b[3], p.b[2], 0x07060302u);
   hi = __builtin_bit_cast(bf16x8, h);
   lo = __builtin_bit_cast(bf16x8, l);
+}
+__device__ inline void lds_pair_op(const uint32_t* row, int ks, int hh, bf16x8& hi,
+                                   bf16x8& lo) {
+  pair_split(lds_pair_raw(row, ks, hh), hi, lo);
 }
 
 // The same for 8 consecutive packed entries (natural order): row + 16*ks +

@@ -30,6 +30,8 @@
 // score tile (token row_of(ks*E+e, hh)), so one set of V registers serves
 // both P V and the commit.  As in the commit kernel, phi(K) enters the state
 // update as a bf16 pair hi + lo on the bf16 path.
+#include <type_traits>
+
 #include "device.h"
 #include "featmap.h"
 #include "launch.h"
@@ -368,54 +370,57 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_prefill_kernel(
 
 // ---------------------------------------------------------------------------
 // Pipelined walk (bf16, F <= 64, outputs wanted): one workgroup per (request,
-// head, segment) with producer and state waves working on consecutive blocks.
-//   producer waves (NP = 2 + D/64), block c+1:
-//     wave 0: phi(Q) of the block, the whole feature map in one wave;
-//     wave 1: phi(K), likewise, written transposed (the commit's A operand);
-//     waves 2..: the in-block softmax branch for 64 columns each: scores,
-//                row max and sum, P V relative to the row max;
-//   state waves (D/32), block c: the readout against the state of the blocks
-//     before c, the merge, the output store, the commit of c into S
-//     (columns 32w..32w+31 in fp32 accumulators) and z.
-// The two groups meet at one barrier per block; everything they exchange is
-// double-buffered in LDS, and z too (the state waves read z_c while writing
-// z_{c+1}).  Within a group no barrier is needed: the feature map's row
-// maximum and sum stay inside the wave.  Arithmetic and operand precision
-// are those of the single-group walk above.
+// head, segment), 4 + D/32 waves.  The roles work on different blocks of the
+// segment and meet at one barrier per iteration; in iteration it:
+//   QS waves (0, 1: even and odd blocks): phi(Q) and the in-block softmax of
+//     a block over two iterations -- the logits, the scores, the first
+//     exponentials and the softmax rows of block it+1, then the rest of
+//     phi(Q) of block it, its store and the store of P (a bf16 pair hi + lo);
+//   K waves (2, 3): phi(K) likewise, stored transposed as hi | lo pairs;
+//   state waves (D/32): the merge and output store of block it-2; then, for
+//     block it-1: the V^T operands of the wave's 32 columns, the readout
+//     phi(Q) S against the state of the blocks before it, the wave's share
+//     of lin_den = phi(Q) z (its feature tiles of z, on the MFMAs), P V of
+//     its columns and the commit into S columns 32w .. 32w+31 (fp32
+//     accumulators) and z.
+// The QS and K waves hand a block to the state waves through a double
+// buffer (written in iteration c, read in c+1); the lin_den shares go from
+// the state waves to each other through a second one; W_h^T stays in LDS.
+// Arithmetic and operand precision are those of the single-group walk above.
 // ---------------------------------------------------------------------------
 template <typename T, int D, int F>
 struct PrefillPipeCfg {
   typedef Mma<T> M;
   typedef typename M::op_t op_t;
-  static constexpr int NC = D / kTile;              // state waves
-  static constexpr int NSM = D / 64 > 0 ? D / 64 : 1;  // softmax waves
-  static constexpr int CT = NC / NSM;               // column tiles per softmax wave
-  static constexpr int NP = 2 + NSM;                // producer waves
-  static constexpr int NWAVE = NP + NC;
+  static constexpr int NC = D / kTile;  // state waves
+  static constexpr int NWAVE = 4 + NC;
   static constexpr int f = 2 * F;
+  static constexpr int NT = F / kTile;
+  static constexpr int NPAIR = 2 * NT;
   static constexpr int NRT = f / kTile;
+  static constexpr int ZPW = (NRT + NC - 1) / NC;  // z tiles per state wave
   static constexpr int KD = D / M::KW;
   static constexpr int KL = kTile / M::KW;
   static constexpr int KF = f / M::KW;
   static constexpr int PAD = 16 / (int)sizeof(T);
-  typedef WaveFeatMap<T, D, F> WFM;
-  struct alignas(16) Buf {
-    T phiQ[kTile][f + PAD];          // phi(q_i)[r] at [i][r]
-    uint32_t phiKT[f][kTile + 4];    // phi(k_t)[r] at [r][t]: bf16 hi | lo << 16
-    float sm[kTile][D + 4];          // P V relative to the row max, [i][c];
-                                     // then the state waves' outputs
-    float m[kTile], den[kTile];
-    op_t vop[NC][KL][kWave];         // V operands (column tile, k-step, lane)
+  struct alignas(16) Buf {            // written in iteration c, read in c + 1
+    T phiQ[kTile][f + PAD];           // phi(q_i)[r] at [i][r]
+    uint32_t phiKT[f][kTile + 4];     // phi(k_t)[r] at [r][t]: bf16 hi | lo << 16
+    T ph[kTile][kTile + PAD];         // P (relative to the row max) as hi + lo,
+    T pl[kTile][kTile + PAD];         //   [query][key]
+    float m[kTile], den[kTile];       // row max and sum of the block scores
   };
   struct alignas(16) Smem {
     Buf buf[2];
-    float z[2][f];
+    float lden[2][NC][kTile];         // lin_den shares
+    float stage[NC][kTile][kTile + 4];  // output staging, one tile per state wave
+    T W[F][D + PAD];                  // W_h^T
   };
 };
 
 template <int D>
 constexpr int pipe_threads() {
-  return kWave * (2 + (D / 64 > 0 ? D / 64 : 1) + D / kTile);
+  return kWave * (4 + D / kTile);
 }
 
 template <typename T, int D, int F>
@@ -424,8 +429,9 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
   typedef PrefillPipeCfg<T, D, F> C;
   typedef typename C::M M;
   typedef typename C::op_t op_t;
-  typedef typename C::WFM WFM;
-  constexpr int f = C::f, E = M::E, KW = M::KW, NP = C::NP, NC = C::NC;
+  typedef WaveFeatMap<T, D, F> WFM;
+  constexpr int f = C::f, E = M::E, KW = M::KW, NT = C::NT, NC = C::NC;
+  static_assert(sizeof(T) == 2, "the pipelined walk is the bf16 path");
   static_assert(pipe_threads<D>() == kWave * C::NWAVE, "launch bounds match the waves");
   __shared__ typename C::Smem sh;
 
@@ -444,6 +450,7 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
   const size_t qstride = (size_t)Hq * D, kstride = (size_t)Hkv * D;
   const int nblk = T_ / L;
   const int blk0 = seg * seg_blocks, blk1 = min(nblk, blk0 + seg_blocks);
+  const int nit = blk1 - blk0 + 3;  // iterations blk0-1 .. blk1+1
   if (slot < 0 || slot >= a.s.n_slots) {  // uniform per workgroup
     const size_t ob = ((size_t)b * T_ * Hq + h) * D;
     for (int t = blk0 * L; t < blk1 * L; ++t)
@@ -451,167 +458,235 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
         store_out1<T>(a.out, ob + (size_t)t * qstride + c, __builtin_nanf(""), a.s.out_f32);
     return;
   }
-  const bool producer = w < NP;
-  const int cw = w - NP;                    // state wave index (columns 32cw..)
-  const int col = cw * kTile + li;
-  const size_t sbase = (size_t)slot * Hq + h;
-  float* __restrict__ Sh = a.S + sbase * f * D;
-  float* __restrict__ zh = a.z + sbase * f;
-  float* __restrict__ wsS = a.ws + (size_t)u * (nseg - 1) * D * f;
-  float* __restrict__ wsz = a.ws + (size_t)units * (nseg - 1) * D * f + (size_t)u * (nseg - 1) * f;
-  const float* __restrict__ S0 = nseg > 1 ? prefill_snapshot_S(a, nseg, u) : Sh;
-  const float* __restrict__ z0 = nseg > 1 ? prefill_snapshot_z(a, nseg, u) : zh;
   const bool row_ok = li < L;
   const int lrow = min(li, L - 1);
-
-  // z + the earlier segments' increments into z[0] (the state waves' S
-  // likewise, in their own branch below).
-  if (!producer) {
-    for (int r = tid - NP * kWave; r < f; r += NC * kWave) {
-      float zr = z0[r];
-      for (int s = 0; s < seg; ++s) zr += wsz[(size_t)s * f + r];
-      sh.z[0][r] = zr;
-    }
-  }
-
-  const float scale = 1.0f / sqrtf((float)D);
-  const float lw = log_sigmoid(a.alpha[h]);
-  auto qbase = [&](int blk) {
-    return (const T*)a.q + (((size_t)b * T_ + (size_t)blk * L) * Hq + h) * D;
-  };
-  auto kbase = [&](int blk) {
-    return (const T*)a.k + (((size_t)b * T_ + (size_t)blk * L) * Hkv + g) * D;
-  };
-  auto vbase = [&](int blk) {
-    return (const T*)a.v + (((size_t)b * T_ + (size_t)blk * L) * Hkv + g) * D;
-  };
+  // Raw buffers over this request's rows of q, k and v: a block's offset is
+  // a scalar, a lane's row offset one 32-bit register, a k-step's the
+  // immediate (the launcher keeps a request's rows under 2 GiB).
+  const __amdgpu_buffer_rsrc_t qrs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<T*>((const T*)a.q + (size_t)b * T_ * qstride), 0, (int)(T_ * qstride * sizeof(T)),
+      kBufferWord3);
+  const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<T*>((const T*)a.k + (size_t)b * T_ * kstride), 0, (int)(T_ * kstride * sizeof(T)),
+      kBufferWord3);
+  const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<T*>((const T*)a.v + (size_t)b * T_ * kstride), 0, (int)(T_ * kstride * sizeof(T)),
+      kBufferWord3);
+  const int qlane = (lrow * (int)qstride + hh * E) * (int)sizeof(T);
+  const int klane = (lrow * (int)kstride + hh * E) * (int)sizeof(T);
+  auto qoff = [&](int blk) { return (int)(((size_t)blk * L * qstride + (size_t)h * D) * sizeof(T)); };
+  auto koff = [&](int blk) { return (int)(((size_t)blk * L * kstride + (size_t)g * D) * sizeof(T)); };
   // Rows of a block tile as operands (rows past the block length read row
   // L-1; the roles mask them).
-  auto load_rows = [&](const T* base, size_t stride, op_t (&o)[C::KD]) {
-    const T* row = base + (size_t)lrow * stride + hh * E;
+  auto load_q = [&](int blk, op_t (&o)[C::KD]) {
+    const int so = qoff(blk);
 #pragma unroll
-    for (int ks = 0; ks < C::KD; ++ks) o[ks] = load_op<T>(row + ks * KW);
+    for (int ks = 0; ks < C::KD; ++ks) o[ks] = buf_op<T>(qrs, qlane + ks * KW * (int)sizeof(T), so);
   };
-  lds_barrier();  // z[0] ready
-
-  // Each role runs its own loop over the iterations blk0 .. blk1 (producers
-  // work on block it, the state waves on block it - 1) with one barrier per
-  // iteration, so that every role keeps only its own operands in registers.
-  if (w < 2) {
-    // ---- feature map of Q (wave 0) or K (wave 1) ----
-    const T* __restrict__ Wt_h = (const T*)a.W + (size_t)h * F * D;
-    op_t wop[WFM::NT][C::KD];
-    WFM::load_w(Wt_h, li, hh, wop);
-    op_t x[C::KD];
-    auto load = [&](int blk) {
-      if (w == 0) load_rows(qbase(blk), qstride, x);
-      else load_rows(kbase(blk), kstride, x);
-    };
-    if (blk0 < blk1) load(blk0);
-    for (int it = blk0; it <= blk1; ++it) {
-      if (it < blk1) {
-        typename C::Buf& B = sh.buf[(it - blk0) & 1];
-        // a padding row reads row L-1 (finite); keep = row_ok zeroes its phi
-        float phi[WFM::NPAIR][16];
-        WFM::logits(wop, x, phi);
-        if (it + 1 < blk1) load(it + 1);  // next block in flight
-        WFM::softmax(phi, row_ok);
-        if (w == 0) {
+  auto load_k = [&](int blk, op_t (&o)[C::KD]) {
+    const int so = koff(blk);
 #pragma unroll
-          for (int p = 0; p < WFM::NPAIR; ++p)
+    for (int ks = 0; ks < C::KD; ++ks) o[ks] = buf_op<T>(krs, klane + ks * KW * (int)sizeof(T), so);
+  };
+
+  // Set-up: W_h^T into LDS.
+  {
+    const T* __restrict__ Wt_h = (const T*)a.W + (size_t)h * F * D;
+    constexpr int RP = D / 8;  // 16-byte pieces per row
+    for (int i = tid; i < F * RP; i += C::NWAVE * kWave) {
+      const int r = i / RP, c = (i % RP) * 8;
+      *reinterpret_cast<uint4*>(&sh.W[r][c]) = *reinterpret_cast<const uint4*>(Wt_h + (size_t)r * D + c);
+    }
+  }
+  lds_barrier();  // W ready
+
+  constexpr float kLog2e = 1.4426950408889634f;
+  // logits U^T = W^T X^T of the rows x, from the LDS copy of W_h^T
+  // (the W operands of a tile requested together, then its products)
+  auto logits = [&](const op_t (&x)[C::KD], float (&phi)[C::NPAIR][16]) {
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      op_t wo[C::KD];
+#pragma unroll
+      for (int ks = 0; ks < C::KD; ++ks) wo[ks] = load_op<T>(&sh.W[t * kTile + li][ks * KW + hh * E]);
+      __builtin_amdgcn_sched_barrier(0);
+      f32x16 acc = {};
+#pragma unroll
+      for (int ks = 0; ks < C::KD; ++ks) acc = M::mma(wo[ks], x[ks], acc);
+#pragma unroll
+      for (int i = 0; i < 16; ++i) phi[t][i] = acc[i];
+    }
+  };
+  // Feature-map halves: the row extremes, every first-sign exponential and
+  // the first NA of the second sign (the other second-sign slots keep the
+  // logit); then the rest, the sums and the normalisation (keep = row_ok
+  // zeroes a padding row).  e^(u - mx) = 2^(u log2 e - mx log2 e): one fma
+  // per exponent; the rounding of mx log2 e is common to the row and cancels
+  // in the ratio.
+  auto fm_first = [&](float (&phi)[C::NPAIR][16], int NA, float& mnl, float& sp, float& sn) {
+    float mx = -INFINITY, mn = INFINITY;
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        mx = fmaxf(mx, phi[t][i]);
+        mn = fminf(mn, phi[t][i]);
+      }
+    mx = fmaxf(mx, xor32(mx));
+    mn = fminf(mn, xor32(mn));
+    const float mxl = mx * kLog2e;
+    mnl = mn * kLog2e;
+    sp = 0.0f;
+    sn = 0.0f;
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const float uu = phi[t][i];
+        if (t * 16 + i < NA) {
+          phi[NT + t][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(-uu, kLog2e, mnl));
+          sn += phi[NT + t][i];
+        } else {
+          phi[NT + t][i] = uu;
+        }
+        phi[t][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(uu, kLog2e, -mxl));
+        sp += phi[t][i];
+      }
+  };
+  auto fm_second = [&](float (&phi)[C::NPAIR][16], int NA, float mnl, float sp, float sn) {
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        if (t * 16 + i < NA) continue;
+        phi[NT + t][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(-phi[NT + t][i], kLog2e, mnl));
+        sn += phi[NT + t][i];
+      }
+    sp += xor32(sp);
+    sn += xor32(sn);
+    const float ip = row_ok ? 1.0f / sp : 0.0f, in = row_ok ? 1.0f / sn : 0.0f;
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        phi[t][i] *= ip;
+        phi[NT + t][i] *= in;
+      }
+  };
+
+  if (w < 4) {
+    // ---- QS waves (0, 1) and K waves (2, 3): blocks c = blk0 + par + 2j;
+    // the first half of block c in iteration c-1, the second in iteration c;
+    // the odd wave idles in the first iteration, and both idle after their
+    // last block, so that every wave passes nit barriers, as the state waves
+    // do ----
+    const int par = w & 1;
+    auto role = [&](auto key) {
+      constexpr bool K = decltype(key)::value;
+      // phi(K) stores more (the hi | lo pairs), so it moves more of its
+      // exponentials into the first half
+      constexpr int NA = K ? NT * 8 : 0;
+      op_t x[C::KD], xk[K ? 1 : C::KD];
+      auto load = [&](int blk) {
+        if constexpr (K) {
+          load_k(blk, x);
+        } else {
+          load_q(blk, x);
+          load_k(blk, xk);
+        }
+      };
+      if (blk0 + par < blk1) load(blk0 + par);
+      int nbar = 0;
+      if (par) {
+        lds_barrier();
+        ++nbar;
+      }
+      const float scale = 1.0f / sqrtf((float)D);
+      for (int c = blk0 + par; c < blk1; c += 2) {
+        // ---- iteration c-1 ----
+        float phi[C::NPAIR][16];
+        logits(x, phi);
+        f32x16 sc = {};
+        if constexpr (!K) {
+          // scores: keys in rows, queries in columns
+#pragma unroll
+          for (int ks = 0; ks < C::KD; ++ks)
+            sc = M::mma(keep_if<T>(row_ok, xk[ks]), keep_if<T>(row_ok, x[ks]), sc);
+        }
+        // (the operands are read by the products above before the rows of
+        // this wave's next block land in the same registers)
+        __builtin_amdgcn_sched_barrier(0);
+        if (c + 2 < blk1) load(c + 2);
+        float mnl, sp, sn;
+        fm_first(phi, NA, mnl, sp, sn);
+        float pr[16], m = 0.0f, den = 0.0f;
+        if constexpr (!K) {
+          m = -INFINITY;
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            pr[i] = row_of(i, hh) < L ? sc[i] * scale : -INFINITY;
+            m = fmaxf(m, pr[i]);
+          }
+          m = fmaxf(m, xor32(m));
+#pragma unroll
+          for (int i = 0; i < 16; ++i) {
+            pr[i] = row_of(i, hh) < L ? fast_exp(pr[i] - m) : 0.0f;
+            den += pr[i];
+          }
+          den += xor32(den);
+        }
+        lds_barrier();
+        // ---- iteration c ----
+        fm_second(phi, NA, mnl, sp, sn);
+        typename C::Buf& B = sh.buf[(c - blk0) & 1];
+        if constexpr (!K) {
+#pragma unroll
+          for (int p = 0; p < C::NPAIR; ++p)
 #pragma unroll
             for (int i = 0; i < 16; ++i) B.phiQ[li][WFM::feature(16 * p + i, hh)] = from_f32<T>(phi[p][i]);
+          // P of query li, keys row_of(i, hh): runs of 4 consecutive keys
+#pragma unroll
+          for (int i = 0; i < 16; i += 4) {
+            bf16x4 hi4, lo4;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              hi4[e] = (T)pr[i + e];
+              lo4[e] = (T)(pr[i + e] - (float)hi4[e]);
+            }
+            *reinterpret_cast<bf16x4*>(&B.ph[li][row_of(i, hh)]) = hi4;
+            *reinterpret_cast<bf16x4*>(&B.pl[li][row_of(i, hh)]) = lo4;
+          }
+          if (hh == 0) {
+            B.m[li] = m;
+            B.den[li] = den;
+          }
         } else {
 #pragma unroll
-          for (int p = 0; p < WFM::NPAIR; ++p)
+          for (int p = 0; p < C::NPAIR; ++p)
 #pragma unroll
             for (int i = 0; i < 16; i += 2)
               pack_hi_lo2(phi[p][i], phi[p][i + 1], B.phiKT[WFM::feature(16 * p + i, hh)][li],
                           B.phiKT[WFM::feature(16 * p + i + 1, hh)][li]);
         }
+        lds_barrier();
+        nbar += 2;
       }
-      lds_barrier();
-    }
-  } else if (producer) {
-    // ---- in-block softmax branch for column tiles c0 .. c0+CT-1 ----
-    const int c0 = (w - 2) * C::CT;
-    // V rows of this wave's column tiles (lane: token, 16 contiguous bytes
-    // per load), turned into V^T operands by a product with the identity
-    op_t ko[C::KD], qo[C::KD], vx[C::CT][C::KL];
-    auto load = [&](int blk) {
-      load_rows(kbase(blk), kstride, ko);
-      load_rows(qbase(blk), qstride, qo);
-      const T* vrow = vbase(blk) + (size_t)lrow * kstride + hh * E;
-#pragma unroll
-      for (int ct = 0; ct < C::CT; ++ct)
-#pragma unroll
-        for (int ks = 0; ks < C::KL; ++ks) vx[ct][ks] = load_op<T>(vrow + (c0 + ct) * kTile + ks * KW);
+      for (; nbar < nit; ++nbar) lds_barrier();
     };
-    op_t ident[C::KL];
-#pragma unroll
-    for (int ks = 0; ks < C::KL; ++ks)
-#pragma unroll
-      for (int e = 0; e < E; ++e) ident[ks][e] = (T)(ks * KW + hh * E + e == li ? 1.0f : 0.0f);
-    if (blk0 < blk1) load(blk0);
-    for (int it = blk0; it <= blk1; ++it) {
-      if (it < blk1) {
-        typename C::Buf& B = sh.buf[(it - blk0) & 1];
-        // keys in rows, queries in columns
-        f32x16 sc = {};
-#pragma unroll
-        for (int ks = 0; ks < C::KD; ++ks)
-          sc = M::mma(keep_if<T>(row_ok, ko[ks]), keep_if<T>(row_ok, qo[ks]), sc);
-        // V^T (lane: column, elements: tokens in row_of order; padding
-        // tokens zero) from V_c = V_c I, exact: one nonzero product per entry
-        op_t vc[C::CT][C::KL];
-#pragma unroll
-        for (int ct = 0; ct < C::CT; ++ct) {
-          f32x16 va = {};
-#pragma unroll
-          for (int ks = 0; ks < C::KL; ++ks) va = M::mma(keep_if<T>(row_ok, vx[ct][ks]), ident[ks], va);
-#pragma unroll
-          for (int ks = 0; ks < C::KL; ++ks) vc[ct][ks] = acc_op_exact<T>(va, ks);
-        }
-        if (it + 1 < blk1) load(it + 1);  // next block in flight
-        float pr[16];
-        float m = -INFINITY;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          pr[i] = row_of(i, hh) < L ? sc[i] * scale : -INFINITY;
-          m = fmaxf(m, pr[i]);
-        }
-        m = fmaxf(m, xor32(m));
-        float den = 0.0f;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          pr[i] = row_of(i, hh) < L ? fast_exp(pr[i] - m) : 0.0f;
-          den += pr[i];
-        }
-        den += xor32(den);
-#pragma unroll
-        for (int ct = 0; ct < C::CT; ++ct) {
-          f32x16 acc = {};
-#pragma unroll
-          for (int ks = 0; ks < C::KL; ++ks) acc = mma_split_b<T>(vc[ct][ks], &pr[ks * E], acc);
-#pragma unroll
-          for (int i = 0; i < 16; i += 4)
-            *reinterpret_cast<f32x4*>(&B.sm[li][(c0 + ct) * kTile + row_of(i, hh)]) =
-                f32x4{acc[i], acc[i + 1], acc[i + 2], acc[i + 3]};
-        }
-        if (w == 2 && hh == 0) {
-          B.m[li] = m;
-          B.den[li] = den;
-        }
-        // the same V operands serve the state waves' commit of this block
-#pragma unroll
-        for (int ct = 0; ct < C::CT; ++ct)
-#pragma unroll
-          for (int ks = 0; ks < C::KL; ++ks) B.vop[c0 + ct][ks][lane] = vc[ct][ks];
-      }
-      lds_barrier();
-    }
+    if (w >= 2) role(std::true_type{});
+    else role(std::false_type{});
   } else {
-    // ---- state waves: readout, merge, store and commit of block it - 1 ----
+    // ---- state waves: merge and store of block it-2; V^T, readout,
+    // lin_den share, P V and commit of block it-1 ----
+    const int cw = w - 4;
+    const int col = cw * kTile + li;
+    const size_t sbase = (size_t)slot * Hq + h;
+    float* __restrict__ Sh = a.S + sbase * f * D;
+    float* __restrict__ zh = a.z + sbase * f;
+    const float* __restrict__ wsS = a.ws + (size_t)u * (nseg - 1) * D * f;
+    const float* __restrict__ wsz = a.ws + (size_t)units * (nseg - 1) * D * f + (size_t)u * (nseg - 1) * f;
+    const float* __restrict__ S0 = nseg > 1 ? prefill_snapshot_S(a, nseg, u) : Sh;
+    const float* __restrict__ z0 = nseg > 1 ? prefill_snapshot_z(a, nseg, u) : zh;
     // S columns col of all f rows: S + the earlier segments' increments.
     // (Declared here, not before the role branches: a value live across the
     // other roles' code takes registers there too.)
@@ -620,131 +695,251 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
     for (int rt = 0; rt < C::NRT; ++rt)
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        f32x4 x = *reinterpret_cast<const f32x4*>(S0 + (size_t)col * f + rt * kTile + row_of(4 * j, hh));
-        for (int s = 0; s < seg; ++s) {
-          const f32x4 y = *reinterpret_cast<const f32x4*>(
-              wsS + (size_t)s * D * f + (size_t)col * f + rt * kTile + row_of(4 * j, hh));
-#pragma unroll
-          for (int r = 0; r < 4; ++r) x[r] += y[r];
-        }
+        const f32x4 x = *reinterpret_cast<const f32x4*>(S0 + (size_t)col * f + rt * kTile + row_of(4 * j, hh));
 #pragma unroll
         for (int r = 0; r < 4; ++r) sacc[rt][4 * j + r] = x[r];
       }
+    for (int s = 0; s < seg; ++s) {
+#pragma unroll
+      for (int rt = 0; rt < C::NRT; ++rt) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const f32x4 y = *reinterpret_cast<const f32x4*>(
+              wsS + (size_t)s * D * f + (size_t)col * f + rt * kTile + row_of(4 * j, hh));
+#pragma unroll
+          for (int r = 0; r < 4; ++r) sacc[rt][4 * j + r] += y[r];
+        }
+        // (one row tile of the increment in flight at a time)
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
     // z of the feature tiles cw, cw + NC, ... as accumulator tiles whose
     // columns are all equal: the commit adds phi(K)^T 1 on the MFMAs
-    constexpr int ZPW = (C::NRT + NC - 1) / NC;
-    f32x16 zt[ZPW];
+    f32x16 zt[C::ZPW];
 #pragma unroll
-    for (int j = 0; j < ZPW; ++j) {
+    for (int j = 0; j < C::ZPW; ++j) {
       const int p = cw + j * NC;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) zt[j][i] = p < C::NRT ? sh.z[0][p * kTile + row_of(i, hh)] : 0.0f;
+      for (int i = 0; i < 16; ++i) {
+        float zr = 0.0f;
+        if (p < C::NRT) {
+          const int r = p * kTile + row_of(i, hh);
+          zr = z0[r];
+          for (int s = 0; s < seg; ++s) zr += wsz[(size_t)s * f + r];
+        }
+        zt[j][i] = zr;
+      }
     }
     op_t ones;
 #pragma unroll
     for (int e = 0; e < E; ++e) ones[e] = (T)1.0f;
-    // (iteration blk0, where the producers fill the first buffer, is peeled:
-    // a branch inside the loop would make the compiler keep a second copy of
-    // the accumulators)
-    lds_barrier();
-    for (int it = blk0 + 1; it <= blk1; ++it) {
-      const int cblk = it - 1;
-      {
-        typename C::Buf& B = sh.buf[(cblk - blk0) & 1];
-        const float* zr = sh.z[(cblk - blk0) & 1];
-        float* zw = sh.z[(cblk - blk0 + 1) & 1];
-        // lin_den = phi(q_li) . z, each lane half over half the features
-        float lden = 0.0f;
+    // V^T operands of this wave's columns, one block ahead: lane li holds
+    // column 32cw + li and, for k-step ks, the tokens row_of(ks*E + e, hh)
+    // (the order in which P and phi(K)^T enter the products), gathered as
+    // 2-byte loads: the token's row is a scalar offset (lane half 1 is 4 rows
+    // further, in the lane's offset), the column the lane's own.  A token at
+    // or past the block length reads the next rows of the request (zero past
+    // its end) and is zeroed.
+    const int vlane = (4 * hh * (int)kstride + cw * kTile + li) * (int)sizeof(T);
+    uint16_t vraw[C::KL][E];
+    auto load_v = [&](int blk) {
+      const int so = koff(blk);
 #pragma unroll
-        for (int r = hh * (f / 2); r < (hh + 1) * (f / 2); r += 8) {
-          const uint4 xq = *reinterpret_cast<const uint4*>(&B.phiQ[li][r]);
-          const T* xt = reinterpret_cast<const T*>(&xq);
+      for (int ks = 0; ks < C::KL; ++ks)
 #pragma unroll
-          for (int e = 0; e < 8; ++e) lden += to_f32(xt[e]) * zr[r + e];
+        for (int e = 0; e < E; ++e)
+          vraw[ks][e] = __builtin_amdgcn_raw_buffer_load_b16(
+              vrs, vlane, so + row_of(ks * E + e, 0) * (int)(kstride * sizeof(T)), 0);
+    };
+    if (blk0 < blk1) load_v(blk0);
+    const float lw = log_sigmoid(a.alpha[h]);
+    // the products of a block, kept from its iteration to its merge in the
+    // next
+    f32x16 olin = {}, apv = {};
+    float m_k = 0.0f, den_k = 0.0f;
+    constexpr int RH = (C::NRT + 1) / 2;
+    for (int it = blk0 - 1; it <= blk1 + 1; ++it) {
+      const int cr = it - 1, cm = it - 2;
+      float (*st)[kTile + 4] = sh.stage[cw];
+      // ---- merge of block cm (its products are in olin, apv) into the
+      // staging tile, then its rows to the output: 8 columns (16 bytes of
+      // bf16) per lane, 64 contiguous bytes per token.  The staging slots are
+      // written by other lanes of this wave; LDS operations of one wave
+      // complete in order, and the wait keeps the compiler from moving the
+      // reads up ----
+      if (cm >= blk0 && cm < blk1) {
+        if (row_ok) {
+          float lden = 0.0f;
+#pragma unroll
+          for (int s = 0; s < NC; ++s) lden += sh.lden[(cm - blk0) & 1][s][li];
+          float ca = 1.0f, cz = 0.0f, rz = 0.0f;
+          if (lden > 0.0f) {
+            const float la = lw + m_k, lb = logf(lden);
+            const float c = fmaxf(la, lb);
+            ca = expf(la - c);
+            cz = expf(lb - c);
+            rz = 1.0f / lden;
+          }
+          const float inv = 1.0f / (ca * den_k + cz);
+#pragma unroll
+          for (int i = 0; i < 16; i += 4) {
+            f32x4 o;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) o[e] = (ca * apv[i + e] + cz * (olin[i + e] * rz)) * inv;
+            *reinterpret_cast<f32x4*>(&st[li][row_of(i, hh)]) = o;
+          }
         }
-        lden += xor32(lden);
-        // readout against the state of the blocks before cblk
-        f32x16 acc_lin = {};
+        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+#pragma unroll
+        for (int pass = 0; pass < 2; ++pass) {
+          const int t = pass * 16 + lane / 4, c8 = (lane & 3) * 8;
+          if (t < L) {
+            const f32x4 x0 = *reinterpret_cast<const f32x4*>(&st[t][c8]);
+            const f32x4 x1 = *reinterpret_cast<const f32x4*>(&st[t][c8 + 4]);
+            const float o8[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+            const size_t oidx = (((size_t)b * T_ + (size_t)cm * L + t) * Hq + h) * D + cw * kTile + c8;
+            store_out8<T>(a.out, oidx, o8, a.s.out_f32);
+          }
+        }
+      }
+      if (cr >= blk0 && cr < blk1) {
+        typename C::Buf& B = sh.buf[(cr - blk0) & 1];
+        // LDS operands are requested in batches ahead of the products that
+        // use them, a scheduling barrier after each batch: fetched one at a
+        // time next to its product, every operand costs a full LDS round
+        // trip.  Batch 1: the row statistics and the operands of the readout
+        // and of the lin_den share.
+        const float m_n = B.m[li], den_n = B.den[li];
+        op_t pb[C::KF], qz[C::ZPW][C::KL];
+#pragma unroll
+        for (int ks = 0; ks < C::KF; ++ks) pb[ks] = lds_op_perm<T>(&B.phiQ[li][0], ks, hh, 0);
+#pragma unroll
+        for (int j = 0; j < C::ZPW; ++j) {
+          // (the tile index is wave-dependent: these operands come from LDS
+          // again rather than from a runtime index into pb)
+          const int p = min(cw + j * NC, C::NRT - 1);
+#pragma unroll
+          for (int kk = 0; kk < C::KL; ++kk) qz[j][kk] = lds_op_perm<T>(&B.phiQ[li][0], p * C::KL + kk, hh, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        // V^T operands of block cr, the next block's gather issued
+        op_t vk[C::KL];
+#pragma unroll
+        for (int ks = 0; ks < C::KL; ++ks)
+#pragma unroll
+          for (int e = 0; e < E; ++e) {
+            const T x = __builtin_bit_cast(T, vraw[ks][e]);
+            vk[ks][e] = row_of(ks * E + e, hh) < L ? x : (T)0.0f;
+          }
+        __builtin_amdgcn_sched_barrier(0);
+        if (cr + 1 < blk1) load_v(cr + 1);
+        // lin_den share: z of this wave's feature tiles (every row of the
+        // tile as A operand, a bf16 pair hi + lo) against phi(Q); taken
+        // before the commit adds block cr
+        f32x16 ld = {};
+#pragma unroll
+        for (int j = 0; j < C::ZPW; ++j) {
+          const int p = cw + j * NC;
+          if (p >= C::NRT) continue;  // uniform
+#pragma unroll
+          for (int kk = 0; kk < C::KL; ++kk) {
+            op_t zhi, zlo;
+#pragma unroll
+            for (int e = 0; e < E; ++e) {
+              const float zv = zt[j][kk * E + e];
+              zhi[e] = (T)zv;
+              zlo[e] = (T)(zv - (float)zhi[e]);
+            }
+            ld = M::mma(zhi, qz[j][kk], ld);
+            ld = M::mma(zlo, qz[j][kk], ld);
+          }
+        }
+        // readout against the state of the blocks before cr
+        f32x16 ol = {};
 #pragma unroll
         for (int ks = 0; ks < C::KF; ++ks) {
-          const op_t pb = lds_op_perm<T>(&B.phiQ[li][0], ks, hh, 0);
           op_t sa;
 #pragma unroll
           for (int e = 0; e < E; ++e) {
             const int j = ks * E + e;
             sa[e] = (T)sacc[j / 16][j % 16];
           }
-          acc_lin = M::mma(sa, pb, acc_lin);
+          ol = M::mma(sa, pb[ks], ol);
         }
-        if (row_ok) {
-          const float m = B.m[li], den = B.den[li];
-          float ca = 1.0f, cz = 0.0f, rz = 0.0f;
-          if (lden > 0.0f) {
-            const float la = lw + m, lb = logf(lden);
-            const float c = fmaxf(la, lb);
-            ca = expf(la - c);
-            cz = expf(lb - c);
-            rz = 1.0f / lden;
-          }
-          const float inv = 1.0f / (ca * den + cz);
-          // outputs over the numerators just read (this lane's own slots)
+        __builtin_amdgcn_sched_barrier(0);
+        // Batch 2: P of block cr and the commit operands of the first half
+        // of the row tiles.
+        op_t pph[C::KL], ppl[C::KL];
+        PairRaw kr[RH][C::KL];
 #pragma unroll
-          for (int i = 0; i < 16; i += 4) {
-            float* sp = &B.sm[li][cw * kTile + row_of(i, hh)];
-            const f32x4 smv = *reinterpret_cast<const f32x4*>(sp);
-            f32x4 o;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) o[e] = (ca * smv[e] + cz * (acc_lin[i + e] * rz)) * inv;
-            *reinterpret_cast<f32x4*>(sp) = o;
-          }
+        for (int ks = 0; ks < C::KL; ++ks) {
+          pph[ks] = lds_op_perm<T>(&B.ph[li][0], ks, hh, 0);
+          ppl[ks] = lds_op_perm<T>(&B.pl[li][0], ks, hh, 0);
         }
-        // This wave's 32 columns of the block's rows, 8 columns (16 bytes of
-        // bf16) per lane: 64 contiguous bytes per token.  The staging slots
-        // were written by other lanes of this wave just above; LDS operations
-        // of one wave complete in order, and the wait keeps the compiler from
-        // moving the reads up.
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
 #pragma unroll
-        for (int pass = 0; pass < 2; ++pass) {
-          const int t = pass * 16 + lane / 4, c8 = (lane & 3) * 8;
-          if (t < L) {
-            const float* sp = &B.sm[t][cw * kTile + c8];
-            const f32x4 x0 = *reinterpret_cast<const f32x4*>(sp);
-            const f32x4 x1 = *reinterpret_cast<const f32x4*>(sp + 4);
-            const float o8[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
-            const size_t oidx = (((size_t)b * T_ + (size_t)cblk * L + t) * Hq + h) * D + cw * kTile + c8;
-            store_out8<T>(a.out, oidx, o8, a.s.out_f32);
-          }
+        for (int rt = 0; rt < RH; ++rt)
+#pragma unroll
+          for (int ks = 0; ks < C::KL; ++ks) kr[rt][ks] = lds_pair_raw(&B.phiKT[rt * kTile + li][0], ks, hh);
+        __builtin_amdgcn_sched_barrier(0);
+        // P V of this wave's columns (P as a bf16 pair hi + lo)
+        f32x16 pv = {};
+#pragma unroll
+        for (int ks = 0; ks < C::KL; ++ks) {
+          pv = M::mma(vk[ks], pph[ks], pv);
+          pv = M::mma(vk[ks], ppl[ks], pv);
         }
-        // commit: S += phi(K)^T V (this wave's columns); z_{c+1} = z_c + sum phi(k)
+        // commit: S += phi(K)^T V (this wave's columns), first half
 #pragma unroll
-        for (int rt = 0; rt < C::NRT; ++rt)
+        for (int rt = 0; rt < RH; ++rt)
 #pragma unroll
           for (int ks = 0; ks < C::KL; ++ks) {
             op_t khi, klo;
-            lds_pair_op(&B.phiKT[rt * kTile + li][0], ks, hh, khi, klo);
-            const op_t vk = B.vop[cw][ks][lane];
-            sacc[rt] = M::mma(khi, vk, sacc[rt]);
-            sacc[rt] = M::mma(klo, vk, sacc[rt]);
+            pair_split(kr[rt][ks], khi, klo);
+            sacc[rt] = M::mma(khi, vk[ks], sacc[rt]);
+            sacc[rt] = M::mma(klo, vk[ks], sacc[rt]);
+          }
+        __builtin_amdgcn_sched_barrier(0);
+        // Batch 3: the commit operands of the other row tiles and of z.
+        PairRaw kr2[C::NRT - RH][C::KL], zr2[C::ZPW][C::KL];
+#pragma unroll
+        for (int rt = RH; rt < C::NRT; ++rt)
+#pragma unroll
+          for (int ks = 0; ks < C::KL; ++ks)
+            kr2[rt - RH][ks] = lds_pair_raw(&B.phiKT[rt * kTile + li][0], ks, hh);
+#pragma unroll
+        for (int j = 0; j < C::ZPW; ++j) {
+          const int p = min(cw + j * NC, C::NRT - 1);
+#pragma unroll
+          for (int ks = 0; ks < C::KL; ++ks) zr2[j][ks] = lds_pair_raw(&B.phiKT[p * kTile + li][0], ks, hh);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        // commit, second half, and z += phi(K)^T 1
+#pragma unroll
+        for (int rt = RH; rt < C::NRT; ++rt)
+#pragma unroll
+          for (int ks = 0; ks < C::KL; ++ks) {
+            op_t khi, klo;
+            pair_split(kr2[rt - RH][ks], khi, klo);
+            sacc[rt] = M::mma(khi, vk[ks], sacc[rt]);
+            sacc[rt] = M::mma(klo, vk[ks], sacc[rt]);
           }
 #pragma unroll
-        for (int j = 0; j < ZPW; ++j) {
+        for (int j = 0; j < C::ZPW; ++j) {
           const int p = cw + j * NC;
           if (p >= C::NRT) continue;  // uniform
 #pragma unroll
           for (int ks = 0; ks < C::KL; ++ks) {
             op_t khi, klo;
-            lds_pair_op(&B.phiKT[p * kTile + li][0], ks, hh, khi, klo);
+            pair_split(zr2[j][ks], khi, klo);
             zt[j] = M::mma(khi, ones, zt[j]);
             zt[j] = M::mma(klo, ones, zt[j]);
           }
-          if (li == 0) {
-#pragma unroll
-            for (int i = 0; i < 16; i += 4)
-              *reinterpret_cast<f32x4*>(&zw[p * kTile + row_of(i, hh)]) =
-                  f32x4{zt[j][i], zt[j][i + 1], zt[j][i + 2], zt[j][i + 3]};
-          }
         }
+        if (hh == 0) sh.lden[(cr - blk0) & 1][cw][li] = ld[0];
+        olin = ol;
+        apv = pv;
+        m_k = m_n;
+        den_k = den_n;
       }
       lds_barrier();
     }
@@ -755,8 +950,16 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
         for (int j = 0; j < 4; ++j)
           *reinterpret_cast<f32x4*>(Sh + (size_t)col * f + rt * kTile + row_of(4 * j, hh)) =
               f32x4{sacc[rt][4 * j], sacc[rt][4 * j + 1], sacc[rt][4 * j + 2], sacc[rt][4 * j + 3]};
-      const float* zf = sh.z[(blk1 - blk0) & 1];
-      for (int r = tid - NP * kWave; r < f; r += NC * kWave) zh[r] = zf[r];
+#pragma unroll
+      for (int j = 0; j < C::ZPW; ++j) {
+        const int p = cw + j * NC;
+        if (p < C::NRT && li == 0) {
+#pragma unroll
+          for (int i = 0; i < 16; i += 4)
+            *reinterpret_cast<f32x4*>(zh + p * kTile + row_of(i, hh)) =
+                f32x4{zt[j][i], zt[j][i + 1], zt[j][i + 2], zt[j][i + 3]};
+        }
+      }
     }
   }
 }
@@ -989,7 +1192,8 @@ static hipError_t prefill_go(const PrefillArgs& a, hipStream_t st) {
   // The pipelined walk serves bf16 with F <= 64 when outputs are wanted;
   // the single-group walk serves the rest.
   if constexpr (sizeof(T) == 2 && F <= 64) {
-    if (a.out != nullptr) {
+    // (its buffer loads address a request's rows of q with 32-bit offsets)
+    if (a.out != nullptr && (size_t)a.T * a.s.Hq * D * sizeof(T) < ((size_t)1 << 31)) {
       typedef PrefillPipeCfg<T, D, F> P;
       hipLaunchKernelGGL((hyb_prefill_pipe_kernel<T, D, F>), dim3(units * nseg),
                          dim3(kWave * P::NWAVE), 0, st, a, nseg, seg_blocks);
