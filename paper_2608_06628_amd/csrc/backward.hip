@@ -106,7 +106,7 @@ static BwdLayout bwd_layout(const Shape& s, int T, bool inputs) {
   BwdLayout l;
   size_t o = 0;
   l.dS = o;
-  o = align256(o + prefill_delta_ws_bytes(s, T));
+  o = align256(o + prefill_delta_ws_bytes(s, segment_plan(s, T)));
   l.dG = o;
   o = align256(o + units * nseg * s.D * f * 4);
   l.dgz = o;
@@ -2316,7 +2316,7 @@ static hipError_t bwd_go(const BackwardArgs& a, hipStream_t st) {
     PrefillArgs pa{s, a.T, nullptr, a.k, a.v, a.W, nullptr, nullptr, nullptr,
                    nullptr, nullptr, ka.dS};
     pa.s.n_slots = s.B;
-    if ((e = launch_prefill_delta(pa, st)) != hipSuccess) return e;
+    if ((e = launch_prefill_delta(pa, segment_plan(s, a.T), st)) != hipSuccess) return e;
   }
   // With the input gradients the four-wave walks serve both dtypes (they
   // also write dL/du and Gbar^T phi(K)); otherwise bf16 takes the pipelined

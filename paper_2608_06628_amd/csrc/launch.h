@@ -92,14 +92,33 @@ hipError_t launch_commit(const CommitArgs& a, hipStream_t st);
 hipError_t launch_prefill(const PrefillArgs& a, hipStream_t st);
 hipError_t launch_softmax_prefix(const SoftmaxPrefixArgs& a, hipStream_t st);
 
-// Prefill: number of sequence segments and the workspace they need.
+// How a prompt of nblk blocks is cut for the segment scan: nseg walk
+// segments of sb blocks (the last takes the rest), and the state increments
+// of segments 0 .. nseg-2 computed in ppseg pieces of pb blocks per segment,
+// npieces() in all (every piece non-empty).  Walk segment s starts from the
+// incoming state plus pieces 0 .. s*ppseg - 1.
+struct SegPlan {
+  int nseg = 1, sb = 0, ppseg = 1, pb = 0;
+  __host__ __device__ int npieces() const { return (nseg - 1) * ppseg; }
+  __host__ __device__ int piece_lo(int pc) const { return (pc / ppseg) * sb + (pc % ppseg) * pb; }
+  __host__ __device__ int piece_hi(int pc) const {
+    const int hi = (pc / ppseg) * sb + (pc % ppseg + 1) * pb, end = (pc / ppseg + 1) * sb;
+    return hi < end ? hi : end;
+  }
+};
+// The prefill's plan (one round of walk workgroups over the chip, the
+// increments in about as many workgroups), and the plan with one piece per
+// segment (the backward's walks).
+SegPlan prefill_plan(const Shape& s, int T);
+SegPlan segment_plan(const Shape& s, int T);
+// Prefill: number of sequence segments of the backward's walks.
 int prefill_segments(const Shape& s, int T);
+// The prefill's workspace, and the part the increments take under a plan.
 size_t prefill_ws_bytes(const Shape& s, int T);
-// The part of it that the delta launch writes (the segment increments).
-size_t prefill_delta_ws_bytes(const Shape& s, int T);
-// The prefill's first launch alone: each segment's state increment (all
-// segments but the last) into a.ws; a.S, a.z, a.q, a.alpha are not used.
-hipError_t launch_prefill_delta(const PrefillArgs& a, hipStream_t st);
+size_t prefill_delta_ws_bytes(const Shape& s, const SegPlan& p);
+// The increments alone: piece pc of the plan into a.ws (dS [units][npieces]
+// [D][f], then dz [units][npieces][f]); a.S, a.z, a.q, a.alpha are not used.
+hipError_t launch_prefill_delta(const PrefillArgs& a, const SegPlan& p, hipStream_t st);
 
 // The library-held scratch buffer (scratch.hip) of the entry point that
 // allocates nothing: its size, and its device address on the current device

@@ -5,13 +5,14 @@
 // S += phi(K_c)^T V_c, z += sum phi(K_c).
 //
 // Sequence segments.  The prompt's blocks are cut into nseg segments so that
-// the grid fills the chip.  A first launch (delta mode) computes each
-// segment's own state increment dS_s = sum_{c in s} phi(K_c)^T V_c and dz_s
-// into the caller's workspace (the last segment's is not needed); the second
-// launch (walk mode) starts segment s from S + sum_{s' < s} dS_s' and walks
-// its blocks as below; the last segment writes the final state.  Only the
-// associativity of the sum is used, so the result is the sequential one up to
-// rounding order.  Without outputs, only the last segment walks.
+// the grid fills the chip (SegPlan).  A first launch (delta mode) computes the
+// state increments dS = sum_c phi(K_c)^T V_c and dz of the blocks of segments
+// 0 .. nseg-2, in pieces of a segment each or smaller, into the caller's
+// workspace; the second launch (walk mode) starts segment s from S + the
+// increments of the pieces before it and walks its blocks as below; the last
+// segment writes the final state.  Only the associativity of the sum is used,
+// so the result is the sequential one up to rounding order.  Without outputs,
+// only the last segment walks.
 // Ordering: with nseg > 1 the walk segments start from a snapshot of the
 // incoming S, z that a launch before the walk copies into the workspace, never
 // from S, z themselves, which the last segment overwrites in the same launch
@@ -61,22 +62,22 @@ struct PrefillCfg {
   };
 };
 
-// Workspace layout (nseg > 1): the segment increments dS [units][nseg-1][D][f]
-// and dz [units][nseg-1][f], then the snapshot of the incoming state,
+// Workspace layout (nseg > 1): the increments dS [units][npieces][D][f] and
+// dz [units][npieces][f], then the snapshot of the incoming state,
 // S0 [units][D][f] and z0 [units][f].
-__device__ inline const float* prefill_snapshot_S(const PrefillArgs& a, int nseg, int u) {
+__device__ inline const float* prefill_snapshot_S(const PrefillArgs& a, int npc, int u) {
   const size_t f = 2 * (size_t)a.s.F, units = (size_t)a.s.B * a.s.Hq;
-  return a.ws + units * (nseg - 1) * (a.s.D * f + f) + (size_t)u * a.s.D * f;
+  return a.ws + units * npc * (a.s.D * f + f) + (size_t)u * a.s.D * f;
 }
-__device__ inline const float* prefill_snapshot_z(const PrefillArgs& a, int nseg, int u) {
+__device__ inline const float* prefill_snapshot_z(const PrefillArgs& a, int npc, int u) {
   const size_t f = 2 * (size_t)a.s.F, units = (size_t)a.s.B * a.s.Hq;
-  return a.ws + units * (nseg - 1) * (a.s.D * f + f) + units * a.s.D * f + (size_t)u * f;
+  return a.ws + units * npc * (a.s.D * f + f) + units * a.s.D * f + (size_t)u * f;
 }
 
 // Snapshot of the incoming state of every (request, head) unit into the
 // workspace, one workgroup per unit, 16-byte copies.  A unit whose slot is
 // out of range is skipped (its walk never reads the snapshot).
-__global__ __launch_bounds__(256) void hyb_prefill_snapshot_kernel(PrefillArgs a, int nseg) {
+__global__ __launch_bounds__(256) void hyb_prefill_snapshot_kernel(PrefillArgs a, int npc) {
   const int u = blockIdx.x, Hq = a.s.Hq;
   const int b = u / Hq, h = u % Hq;
   const int slot = a.slots ? a.slots[b] : b;
@@ -84,15 +85,15 @@ __global__ __launch_bounds__(256) void hyb_prefill_snapshot_kernel(PrefillArgs a
   const size_t f = 2 * (size_t)a.s.F, n = (size_t)a.s.D * f;
   const size_t sbase = (size_t)slot * Hq + h;
   const f32x4* src = reinterpret_cast<const f32x4*>(a.S + sbase * n);
-  f32x4* dst = reinterpret_cast<f32x4*>(const_cast<float*>(prefill_snapshot_S(a, nseg, u)));
+  f32x4* dst = reinterpret_cast<f32x4*>(const_cast<float*>(prefill_snapshot_S(a, npc, u)));
   for (size_t i = threadIdx.x; i < n / 4; i += blockDim.x) dst[i] = src[i];
-  float* dz = const_cast<float*>(prefill_snapshot_z(a, nseg, u));
+  float* dz = const_cast<float*>(prefill_snapshot_z(a, npc, u));
   for (size_t i = threadIdx.x; i < f; i += blockDim.x) dz[i] = a.z[sbase * f + i];
 }
 
 template <typename T, int D, int F>
 __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_prefill_kernel(
-    PrefillArgs a, int nseg, int seg_blocks, int delta) {
+    PrefillArgs a, SegPlan p, int delta) {
   typedef PrefillCfg<T, D, F> C;
   typedef typename C::M M;
   typedef typename C::op_t op_t;
@@ -105,17 +106,20 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_prefill_kernel(
   const int Hq = a.s.Hq, Hkv = a.s.Hkv, L = a.s.L, T_ = a.T;
   // Unit u = (b, h) varies fastest, so the heads of one KV group and segment
   // are neighbours (on one XCD) and share K and V in L2.
-  const int units = a.s.B * Hq, nseg_here = delta ? nseg - 1 : nseg;
-  const int vix = xcd_unit(blockIdx.x, units * nseg_here);
+  // (delta mode: one workgroup per (unit, piece); walk mode: per (unit,
+  // segment))
+  const int units = a.s.B * Hq, nseg = p.nseg, npc = p.npieces();
+  const int vix = xcd_unit(blockIdx.x, units * (delta ? npc : nseg));
   const int u = vix % units, seg = vix / units;
   const int b = u / Hq, h = u % Hq, g = h / (Hq / Hkv);
   const int slot = a.slots ? a.slots[b] : b;
   const bool want_out = !delta && a.out != nullptr;
-  const bool last = seg == nseg - 1;
+  const bool last = !delta && seg == nseg - 1;
   const size_t qstride = (size_t)Hq * D, kstride = (size_t)Hkv * D;
   const int col = w * kTile + li;
   const int nblk = T_ / L;
-  const int blk0 = seg * seg_blocks, blk1 = min(nblk, blk0 + seg_blocks);
+  const int blk0 = delta ? p.piece_lo(seg) : seg * p.sb;
+  const int blk1 = min(nblk, delta ? p.piece_hi(seg) : blk0 + p.sb);
   if (!delta && !want_out && !last) return;  // state only: the last segment walks
   if (slot < 0 || slot >= a.s.n_slots) {  // uniform per workgroup
     if (want_out) {
@@ -130,14 +134,14 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_prefill_kernel(
   const size_t sbase = (size_t)slot * Hq + h;
   float* __restrict__ Sh = a.S + sbase * f * D;
   float* __restrict__ zh = a.z + sbase * f;
-  // Workspace: dS [units][nseg-1][D][f] (transposed, as S), then dz
-  // [units][nseg-1][f].
-  float* __restrict__ wsS = a.ws + (size_t)u * (nseg - 1) * D * f;
-  float* __restrict__ wsz = a.ws + (size_t)units * (nseg - 1) * D * f + (size_t)u * (nseg - 1) * f;
+  // Workspace: dS [units][npieces][D][f] (transposed, as S), then dz
+  // [units][npieces][f].
+  float* __restrict__ wsS = a.ws + (size_t)u * npc * D * f;
+  float* __restrict__ wsz = a.ws + (size_t)units * npc * D * f + (size_t)u * npc * f;
   // (without outputs only the last segment walks, and no snapshot is taken)
   const bool snap = nseg > 1 && a.out != nullptr;
-  const float* __restrict__ S0 = snap ? prefill_snapshot_S(a, nseg, u) : Sh;
-  const float* __restrict__ z0 = snap ? prefill_snapshot_z(a, nseg, u) : zh;
+  const float* __restrict__ S0 = snap ? prefill_snapshot_S(a, npc, u) : Sh;
+  const float* __restrict__ z0 = snap ? prefill_snapshot_z(a, npc, u) : zh;
 
   // Starting state: zero for a delta, else S plus the earlier segments'
   // increments, all in the accumulator layout.
@@ -159,10 +163,10 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_prefill_kernel(
     for (int r = tid; r < f; r += blockDim.x) sh.z[r] = 0.0f;
   } else {
     add_state(S0, true);
-    for (int s = 0; s < seg; ++s) add_state(wsS + (size_t)s * D * f, false);
+    for (int s = 0; s < seg * p.ppseg; ++s) add_state(wsS + (size_t)s * D * f, false);
     for (int r = tid; r < f; r += blockDim.x) {
       float zr = z0[r];
-      for (int s = 0; s < seg; ++s) zr += wsz[(size_t)s * f + r];
+      for (int s = 0; s < seg * p.ppseg; ++s) zr += wsz[(size_t)s * f + r];
       sh.z[r] = zr;
     }
   }
@@ -377,15 +381,19 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_prefill_kernel(
 //     exponentials and the softmax rows of block it+1, then the rest of
 //     phi(Q) of block it, its store and the store of P (a bf16 pair hi + lo);
 //   K waves (2, 3): phi(K) likewise, stored transposed as hi | lo pairs;
-//   state waves (D/32): the merge and output store of block it-2; then, for
-//     block it-1: the V^T operands of the wave's 32 columns, the readout
-//     phi(Q) S against the state of the blocks before it, the wave's share
-//     of lin_den = phi(Q) z (its feature tiles of z, on the MFMAs), P V of
-//     its columns and the commit into S columns 32w .. 32w+31 (fp32
-//     accumulators) and z.
+//     with the store, z_{it+1} = z_it + phi(K_it)^T 1 (on the MFMAs, from
+//     the tile just stored); with the first half of block it+1, lin_den =
+//     phi(Q) z of block it-1 and its merge coefficients;
+//   state waves (D/32): the merge and output store of block it-2 (two
+//     coefficients per row); then, for block it-1: the V^T operands of the
+//     wave's 32 columns, the readout phi(Q) S against the state of the
+//     blocks before it, P V of its columns and the commit into S columns
+//     32w .. 32w+31 (fp32 accumulators).
 // The QS and K waves hand a block to the state waves through a double
-// buffer (written in iteration c, read in c+1); the lin_den shares go from
-// the state waves to each other through a second one; W_h^T stays in LDS.
+// buffer (written in iteration c, read in c+1), the merge coefficients
+// through a second (written in c+1, read in c+2); z goes from one K wave to
+// the other through a triple buffer (z_c is written in iteration c-1 and read
+// in c and c+1); W_h^T stays in LDS.
 // Arithmetic and operand precision are those of the single-group walk above.
 // ---------------------------------------------------------------------------
 template <typename T, int D, int F>
@@ -402,19 +410,21 @@ struct PrefillPipeCfg {
   static constexpr int KD = D / M::KW;
   static constexpr int KL = kTile / M::KW;
   static constexpr int KF = f / M::KW;
-  static constexpr int PAD = 16 / (int)sizeof(T);
+  // Row strides of the bf16 tiles read as 8-byte pieces by 32 lanes at a
+  // time: an odd number of dword pairs, so that the 32 rows fall in distinct
+  // bank pairs.
+  static constexpr int QLD = f + 4, PLD = kTile + 4;
   struct alignas(16) Buf {            // written in iteration c, read in c + 1
-    T phiQ[kTile][f + PAD];           // phi(q_i)[r] at [i][r]
+    T phiQ[kTile][QLD];               // phi(q_i)[r] at [i][r]
     uint32_t phiKT[f][kTile + 4];     // phi(k_t)[r] at [r][t]: bf16 hi | lo << 16
-    T ph[kTile][kTile + PAD];         // P (relative to the row max) as hi + lo,
-    T pl[kTile][kTile + PAD];         //   [query][key]
+    T ph[kTile][PLD];                 // P (relative to the row max) as hi + lo,
+    T pl[kTile][PLD];                 //   [query][key]
     float m[kTile], den[kTile];       // row max and sum of the block scores
   };
   struct alignas(16) Smem {
     Buf buf[2];
-    float lden[2][NC][kTile];         // lin_den shares
-    float stage[NC][kTile][kTile + 4];  // output staging, one tile per state wave
-    T W[F][D + PAD];                  // W_h^T
+    float2 coef[2][kTile];            // merge: out = x P V + y phi(Q) S per row
+    float z[3][f];                    // z_c at [(c - first block) % 3]
   };
 };
 
@@ -425,7 +435,7 @@ constexpr int pipe_threads() {
 
 template <typename T, int D, int F>
 __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
-    PrefillArgs a, int nseg, int seg_blocks) {
+    PrefillArgs a, SegPlan p) {
   typedef PrefillPipeCfg<T, D, F> C;
   typedef typename C::M M;
   typedef typename C::op_t op_t;
@@ -441,7 +451,7 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
   const int w = __builtin_amdgcn_readfirstlane(tid / kWave);
   const int li = lane & 31, hh = lane >> 5;
   const int Hq = a.s.Hq, Hkv = a.s.Hkv, L = a.s.L, T_ = a.T;
-  const int units = a.s.B * Hq;
+  const int units = a.s.B * Hq, nseg = p.nseg, npc = p.npieces();
   const int vix = xcd_unit(blockIdx.x, units * nseg);
   const int u = vix % units, seg = vix / units;
   const int b = u / Hq, h = u % Hq, g = h / (Hq / Hkv);
@@ -449,7 +459,7 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
   const bool last = seg == nseg - 1;
   const size_t qstride = (size_t)Hq * D, kstride = (size_t)Hkv * D;
   const int nblk = T_ / L;
-  const int blk0 = seg * seg_blocks, blk1 = min(nblk, blk0 + seg_blocks);
+  const int blk0 = seg * p.sb, blk1 = min(nblk, blk0 + p.sb);
   const int nit = blk1 - blk0 + 3;  // iterations blk0-1 .. blk1+1
   if (slot < 0 || slot >= a.s.n_slots) {  // uniform per workgroup
     const size_t ob = ((size_t)b * T_ * Hq + h) * D;
@@ -489,30 +499,27 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
     for (int ks = 0; ks < C::KD; ++ks) o[ks] = buf_op<T>(krs, klane + ks * KW * (int)sizeof(T), so);
   };
 
-  // Set-up: W_h^T into LDS.
+  // Set-up: z + the earlier segments' increments into z[0].
   {
-    const T* __restrict__ Wt_h = (const T*)a.W + (size_t)h * F * D;
-    constexpr int RP = D / 8;  // 16-byte pieces per row
-    for (int i = tid; i < F * RP; i += C::NWAVE * kWave) {
-      const int r = i / RP, c = (i % RP) * 8;
-      *reinterpret_cast<uint4*>(&sh.W[r][c]) = *reinterpret_cast<const uint4*>(Wt_h + (size_t)r * D + c);
+    const float* __restrict__ wsz = a.ws + (size_t)units * npc * D * f + (size_t)u * npc * f;
+    const float* __restrict__ z0 = nseg > 1 ? prefill_snapshot_z(a, npc, u) : a.z + ((size_t)slot * Hq + h) * f;
+    for (int r = tid; r < f; r += C::NWAVE * kWave) {
+      float zr = z0[r];
+      for (int s = 0; s < seg * p.ppseg; ++s) zr += wsz[(size_t)s * f + r];
+      sh.z[0][r] = zr;
     }
   }
-  lds_barrier();  // W ready
+  lds_barrier();  // z ready
 
   constexpr float kLog2e = 1.4426950408889634f;
   // logits U^T = W^T X^T of the rows x, from the LDS copy of W_h^T
-  // (the W operands of a tile requested together, then its products)
-  auto logits = [&](const op_t (&x)[C::KD], float (&phi)[C::NPAIR][16]) {
+  // (W_h^T is held in the feature-map waves' registers, wop)
+  auto logits = [&](const op_t (&wop)[NT][C::KD], const op_t (&x)[C::KD], float (&phi)[C::NPAIR][16]) {
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
-      op_t wo[C::KD];
-#pragma unroll
-      for (int ks = 0; ks < C::KD; ++ks) wo[ks] = load_op<T>(&sh.W[t * kTile + li][ks * KW + hh * E]);
-      __builtin_amdgcn_sched_barrier(0);
       f32x16 acc = {};
 #pragma unroll
-      for (int ks = 0; ks < C::KD; ++ks) acc = M::mma(wo[ks], x[ks], acc);
+      for (int ks = 0; ks < C::KD; ++ks) acc = M::mma(wop[t][ks], x[ks], acc);
 #pragma unroll
       for (int i = 0; i < 16; ++i) phi[t][i] = acc[i];
     }
@@ -581,12 +588,16 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
     // last block, so that every wave passes nit barriers, as the state waves
     // do ----
     const int par = w & 1;
+    op_t ones;
+#pragma unroll
+    for (int e = 0; e < E; ++e) ones[e] = (T)1.0f;
     auto role = [&](auto key) {
       constexpr bool K = decltype(key)::value;
       // phi(K) stores more (the hi | lo pairs), so it moves more of its
       // exponentials into the first half
       constexpr int NA = K ? NT * 8 : 0;
-      op_t x[C::KD], xk[K ? 1 : C::KD];
+      op_t x[C::KD], xk[K ? 1 : C::KD], wop[NT][C::KD];
+      WFM::load_w((const T*)a.W + (size_t)h * F * D, li, hh, wop);
       auto load = [&](int blk) {
         if constexpr (K) {
           load_k(blk, x);
@@ -602,10 +613,51 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
         ++nbar;
       }
       const float scale = 1.0f / sqrtf((float)D);
+      const float lw = log_sigmoid(a.alpha[h]);
+      // lin_den = phi(q) . z of block c and the two merge coefficients of
+      // each row, for the state waves' merge of block c an iteration later:
+      // out = (ca P V + cz phi(Q) S / lin_den) / (ca den + cz), with the
+      // overflow-safe ca, cz of the single-group walk; lin_den <= 0 leaves
+      // the in-block softmax alone.
+      auto coefs = [&](int c) {
+        const typename C::Buf& Bc = sh.buf[(c - blk0) & 1];
+        const float* zc = sh.z[(c - blk0) % 3];
+        float part[4] = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+        for (int r = 0; r < f / 2; r += 8) {
+          const int r0 = hh * (f / 2) + r;
+          const bf16x4 xa = *reinterpret_cast<const bf16x4*>(&Bc.phiQ[li][r0]);
+          const bf16x4 xb = *reinterpret_cast<const bf16x4*>(&Bc.phiQ[li][r0 + 4]);
+          const f32x4 z0v = *reinterpret_cast<const f32x4*>(zc + r0);
+          const f32x4 z1v = *reinterpret_cast<const f32x4*>(zc + r0 + 4);
+          const T xt[8] = {xa[0], xa[1], xa[2], xa[3], xb[0], xb[1], xb[2], xb[3]};
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            part[e] += to_f32(xt[e]) * z0v[e];
+            part[e] += to_f32(xt[4 + e]) * z1v[e];
+          }
+        }
+        float lden = (part[0] + part[1]) + (part[2] + part[3]);
+        lden += xor32(lden);
+        const float m = Bc.m[li], den = Bc.den[li];
+        float ca = 1.0f, cz = 0.0f, rz = 0.0f;
+        if (lden > 0.0f) {
+          const float la = lw + m, lb = logf(lden);
+          const float cc = fmaxf(la, lb);
+          ca = expf(la - cc);
+          cz = expf(lb - cc);
+          rz = 1.0f / lden;
+        }
+        const float inv = 1.0f / (ca * den + cz);
+        if (hh == 0) sh.coef[(c - blk0) & 1][li] = make_float2(ca * inv, cz * rz * inv);
+      };
       for (int c = blk0 + par; c < blk1; c += 2) {
         // ---- iteration c-1 ----
+        if constexpr (K) {
+          if (c - 2 >= blk0) coefs(c - 2);
+        }
         float phi[C::NPAIR][16];
-        logits(x, phi);
+        logits(wop, x, phi);
         f32x16 sc = {};
         if constexpr (!K) {
           // scores: keys in rows, queries in columns
@@ -667,26 +719,69 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
             for (int i = 0; i < 16; i += 2)
               pack_hi_lo2(phi[p][i], phi[p][i + 1], B.phiKT[WFM::feature(16 * p + i, hh)][li],
                           B.phiKT[WFM::feature(16 * p + i + 1, hh)][li]);
+          // z_{c+1} = z_c + phi(K_c)^T 1: the tile just stored read back in
+          // operand order (this wave's own LDS writes complete first) as
+          // accumulator tiles whose columns are all equal
+          asm volatile("" ::: "memory");
+          PairRaw kz[C::NRT][C::KL];
+#pragma unroll
+          for (int p = 0; p < C::NRT; ++p)
+#pragma unroll
+            for (int ks = 0; ks < C::KL; ++ks) kz[p][ks] = lds_pair_raw(&B.phiKT[p * kTile + li][0], ks, hh);
+          const float* zc = sh.z[(c - blk0) % 3];
+          float* zn = sh.z[(c + 1 - blk0) % 3];
+#pragma unroll
+          for (int p = 0; p < C::NRT; ++p) {
+            f32x16 dz;
+#pragma unroll
+            for (int i = 0; i < 16; ++i) dz[i] = zc[p * kTile + row_of(i, hh)];
+#pragma unroll
+            for (int ks = 0; ks < C::KL; ++ks) {
+              op_t khi, klo;
+              pair_split(kz[p][ks], khi, klo);
+              dz = M::mma(khi, ones, dz);
+              dz = M::mma(klo, ones, dz);
+            }
+            if (li == 0) {
+#pragma unroll
+              for (int i = 0; i < 16; i += 4)
+                *reinterpret_cast<f32x4*>(&zn[p * kTile + row_of(i, hh)]) =
+                    f32x4{dz[i], dz[i + 1], dz[i + 2], dz[i + 3]};
+              if (last && c + 1 == blk1) {
+                float* zh = a.z + ((size_t)slot * Hq + h) * f;
+#pragma unroll
+                for (int i = 0; i < 16; i += 4)
+                  *reinterpret_cast<f32x4*>(zh + p * kTile + row_of(i, hh)) =
+                      f32x4{dz[i], dz[i + 1], dz[i + 2], dz[i + 3]};
+              }
+            }
+          }
         }
         lds_barrier();
         nbar += 2;
+      }
+      // the coefficients of this wave's last block, an iteration after it
+      if constexpr (K) {
+        const int clast = blk0 + par + 2 * ((blk1 - blk0 - par - 1) / 2);
+        if (clast >= blk0 + par && clast < blk1) {
+          coefs(clast);
+          lds_barrier();
+          ++nbar;
+        }
       }
       for (; nbar < nit; ++nbar) lds_barrier();
     };
     if (w >= 2) role(std::true_type{});
     else role(std::false_type{});
   } else {
-    // ---- state waves: merge and store of block it-2; V^T, readout,
-    // lin_den share, P V and commit of block it-1 ----
+    // ---- state waves: merge and store of block it-2; V^T, readout, P V
+    // and commit of block it-1 ----
     const int cw = w - 4;
     const int col = cw * kTile + li;
     const size_t sbase = (size_t)slot * Hq + h;
     float* __restrict__ Sh = a.S + sbase * f * D;
-    float* __restrict__ zh = a.z + sbase * f;
-    const float* __restrict__ wsS = a.ws + (size_t)u * (nseg - 1) * D * f;
-    const float* __restrict__ wsz = a.ws + (size_t)units * (nseg - 1) * D * f + (size_t)u * (nseg - 1) * f;
-    const float* __restrict__ S0 = nseg > 1 ? prefill_snapshot_S(a, nseg, u) : Sh;
-    const float* __restrict__ z0 = nseg > 1 ? prefill_snapshot_z(a, nseg, u) : zh;
+    const float* __restrict__ wsS = a.ws + (size_t)u * npc * D * f;
+    const float* __restrict__ S0 = nseg > 1 ? prefill_snapshot_S(a, npc, u) : Sh;
     // S columns col of all f rows: S + the earlier segments' increments.
     // (Declared here, not before the role branches: a value live across the
     // other roles' code takes registers there too.)
@@ -699,7 +794,7 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
 #pragma unroll
         for (int r = 0; r < 4; ++r) sacc[rt][4 * j + r] = x[r];
       }
-    for (int s = 0; s < seg; ++s) {
+    for (int s = 0; s < seg * p.ppseg; ++s) {
 #pragma unroll
       for (int rt = 0; rt < C::NRT; ++rt) {
 #pragma unroll
@@ -713,26 +808,6 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
         __builtin_amdgcn_sched_barrier(0);
       }
     }
-    // z of the feature tiles cw, cw + NC, ... as accumulator tiles whose
-    // columns are all equal: the commit adds phi(K)^T 1 on the MFMAs
-    f32x16 zt[C::ZPW];
-#pragma unroll
-    for (int j = 0; j < C::ZPW; ++j) {
-      const int p = cw + j * NC;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        float zr = 0.0f;
-        if (p < C::NRT) {
-          const int r = p * kTile + row_of(i, hh);
-          zr = z0[r];
-          for (int s = 0; s < seg; ++s) zr += wsz[(size_t)s * f + r];
-        }
-        zt[j][i] = zr;
-      }
-    }
-    op_t ones;
-#pragma unroll
-    for (int e = 0; e < E; ++e) ones[e] = (T)1.0f;
     // V^T operands of this wave's columns, one block ahead: lane li holds
     // column 32cw + li and, for k-step ks, the tokens row_of(ks*E + e, hh)
     // (the order in which P and phi(K)^T enter the products), gathered as
@@ -752,54 +827,24 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
               vrs, vlane, so + row_of(ks * E + e, 0) * (int)(kstride * sizeof(T)), 0);
     };
     if (blk0 < blk1) load_v(blk0);
-    const float lw = log_sigmoid(a.alpha[h]);
     // the products of a block, kept from its iteration to its merge in the
     // next
     f32x16 olin = {}, apv = {};
-    float m_k = 0.0f, den_k = 0.0f;
     constexpr int RH = (C::NRT + 1) / 2;
     for (int it = blk0 - 1; it <= blk1 + 1; ++it) {
       const int cr = it - 1, cm = it - 2;
-      float (*st)[kTile + 4] = sh.stage[cw];
-      // ---- merge of block cm (its products are in olin, apv) into the
-      // staging tile, then its rows to the output: 8 columns (16 bytes of
-      // bf16) per lane, 64 contiguous bytes per token.  The staging slots are
-      // written by other lanes of this wave; LDS operations of one wave
-      // complete in order, and the wait keeps the compiler from moving the
-      // reads up ----
-      if (cm >= blk0 && cm < blk1) {
-        if (row_ok) {
-          float lden = 0.0f;
+      // ---- merge and output store of block cm: 4 consecutive columns per
+      // run, the two lane halves of a row writing 16 contiguous bytes of bf16
+      // per run ----
+      if (cm >= blk0 && cm < blk1 && row_ok) {
+        const float2 cf = sh.coef[(cm - blk0) & 1][li];
+        const size_t ob = (((size_t)b * T_ + (size_t)cm * L + li) * Hq + h) * D + cw * kTile;
 #pragma unroll
-          for (int s = 0; s < NC; ++s) lden += sh.lden[(cm - blk0) & 1][s][li];
-          float ca = 1.0f, cz = 0.0f, rz = 0.0f;
-          if (lden > 0.0f) {
-            const float la = lw + m_k, lb = logf(lden);
-            const float c = fmaxf(la, lb);
-            ca = expf(la - c);
-            cz = expf(lb - c);
-            rz = 1.0f / lden;
-          }
-          const float inv = 1.0f / (ca * den_k + cz);
+        for (int i = 0; i < 16; i += 4) {
+          float o[4];
 #pragma unroll
-          for (int i = 0; i < 16; i += 4) {
-            f32x4 o;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) o[e] = (ca * apv[i + e] + cz * (olin[i + e] * rz)) * inv;
-            *reinterpret_cast<f32x4*>(&st[li][row_of(i, hh)]) = o;
-          }
-        }
-        asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-#pragma unroll
-        for (int pass = 0; pass < 2; ++pass) {
-          const int t = pass * 16 + lane / 4, c8 = (lane & 3) * 8;
-          if (t < L) {
-            const f32x4 x0 = *reinterpret_cast<const f32x4*>(&st[t][c8]);
-            const f32x4 x1 = *reinterpret_cast<const f32x4*>(&st[t][c8 + 4]);
-            const float o8[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
-            const size_t oidx = (((size_t)b * T_ + (size_t)cm * L + t) * Hq + h) * D + cw * kTile + c8;
-            store_out8<T>(a.out, oidx, o8, a.s.out_f32);
-          }
+          for (int e = 0; e < 4; ++e) o[e] = cf.x * apv[i + e] + cf.y * olin[i + e];
+          store_out4<T>(a.out, ob + row_of(i, hh), o, a.s.out_f32);
         }
       }
       if (cr >= blk0 && cr < blk1) {
@@ -807,20 +852,10 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
         // LDS operands are requested in batches ahead of the products that
         // use them, a scheduling barrier after each batch: fetched one at a
         // time next to its product, every operand costs a full LDS round
-        // trip.  Batch 1: the row statistics and the operands of the readout
-        // and of the lin_den share.
-        const float m_n = B.m[li], den_n = B.den[li];
-        op_t pb[C::KF], qz[C::ZPW][C::KL];
+        // trip.  Batch 1: the operands of the readout.
+        op_t pb[C::KF];
 #pragma unroll
         for (int ks = 0; ks < C::KF; ++ks) pb[ks] = lds_op_perm<T>(&B.phiQ[li][0], ks, hh, 0);
-#pragma unroll
-        for (int j = 0; j < C::ZPW; ++j) {
-          // (the tile index is wave-dependent: these operands come from LDS
-          // again rather than from a runtime index into pb)
-          const int p = min(cw + j * NC, C::NRT - 1);
-#pragma unroll
-          for (int kk = 0; kk < C::KL; ++kk) qz[j][kk] = lds_op_perm<T>(&B.phiQ[li][0], p * C::KL + kk, hh, 0);
-        }
         __builtin_amdgcn_sched_barrier(0);
         // V^T operands of block cr, the next block's gather issued
         op_t vk[C::KL];
@@ -833,27 +868,6 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
           }
         __builtin_amdgcn_sched_barrier(0);
         if (cr + 1 < blk1) load_v(cr + 1);
-        // lin_den share: z of this wave's feature tiles (every row of the
-        // tile as A operand, a bf16 pair hi + lo) against phi(Q); taken
-        // before the commit adds block cr
-        f32x16 ld = {};
-#pragma unroll
-        for (int j = 0; j < C::ZPW; ++j) {
-          const int p = cw + j * NC;
-          if (p >= C::NRT) continue;  // uniform
-#pragma unroll
-          for (int kk = 0; kk < C::KL; ++kk) {
-            op_t zhi, zlo;
-#pragma unroll
-            for (int e = 0; e < E; ++e) {
-              const float zv = zt[j][kk * E + e];
-              zhi[e] = (T)zv;
-              zlo[e] = (T)(zv - (float)zhi[e]);
-            }
-            ld = M::mma(zhi, qz[j][kk], ld);
-            ld = M::mma(zlo, qz[j][kk], ld);
-          }
-        }
         // readout against the state of the blocks before cr
         f32x16 ol = {};
 #pragma unroll
@@ -899,21 +913,15 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
             sacc[rt] = M::mma(klo, vk[ks], sacc[rt]);
           }
         __builtin_amdgcn_sched_barrier(0);
-        // Batch 3: the commit operands of the other row tiles and of z.
-        PairRaw kr2[C::NRT - RH][C::KL], zr2[C::ZPW][C::KL];
+        // Batch 3: the commit operands of the other row tiles.
+        PairRaw kr2[C::NRT - RH][C::KL];
 #pragma unroll
         for (int rt = RH; rt < C::NRT; ++rt)
 #pragma unroll
           for (int ks = 0; ks < C::KL; ++ks)
             kr2[rt - RH][ks] = lds_pair_raw(&B.phiKT[rt * kTile + li][0], ks, hh);
-#pragma unroll
-        for (int j = 0; j < C::ZPW; ++j) {
-          const int p = min(cw + j * NC, C::NRT - 1);
-#pragma unroll
-          for (int ks = 0; ks < C::KL; ++ks) zr2[j][ks] = lds_pair_raw(&B.phiKT[p * kTile + li][0], ks, hh);
-        }
         __builtin_amdgcn_sched_barrier(0);
-        // commit, second half, and z += phi(K)^T 1
+        // commit, second half
 #pragma unroll
         for (int rt = RH; rt < C::NRT; ++rt)
 #pragma unroll
@@ -923,23 +931,8 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
             sacc[rt] = M::mma(khi, vk[ks], sacc[rt]);
             sacc[rt] = M::mma(klo, vk[ks], sacc[rt]);
           }
-#pragma unroll
-        for (int j = 0; j < C::ZPW; ++j) {
-          const int p = cw + j * NC;
-          if (p >= C::NRT) continue;  // uniform
-#pragma unroll
-          for (int ks = 0; ks < C::KL; ++ks) {
-            op_t khi, klo;
-            pair_split(zr2[j][ks], khi, klo);
-            zt[j] = M::mma(khi, ones, zt[j]);
-            zt[j] = M::mma(klo, ones, zt[j]);
-          }
-        }
-        if (hh == 0) sh.lden[(cr - blk0) & 1][cw][li] = ld[0];
         olin = ol;
         apv = pv;
-        m_k = m_n;
-        den_k = den_n;
       }
       lds_barrier();
     }
@@ -950,16 +943,6 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
         for (int j = 0; j < 4; ++j)
           *reinterpret_cast<f32x4*>(Sh + (size_t)col * f + rt * kTile + row_of(4 * j, hh)) =
               f32x4{sacc[rt][4 * j], sacc[rt][4 * j + 1], sacc[rt][4 * j + 2], sacc[rt][4 * j + 3]};
-#pragma unroll
-      for (int j = 0; j < C::ZPW; ++j) {
-        const int p = cw + j * NC;
-        if (p < C::NRT && li == 0) {
-#pragma unroll
-          for (int i = 0; i < 16; i += 4)
-            *reinterpret_cast<f32x4*>(zh + p * kTile + row_of(i, hh)) =
-                f32x4{zt[j][i], zt[j][i + 1], zt[j][i + 2], zt[j][i + 3]};
-        }
-      }
     }
   }
 }
@@ -1002,7 +985,7 @@ constexpr int delta_pipe_threads() {
 
 template <typename T, int D, int F>
 __global__ __launch_bounds__(delta_pipe_threads<D>()) void hyb_prefill_delta_pipe_kernel(
-    PrefillArgs a, int nseg, int seg_blocks) {
+    PrefillArgs a, SegPlan pl) {
   typedef DeltaPipeCfg<T, D, F> C;
   typedef typename C::M M;
   typedef typename C::op_t op_t;
@@ -1016,20 +999,22 @@ __global__ __launch_bounds__(delta_pipe_threads<D>()) void hyb_prefill_delta_pip
   const int li = lane & 31, hh = lane >> 5;
   const int Hq = a.s.Hq, Hkv = a.s.Hkv, L = a.s.L, T_ = a.T;
   const int units = a.s.B * Hq;
-  // segments 0 .. nseg-2 (the last segment's increment is never needed)
-  const int vix = xcd_unit(blockIdx.x, units * (nseg - 1));
-  const int u = vix % units, seg = vix / units;
+  // pieces of segments 0 .. nseg-2 (the last segment's increment is never
+  // needed)
+  const int npc = pl.npieces();
+  const int vix = xcd_unit(blockIdx.x, units * npc);
+  const int u = vix % units, pc = vix / units;
   const int b = u / Hq, h = u % Hq, g = h / (Hq / Hkv);
   const int slot = a.slots ? a.slots[b] : b;
   if (slot < 0 || slot >= a.s.n_slots) return;  // uniform: no increment needed
   const size_t kstride = (size_t)Hkv * D;
   const int nblk = T_ / L;
-  const int blk0 = seg * seg_blocks, blk1 = min(nblk, blk0 + seg_blocks);
-  const int npair = (blk1 - blk0 + 1) / 2;
+  const int blk0 = pl.piece_lo(pc), blk1 = min(nblk, pl.piece_hi(pc));
+  const int npair = max(0, (blk1 - blk0 + 1) / 2);
   const bool row_ok = li < L;
   const int lrow = min(li, L - 1);
-  float* __restrict__ wsS = a.ws + ((size_t)u * (nseg - 1) + seg) * D * f;
-  float* __restrict__ wsz = a.ws + (size_t)units * (nseg - 1) * D * f + ((size_t)u * (nseg - 1) + seg) * f;
+  float* __restrict__ wsS = a.ws + ((size_t)u * npc + pc) * D * f;
+  float* __restrict__ wsz = a.ws + (size_t)units * npc * D * f + ((size_t)u * npc + pc) * f;
   auto kbase = [&](int blk) {
     return (const T*)a.k + (((size_t)b * T_ + (size_t)blk * L) * Hkv + g) * D;
   };
@@ -1170,23 +1155,22 @@ __global__ __launch_bounds__(delta_pipe_threads<D>()) void hyb_prefill_delta_pip
 }
 
 template <typename T, int D, int F>
-static hipError_t prefill_delta_go(const PrefillArgs& a, hipStream_t st);
+static hipError_t prefill_delta_go(const PrefillArgs& a, const SegPlan& p, hipStream_t st);
 
 template <typename T, int D, int F>
 static hipError_t prefill_go(const PrefillArgs& a, hipStream_t st) {
-  const int units = a.s.B * a.s.Hq, nblk = a.T / a.s.L;
-  const int nseg = prefill_segments(a.s, a.T);
-  const int seg_blocks = (nblk + nseg - 1) / nseg;
+  const int units = a.s.B * a.s.Hq;
+  const SegPlan p = prefill_plan(a.s, a.T);
   const dim3 block(kWave * (D / kTile));
-  if (nseg > 1) {
+  if (p.nseg > 1) {
     // only the last segment walks when no outputs are wanted, and it alone
     // writes the state: no snapshot is needed then
     if (a.out != nullptr) {
-      hipLaunchKernelGGL(hyb_prefill_snapshot_kernel, dim3(units), dim3(256), 0, st, a, nseg);
+      hipLaunchKernelGGL(hyb_prefill_snapshot_kernel, dim3(units), dim3(256), 0, st, a, p.npieces());
       const hipError_t e0 = hipGetLastError();
       if (e0 != hipSuccess) return e0;
     }
-    const hipError_t e = prefill_delta_go<T, D, F>(a, st);
+    const hipError_t e = prefill_delta_go<T, D, F>(a, p, st);
     if (e != hipSuccess) return e;
   }
   // The pipelined walk serves bf16 with F <= 64 when outputs are wanted;
@@ -1195,51 +1179,49 @@ static hipError_t prefill_go(const PrefillArgs& a, hipStream_t st) {
     // (its buffer loads address a request's rows of q with 32-bit offsets)
     if (a.out != nullptr && (size_t)a.T * a.s.Hq * D * sizeof(T) < ((size_t)1 << 31)) {
       typedef PrefillPipeCfg<T, D, F> P;
-      hipLaunchKernelGGL((hyb_prefill_pipe_kernel<T, D, F>), dim3(units * nseg),
-                         dim3(kWave * P::NWAVE), 0, st, a, nseg, seg_blocks);
+      hipLaunchKernelGGL((hyb_prefill_pipe_kernel<T, D, F>), dim3(units * p.nseg),
+                         dim3(kWave * P::NWAVE), 0, st, a, p);
       return hipGetLastError();
     }
   }
-  hipLaunchKernelGGL((hyb_prefill_kernel<T, D, F>), dim3(units * nseg), block, 0, st, a, nseg,
-                     seg_blocks, 0);
+  hipLaunchKernelGGL((hyb_prefill_kernel<T, D, F>), dim3(units * p.nseg), block, 0, st, a, p, 0);
   return hipGetLastError();
 }
 
 template <typename T, int D, int F>
-static hipError_t prefill_delta_go(const PrefillArgs& a, hipStream_t st) {
-  const int units = a.s.B * a.s.Hq, nblk = a.T / a.s.L;
-  const int nseg = prefill_segments(a.s, a.T);
-  const int seg_blocks = (nblk + nseg - 1) / nseg;
-  if (nseg <= 1) return hipSuccess;
+static hipError_t prefill_delta_go(const PrefillArgs& a, const SegPlan& p, hipStream_t st) {
+  const int units = a.s.B * a.s.Hq;
+  if (p.npieces() <= 0) return hipSuccess;
   if constexpr (sizeof(T) == 2 && F <= 64) {
-    hipLaunchKernelGGL((hyb_prefill_delta_pipe_kernel<T, D, F>), dim3(units * (nseg - 1)),
-                       dim3(delta_pipe_threads<D>()), 0, st, a, nseg, seg_blocks);
+    hipLaunchKernelGGL((hyb_prefill_delta_pipe_kernel<T, D, F>), dim3(units * p.npieces()),
+                       dim3(delta_pipe_threads<D>()), 0, st, a, p);
     return hipGetLastError();
   }
-  hipLaunchKernelGGL((hyb_prefill_kernel<T, D, F>), dim3(units * (nseg - 1)),
-                     dim3(kWave * (D / kTile)), 0, st, a, nseg, seg_blocks, 1);
+  hipLaunchKernelGGL((hyb_prefill_kernel<T, D, F>), dim3(units * p.npieces()),
+                     dim3(kWave * (D / kTile)), 0, st, a, p, 1);
   return hipGetLastError();
 }
 
 template <typename T, int D>
-static hipError_t prefill_delta_f(const PrefillArgs& a, hipStream_t st) {
+static hipError_t prefill_delta_f(const PrefillArgs& a, const SegPlan& p, hipStream_t st) {
   switch (a.s.F) {
-    case 32: return prefill_delta_go<T, D, 32>(a, st);
-    case 64: return prefill_delta_go<T, D, 64>(a, st);
-    case 128: return prefill_delta_go<T, D, 128>(a, st);
+    case 32: return prefill_delta_go<T, D, 32>(a, p, st);
+    case 64: return prefill_delta_go<T, D, 64>(a, p, st);
+    case 128: return prefill_delta_go<T, D, 128>(a, p, st);
   }
   return hipErrorInvalidValue;
 }
 
-hipError_t launch_prefill_delta(const PrefillArgs& a, hipStream_t st) {
+hipError_t launch_prefill_delta(const PrefillArgs& a, const SegPlan& p, hipStream_t st) {
   if (a.s.dtype == 1)
-    return a.s.D == 64 ? prefill_delta_f<bf16, 64>(a, st) : prefill_delta_f<bf16, 128>(a, st);
-  return a.s.D == 64 ? prefill_delta_f<float, 64>(a, st) : prefill_delta_f<float, 128>(a, st);
+    return a.s.D == 64 ? prefill_delta_f<bf16, 64>(a, p, st) : prefill_delta_f<bf16, 128>(a, p, st);
+  return a.s.D == 64 ? prefill_delta_f<float, 64>(a, p, st) : prefill_delta_f<float, 128>(a, p, st);
 }
 
-// Segments: enough (request, head, segment) workgroups to cover the chip
-// about twice, at most 8 segments (the walk of segment s reads the s earlier
-// increments) and at least 4 blocks per segment.
+// Segments of the backward's walks: enough (request, head, segment)
+// workgroups to cover the chip about twice, at most 8 segments (the walk of
+// segment s reads the s earlier increments) and at least 4 blocks per
+// segment.
 int prefill_segments(const Shape& s, int T) {
   const int units = s.B * s.Hq, nblk = T / s.L;
   int nseg = (512 + units - 1) / units;
@@ -1252,19 +1234,57 @@ int prefill_segments(const Shape& s, int T) {
   return nseg;
 }
 
-size_t prefill_delta_ws_bytes(const Shape& s, int T) {
-  const int nseg = prefill_segments(s, T);
-  if (nseg <= 1) return 0;
+SegPlan segment_plan(const Shape& s, int T) {
+  const int nblk = T / s.L, nseg = prefill_segments(s, T);
+  const int sb = (nblk + nseg - 1) / nseg;
+  return SegPlan{nseg, sb, 1, sb};
+}
+
+// The prefill's plan.  A walk workgroup takes a whole CU (its LDS), so the
+// walk takes about one workgroup per CU (256 CUs): segments are what the
+// batch's (request, head) units leave to fill; at most 8 segments and at
+// least 4 blocks per segment.  The increments of segments 0 .. nseg-2 are cut
+// into pieces so that they too take about one workgroup per CU, with at
+// least 2 blocks per piece (the increment kernel takes blocks in pairs).
+SegPlan prefill_plan(const Shape& s, int T) {
+  constexpr int kCUs = 256;
+  const int units = s.B * s.Hq, nblk = T / s.L;
+  int nseg = (kCUs + units - 1) / units;
+  if (nseg > 8) nseg = 8;
+  if (nseg > nblk / 4) nseg = nblk / 4;
+  if (nseg < 1) nseg = 1;
+  for (; nseg > 1; --nseg)
+    if ((nseg - 1) * ((nblk + nseg - 1) / nseg) < nblk) break;
+  SegPlan p;
+  p.nseg = nseg;
+  p.sb = (nblk + nseg - 1) / nseg;
+  p.ppseg = 1;
+  p.pb = p.sb;
+  if (nseg > 1) {
+    int pp = (kCUs + units * (nseg - 1) - 1) / (units * (nseg - 1));
+    if (pp > p.sb / 2) pp = p.sb / 2;
+    if (pp < 1) pp = 1;
+    // every piece non-empty
+    for (; pp > 1; --pp)
+      if ((pp - 1) * ((p.sb + pp - 1) / pp) < p.sb) break;
+    p.ppseg = pp;
+    p.pb = (p.sb + pp - 1) / pp;
+  }
+  return p;
+}
+
+size_t prefill_delta_ws_bytes(const Shape& s, const SegPlan& p) {
+  if (p.npieces() <= 0) return 0;
   const size_t f = 2 * (size_t)s.F;
-  return (size_t)s.B * s.Hq * (nseg - 1) * ((size_t)s.D * f + f) * 4;
+  return (size_t)s.B * s.Hq * p.npieces() * ((size_t)s.D * f + f) * 4;
 }
 
 size_t prefill_ws_bytes(const Shape& s, int T) {
-  const int nseg = prefill_segments(s, T);
-  if (nseg <= 1) return 0;
+  const SegPlan p = prefill_plan(s, T);
+  if (p.nseg <= 1) return 0;
   const size_t f = 2 * (size_t)s.F;
   // the increments, then the snapshot of the incoming state
-  return prefill_delta_ws_bytes(s, T) + (size_t)s.B * s.Hq * ((size_t)s.D * f + f) * 4;
+  return prefill_delta_ws_bytes(s, p) + (size_t)s.B * s.Hq * ((size_t)s.D * f + f) * 4;
 }
 
 template <typename T, int D>
