@@ -384,11 +384,13 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_prefill_kernel(
 //     with the store, z_{it+1} = z_it + phi(K_it)^T 1 (on the MFMAs, from
 //     the tile just stored); with the first half of block it+1, lin_den =
 //     phi(Q) z of block it-1 and its merge coefficients;
-//   state waves (D/32): the merge and output store of block it-2 (two
-//     coefficients per row); then, for block it-1: the V^T operands of the
-//     wave's 32 columns, the readout phi(Q) S against the state of the
-//     blocks before it, P V of its columns and the commit into S columns
-//     32w .. 32w+31 (fp32 accumulators).
+//   state waves (D/32): the output store of block it-3 (whole rows, from
+//     the LDS staging tile the state waves filled an iteration before), the
+//     merge of block it-2 (two coefficients per row) into staging; then, for
+//     block it-1: the V^T operands of the wave's 32 columns, the readout
+//     phi(Q) S against the state of the blocks before it, P V of its
+//     columns and the commit into S columns 32w .. 32w+31 (fp32
+//     accumulators).
 // The QS and K waves hand a block to the state waves through a double
 // buffer (written in iteration c, read in c+1), the merge coefficients
 // through a second (written in c+1, read in c+2); z goes from one K wave to
@@ -425,6 +427,7 @@ struct PrefillPipeCfg {
     Buf buf[2];
     float2 coef[2][kTile];            // merge: out = x P V + y phi(Q) S per row
     float z[3][f];                    // z_c at [(c - first block) % 3]
+    float stage[2][kTile][D + 4];     // merged outputs of a block, [row][column]
   };
 };
 
@@ -460,7 +463,7 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
   const size_t qstride = (size_t)Hq * D, kstride = (size_t)Hkv * D;
   const int nblk = T_ / L;
   const int blk0 = seg * p.sb, blk1 = min(nblk, blk0 + p.sb);
-  const int nit = blk1 - blk0 + 3;  // iterations blk0-1 .. blk1+1
+  const int nit = blk1 - blk0 + 4;  // iterations blk0-1 .. blk1+2
   if (slot < 0 || slot >= a.s.n_slots) {  // uniform per workgroup
     const size_t ob = ((size_t)b * T_ * Hq + h) * D;
     for (int t = blk0 * L; t < blk1 * L; ++t)
@@ -831,20 +834,37 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
     // next
     f32x16 olin = {}, apv = {};
     constexpr int RH = (C::NRT + 1) / 2;
-    for (int it = blk0 - 1; it <= blk1 + 1; ++it) {
-      const int cr = it - 1, cm = it - 2;
-      // ---- merge and output store of block cm: 4 consecutive columns per
-      // run, the two lane halves of a row writing 16 contiguous bytes of bf16
-      // per run ----
+    for (int it = blk0 - 1; it <= blk1 + 2; ++it) {
+      const int cr = it - 1, cm = it - 2, cs = it - 3;
+      // ---- output store of block cs: this wave's share of the rows of the
+      // staging tile, D/8 lanes per row (8 columns, 16 bytes of bf16, each),
+      // so that every store covers whole rows ----
+      if (cs >= blk0 && cs < blk1) {
+        const float (*st)[D + 4] = sh.stage[(cs - blk0) & 1];
+        constexpr int LPR = D / 8, RPW = kTile / NC;  // lanes per row, rows per wave
+#pragma unroll
+        for (int pass = 0; pass < RPW * LPR / kWave; ++pass) {
+          const int t = cw * RPW + pass * (kWave / LPR) + lane / LPR, c8 = (lane % LPR) * 8;
+          if (t < L) {
+            const f32x4 x0 = *reinterpret_cast<const f32x4*>(&st[t][c8]);
+            const f32x4 x1 = *reinterpret_cast<const f32x4*>(&st[t][c8 + 4]);
+            const float o8[8] = {x0[0], x0[1], x0[2], x0[3], x1[0], x1[1], x1[2], x1[3]};
+            const size_t oidx = (((size_t)b * T_ + (size_t)cs * L + t) * Hq + h) * D + c8;
+            store_out8<T>(a.out, oidx, o8, a.s.out_f32);
+          }
+        }
+      }
+      // ---- merge of block cm into the staging tile (this wave's columns);
+      // stored by all state waves after the next barrier ----
       if (cm >= blk0 && cm < blk1 && row_ok) {
         const float2 cf = sh.coef[(cm - blk0) & 1][li];
-        const size_t ob = (((size_t)b * T_ + (size_t)cm * L + li) * Hq + h) * D + cw * kTile;
+        float (*st)[D + 4] = sh.stage[(cm - blk0) & 1];
 #pragma unroll
         for (int i = 0; i < 16; i += 4) {
-          float o[4];
+          f32x4 o;
 #pragma unroll
           for (int e = 0; e < 4; ++e) o[e] = cf.x * apv[i + e] + cf.y * olin[i + e];
-          store_out4<T>(a.out, ob + row_of(i, hh), o, a.s.out_f32);
+          *reinterpret_cast<f32x4*>(&st[li][cw * kTile + row_of(i, hh)]) = o;
         }
       }
       if (cr >= blk0 && cr < blk1) {
