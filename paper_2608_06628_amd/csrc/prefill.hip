@@ -428,6 +428,7 @@ struct PrefillPipeCfg {
     float2 coef[2][kTile];            // merge: out = x P V + y phi(Q) S per row
     float z[3][f];                    // z_c at [(c - first block) % 3]
     float stage[2][kTile][D + 4];     // merged outputs of a block, [row][column]
+    T vt[NC][kTile][kTile + 8];       // V rows of each state wave's columns
   };
 };
 
@@ -811,24 +812,22 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
         __builtin_amdgcn_sched_barrier(0);
       }
     }
-    // V^T operands of this wave's columns, one block ahead: lane li holds
-    // column 32cw + li and, for k-step ks, the tokens row_of(ks*E + e, hh)
-    // (the order in which P and phi(K)^T enter the products), gathered as
-    // 2-byte loads: the token's row is a scalar offset (lane half 1 is 4 rows
-    // further, in the lane's offset), the column the lane's own.  A token at
-    // or past the block length reads the next rows of the request (zero past
-    // its end) and is zeroed.
-    const int vlane = (4 * hh * (int)kstride + cw * kTile + li) * (int)sizeof(T);
-    uint16_t vraw[C::KL][E];
+    // V rows of this wave's 32 columns, one block ahead: 4 lanes per row
+    // (16 bytes each), 16 rows per load; a row at or past the block length
+    // reads the next rows of the request (zero past its end) and is zeroed
+    // when the operands are formed.  The V^T operands (lane li: column
+    // 32cw + li; k-step ks: the tokens row_of(ks*E + e, hh), the order in
+    // which P and phi(K)^T enter the products) are then read from this
+    // wave's LDS copy of the rows.
+    const int vlane = ((lane >> 2) * (int)kstride + cw * kTile + (lane & 3) * 8) * (int)sizeof(T);
+    op_t vrow[2];
     auto load_v = [&](int blk) {
       const int so = koff(blk);
 #pragma unroll
-      for (int ks = 0; ks < C::KL; ++ks)
-#pragma unroll
-        for (int e = 0; e < E; ++e)
-          vraw[ks][e] = __builtin_amdgcn_raw_buffer_load_b16(
-              vrs, vlane, so + row_of(ks * E + e, 0) * (int)(kstride * sizeof(T)), 0);
+      for (int s2 = 0; s2 < 2; ++s2)
+        vrow[s2] = buf_op<T>(vrs, vlane, so + s2 * 16 * (int)(kstride * sizeof(T)));
     };
+    T (*vt)[kTile + 8] = sh.vt[cw];
     if (blk0 < blk1) load_v(blk0);
     // the products of a block, kept from its iteration to its merge in the
     // next
@@ -877,17 +876,23 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
 #pragma unroll
         for (int ks = 0; ks < C::KF; ++ks) pb[ks] = lds_op_perm<T>(&B.phiQ[li][0], ks, hh, 0);
         __builtin_amdgcn_sched_barrier(0);
-        // V^T operands of block cr, the next block's gather issued
+        // V^T operands of block cr through this wave's LDS rows (its own
+        // writes complete before its reads), the next block's rows issued
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2)
+          *reinterpret_cast<op_t*>(&vt[s2 * 16 + (lane >> 2)][(lane & 3) * 8]) = vrow[s2];
+        __builtin_amdgcn_sched_barrier(0);
+        if (cr + 1 < blk1) load_v(cr + 1);
+        asm volatile("" ::: "memory");
         op_t vk[C::KL];
 #pragma unroll
         for (int ks = 0; ks < C::KL; ++ks)
 #pragma unroll
           for (int e = 0; e < E; ++e) {
-            const T x = __builtin_bit_cast(T, vraw[ks][e]);
-            vk[ks][e] = row_of(ks * E + e, hh) < L ? x : (T)0.0f;
+            const int t = row_of(ks * E + e, hh);
+            vk[ks][e] = t < L ? vt[t][li] : (T)0.0f;
           }
         __builtin_amdgcn_sched_barrier(0);
-        if (cr + 1 < blk1) load_v(cr + 1);
         // readout against the state of the blocks before cr
         f32x16 ol = {};
 #pragma unroll
