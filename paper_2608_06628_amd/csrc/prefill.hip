@@ -974,32 +974,40 @@ __global__ __launch_bounds__(pipe_threads<D>()) void hyb_prefill_pipe_kernel(
 
 
 // ---------------------------------------------------------------------------
-// Pipelined delta (bf16, F <= 64): a segment's own increment
-// dS = sum_c phi(K_c)^T V_c, dz = sum_c sum_t phi(k_t), two blocks per
-// iteration.  Waves 0 and 1 compute phi(K) of the pair's two blocks (the
-// whole feature map in one wave), waves 2 and 3 load their V rows and turn
-// them into V^T operands, and the D/32 state waves commit the previous pair
-// into S columns 32w..32w+31 and dz (as phi(K)^T 1) in fp32 accumulators; one
-// barrier per pair, buffers double-buffered.
+// Pipelined increment (bf16, F <= 64): the increment of one piece of the
+// plan, dS = sum_c phi(K_c)^T V_c and dz = sum_c sum_t phi(k_t), a pair of
+// blocks per iteration, 4 + D/32 waves:
+//   feature-map waves (4): phi(K) of the piece's blocks, wave w taking the
+//     blocks 4m + w; a map spans two iterations (the logits, the row extremes
+//     and most exponentials, then the rest and the store of phi(K)^T as
+//     hi | lo pairs), so the four waves finish a pair per iteration;
+//   state waves (D/32): the commit of the previous pair into S columns
+//     32w .. 32w+31 and dz (as phi(K)^T 1) in fp32 accumulators, with the V^T
+//     operands of their columns from whole V rows through a per-wave LDS
+//     tile.
+// One barrier per iteration; phi(K)^T is double-buffered (written in
+// iteration j for pair j, read in j + 1).
 // ---------------------------------------------------------------------------
 template <typename T, int D, int F>
 struct DeltaPipeCfg {
   typedef Mma<T> M;
   typedef typename M::op_t op_t;
   static constexpr int NC = D / kTile;   // state waves
-  static constexpr int NP = 4;           // 2 feature-map + 2 V waves
-  static constexpr int NWAVE = NP + NC;
+  static constexpr int NWAVE = 4 + NC;
   static constexpr int f = 2 * F;
+  static constexpr int NT = F / kTile;
+  static constexpr int NPAIR = 2 * NT;
   static constexpr int NRT = f / kTile;
+  static constexpr int ZPW = (NRT + NC - 1) / NC;  // z tiles per state wave
   static constexpr int KD = D / M::KW;
   static constexpr int KL = kTile / M::KW;
   typedef WaveFeatMap<T, D, F> WFM;
   struct alignas(16) Buf {
     uint32_t phiKT[2][f][kTile + 4];     // per block of the pair: bf16 hi | lo << 16
-    op_t vop[2][NC][KL][kWave];          // per block of the pair: V operands
   };
   struct alignas(16) Smem {
     Buf buf[2];
+    T vt[NC][2][kTile][kTile + 8];       // V rows of each state wave's columns
   };
 };
 
@@ -1015,7 +1023,8 @@ __global__ __launch_bounds__(delta_pipe_threads<D>()) void hyb_prefill_delta_pip
   typedef typename C::M M;
   typedef typename C::op_t op_t;
   typedef typename C::WFM WFM;
-  constexpr int f = C::f, E = M::E, KW = M::KW, NP = C::NP, NC = C::NC;
+  constexpr int f = C::f, E = M::E, KW = M::KW, NT = C::NT, NC = C::NC;
+  static_assert(sizeof(T) == 2, "the pipelined increment is the bf16 path");
   static_assert(delta_pipe_threads<D>() == kWave * C::NWAVE, "launch bounds match the waves");
   __shared__ typename C::Smem sh;
 
@@ -1036,124 +1045,242 @@ __global__ __launch_bounds__(delta_pipe_threads<D>()) void hyb_prefill_delta_pip
   const int nblk = T_ / L;
   const int blk0 = pl.piece_lo(pc), blk1 = min(nblk, pl.piece_hi(pc));
   const int npair = max(0, (blk1 - blk0 + 1) / 2);
+  const int nit = npair + 2;  // iterations -1 .. npair
   const bool row_ok = li < L;
-  const int lrow = min(li, L - 1);
   float* __restrict__ wsS = a.ws + ((size_t)u * npc + pc) * D * f;
   float* __restrict__ wsz = a.ws + (size_t)units * npc * D * f + ((size_t)u * npc + pc) * f;
-  auto kbase = [&](int blk) {
-    return (const T*)a.k + (((size_t)b * T_ + (size_t)blk * L) * Hkv + g) * D;
-  };
-  auto vbase = [&](int blk) {
-    return (const T*)a.v + (((size_t)b * T_ + (size_t)blk * L) * Hkv + g) * D;
-  };
-  if (w < 2) {
-    // ---- phi(K) of block blk0 + 2j + w ----
-    const T* __restrict__ Wt_h = (const T*)a.W + (size_t)h * F * D;
-    op_t wop[WFM::NT][C::KD];
-    WFM::load_w(Wt_h, li, hh, wop);
-    op_t x[C::KD];
-    auto load = [&](int blk) {
-      const T* row = kbase(blk) + (size_t)lrow * kstride + hh * E;
+  // Raw buffers over this request's rows of k and v (the launcher keeps a
+  // request's rows under 2 GiB): a block's offset is a scalar.
+  const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<T*>((const T*)a.k + (size_t)b * T_ * kstride), 0, (int)(T_ * kstride * sizeof(T)),
+      kBufferWord3);
+  const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<T*>((const T*)a.v + (size_t)b * T_ * kstride), 0, (int)(T_ * kstride * sizeof(T)),
+      kBufferWord3);
+  auto koff = [&](int blk) { return (int)(((size_t)blk * L * kstride + (size_t)g * D) * sizeof(T)); };
+  op_t ones;
 #pragma unroll
-      for (int ks = 0; ks < C::KD; ++ks) x[ks] = load_op<T>(row + ks * KW);
+  for (int e = 0; e < E; ++e) ones[e] = (T)1.0f;
+
+  if (w < 4) {
+    // ---- phi(K) of blocks blk0 + w + 4m: the first half in the iteration
+    // before the block's pair is due, the second in the pair's iteration;
+    // waves 2 and 3 idle in the first iteration, all after their last block,
+    // so that every wave passes nit barriers ----
+    constexpr float kLog2e = 1.4426950408889634f;
+    constexpr int NA = NT * 8;  // second-sign exponentials in the first half
+    op_t wop[NT][C::KD], x[C::KD];
+    WFM::load_w((const T*)a.W + (size_t)h * F * D, li, hh, wop);
+    // rows past the block length read row L-1 (finite); their phi is zeroed
+    const int klane = (min(li, L - 1) * (int)kstride + hh * E) * (int)sizeof(T);
+    auto load = [&](int blk) {
+      const int so = koff(blk);
+#pragma unroll
+      for (int ks = 0; ks < C::KD; ++ks) x[ks] = buf_op<T>(krs, klane + ks * KW * (int)sizeof(T), so);
     };
     if (blk0 + w < blk1) load(blk0 + w);
-    for (int j = 0; j <= npair; ++j) {
-      const int blk = blk0 + 2 * j + w;
-      if (j < npair && blk < blk1) {
-        typename C::Buf& B = sh.buf[j & 1];
-        // a padding row reads row L-1 (finite); keep = row_ok zeroes its phi
-        float phi[WFM::NPAIR][16];
-        WFM::logits(wop, x, phi);
-        if (blk + 2 < blk1) load(blk + 2);  // next pair's block in flight
-        WFM::softmax(phi, row_ok);
-#pragma unroll
-        for (int p = 0; p < WFM::NPAIR; ++p)
-#pragma unroll
-          for (int i = 0; i < 16; i += 2)
-            pack_hi_lo2(phi[p][i], phi[p][i + 1], B.phiKT[w][WFM::feature(16 * p + i, hh)][li],
-                        B.phiKT[w][WFM::feature(16 * p + i + 1, hh)][li]);
-      }
+    int nbar = 0;
+    if (w >> 1) {
       lds_barrier();
+      ++nbar;
     }
-  } else if (w < NP) {
-    // ---- V operands of block blk0 + 2j + (w - 2), every column tile: V
-    // rows (lane: token, 16 contiguous bytes per load) turned into V^T by a
-    // product with the identity (exact: one nonzero product per entry) ----
-    const int q = w - 2;
-    op_t vx[NC][C::KL];
-    auto load = [&](int blk) {
-      const T* vrow = vbase(blk) + (size_t)lrow * kstride + hh * E;
+    for (int c = blk0 + w; c < blk1; c += 4) {
+      // ---- first half ----
+      float phi[C::NPAIR][16];
 #pragma unroll
-      for (int ct = 0; ct < NC; ++ct)
+      for (int t = 0; t < NT; ++t) {
+        f32x16 acc = {};
 #pragma unroll
-        for (int ks = 0; ks < C::KL; ++ks) vx[ct][ks] = load_op<T>(vrow + ct * kTile + ks * KW);
-    };
-    op_t ident[C::KL];
+        for (int ks = 0; ks < C::KD; ++ks) acc = M::mma(wop[t][ks], x[ks], acc);
 #pragma unroll
-    for (int ks = 0; ks < C::KL; ++ks)
+        for (int i = 0; i < 16; ++i) phi[t][i] = acc[i];
+      }
+      // (the operands are read by the products above before the rows of
+      // this wave's next block land in the same registers)
+      __builtin_amdgcn_sched_barrier(0);
+      if (c + 4 < blk1) load(c + 4);
+      float mx = -INFINITY, mn = INFINITY;
 #pragma unroll
-      for (int e = 0; e < E; ++e) ident[ks][e] = (T)(ks * KW + hh * E + e == li ? 1.0f : 0.0f);
-    if (blk0 + q < blk1) load(blk0 + q);
-    for (int j = 0; j <= npair; ++j) {
-      const int blk = blk0 + 2 * j + q;
-      if (j < npair && blk < blk1) {
-        typename C::Buf& B = sh.buf[j & 1];
+      for (int t = 0; t < NT; ++t)
 #pragma unroll
-        for (int ct = 0; ct < NC; ++ct) {
-          f32x16 va = {};
-#pragma unroll
-          for (int ks = 0; ks < C::KL; ++ks) va = M::mma(keep_if<T>(row_ok, vx[ct][ks]), ident[ks], va);
-#pragma unroll
-          for (int ks = 0; ks < C::KL; ++ks) B.vop[q][ct][ks][lane] = acc_op_exact<T>(va, ks);
+        for (int i = 0; i < 16; ++i) {
+          mx = fmaxf(mx, phi[t][i]);
+          mn = fminf(mn, phi[t][i]);
         }
-        if (blk + 2 < blk1) load(blk + 2);
-      }
+      mx = fmaxf(mx, xor32(mx));
+      mn = fminf(mn, xor32(mn));
+      // e^(u - mx) = 2^(u log2 e - mx log2 e): one fma per exponent; the
+      // rounding of mx log2 e is common to the row and cancels in the ratio
+      const float mxl = mx * kLog2e, mnl = mn * kLog2e;
+      float sp = 0.0f, sn = 0.0f;
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const float uu = phi[t][i];
+          if (t * 16 + i < NA) {
+            phi[NT + t][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(-uu, kLog2e, mnl));
+            sn += phi[NT + t][i];
+          } else {
+            phi[NT + t][i] = uu;
+          }
+          phi[t][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(uu, kLog2e, -mxl));
+          sp += phi[t][i];
+        }
       lds_barrier();
+      // ---- second half: the remaining exponentials, the sums,
+      // normalisation (keep = row_ok zeroes a padding row) and the store ----
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          if (t * 16 + i < NA) continue;
+          phi[NT + t][i] = __builtin_amdgcn_exp2f(__builtin_fmaf(-phi[NT + t][i], kLog2e, mnl));
+          sn += phi[NT + t][i];
+        }
+      sp += xor32(sp);
+      sn += xor32(sn);
+      const float ip = row_ok ? 1.0f / sp : 0.0f, in = row_ok ? 1.0f / sn : 0.0f;
+#pragma unroll
+      for (int t = 0; t < NT; ++t)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          phi[t][i] *= ip;
+          phi[NT + t][i] *= in;
+        }
+      const int j = (c - blk0) >> 1;
+      uint32_t (*kt)[kTile + 4] = sh.buf[j & 1].phiKT[w & 1];
+#pragma unroll
+      for (int p = 0; p < C::NPAIR; ++p)
+#pragma unroll
+        for (int i = 0; i < 16; i += 2)
+          pack_hi_lo2(phi[p][i], phi[p][i + 1], kt[WFM::feature(16 * p + i, hh)][li],
+                      kt[WFM::feature(16 * p + i + 1, hh)][li]);
+      lds_barrier();
+      nbar += 2;
     }
+    for (; nbar < nit; ++nbar) lds_barrier();
   } else {
-    // ---- state waves: commit the previous pair ----
-    const int cw = w - NP, col = cw * kTile + li;
+    // ---- state waves: commit pair i-1 in iteration i ----
+    const int cw = w - 4, col = cw * kTile + li;
     f32x16 sacc[C::NRT];
 #pragma unroll
     for (int rt = 0; rt < C::NRT; ++rt) sacc[rt] = f32x16{};
     // dz of the feature tiles cw, cw + NC, ... as accumulator tiles whose
     // columns are all equal: phi(K)^T 1 on the MFMAs
-    constexpr int ZPW = (C::NRT + NC - 1) / NC;
-    f32x16 zt[ZPW];
+    f32x16 zt[C::ZPW];
 #pragma unroll
-    for (int j = 0; j < ZPW; ++j) zt[j] = f32x16{};
-    op_t ones;
+    for (int j = 0; j < C::ZPW; ++j) zt[j] = f32x16{};
+    // V rows of this wave's 32 columns for both blocks of a pair, an
+    // iteration ahead: 4 lanes per row (16 bytes each), 16 rows per load; a
+    // row at or past the block length reads the next rows of the request
+    // (zero past its end) and is zeroed when the operands are formed
+    const int vlane = ((lane >> 2) * (int)kstride + cw * kTile + (lane & 3) * 8) * (int)sizeof(T);
+    op_t vrow[2][2];
+    auto load_v = [&](int j) {
 #pragma unroll
-    for (int e = 0; e < E; ++e) ones[e] = (T)1.0f;
-    lds_barrier();  // step 0 (peeled: the producers fill the first buffer)
-    for (int j = 1; j <= npair; ++j) {
-      const int pj = j - 1;
-      {
-        typename C::Buf& B = sh.buf[pj & 1];
+      for (int q = 0; q < 2; ++q) {
+        const int blk = min(blk0 + 2 * j + q, blk1 - 1);
+        const int so = koff(blk);
+#pragma unroll
+        for (int s2 = 0; s2 < 2; ++s2)
+          vrow[q][s2] = buf_op<T>(vrs, vlane, so + s2 * 16 * (int)(kstride * sizeof(T)));
+      }
+    };
+    if (npair > 0) load_v(0);
+    op_t ident[C::KL];
+#pragma unroll
+    for (int ks = 0; ks < C::KL; ++ks)
+#pragma unroll
+      for (int e = 0; e < E; ++e) ident[ks][e] = (T)(ks * KW + hh * E + e == li ? 1.0f : 0.0f);
+    constexpr int RH = (C::NRT + 1) / 2;
+    for (int i = -1; i <= npair; ++i) {
+      const int j = i - 1;
+      if (j >= 0 && j < npair) {
+        typename C::Buf& B = sh.buf[j & 1];
+        // V^T operands of the pair through this wave's LDS rows (its own
+        // writes complete before its reads); the next pair's rows issued
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+#pragma unroll
+          for (int s2 = 0; s2 < 2; ++s2)
+            *reinterpret_cast<op_t*>(&sh.vt[cw][q][s2 * 16 + (lane >> 2)][(lane & 3) * 8]) = vrow[q][s2];
+        __builtin_amdgcn_sched_barrier(0);
+        if (j + 1 < npair) load_v(j + 1);
+        asm volatile("" ::: "memory");
+        // read back as operands (lane li: token li, 16 contiguous bytes of
+        // columns per k-step; padding tokens zeroed) and transposed on the
+        // MFMAs as V^T = (V I)^T, exact: one nonzero product per entry
+        op_t vr[2][C::KL];
+#pragma unroll
+        for (int q = 0; q < 2; ++q)
+#pragma unroll
+          for (int ks = 0; ks < C::KL; ++ks) vr[q][ks] = load_op<T>(&sh.vt[cw][q][li][ks * KW + hh * E]);
+        __builtin_amdgcn_sched_barrier(0);
+        op_t vk[2][C::KL];
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
-          if (blk0 + 2 * pj + q >= blk1) continue;  // uniform
+          f32x16 va = {};
 #pragma unroll
-          for (int rt = 0; rt < C::NRT; ++rt)
+          for (int ks = 0; ks < C::KL; ++ks) va = M::mma(keep_if<T>(row_ok, vr[q][ks]), ident[ks], va);
+#pragma unroll
+          for (int ks = 0; ks < C::KL; ++ks) vk[q][ks] = acc_op_exact<T>(va, ks);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        // LDS operands in batches ahead of their products (a scheduling
+        // barrier after each batch): per block of the pair, the first half
+        // of the row tiles, then the rest with z
+#pragma unroll
+        for (int q = 0; q < 2; ++q) {
+          if (blk0 + 2 * j + q >= blk1) continue;  // uniform
+          PairRaw kr[RH][C::KL];
+#pragma unroll
+          for (int rt = 0; rt < RH; ++rt)
+#pragma unroll
+            for (int ks = 0; ks < C::KL; ++ks) kr[rt][ks] = lds_pair_raw(&B.phiKT[q][rt * kTile + li][0], ks, hh);
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int rt = 0; rt < RH; ++rt)
 #pragma unroll
             for (int ks = 0; ks < C::KL; ++ks) {
               op_t khi, klo;
-              lds_pair_op(&B.phiKT[q][rt * kTile + li][0], ks, hh, khi, klo);
-              const op_t vk = B.vop[q][cw][ks][lane];
-              sacc[rt] = M::mma(khi, vk, sacc[rt]);
-              sacc[rt] = M::mma(klo, vk, sacc[rt]);
+              pair_split(kr[rt][ks], khi, klo);
+              sacc[rt] = M::mma(khi, vk[q][ks], sacc[rt]);
+              sacc[rt] = M::mma(klo, vk[q][ks], sacc[rt]);
+            }
+          __builtin_amdgcn_sched_barrier(0);
+          PairRaw kr2[C::NRT - RH][C::KL], zr2[C::ZPW][C::KL];
+#pragma unroll
+          for (int rt = RH; rt < C::NRT; ++rt)
+#pragma unroll
+            for (int ks = 0; ks < C::KL; ++ks)
+              kr2[rt - RH][ks] = lds_pair_raw(&B.phiKT[q][rt * kTile + li][0], ks, hh);
+#pragma unroll
+          for (int jz = 0; jz < C::ZPW; ++jz) {
+            const int p = min(cw + jz * NC, C::NRT - 1);
+#pragma unroll
+            for (int ks = 0; ks < C::KL; ++ks) zr2[jz][ks] = lds_pair_raw(&B.phiKT[q][p * kTile + li][0], ks, hh);
+          }
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int rt = RH; rt < C::NRT; ++rt)
+#pragma unroll
+            for (int ks = 0; ks < C::KL; ++ks) {
+              op_t khi, klo;
+              pair_split(kr2[rt - RH][ks], khi, klo);
+              sacc[rt] = M::mma(khi, vk[q][ks], sacc[rt]);
+              sacc[rt] = M::mma(klo, vk[q][ks], sacc[rt]);
             }
 #pragma unroll
-          for (int j = 0; j < ZPW; ++j) {
-            const int p = cw + j * NC;
+          for (int jz = 0; jz < C::ZPW; ++jz) {
+            const int p = cw + jz * NC;
             if (p >= C::NRT) continue;  // uniform
 #pragma unroll
             for (int ks = 0; ks < C::KL; ++ks) {
               op_t khi, klo;
-              lds_pair_op(&B.phiKT[q][p * kTile + li][0], ks, hh, khi, klo);
-              zt[j] = M::mma(khi, ones, zt[j]);
-              zt[j] = M::mma(klo, ones, zt[j]);
+              pair_split(zr2[jz][ks], khi, klo);
+              zt[jz] = M::mma(khi, ones, zt[jz]);
+              zt[jz] = M::mma(klo, ones, zt[jz]);
             }
           }
         }
@@ -1167,7 +1294,7 @@ __global__ __launch_bounds__(delta_pipe_threads<D>()) void hyb_prefill_delta_pip
         *reinterpret_cast<f32x4*>(wsS + (size_t)col * f + rt * kTile + row_of(4 * j, hh)) =
             f32x4{sacc[rt][4 * j], sacc[rt][4 * j + 1], sacc[rt][4 * j + 2], sacc[rt][4 * j + 3]};
 #pragma unroll
-    for (int j = 0; j < ZPW; ++j) {
+    for (int j = 0; j < C::ZPW; ++j) {
       const int p = cw + j * NC;
       if (p < C::NRT && li == 0) {
 #pragma unroll
