@@ -624,8 +624,10 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_fwd_kernel(BwdKArgs
 // 2'. Pipelined forward walk (bf16, F <= 64).  Producers prepare block c+1
 // while the state waves finish block c:
 //   wave 0: phi(Q) as packed hi/lo pairs [query][feature] (the readout's
-//           operand, and phi(Q) itself for the feature-map Jacobian);
-//   wave 1: phi(K) transposed and packed (the commit's operand);
+//           operand, and phi(Q) itself for the feature-map Jacobian), and
+//           lin_den = phi(Q) z in fp32 from the map's registers;
+//   wave 1: phi(K) transposed and packed (the commit's operand), and
+//           z_{c+1} = z_c + sum_t phi(k_t) from its previous map;
 //   waves 2 .. NP-1: the in-block softmax numerators P V (relative to the
 //           row maximum) for 64 columns each, the row maxima and sums, and
 //           the V^T operands of the commit; then, once the state waves have
@@ -670,8 +672,8 @@ struct FPipeCfg {
       uint32_t gn[kTile][D + 4];     // dL/dN_i[c] at [i][c], packed
       uint32_t duT[2][F][kTile + 4]; // +-dL/du of each sign at [j][t], packed
     } x;
-    float z[2][f];
-    bf16 zh[2][f], zl[2][f];         // z as a bf16 pair hi + lo
+    float z[2][f];                   // z before block blk0 + n at [n & 1]
+    float lden[2][kTile];            // phi(q_i) . z of block blk0 + n at [n & 1]
     float red[NC][kTile][2];
     float jsum[NRT][kTile];
     float fin[NC][2];
@@ -725,14 +727,11 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
     for (int ks = 0; ks < KD; ++ks) o[ks] = load_op<bf16>(row + ks * KW);
   };
 
-  // z at the segment's start: the earlier segments' sums (fp32, and as a
-  // bf16 pair hi + lo for the products that form lin_den)
+  // z at the segment's start: the earlier segments' sums
   for (int r = tid; r < f; r += blockDim.x) {
     float zr = 0.0f;
     for (int sp = 0; sp < seg; ++sp) zr += ka.dz[((size_t)u * (nseg - 1) + sp) * f + r];
     sh.z[0][r] = zr;
-    sh.zh[0][r] = (bf16)zr;
-    sh.zl[0][r] = (bf16)(zr - as_operand<bf16>(zr));
   }
   // dL/du and the second buffer's Q^T operands start at zero: the softmax
   // waves' first dW update then adds exact zeros, and their loop needs no
@@ -754,10 +753,12 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
     };
     if (nb > 0) load(blk0);
     for (int n = 0; n <= nb; ++n) {
+      // (phi of block blk0 + n stays in registers past the first barrier:
+      // wave 0 forms lin_den from it there)
+      float phi[WFM::NPAIR][16];
       if (n < nb) {
         Buf& B = sh.buf[n & 1];
         // a padding row reads row L-1 (finite); keep = row_ok zeroes its phi
-        float phi[WFM::NPAIR][16];
         WFM::logits(wop, x, phi);
         if (n + 1 < nb) load(blk0 + n + 1);
         WFM::softmax(phi, row_ok);
@@ -778,10 +779,47 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
             for (int i = 0; i < 16; i += 2)
               pack_hi_lo2(phi[p][i], phi[p][i + 1], B.phiKT[WFM::feature(16 * p + i, hh)][li],
                           B.phiKT[WFM::feature(16 * p + i + 1, hh)][li]);
+          // z before block blk0 + n: z before the previous block plus the
+          // sum of its phi(k_t), from the map this wave stored an iteration
+          // ago (a padding key's phi is stored as zero)
+          if (n > 0) {
+            const Buf& Bp = sh.buf[(n - 1) & 1];
+            const float* zp = sh.z[(n - 1) & 1];
+            float* zn = sh.z[n & 1];
+#pragma unroll
+            for (int r = lane; r < f; r += kWave) {
+              float zs = zp[r];
+#pragma unroll
+              for (int t0 = 0; t0 < kTile; t0 += 4) {
+                const uint4 xk = *reinterpret_cast<const uint4*>(&Bp.phiKT[r][t0]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) zs += unpack_hi(xk[e]) + unpack_lo(xk[e]);
+              }
+              zn[r] = zs;
+            }
+          }
         }
       }
+      lds_barrier();  // 1
+      if (w == 0 && n < nb) {
+        // lin_den = phi(q_li) . z of block blk0 + n, in fp32 from the map's
+        // registers, for the state waves' merge an iteration later (z was
+        // posted by the K wave before the barrier)
+        const float* zn = sh.z[n & 1];
+        float part = 0.0f;
 #pragma unroll
-      for (int k = 0; k < NBAR; ++k) lds_barrier();
+        for (int p = 0; p < WFM::NPAIR; ++p)
+#pragma unroll
+          for (int i = 0; i < 16; i += 4) {
+            const f32x4 z4 = *reinterpret_cast<const f32x4*>(&zn[WFM::feature(16 * p + i, hh)]);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) part += phi[p][i + e] * z4[e];
+          }
+        part += xor32(part);
+        if (hh == 0) sh.lden[n & 1][li] = part;
+      }
+#pragma unroll
+      for (int k = 1; k < NBAR; ++k) lds_barrier();
     }
   } else if (w < NP) {
     // ---- in-block softmax branch for column tiles c0 .. c0+CT-1 ----
@@ -962,10 +1000,9 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
       Buf& B = sh.buf[(n - 1) & 1];
       const int zb = (n - 1) & 1;
       const float* zc = sh.z[zb];
-      // -- readout against S_{c-1} and lin_den = phi(q) . z_{c-1}, all
-      // operands as hi + lo pairs.  lin_den is the product of a tile whose
-      // rows all equal z with phi(Q)^T: every row of the result holds it.
-      f32x16 acc_lin = {}, acc_den = {};
+      // -- readout against S_{c-1}, both operands as hi + lo pairs;
+      // lin_den = phi(q) . z_{c-1} from the phi(Q) wave
+      f32x16 acc_lin = {};
 #pragma unroll
       for (int ks = 0; ks < C::KF; ++ks) {
         op_t ph, pl;
@@ -976,12 +1013,8 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
         acc_lin = M::mma(sa, ph, acc_lin);
         acc_lin = M::mma(sl, ph, acc_lin);
         acc_lin = M::mma(sa, pl, acc_lin);
-        const op_t zh = lds_op_perm<bf16>(&sh.zh[zb][0], ks, hh, 0);
-        acc_den = M::mma(zh, ph, acc_den);
-        acc_den = M::mma(lds_op_perm<bf16>(&sh.zl[zb][0], ks, hh, 0), ph, acc_den);
-        acc_den = M::mma(zh, pl, acc_den);
       }
-      const float lden = acc_den[0];
+      const float lden = sh.lden[zb][li];
       // -- merge (scaled by exp(-c) so nothing overflows): out = N / D with
       // w sm_den = exp(la) den, lin_den = exp(lb), c = max(la, lb)
       const float m = B.m[li], den = B.den[li];
@@ -1112,7 +1145,7 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
       }
       lds_barrier();  // 4
       // -- commit the block: S += phi(K)^T V (columns col), S^T += V^T phi(K)
-      // (feature tiles of this wave), z_{c+1} = z_c + sum_t phi(k_t)
+      // (feature tiles of this wave); the K wave forms z_{c+1}
 #pragma unroll
       for (int rt = 0; rt < NRT; ++rt)
 #pragma unroll
@@ -1138,18 +1171,6 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
             sT[j][s] = M::mma(vs, klo, sT[j][s]);
           }
         }
-      }
-      for (int r = tid - NP * kWave; r < f; r += NC * kWave) {
-        float zs = zc[r];
-#pragma unroll
-        for (int t0 = 0; t0 < kTile; t0 += 4) {
-          const uint4 xk = *reinterpret_cast<const uint4*>(&B.phiKT[r][t0]);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) zs += unpack_hi(xk[e]) + unpack_lo(xk[e]);
-        }
-        sh.z[zb ^ 1][r] = zs;
-        sh.zh[zb ^ 1][r] = (bf16)zs;
-        sh.zl[zb ^ 1][r] = (bf16)(zs - as_operand<bf16>(zs));
       }
       lds_barrier();  // 5
     }
