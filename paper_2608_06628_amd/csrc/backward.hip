@@ -984,12 +984,27 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
     float dal = 0.0f, lss = 0.0f;
     // the block's upstream rows (dout, or the teacher's output) at columns
     // 32cw + row_of(i, hh): prefetched a block ahead
-    const bf16* gsrc = (const bf16*)(tmode ? a.target : a.dout);
+    // Global accesses of this role go through buffer descriptors (a scalar
+    // base per request or unit, a 32-bit lane offset, the block as a scalar
+    // offset; the launcher keeps each range under 2 GiB): 64-bit lane
+    // addresses kept across the step would spill, and every reload from
+    // scratch waits for all outstanding memory operations.
+    const __amdgpu_buffer_rsrc_t grs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<bf16*>((const bf16*)(tmode ? a.target : a.dout) + (size_t)b * T_ * qstride), 0,
+        (int)(T_ * qstride * sizeof(bf16)), kBufferWord3);
+    const int glane = (int)(((size_t)lrow * qstride + (size_t)h * D + cw * kTile + 4 * hh) * sizeof(bf16));
+    const __amdgpu_buffer_rsrc_t nrs = __builtin_amdgcn_make_buffer_rsrc(
+        ka.gnT + (size_t)u * ka.nblk * D * kTile, 0, (int)((size_t)ka.nblk * D * kTile * sizeof(float)),
+        kBufferWord3);
+    const int nlane = (int)(((cw * kTile + 4 * hh) * kTile + li) * sizeof(float));
+    const __amdgpu_buffer_rsrc_t drs = __builtin_amdgcn_make_buffer_rsrc(
+        ka.gd + (size_t)u * ka.nblk * kTile, 0, (int)((size_t)ka.nblk * kTile * sizeof(float)), kBufferWord3);
     bf16x4 gin4[4];
     auto load_g = [&](int blk) {
-      const bf16* row = gsrc + (((size_t)b * T_ + (size_t)blk * L + lrow) * Hq + h) * D + cw * kTile;
+      const int so = (int)((size_t)blk * L * qstride * sizeof(bf16));
 #pragma unroll
-      for (int i4 = 0; i4 < 4; ++i4) gin4[i4] = *reinterpret_cast<const bf16x4*>(row + row_of(4 * i4, hh));
+      for (int i4 = 0; i4 < 4; ++i4)
+        gin4[i4] = __builtin_bit_cast(bf16x4, __builtin_amdgcn_raw_buffer_load_b64(grs, glane + 16 * i4, so, 0));
     };
     if (nb > 0) load_g(blk0);
     // step 0: the producers fill the first buffer
@@ -1070,9 +1085,8 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
       if (cw == 0 && hh == 0 && row_ok) dal += ca * one_minus_w * inv * (gs - go * den);
       {
         // dL/dN^T: column 32cw + row_of(i, hh) = 32cw + 4hh + 8(i/4) + i%4,
-        // query li; one base address, the rest immediate offsets
-        float* gnT = ka.gnT + ((size_t)u * ka.nblk + blk) * D * kTile +
-                     (size_t)(cw * kTile + 4 * hh) * kTile + li;
+        // query li; the lane's offset, the block's, the rest immediate
+        const int nso = (int)((size_t)blk * D * kTile * sizeof(float));
 #pragma unroll
         for (int i4 = 0; i4 < 16; i4 += 4) {
           uint4 pk;
@@ -1080,13 +1094,16 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
 #pragma unroll
           for (int e = 0; e < 4; ++e) {
             x[e] = rD * gq[i4 + e];
-            gnT[(2 * i4 + e) * kTile] = x[e];
+            __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, x[e]), nrs,
+                                                  nlane + (2 * i4 + e) * kTile * (int)sizeof(float), nso, 0);
           }
           pack_hi_lo2(x[0], x[1], pk[0], pk[1]);
           pack_hi_lo2(x[2], x[3], pk[2], pk[3]);
           *reinterpret_cast<uint4*>(&sh.x.gn[li][col - li + row_of(i4, hh)]) = pk;
         }
-        if (cw == 0 && hh == 0) ka.gd[((size_t)u * ka.nblk + blk) * kTile + li] = gD;
+        if (cw == 0 && hh == 0)
+          __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, gD), drs, li * (int)sizeof(float),
+                                                (int)(blk * kTile * sizeof(float)), 0);
       }
       lds_barrier();  // 2
       // -- dL/dphi(q_i) = S_{c-1} dL/dN_i + z_{c-1} dL/dD_i for the feature
@@ -2345,8 +2362,15 @@ static hipError_t bwd_go(const BackwardArgs& a, hipStream_t st) {
   if (inputs) {
     hipLaunchKernelGGL((hyb_bwd_fwd_kernel<T, D, F, true>), dim3(units * nseg), block, 0, st, ka);
   } else if constexpr (sizeof(T) == 2) {
-    hipLaunchKernelGGL((hyb_bwd_fpipe_kernel<D, F>), dim3(units * nseg), dim3(fpipe_threads<D>()),
-                       0, st, ka);
+    // (the pipelined walk addresses a request's upstream rows and a unit's
+    // dL/dN^T through 32-bit buffer offsets)
+    const bool fits = (size_t)a.T * s.Hq * D * sizeof(T) < ((size_t)1 << 31) &&
+                      (size_t)ka.nblk * D * kTile * sizeof(float) < ((size_t)1 << 31);
+    if (fits)
+      hipLaunchKernelGGL((hyb_bwd_fpipe_kernel<D, F>), dim3(units * nseg), dim3(fpipe_threads<D>()),
+                         0, st, ka);
+    else
+      hipLaunchKernelGGL((hyb_bwd_fwd_kernel<T, D, F, false>), dim3(units * nseg), block, 0, st, ka);
   } else {
     hipLaunchKernelGGL((hyb_bwd_fwd_kernel<T, D, F, false>), dim3(units * nseg), block, 0, st, ka);
   }
