@@ -1370,13 +1370,15 @@ hipError_t launch_prefill_delta(const PrefillArgs& a, const SegPlan& p, hipStrea
   return a.s.D == 64 ? prefill_delta_f<float, 64>(a, p, st) : prefill_delta_f<float, 128>(a, p, st);
 }
 
-// Segments of the backward's walks: enough (request, head, segment)
-// workgroups to cover the chip about twice, at most 8 segments (the walk of
-// segment s reads the s earlier increments) and at least 4 blocks per
-// segment.
+// Segments of the backward's walks: about one (request, head, segment)
+// workgroup per CU (256), since a walk workgroup takes a whole CU and the
+// walks are chains of block steps: a second round of workgroups would only
+// repeat each workgroup's start (the sum of the earlier segments'
+// increments) and lengthen the increment launches.  At most 8 segments (the
+// walk of segment s reads the s earlier increments), at least 4 blocks each.
 int prefill_segments(const Shape& s, int T) {
   const int units = s.B * s.Hq, nblk = T / s.L;
-  int nseg = (512 + units - 1) / units;
+  int nseg = (256 + units - 1) / units;
   if (nseg > 8) nseg = 8;
   if (nseg > nblk / 4) nseg = nblk / 4;
   if (nseg < 1) nseg = 1;
