@@ -640,6 +640,9 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_fwd_kernel(BwdKArgs
 //           both copies.
 // Five barriers per block, all waves: after the merge's partial sums, after
 // dL/dN, after the per-sign sums, after dL/du, and at the end of the step.
+// The producers do their block's work after the first barrier (the z update
+// aside), so that the state waves' readout and merge, the longest phase,
+// does not share its SIMDs with the feature maps and the block softmax.
 // ---------------------------------------------------------------------------
 template <int D, int F>
 struct FPipeCfg {
@@ -752,9 +755,33 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
       else load_rows(kbase(blk), kstride, x);
     };
     if (nb > 0) load(blk0);
+    // Block blk0 + n is prepared in iteration n, after the state waves'
+    // first barrier: their readout and merge phase, the longest of the step
+    // and the one with the most VALU work, then has the SIMDs it shares with
+    // this wave to itself.  Only the K wave's z update runs before it.
     for (int n = 0; n <= nb; ++n) {
-      // (phi of block blk0 + n stays in registers past the first barrier:
-      // wave 0 forms lin_den from it there)
+      if (w == 1 && n > 0 && n < nb) {
+        // z before block blk0 + n: z before the previous block plus the sum
+        // of its phi(k_t), from the map this wave stored an iteration ago (a
+        // padding key's phi is stored as zero)
+        const Buf& Bp = sh.buf[(n - 1) & 1];
+        const float* zp = sh.z[(n - 1) & 1];
+        float* zn = sh.z[n & 1];
+#pragma unroll
+        for (int r = lane; r < f; r += kWave) {
+          float zs = zp[r];
+#pragma unroll
+          for (int t0 = 0; t0 < kTile; t0 += 4) {
+            const uint4 xk = *reinterpret_cast<const uint4*>(&Bp.phiKT[r][t0]);
+#pragma unroll
+            for (int e = 0; e < 4; ++e) zs += unpack_hi(xk[e]) + unpack_lo(xk[e]);
+          }
+          zn[r] = zs;
+        }
+      }
+      lds_barrier();  // 1
+      // (phi stays in registers past the second barrier: wave 0 forms
+      // lin_den from it there)
       float phi[WFM::NPAIR][16];
       if (n < nb) {
         Buf& B = sh.buf[n & 1];
@@ -779,32 +806,13 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
             for (int i = 0; i < 16; i += 2)
               pack_hi_lo2(phi[p][i], phi[p][i + 1], B.phiKT[WFM::feature(16 * p + i, hh)][li],
                           B.phiKT[WFM::feature(16 * p + i + 1, hh)][li]);
-          // z before block blk0 + n: z before the previous block plus the
-          // sum of its phi(k_t), from the map this wave stored an iteration
-          // ago (a padding key's phi is stored as zero)
-          if (n > 0) {
-            const Buf& Bp = sh.buf[(n - 1) & 1];
-            const float* zp = sh.z[(n - 1) & 1];
-            float* zn = sh.z[n & 1];
-#pragma unroll
-            for (int r = lane; r < f; r += kWave) {
-              float zs = zp[r];
-#pragma unroll
-              for (int t0 = 0; t0 < kTile; t0 += 4) {
-                const uint4 xk = *reinterpret_cast<const uint4*>(&Bp.phiKT[r][t0]);
-#pragma unroll
-                for (int e = 0; e < 4; ++e) zs += unpack_hi(xk[e]) + unpack_lo(xk[e]);
-              }
-              zn[r] = zs;
-            }
-          }
         }
       }
-      lds_barrier();  // 1
+      lds_barrier();  // 2
       if (w == 0 && n < nb) {
         // lin_den = phi(q_li) . z of block blk0 + n, in fp32 from the map's
         // registers, for the state waves' merge an iteration later (z was
-        // posted by the K wave before the barrier)
+        // posted by the K wave before the first barrier)
         const float* zn = sh.z[n & 1];
         float part = 0.0f;
 #pragma unroll
@@ -819,22 +827,50 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
         if (hh == 0) sh.lden[n & 1][li] = part;
       }
 #pragma unroll
-      for (int k = 1; k < NBAR; ++k) lds_barrier();
+      for (int k = 2; k < NBAR; ++k) lds_barrier();
     }
   } else if (w < NP) {
     // ---- in-block softmax branch for column tiles c0 .. c0+CT-1 ----
     const int c0 = (w - 2) * C::CT;
     const float scale = 1.0f / sqrtf((float)D);
-    op_t ko[KD], qo[KD], vo[C::CT][KL];
+    // K, Q and V rows through buffer descriptors over the request's rows (a
+    // scalar base, a 32-bit lane offset, the block as a scalar offset; the
+    // launcher keeps them under 2 GiB): 64-bit lane addresses kept across
+    // the step would spill, and each reload from scratch would wait for the
+    // next block's loads in flight.  V comes as rows too, 16 bytes of this
+    // wave's columns per lane and k-step, and is turned into V^T operands by
+    // the identity product, like Q^T.
+    const __amdgpu_buffer_rsrc_t qrs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<bf16*>((const bf16*)a.q + (size_t)b * T_ * qstride), 0,
+        (int)(T_ * qstride * sizeof(bf16)), kBufferWord3);
+    const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<bf16*>((const bf16*)a.k + (size_t)b * T_ * kstride), 0,
+        (int)(T_ * kstride * sizeof(bf16)), kBufferWord3);
+    const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc(
+        const_cast<bf16*>((const bf16*)a.v + (size_t)b * T_ * kstride), 0,
+        (int)(T_ * kstride * sizeof(bf16)), kBufferWord3);
+    const int qlane = (int)(((size_t)lrow * qstride + (size_t)h * D + hh * E) * sizeof(bf16));
+    const int klane = (int)(((size_t)lrow * kstride + (size_t)g * D + hh * E) * sizeof(bf16));
+    op_t ko[KD], qo[KD], vr[C::CT][KL];
     auto load = [&](int blk) {
-      load_rows(kbase(blk), kstride, ko);
-      load_rows(qbase(blk), qstride, qo);
+      const int qso = (int)((size_t)blk * L * qstride * sizeof(bf16));
+      const int kso = (int)((size_t)blk * L * kstride * sizeof(bf16));
+#pragma unroll
+      for (int ks = 0; ks < KD; ++ks) ko[ks] = buf_op<bf16>(krs, klane + ks * KW * (int)sizeof(bf16), kso);
+#pragma unroll
+      for (int ks = 0; ks < KD; ++ks) qo[ks] = buf_op<bf16>(qrs, qlane + ks * KW * (int)sizeof(bf16), qso);
 #pragma unroll
       for (int ct = 0; ct < C::CT; ++ct)
 #pragma unroll
-        for (int ks = 0; ks < KL; ++ks)
-          vo[ct][ks] = load_rows_op<bf16>(vbase(blk) + (c0 + ct) * kTile + li, kstride, ks, hh, L, false);
+        for (int kk = 0; kk < KL; ++kk)
+          vr[ct][kk] = buf_op<bf16>(vrs, klane + ((c0 + ct) * kTile + kk * KW) * (int)sizeof(bf16), kso);
     };
+    // the identity's k-steps: B[k][n] = (k == n) for n = li
+    op_t idop[KL];
+#pragma unroll
+    for (int kk = 0; kk < KL; ++kk)
+#pragma unroll
+      for (int e = 0; e < E; ++e) idop[kk][e] = (bf16)(kk * KW + hh * E + e == li ? 1.0f : 0.0f);
     // the query part of dW^T for columns 32(c0+ct)..: rows j of tile t
     f32x16 dwacc[NT][C::CT];
 #pragma unroll
@@ -843,6 +879,9 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
       for (int ct = 0; ct < C::CT; ++ct) dwacc[t][ct] = f32x16{};
     if (nb > 0) load(blk0);
     for (int n = 0; n <= nb; ++n) {
+      // block blk0 + n after the state waves' first barrier, as for the
+      // feature maps
+      lds_barrier();  // 1
       if (n < nb) {
         Buf& B = sh.buf[n & 1];
         // keys in rows, queries in columns
@@ -864,18 +903,20 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
 #pragma unroll
               for (int kk = 0; kk < KL; ++kk) qsel[ct][kk] = qo[(sw * C::CT + ct) * KL + kk];
           }
+        op_t vo[C::CT][KL];
 #pragma unroll
         for (int ct = 0; ct < C::CT; ++ct) {
-          f32x16 qa = {};
+          f32x16 qa = {}, va = {};
 #pragma unroll
           for (int kk = 0; kk < KL; ++kk) {
-            op_t id;
-#pragma unroll
-            for (int e = 0; e < E; ++e) id[e] = (bf16)(kk * KW + hh * E + e == li ? 1.0f : 0.0f);
-            qa = M::mma(keep_if<bf16>(row_ok, qsel[ct][kk]), id, qa);
+            qa = M::mma(keep_if<bf16>(row_ok, qsel[ct][kk]), idop[kk], qa);
+            va = M::mma(keep_if<bf16>(row_ok, vr[ct][kk]), idop[kk], va);
           }
 #pragma unroll
-          for (int kk = 0; kk < KL; ++kk) B.qtop[c0 + ct][kk][lane] = acc_op<bf16>(qa, kk);
+          for (int kk = 0; kk < KL; ++kk) {
+            B.qtop[c0 + ct][kk][lane] = acc_op<bf16>(qa, kk);
+            vo[ct][kk] = acc_op<bf16>(va, kk);
+          }
         }
         float pr[16];
         float m = -INFINITY;
@@ -913,7 +954,7 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
         if (n + 1 < nb) load(blk0 + n + 1);  // next block in flight
       }
 #pragma unroll
-      for (int k = 0; k < NBAR - 1; ++k) lds_barrier();
+      for (int k = 1; k < NBAR - 1; ++k) lds_barrier();
       {
         // dW^T += dL/du^T Q for the block the state waves are finishing
         // (its dL/du is in LDS between their fourth and fifth barrier; zeros
@@ -1140,7 +1181,12 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
           }
         }
         js += xor32(js);
-        if (hh == 0) sh.jsum[p][li] = js;
+        // (the lane index through an opaque copy: an LDS address kept live
+        // across the step is spilled, and its reload here would wait for the
+        // dL/dN^T stores in flight)
+        int lj = li;
+        asm volatile("" : "+v"(lj));
+        if (hh == 0) sh.jsum[p][lj] = js;
       }
       lds_barrier();  // 3
       // -- feature-map backward: dL/du of each sign, transposed and packed
@@ -1163,13 +1209,15 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
       lds_barrier();  // 4
       // -- commit the block: S += phi(K)^T V (columns col), S^T += V^T phi(K)
       // (feature tiles of this wave); the K wave forms z_{c+1}
+      int lv = lane;  // (an opaque copy, as above)
+      asm volatile("" : "+v"(lv));
 #pragma unroll
       for (int rt = 0; rt < NRT; ++rt)
 #pragma unroll
         for (int ks = 0; ks < KL; ++ks) {
           op_t khi, klo;
           lds_pair_op(&B.phiKT[rt * kTile + li][0], ks, hh, khi, klo);
-          const op_t vk = B.vop[cw][ks][lane];
+          const op_t vk = B.vop[cw][ks][lv];
           sacc[rt] = M::mma(khi, vk, sacc[rt]);
           sacc[rt] = M::mma(klo, vk, sacc[rt]);
         }
@@ -1183,7 +1231,7 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
           lds_pair_op(&B.phiKT[p * kTile + li][0], ks, hh, khi, klo);
 #pragma unroll
           for (int s = 0; s < NC; ++s) {
-            const op_t vs = B.vop[s][ks][lane];
+            const op_t vs = B.vop[s][ks][lv];
             sT[j][s] = M::mma(vs, khi, sT[j][s]);
             sT[j][s] = M::mma(vs, klo, sT[j][s]);
           }
