@@ -638,11 +638,12 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_fwd_kernel(BwdKArgs
 //           the head dimension) both in fp32 accumulators; the merge, dL/dN,
 //           dL/dD, dL/dphi(Q) and dL/du; then the commit of the block into
 //           both copies.
-// Five barriers per block, all waves: after the merge's partial sums, after
-// dL/dN, after the per-sign sums, after dL/du, and at the end of the step.
-// The producers do their block's work after the first barrier (the z update
-// aside), so that the state waves' readout and merge, the longest phase,
-// does not share its SIMDs with the feature maps and the block softmax.
+// Four barriers per block, all waves: after the merge's partial sums, after
+// dL/dN, after the per-sign sums and after dL/du.  The producers do their
+// block's work after the first barrier (the z update aside), which also
+// makes an end-of-step barrier unnecessary: the buffer that the state waves'
+// commit reads is refilled only after the next first barrier, and the
+// softmax waves' dW, which reads dL/du, ends before they reach it.
 // ---------------------------------------------------------------------------
 template <int D, int F>
 struct FPipeCfg {
@@ -697,7 +698,7 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
   typedef typename C::Buf Buf;
   constexpr int f = C::f, E = M::E, KW = M::KW, NP = C::NP, NC = C::NC;
   constexpr int NRT = C::NRT, NT = C::NT, RPW = C::RPW, KD = C::KD, KL = C::KL;
-  constexpr int NBAR = 5;  // barriers per block step
+  constexpr int NBAR = 4;  // barriers per block step
   static_assert(fpipe_threads<D>() == kWave * C::NWAVE, "launch bounds match the waves");
   __shared__ typename C::Smem sh;
   const BackwardArgs& a = ka.a;
@@ -954,11 +955,11 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
         if (n + 1 < nb) load(blk0 + n + 1);  // next block in flight
       }
 #pragma unroll
-      for (int k = 1; k < NBAR - 1; ++k) lds_barrier();
+      for (int k = 1; k < NBAR; ++k) lds_barrier();
       {
         // dW^T += dL/du^T Q for the block the state waves are finishing
-        // (its dL/du is in LDS between their fourth and fifth barrier; zeros
-        // at n = 0)
+        // (its dL/du is in LDS from their fourth barrier until they post the
+        // next block's dL/dN after the next first barrier; zeros at n = 0)
         const Buf& Bp = sh.buf[(n - 1) & 1];
 #pragma unroll
         for (int t = 0; t < NT; ++t)
@@ -976,7 +977,6 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
               }
             }
       }
-      lds_barrier();
     }
     float* dwq = ka.dwq + ((size_t)u * nseg + seg) * F * D;
 #pragma unroll
@@ -1237,7 +1237,6 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
           }
         }
       }
-      lds_barrier();  // 5
     }
     // partials of this (request, head, segment)
     dal = wave_sum(dal);
