@@ -1754,8 +1754,11 @@ __global__ __launch_bounds__(gdelta_threads<D>()) void hyb_bwd_gdelta_kernel(Bwd
 //           own, the per-sign sums, dL/du (packed hi/lo, transposed), then
 //           the Gbar and gz updates, then dW += dL/du^T K for columns
 //           32w..32w+31.  Gbar^T and the partial dW stay in registers.
-// Three barriers per block (all waves take part): after the per-sign
-// partial sums, after dL/du, and at the end of the step.
+// Two barriers per block (all waves take part): after the per-sign partial
+// sums and after dL/du.  No end-of-step barrier: the state waves take the
+// block's last operands from the buffer (K^T) before the second barrier, and
+// the producers refill it only after that barrier; dL/du is rewritten only
+// after the next first barrier, which the state waves reach after their dW.
 // ---------------------------------------------------------------------------
 template <int D, int F>
 struct RWalkCfg {
@@ -1867,7 +1870,6 @@ __global__ __launch_bounds__(rwalk_threads<D>()) void hyb_bwd_rwalk_kernel(BwdKA
       }
       lds_barrier();
       lds_barrier();
-      lds_barrier();
     }
   } else if (w == 2) {
     // ---- V rows (operands of dL/dphi(K)) and K^T (operands of dW) ----
@@ -1895,7 +1897,6 @@ __global__ __launch_bounds__(rwalk_threads<D>()) void hyb_bwd_rwalk_kernel(BwdKA
           }
         if (n + 1 < nb) load(blk_of(n + 1));
       }
-      lds_barrier();
       lds_barrier();
       lds_barrier();
     }
@@ -1931,7 +1932,6 @@ __global__ __launch_bounds__(rwalk_threads<D>()) void hyb_bwd_rwalk_kernel(BwdKA
         if (lane < kTile) B.gd[lane] = gdv;
         if (n + 1 < nb) load(blk_of(n + 1));
       }
-      lds_barrier();
       lds_barrier();
       lds_barrier();
     }
@@ -1975,7 +1975,6 @@ __global__ __launch_bounds__(rwalk_threads<D>()) void hyb_bwd_rwalk_kernel(BwdKA
 #pragma unroll
     for (int t = 0; t < NT; ++t) dwacc[t] = f32x16{};
     // step 0: the producers fill the first buffer
-    lds_barrier();
     lds_barrier();
     lds_barrier();
     for (int n = 1; n <= nb; ++n) {
@@ -2060,6 +2059,11 @@ __global__ __launch_bounds__(rwalk_threads<D>()) void hyb_bwd_rwalk_kernel(BwdKA
             }
           }
         }
+        // the K^T operands of dW, read before the barrier: the producers
+        // refill this buffer right after it
+        op_t kb[C::KL];
+#pragma unroll
+        for (int ks = 0; ks < C::KL; ++ks) kb[ks] = B.ktop[cw][ks][lane];
         lds_barrier();
         // dW^T tiles (rows j of tile t, columns 32cw..) += dL/du^T K
 #pragma unroll
@@ -2070,13 +2074,11 @@ __global__ __launch_bounds__(rwalk_threads<D>()) void hyb_bwd_rwalk_kernel(BwdKA
             for (int ks = 0; ks < C::KL; ++ks) {
               op_t uh, ul;
               lds_pair_op(&sh.duT[sg][t * kTile + li][0], ks, hh, uh, ul);
-              const op_t kb = B.ktop[cw][ks][lane];
-              dwacc[t] = M::mma(uh, kb, dwacc[t]);
-              dwacc[t] = M::mma(ul, kb, dwacc[t]);
+              dwacc[t] = M::mma(uh, kb[ks], dwacc[t]);
+              dwacc[t] = M::mma(ul, kb[ks], dwacc[t]);
               __builtin_amdgcn_sched_barrier(0);
             }
       }
-      lds_barrier();
     }
     float* dwk = ka.dwk + ((size_t)u * nseg + seg) * F * D;
 #pragma unroll
