@@ -994,6 +994,8 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
     const float one_minus_w = expf(log_sigmoid(-a.alpha[h]));
     // S (columns col) and S^T (feature tiles cw + j*NC): the earlier
     // segments' increments
+    // (the first increment is loaded straight into the accumulators, so all
+    // its loads are in flight at once; the others are added one by one)
     f32x16 sacc[NRT], sT[RPW][NC];
 #pragma unroll
     for (int rt = 0; rt < NRT; ++rt) sacc[rt] = f32x16{};
@@ -1001,7 +1003,7 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
     for (int j = 0; j < RPW; ++j)
 #pragma unroll
       for (int s = 0; s < NC; ++s) sT[j][s] = f32x16{};
-    for (int sp = 0; sp < seg; ++sp) {
+    auto add_increment = [&](int sp, bool first) {
       const float* src = ka.dS + ((size_t)u * (nseg - 1) + sp) * D * f;
 #pragma unroll
       for (int rt = 0; rt < NRT; ++rt)
@@ -1009,7 +1011,7 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
         for (int i = 0; i < 16; i += 4) {
           const f32x4 y = *reinterpret_cast<const f32x4*>(src + (size_t)col * f + rt * kTile + row_of(i, hh));
 #pragma unroll
-          for (int e = 0; e < 4; ++e) sacc[rt][i + e] += y[e];
+          for (int e = 0; e < 4; ++e) sacc[rt][i + e] = first ? y[e] : sacc[rt][i + e] + y[e];
         }
 #pragma unroll
       for (int j = 0; j < RPW; ++j) {
@@ -1018,10 +1020,14 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
 #pragma unroll
         for (int s = 0; s < NC; ++s)
 #pragma unroll
-          for (int i = 0; i < 16; ++i)
-            sT[j][s][i] += src[(size_t)(s * kTile + row_of(i, hh)) * f + p * kTile + li];
+          for (int i = 0; i < 16; ++i) {
+            const float y = src[(size_t)(s * kTile + row_of(i, hh)) * f + p * kTile + li];
+            sT[j][s][i] = first ? y : sT[j][s][i] + y;
+          }
       }
-    }
+    };
+    if (seg > 0) add_increment(0, true);
+    for (int sp = 1; sp < seg; ++sp) add_increment(sp, false);
     float dal = 0.0f, lss = 0.0f;
     // the block's upstream rows (dout, or the teacher's output) at columns
     // 32cw + row_of(i, hh): prefetched a block ahead
@@ -1940,12 +1946,14 @@ __global__ __launch_bounds__(rwalk_threads<D>()) void hyb_bwd_rwalk_kernel(BwdKA
     const int cw = w - NP, col = cw * kTile + li;
     // Gbar^T tiles (rows c of slice s, columns of feature tile p): the sums
     // over the later segments
+    // (the first increment straight into the accumulators, as in the
+    // forward walk)
     f32x16 gacc[RPW][NC];
 #pragma unroll
     for (int j = 0; j < RPW; ++j)
 #pragma unroll
       for (int s = 0; s < NC; ++s) gacc[j][s] = f32x16{};
-    for (int sp = seg + 1; sp < nseg; ++sp) {
+    auto add_increment = [&](int sp, bool first) {
       const float* src = ka.dG + ((size_t)u * nseg + sp) * D * f;
 #pragma unroll
       for (int j = 0; j < RPW; ++j) {
@@ -1954,10 +1962,14 @@ __global__ __launch_bounds__(rwalk_threads<D>()) void hyb_bwd_rwalk_kernel(BwdKA
 #pragma unroll
         for (int s = 0; s < NC; ++s)
 #pragma unroll
-          for (int i = 0; i < 16; ++i)
-            gacc[j][s][i] += src[(size_t)(s * kTile + row_of(i, hh)) * f + p * kTile + li];
+          for (int i = 0; i < 16; ++i) {
+            const float y = src[(size_t)(s * kTile + row_of(i, hh)) * f + p * kTile + li];
+            gacc[j][s][i] = first ? y : gacc[j][s][i] + y;
+          }
       }
-    }
+    };
+    if (seg + 1 < nseg) add_increment(seg + 1, true);
+    for (int sp = seg + 2; sp < nseg; ++sp) add_increment(sp, false);
     // gz for the same feature tiles, as accumulator tiles whose columns are
     // all equal (register i: feature 32p + row_of(i, hh)); its update
     // phi(Q)^T dL/dD runs on the MFMAs against a broadcast dL/dD operand
