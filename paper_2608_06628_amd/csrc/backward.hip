@@ -102,7 +102,7 @@ static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 static BwdLayout bwd_layout(const Shape& s, int T, bool inputs) {
   const size_t units = (size_t)s.B * s.Hq, f = 2 * (size_t)s.F;
-  const int nseg = prefill_segments(s, T), nblk = T / s.L;
+  const int nseg = segment_plan(s, T).nseg, nblk = T / s.L;
   BwdLayout l;
   size_t o = 0;
   l.dS = o;
@@ -141,6 +141,10 @@ size_t backward_ws_bytes(const Shape& s, int T, bool inputs) {
 struct BwdKArgs {
   BackwardArgs a;
   int nseg, seg_blocks, nblk;
+  // the state increments come in ppseg pieces per segment (npc in all):
+  // dS [units][npc][D][f], dz [units][npc][f]; segment s starts from the sum
+  // of pieces 0 .. s*ppseg - 1
+  int ppseg, npc;
   float *dS, *dz, *dG, *dgz, *gd, *dwq, *dwk, *red, *gnT;
   float *duq, *duk, *dvl;  // input-gradient intermediates (null otherwise)
 };
@@ -280,13 +284,13 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_fwd_kernel(BwdKArgs
 #pragma unroll
   for (int rt = 0; rt < NRT; ++rt) sacc[rt] = f32x16{};
   for (int r = tid; r < f; r += blockDim.x) sh.z[r] = 0.0f;
-  for (int sp = 0; sp < seg; ++sp) {
-    const float* src = ka.dS + ((size_t)u * (nseg - 1) + sp) * D * f;
+  for (int pc = 0; pc < seg * ka.ppseg; ++pc) {
+    const float* src = ka.dS + ((size_t)u * ka.npc + pc) * D * f;
 #pragma unroll
     for (int rt = 0; rt < NRT; ++rt)
 #pragma unroll
       for (int i = 0; i < 16; ++i) sacc[rt][i] += src[(size_t)col * f + rt * kTile + row_of(i, hh)];
-    const float* zs = ka.dz + ((size_t)u * (nseg - 1) + sp) * f;
+    const float* zs = ka.dz + ((size_t)u * ka.npc + pc) * f;
     for (int r = tid; r < f; r += blockDim.x) sh.z[r] += zs[r];
   }
 
@@ -734,7 +738,7 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
   // z at the segment's start: the earlier segments' sums
   for (int r = tid; r < f; r += blockDim.x) {
     float zr = 0.0f;
-    for (int sp = 0; sp < seg; ++sp) zr += ka.dz[((size_t)u * (nseg - 1) + sp) * f + r];
+    for (int pc = 0; pc < seg * ka.ppseg; ++pc) zr += ka.dz[((size_t)u * ka.npc + pc) * f + r];
     sh.z[0][r] = zr;
   }
   // dL/du and the second buffer's Q^T operands start at zero: the softmax
@@ -1003,8 +1007,8 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
     for (int j = 0; j < RPW; ++j)
 #pragma unroll
       for (int s = 0; s < NC; ++s) sT[j][s] = f32x16{};
-    auto add_increment = [&](int sp, bool first) {
-      const float* src = ka.dS + ((size_t)u * (nseg - 1) + sp) * D * f;
+    auto add_increment = [&](int pc, bool first) {
+      const float* src = ka.dS + ((size_t)u * ka.npc + pc) * D * f;
 #pragma unroll
       for (int rt = 0; rt < NRT; ++rt)
 #pragma unroll
@@ -1027,7 +1031,7 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
       }
     };
     if (seg > 0) add_increment(0, true);
-    for (int sp = 1; sp < seg; ++sp) add_increment(sp, false);
+    for (int pc = 1; pc < seg * ka.ppseg; ++pc) add_increment(pc, false);
     float dal = 0.0f, lss = 0.0f;
     // the block's upstream rows (dout, or the teacher's output) at columns
     // 32cw + row_of(i, hh): prefetched a block ahead
@@ -2385,8 +2389,9 @@ template <typename T, int D, int F>
 static hipError_t bwd_go(const BackwardArgs& a, hipStream_t st) {
   const Shape& s = a.s;
   const int units = s.B * s.Hq, nblk = a.T / s.L;
-  const int nseg = prefill_segments(s, a.T);
-  const int seg_blocks = (nblk + nseg - 1) / nseg;
+  const SegPlan plan = segment_plan(s, a.T);
+  const int nseg = plan.nseg;
+  const int seg_blocks = plan.sb;
   const bool inputs = a.dq != nullptr;
   const BwdLayout l = bwd_layout(s, a.T, inputs);
   char* ws = (char*)a.ws;
@@ -2395,9 +2400,11 @@ static hipError_t bwd_go(const BackwardArgs& a, hipStream_t st) {
   ka.a = a;
   ka.nseg = nseg;
   ka.seg_blocks = seg_blocks;
+  ka.ppseg = plan.ppseg;
+  ka.npc = plan.npieces();
   ka.nblk = nblk;
   ka.dS = (float*)(ws + l.dS);
-  ka.dz = ka.dS + (size_t)units * (nseg - 1) * s.D * f;
+  ka.dz = ka.dS + (size_t)units * ka.npc * s.D * f;
   ka.dG = (float*)(ws + l.dG);
   ka.dgz = (float*)(ws + l.dgz);
   ka.gnT = (float*)(ws + l.gnT);
@@ -2415,7 +2422,7 @@ static hipError_t bwd_go(const BackwardArgs& a, hipStream_t st) {
     PrefillArgs pa{s, a.T, nullptr, a.k, a.v, a.W, nullptr, nullptr, nullptr,
                    nullptr, nullptr, ka.dS};
     pa.s.n_slots = s.B;
-    if ((e = launch_prefill_delta(pa, segment_plan(s, a.T), st)) != hipSuccess) return e;
+    if ((e = launch_prefill_delta(pa, plan, st)) != hipSuccess) return e;
   }
   // With the input gradients the four-wave walks serve both dtypes (they
   // also write dL/du and Gbar^T phi(K)); otherwise bf16 takes the pipelined

@@ -107,12 +107,9 @@ struct SegPlan {
   }
 };
 // The prefill's plan (one round of walk workgroups over the chip, the
-// increments in about as many workgroups), and the plan with one piece per
-// segment (the backward's walks).
+// increments in about as many workgroups), and the backward's (the same).
 SegPlan prefill_plan(const Shape& s, int T);
 SegPlan segment_plan(const Shape& s, int T);
-// Prefill: number of sequence segments of the backward's walks.
-int prefill_segments(const Shape& s, int T);
 // The prefill's workspace, and the part the increments take under a plan.
 size_t prefill_ws_bytes(const Shape& s, int T);
 size_t prefill_delta_ws_bytes(const Shape& s, const SegPlan& p);

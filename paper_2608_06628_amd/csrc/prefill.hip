@@ -1370,29 +1370,6 @@ hipError_t launch_prefill_delta(const PrefillArgs& a, const SegPlan& p, hipStrea
   return a.s.D == 64 ? prefill_delta_f<float, 64>(a, p, st) : prefill_delta_f<float, 128>(a, p, st);
 }
 
-// Segments of the backward's walks: about one (request, head, segment)
-// workgroup per CU (256), since a walk workgroup takes a whole CU and the
-// walks are chains of block steps: a second round of workgroups would only
-// repeat each workgroup's start (the sum of the earlier segments'
-// increments) and lengthen the increment launches.  At most 8 segments (the
-// walk of segment s reads the s earlier increments), at least 4 blocks each.
-int prefill_segments(const Shape& s, int T) {
-  const int units = s.B * s.Hq, nblk = T / s.L;
-  int nseg = (256 + units - 1) / units;
-  if (nseg > 8) nseg = 8;
-  if (nseg > nblk / 4) nseg = nblk / 4;
-  if (nseg < 1) nseg = 1;
-  // Every segment must own at least one block at the rounded-up length.
-  for (; nseg > 1; --nseg)
-    if ((nseg - 1) * ((nblk + nseg - 1) / nseg) < nblk) break;
-  return nseg;
-}
-
-SegPlan segment_plan(const Shape& s, int T) {
-  const int nblk = T / s.L, nseg = prefill_segments(s, T);
-  const int sb = (nblk + nseg - 1) / nseg;
-  return SegPlan{nseg, sb, 1, sb};
-}
 
 // The prefill's plan.  A walk workgroup takes a whole CU (its LDS), so the
 // walk takes about one workgroup per CU (256 CUs): segments are what the
@@ -1426,6 +1403,12 @@ SegPlan prefill_plan(const Shape& s, int T) {
   }
   return p;
 }
+
+// The backward's walks use the prefill's plan: the same one round of walk
+// workgroups (a walk workgroup takes a whole CU, and a second round would
+// only repeat each workgroup's start, the sum of the earlier increments) and
+// the same increment pieces.
+SegPlan segment_plan(const Shape& s, int T) { return prefill_plan(s, T); }
 
 size_t prefill_delta_ws_bytes(const Shape& s, const SegPlan& p) {
   if (p.npieces() <= 0) return 0;
