@@ -102,15 +102,17 @@ static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 static BwdLayout bwd_layout(const Shape& s, int T, bool inputs) {
   const size_t units = (size_t)s.B * s.Hq, f = 2 * (size_t)s.F;
-  const int nseg = segment_plan(s, T).nseg, nblk = T / s.L;
+  const SegPlan plan = segment_plan(s, T);
+  const int nseg = plan.nseg, nblk = T / s.L;
+  const size_t npc = plan.npieces() > 0 ? plan.npieces() : 1;
   BwdLayout l;
   size_t o = 0;
   l.dS = o;
-  o = align256(o + prefill_delta_ws_bytes(s, segment_plan(s, T)));
+  o = align256(o + prefill_delta_ws_bytes(s, plan));
   l.dG = o;
-  o = align256(o + units * nseg * s.D * f * 4);
+  o = align256(o + units * npc * s.D * f * 4);
   l.dgz = o;
-  o = align256(o + units * nseg * f * 4);
+  o = align256(o + units * npc * f * 4);
   l.gnT = o;
   o = align256(o + units * nblk * s.D * kTile * 4);
   l.gd = o;
@@ -141,13 +143,25 @@ size_t backward_ws_bytes(const Shape& s, int T, bool inputs) {
 struct BwdKArgs {
   BackwardArgs a;
   int nseg, seg_blocks, nblk;
-  // the state increments come in ppseg pieces per segment (npc in all):
-  // dS [units][npc][D][f], dz [units][npc][f]; segment s starts from the sum
-  // of pieces 0 .. s*ppseg - 1
-  int ppseg, npc;
+  // The increments come in pieces of at most pb blocks, ppseg per segment,
+  // npc in all.  State increments: pieces of segments 0 .. nseg-2, dS
+  // [units][npc][D][f] and dz [units][npc][f]; the forward walk of segment s
+  // starts from the sum of pieces 0 .. s*ppseg - 1.  Reverse increments:
+  // pieces of segments 1 .. nseg-1 (rev_piece), dG [units][npc][D][f] and
+  // dgz [units][npc][f]; the reverse walk of segment s starts from the sum
+  // of pieces s*ppseg .. npc - 1.
+  int ppseg, npc, pb;
   float *dS, *dz, *dG, *dgz, *gd, *dwq, *dwk, *red, *gnT;
   float *duq, *duk, *dvl;  // input-gradient intermediates (null otherwise)
 };
+
+// Blocks blk0 .. blk1-1 of piece pc of the reverse increments (empty where
+// the last segment is short).
+__device__ inline void rev_piece(const BwdKArgs& ka, int pc, int& blk0, int& blk1) {
+  const int seg = pc / ka.ppseg + 1, k = pc % ka.ppseg;
+  blk0 = min(ka.nblk, seg * ka.seg_blocks + k * ka.pb);
+  blk1 = max(blk0, min(ka.nblk, min(seg * ka.seg_blocks + (k + 1) * ka.pb, (seg + 1) * ka.seg_blocks)));
+}
 
 // LDS of the reverse walk's extra work when the input gradients are formed:
 // Gbar^T of the blocks after this one and phi(K), as operands.
@@ -1288,14 +1302,15 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_rev_kernel(BwdKArgs
   const int li = lane & 31, hh = lane >> 5;
   const int Hq = a.s.Hq, Hkv = a.s.Hkv, L = a.s.L, T_ = a.T;
   const int units = a.s.B * Hq, nseg = ka.nseg;
-  // delta covers segments 1 .. nseg-1 (segment 0's sum is never needed)
-  const int nseg_here = delta ? nseg - 1 : nseg;
-  const int vix = xcd_unit(blockIdx.x, units * nseg_here);
-  const int u = vix % units, seg = vix / units + (delta ? 1 : 0);
+  // delta: one workgroup per (unit, piece of segments 1 .. nseg-1; segment
+  // 0's sum is never needed); walk: per (unit, segment)
+  const int vix = xcd_unit(blockIdx.x, units * (delta ? ka.npc : nseg));
+  const int u = vix % units, seg = vix / units;  // (delta: the piece)
   const int b = u / Hq, h = u % Hq, g = h / (Hq / Hkv);
   const size_t qstride = (size_t)Hq * D, kstride = (size_t)Hkv * D;
   const int col = w * kTile + li;
-  const int blk0 = seg * ka.seg_blocks, blk1 = min(ka.nblk, blk0 + ka.seg_blocks);
+  int blk0 = seg * ka.seg_blocks, blk1 = min(ka.nblk, blk0 + ka.seg_blocks);
+  if (delta) rev_piece(ka, seg, blk0, blk1);
 
   // Gbar^T tiles (rows c of slice s, columns of feature tile p) and gz:
   // the sums over the later segments.
@@ -1306,8 +1321,8 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_rev_kernel(BwdKArgs
     for (int s = 0; s < NW; ++s) gacc[j][s] = f32x16{};
   for (int r = tid; r < f; r += blockDim.x) sh.gz[r] = 0.0f;
   if (!delta) {
-    for (int sp = seg + 1; sp < nseg; ++sp) {
-      const float* src = ka.dG + ((size_t)u * nseg + sp) * D * f;
+    for (int sp = seg * ka.ppseg; sp < ka.npc; ++sp) {
+      const float* src = ka.dG + ((size_t)u * ka.npc + sp) * D * f;
 #pragma unroll
       for (int j = 0; j < RPW; ++j) {
         const int p = w + j * NW;
@@ -1318,7 +1333,7 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_rev_kernel(BwdKArgs
           for (int i = 0; i < 16; ++i)
             gacc[j][s][i] += src[(size_t)(s * kTile + row_of(i, hh)) * f + p * kTile + li];
       }
-      const float* zs = ka.dgz + ((size_t)u * nseg + sp) * f;
+      const float* zs = ka.dgz + ((size_t)u * ka.npc + sp) * f;
       for (int r = tid; r < f; r += blockDim.x) sh.gz[r] += zs[r];
     }
   }
@@ -1544,7 +1559,7 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_rev_kernel(BwdKArgs
   }
 
   if (delta) {
-    float* dst = ka.dG + ((size_t)u * nseg + seg) * D * f;
+    float* dst = ka.dG + ((size_t)u * ka.npc + seg) * D * f;
 #pragma unroll
     for (int j = 0; j < RPW; ++j) {
       const int p = w + j * NW;
@@ -1556,7 +1571,7 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_rev_kernel(BwdKArgs
           dst[(size_t)(s * kTile + row_of(i, hh)) * f + p * kTile + li] = gacc[j][s][i];
     }
     lds_barrier();
-    float* zd = ka.dgz + ((size_t)u * nseg + seg) * f;
+    float* zd = ka.dgz + ((size_t)u * ka.npc + seg) * f;
     for (int r = tid; r < f; r += blockDim.x) zd[r] = sh.gz[r];
   } else {
     float* dwk = ka.dwk + ((size_t)u * nseg + seg) * F * D;
@@ -1622,12 +1637,13 @@ __global__ __launch_bounds__(gdelta_threads<D>()) void hyb_bwd_gdelta_kernel(Bwd
   const int li = lane & 31, hh = lane >> 5;
   const int Hq = a.s.Hq, L = a.s.L, T_ = a.T;
   const int units = a.s.B * Hq, nseg = ka.nseg;
-  // segments 1 .. nseg-1 (segment 0's sum is never needed)
-  const int vix = xcd_unit(blockIdx.x, units * (nseg - 1));
-  const int u = vix % units, seg = vix / units + 1;
+  // pieces of segments 1 .. nseg-1 (segment 0's sum is never needed)
+  const int vix = xcd_unit(blockIdx.x, units * ka.npc);
+  const int u = vix % units, pc = vix / units;
   const int b = u / Hq, h = u % Hq;
   const size_t qstride = (size_t)Hq * D;
-  const int blk0 = seg * ka.seg_blocks, blk1 = min(ka.nblk, blk0 + ka.seg_blocks);
+  int blk0, blk1;
+  rev_piece(ka, pc, blk0, blk1);
   const int npair = (blk1 - blk0 + 1) / 2;
   const bool row_ok = li < L;
   const int lrow = min(li, L - 1);
@@ -1739,14 +1755,14 @@ __global__ __launch_bounds__(gdelta_threads<D>()) void hyb_bwd_gdelta_kernel(Bwd
       lds_barrier();
     }
     // Gbar^T tiles as the reverse walk reads them: element (c, r) at c*f + r
-    float* dst = ka.dG + ((size_t)u * nseg + seg) * D * f;
+    float* dst = ka.dG + ((size_t)u * ka.npc + pc) * D * f;
 #pragma unroll
     for (int rt = 0; rt < C::NRT; ++rt)
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj)
         *reinterpret_cast<f32x4*>(dst + (size_t)col * f + rt * kTile + row_of(4 * jj, hh)) =
             f32x4{gacc[rt][4 * jj], gacc[rt][4 * jj + 1], gacc[rt][4 * jj + 2], gacc[rt][4 * jj + 3]};
-    float* zd = ka.dgz + ((size_t)u * nseg + seg) * f;
+    float* zd = ka.dgz + ((size_t)u * ka.npc + pc) * f;
     for (int r = tid - NP * kWave; r < f; r += NC * kWave) zd[r] = sh.gz[r];
   }
 }
@@ -1958,7 +1974,7 @@ __global__ __launch_bounds__(rwalk_threads<D>()) void hyb_bwd_rwalk_kernel(BwdKA
 #pragma unroll
       for (int s = 0; s < NC; ++s) gacc[j][s] = f32x16{};
     auto add_increment = [&](int sp, bool first) {
-      const float* src = ka.dG + ((size_t)u * nseg + sp) * D * f;
+      const float* src = ka.dG + ((size_t)u * ka.npc + sp) * D * f;
 #pragma unroll
       for (int j = 0; j < RPW; ++j) {
         const int p = cw + j * NC;
@@ -1972,8 +1988,8 @@ __global__ __launch_bounds__(rwalk_threads<D>()) void hyb_bwd_rwalk_kernel(BwdKA
           }
       }
     };
-    if (seg + 1 < nseg) add_increment(seg + 1, true);
-    for (int sp = seg + 2; sp < nseg; ++sp) add_increment(sp, false);
+    if (seg * ka.ppseg < ka.npc) add_increment(seg * ka.ppseg, true);
+    for (int sp = seg * ka.ppseg + 1; sp < ka.npc; ++sp) add_increment(sp, false);
     // gz for the same feature tiles, as accumulator tiles whose columns are
     // all equal (register i: feature 32p + row_of(i, hh)); its update
     // phi(Q)^T dL/dD runs on the MFMAs against a broadcast dL/dD operand
@@ -1983,9 +1999,9 @@ __global__ __launch_bounds__(rwalk_threads<D>()) void hyb_bwd_rwalk_kernel(BwdKA
       gzt[j] = f32x16{};
       const int p = cw + j * NC;
       if (p >= NRT) continue;
-      for (int sp = seg + 1; sp < nseg; ++sp)
+      for (int sp = seg * ka.ppseg; sp < ka.npc; ++sp)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) gzt[j][i] += ka.dgz[((size_t)u * nseg + sp) * f + p * kTile + row_of(i, hh)];
+        for (int i = 0; i < 16; ++i) gzt[j][i] += ka.dgz[((size_t)u * ka.npc + sp) * f + p * kTile + row_of(i, hh)];
     }
     f32x16 dwacc[NT];
 #pragma unroll
@@ -2402,6 +2418,7 @@ static hipError_t bwd_go(const BackwardArgs& a, hipStream_t st) {
   ka.seg_blocks = seg_blocks;
   ka.ppseg = plan.ppseg;
   ka.npc = plan.npieces();
+  ka.pb = plan.pb;
   ka.nblk = nblk;
   ka.dS = (float*)(ws + l.dS);
   ka.dz = ka.dS + (size_t)units * ka.npc * s.D * f;
@@ -2445,10 +2462,10 @@ static hipError_t bwd_go(const BackwardArgs& a, hipStream_t st) {
   if ((e = hipGetLastError()) != hipSuccess) return e;
   if (nseg > 1) {
     if constexpr (sizeof(T) == 2) {
-      hipLaunchKernelGGL((hyb_bwd_gdelta_kernel<D, F>), dim3(units * (nseg - 1)),
+      hipLaunchKernelGGL((hyb_bwd_gdelta_kernel<D, F>), dim3(units * ka.npc),
                          dim3(gdelta_threads<D>()), 0, st, ka);
     } else {
-      hipLaunchKernelGGL((hyb_bwd_rev_kernel<T, D, F, false>), dim3(units * (nseg - 1)), block, 0,
+      hipLaunchKernelGGL((hyb_bwd_rev_kernel<T, D, F, false>), dim3(units * ka.npc), block, 0,
                          st, ka, 1);
     }
     if ((e = hipGetLastError()) != hipSuccess) return e;
