@@ -2210,13 +2210,25 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_inputs_kernel(BwdKA
   const int cc = w * kTile + li;  // this lane's output column
   const bool lrow = li < L;
 
+  // The staging loops below have compile-time trip counts (NTHR threads)
+  // and issue all of a thread's loads before its first LDS store: a loop
+  // that stores each value as it lands waits a full memory round trip per
+  // iteration.
+  constexpr int NTHR = kWave * C::NW;
   // rows of a [.][stride] tensor into a [32][LD] LDS tile, rows past L zero
   auto stage_rows = [&](T (*dst)[LD], const T* src, size_t stride) {
-    for (int it = tid; it < kTile * (D / EPC); it += blockDim.x) {
-      const int r = it / (D / EPC), c = (it % (D / EPC)) * EPC;
-      uint4 x = {0u, 0u, 0u, 0u};
-      if (r < L) x = *reinterpret_cast<const uint4*>(src + (size_t)r * stride + c);
-      *reinterpret_cast<uint4*>(&dst[r][c]) = x;
+    constexpr int N = kTile * (D / EPC) / NTHR;
+    static_assert(N * NTHR == kTile * (D / EPC), "whole passes");
+    uint4 x[N];
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+      const int it = tid + k * NTHR, r = it / (D / EPC), c = (it % (D / EPC)) * EPC;
+      x[k] = *reinterpret_cast<const uint4*>(src + (size_t)min(r, L - 1) * stride + c);
+    }
+#pragma unroll
+    for (int k = 0; k < N; ++k) {
+      const int it = tid + k * NTHR, r = it / (D / EPC), c = (it % (D / EPC)) * EPC;
+      *reinterpret_cast<uint4*>(&dst[r][c]) = r < L ? x[k] : uint4{0u, 0u, 0u, 0u};
     }
   };
   stage_rows(sh.k, (const T*)a.k + (((size_t)b * T_ + t0) * Hkv + g) * D, kstride);
@@ -2231,19 +2243,32 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_inputs_kernel(BwdKA
     stage_rows(sh.q, (const T*)a.q + (((size_t)b * T_ + t0) * Hq + h) * D, qstride);
     {
       const float* gn = ka.gnT + (u * nblk + blk) * D * kTile;  // dL/dN^T [c][i]
-      for (int it = tid; it < D * kTile; it += blockDim.x) {
-        const int c = it / kTile, i = it % kTile;
-        const float x = i < L ? gn[it] : 0.0f;
+      constexpr int NG = D * kTile / NTHR, NWT = F * (D / EPC) / NTHR;
+      static_assert(NG * NTHR == D * kTile && NWT * NTHR == F * (D / EPC), "whole passes");
+      float xg[NG];
+#pragma unroll
+      for (int k = 0; k < NG; ++k) xg[k] = gn[tid + k * NTHR];
+      const T* wsrc = (const T*)a.W + (size_t)h * F * D;
+      uint4 xw[NWT];
+#pragma unroll
+      for (int k = 0; k < NWT; ++k) {
+        const int it = tid + k * NTHR, j = it / (D / EPC), c = (it % (D / EPC)) * EPC;
+        xw[k] = *reinterpret_cast<const uint4*>(wsrc + (size_t)j * D + c);
+      }
+      const float gdl = tid < kTile ? ka.gd[(u * nblk + blk) * kTile + tid] : 0.0f;
+#pragma unroll
+      for (int k = 0; k < NG; ++k) {
+        const int it = tid + k * NTHR, c = it / kTile, i = it % kTile;
+        const float x = i < L ? xg[k] : 0.0f;
         const T xh = from_f32<T>(x);
         sh.dn[0][i][c] = xh;
         if constexpr (C::NPART == 2) sh.dn[1][i][c] = from_f32<T>(x - to_f32(xh));
       }
-      if (tid < kTile) sh.gd[tid] = tid < L ? ka.gd[(u * nblk + blk) * kTile + tid] : 0.0f;
-      const T* wsrc = (const T*)a.W + (size_t)h * F * D;
-      for (int it = tid; it < F * (D / EPC); it += blockDim.x) {
-        const int j = it / (D / EPC), c = (it % (D / EPC)) * EPC;
-        *reinterpret_cast<uint4*>(&sh.wt[j][c]) =
-            *reinterpret_cast<const uint4*>(wsrc + (size_t)j * D + c);
+      if (tid < kTile) sh.gd[tid] = tid < L ? gdl : 0.0f;
+#pragma unroll
+      for (int k = 0; k < NWT; ++k) {
+        const int it = tid + k * NTHR, j = it / (D / EPC), c = (it % (D / EPC)) * EPC;
+        *reinterpret_cast<uint4*>(&sh.wt[j][c]) = xw[k];
       }
     }
     lds_barrier();
