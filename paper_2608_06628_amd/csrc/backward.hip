@@ -2234,43 +2234,71 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_inputs_kernel(BwdKA
   stage_rows(sh.k, (const T*)a.k + (((size_t)b * T_ + t0) * Hkv + g) * D, kstride);
   stage_rows(sh.v, (const T*)a.v + (((size_t)b * T_ + t0) * Hkv + g) * D, kstride);
 
+  // A head's staged operands (its Q rows, dL/dN^T, W_h and dL/dD) are
+  // fetched into registers while the previous head is computed, then moved
+  // to LDS.
+  constexpr int NQ = kTile * (D / EPC) / NTHR, NG = D * kTile / NTHR, NWT = F * (D / EPC) / NTHR;
+  static_assert(NQ * NTHR == kTile * (D / EPC) && NG * NTHR == D * kTile &&
+                    NWT * NTHR == F * (D / EPC),
+                "whole passes");
+  struct HeadRegs {
+    uint4 xq[NQ];
+    float xg[NG];
+    uint4 xw[NWT];
+    float gdl;
+  };
+  auto fetch = [&](int hq, HeadRegs& r) {
+    const int h = g * G + hq;
+    const size_t u = (size_t)b * Hq + h;
+    const T* qsrc = (const T*)a.q + (((size_t)b * T_ + t0) * Hq + h) * D;
+#pragma unroll
+    for (int k = 0; k < NQ; ++k) {
+      const int it = tid + k * NTHR, rr = it / (D / EPC), c = (it % (D / EPC)) * EPC;
+      r.xq[k] = *reinterpret_cast<const uint4*>(qsrc + (size_t)min(rr, L - 1) * qstride + c);
+    }
+    const float* gn = ka.gnT + (u * nblk + blk) * D * kTile;  // dL/dN^T [c][i]
+#pragma unroll
+    for (int k = 0; k < NG; ++k) r.xg[k] = gn[tid + k * NTHR];
+    const T* wsrc = (const T*)a.W + (size_t)h * F * D;
+#pragma unroll
+    for (int k = 0; k < NWT; ++k) {
+      const int it = tid + k * NTHR, j = it / (D / EPC), c = (it % (D / EPC)) * EPC;
+      r.xw[k] = *reinterpret_cast<const uint4*>(wsrc + (size_t)j * D + c);
+    }
+    r.gdl = tid < kTile ? ka.gd[(u * nblk + blk) * kTile + tid] : 0.0f;
+  };
+  auto put = [&](const HeadRegs& r) {
+#pragma unroll
+    for (int k = 0; k < NQ; ++k) {
+      const int it = tid + k * NTHR, rr = it / (D / EPC), c = (it % (D / EPC)) * EPC;
+      *reinterpret_cast<uint4*>(&sh.q[rr][c]) = rr < L ? r.xq[k] : uint4{0u, 0u, 0u, 0u};
+    }
+#pragma unroll
+    for (int k = 0; k < NG; ++k) {
+      const int it = tid + k * NTHR, c = it / kTile, i = it % kTile;
+      const float x = i < L ? r.xg[k] : 0.0f;
+      const T xh = from_f32<T>(x);
+      sh.dn[0][i][c] = xh;
+      if constexpr (C::NPART == 2) sh.dn[1][i][c] = from_f32<T>(x - to_f32(xh));
+    }
+    if (tid < kTile) sh.gd[tid] = tid < L ? r.gdl : 0.0f;
+#pragma unroll
+    for (int k = 0; k < NWT; ++k) {
+      const int it = tid + k * NTHR, j = it / (D / EPC), c = (it % (D / EPC)) * EPC;
+      *reinterpret_cast<uint4*>(&sh.wt[j][c]) = r.xw[k];
+    }
+  };
+  HeadRegs hr;
+  fetch(0, hr);
+
   f32x16 dks = {}, dkl = {}, dva = {};
   for (int hq = 0; hq < G; ++hq) {
     const int h = g * G + hq;
     const size_t u = (size_t)b * Hq + h;
     const float lw = log_sigmoid(a.alpha[h]);
     lds_barrier();  // the previous head's readers are done
-    stage_rows(sh.q, (const T*)a.q + (((size_t)b * T_ + t0) * Hq + h) * D, qstride);
-    {
-      const float* gn = ka.gnT + (u * nblk + blk) * D * kTile;  // dL/dN^T [c][i]
-      constexpr int NG = D * kTile / NTHR, NWT = F * (D / EPC) / NTHR;
-      static_assert(NG * NTHR == D * kTile && NWT * NTHR == F * (D / EPC), "whole passes");
-      float xg[NG];
-#pragma unroll
-      for (int k = 0; k < NG; ++k) xg[k] = gn[tid + k * NTHR];
-      const T* wsrc = (const T*)a.W + (size_t)h * F * D;
-      uint4 xw[NWT];
-#pragma unroll
-      for (int k = 0; k < NWT; ++k) {
-        const int it = tid + k * NTHR, j = it / (D / EPC), c = (it % (D / EPC)) * EPC;
-        xw[k] = *reinterpret_cast<const uint4*>(wsrc + (size_t)j * D + c);
-      }
-      const float gdl = tid < kTile ? ka.gd[(u * nblk + blk) * kTile + tid] : 0.0f;
-#pragma unroll
-      for (int k = 0; k < NG; ++k) {
-        const int it = tid + k * NTHR, c = it / kTile, i = it % kTile;
-        const float x = i < L ? xg[k] : 0.0f;
-        const T xh = from_f32<T>(x);
-        sh.dn[0][i][c] = xh;
-        if constexpr (C::NPART == 2) sh.dn[1][i][c] = from_f32<T>(x - to_f32(xh));
-      }
-      if (tid < kTile) sh.gd[tid] = tid < L ? gdl : 0.0f;
-#pragma unroll
-      for (int k = 0; k < NWT; ++k) {
-        const int it = tid + k * NTHR, j = it / (D / EPC), c = (it % (D / EPC)) * EPC;
-        *reinterpret_cast<uint4*>(&sh.wt[j][c]) = xw[k];
-      }
-    }
+    put(hr);
+    if (hq + 1 < G) fetch(hq + 1, hr);  // the next head's operands in flight
     lds_barrier();
 
     // Scores and dL/dP = dL/dN_i . v_j: queries in lanes (sq, pq: rows j,
