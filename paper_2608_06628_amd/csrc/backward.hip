@@ -2245,7 +2245,8 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_inputs_kernel(BwdKA
     uint4 xq[NQ];
     float xg[NG];
     uint4 xw[NWT];
-    float gdl;
+    float gdl, alpha;
+    float xv[16];  // the state part of dv at this lane's rows (below)
   };
   auto fetch = [&](int hq, HeadRegs& r) {
     const int h = g * G + hq;
@@ -2266,6 +2267,12 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_inputs_kernel(BwdKA
       r.xw[k] = *reinterpret_cast<const uint4*>(wsrc + (size_t)j * D + c);
     }
     r.gdl = tid < kTile ? ka.gd[(u * nblk + blk) * kTile + tid] : 0.0f;
+    r.alpha = a.alpha[h];
+    // Gbar^T phi(k_j) from the reverse walk, rows j = row_of(r, hh) (rows
+    // past the block read row L-1 and are dropped where they are added)
+    const float* vsrc = ka.dvl + (u * T_ + t0) * D + cc;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) r.xv[i] = vsrc[(size_t)min(row_of(i, hh), L - 1) * D];
   };
   auto put = [&](const HeadRegs& r) {
 #pragma unroll
@@ -2295,7 +2302,10 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_inputs_kernel(BwdKA
   for (int hq = 0; hq < G; ++hq) {
     const int h = g * G + hq;
     const size_t u = (size_t)b * Hq + h;
-    const float lw = log_sigmoid(a.alpha[h]);
+    const float lw = log_sigmoid(hr.alpha);
+    float xv[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) xv[i] = hr.xv[i];
     lds_barrier();  // the previous head's readers are done
     put(hr);
     if (hq + 1 < G) fetch(hq + 1, hr);  // the next head's operands in flight
@@ -2387,14 +2397,9 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_inputs_kernel(BwdKA
       }
     }
     // the state part of dv: Gbar^T phi(k_j) from the reverse walk
-    {
-      const float* src = ka.dvl + (u * T_ + t0) * D + cc;
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int j = row_of(r, hh);
-        if (j < L) dva[r] += src[(size_t)j * D];
-      }
-    }
+    for (int r = 0; r < 16; ++r)
+      if (row_of(r, hh) < L) dva[r] += xv[r];
   }
   // dk, dv of the KV head: rows j (keys), column cc
   float* dkd = a.dk + (((size_t)b * T_ + t0) * Hkv + g) * D + cc;
