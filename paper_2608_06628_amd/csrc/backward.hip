@@ -994,6 +994,27 @@ __global__ __launch_bounds__(fpipe_threads<D>()) void hyb_bwd_fpipe_kernel(BwdKA
                 dwacc[t][ct] = M::mma(ul, qt, dwacc[t][ct]);
               }
             }
+        if (ka.duq != nullptr && n > 0) {
+          // with the input gradients: dL/du of the same block's queries, both
+          // signs summed (each as its pair hi + lo), for dL/dq = W_h dL/du
+          float* dst = ka.duq + ((size_t)u * T_ + (size_t)(blk0 + n - 1) * L) * F;
+          for (int it = (w - 2) * kWave + lane; it < L * (F / 4); it += C::NSM * kWave) {
+            const int t = it / (F / 4), j4 = (it % (F / 4)) * 4;
+            f32x4 x;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              float acc = 0.0f;
+#pragma unroll
+              for (int sg = 0; sg < 2; ++sg) {
+                const uint32_t pk = sh.x.duT[sg][j4 + e][t];
+                acc += unpack_hi(pk);
+                acc += unpack_lo(pk);
+              }
+              x[e] = acc;
+            }
+            *reinterpret_cast<f32x4*>(dst + (size_t)t * F + j4) = x;
+          }
+        }
       }
     }
     float* dwq = ka.dwq + ((size_t)u * nseg + seg) * F * D;
@@ -2499,12 +2520,11 @@ static hipError_t bwd_go(const BackwardArgs& a, hipStream_t st) {
     pa.s.n_slots = s.B;
     if ((e = launch_prefill_delta(pa, plan, st)) != hipSuccess) return e;
   }
-  // With the input gradients the four-wave walks serve both dtypes (they
-  // also write dL/du and Gbar^T phi(K)); otherwise bf16 takes the pipelined
-  // walks.
-  if (inputs) {
-    hipLaunchKernelGGL((hyb_bwd_fwd_kernel<T, D, F, true>), dim3(units * nseg), block, 0, st, ka);
-  } else if constexpr (sizeof(T) == 2) {
+  // bf16 takes the pipelined forward walk (which also writes dL/du of the
+  // queries when the input gradients are asked for); fp32 the four-wave one.
+  // The reverse walk with the input gradients is the four-wave one for both
+  // dtypes (it also writes dL/du of the keys and Gbar^T phi(K)).
+  if constexpr (sizeof(T) == 2) {
     // (the pipelined walk addresses a request's upstream rows and a unit's
     // dL/dN^T through 32-bit buffer offsets)
     const bool fits = (size_t)a.T * s.Hq * D * sizeof(T) < ((size_t)1 << 31) &&
@@ -2512,8 +2532,12 @@ static hipError_t bwd_go(const BackwardArgs& a, hipStream_t st) {
     if (fits)
       hipLaunchKernelGGL((hyb_bwd_fpipe_kernel<D, F>), dim3(units * nseg), dim3(fpipe_threads<D>()),
                          0, st, ka);
+    else if (inputs)
+      hipLaunchKernelGGL((hyb_bwd_fwd_kernel<T, D, F, true>), dim3(units * nseg), block, 0, st, ka);
     else
       hipLaunchKernelGGL((hyb_bwd_fwd_kernel<T, D, F, false>), dim3(units * nseg), block, 0, st, ka);
+  } else if (inputs) {
+    hipLaunchKernelGGL((hyb_bwd_fwd_kernel<T, D, F, true>), dim3(units * nseg), block, 0, st, ka);
   } else {
     hipLaunchKernelGGL((hyb_bwd_fwd_kernel<T, D, F, false>), dim3(units * nseg), block, 0, st, ka);
   }
