@@ -1389,9 +1389,32 @@ __global__ __launch_bounds__(kWave*(D / kTile)) void hyb_bwd_rev_kernel(BwdKArgs
 #pragma unroll
           for (int ks = 0; ks < C::KL; ++ks)
             vrow[s][ks] = keep_if<T>(row_ok, lds_op_perm<T>(vr, ks, hh, s * kTile));
+        if constexpr (sizeof(T) == 2) {
+          // K^T operands of this wave's columns: its K row operands times
+          // the identity (exact), rather than 2-byte gathers (pairs of them
+          // share a register, and each waits for the other)
+          op_t ksel[C::KL];
 #pragma unroll
-        for (int ks = 0; ks < C::KL; ++ks)
-          ktop[ks] = load_rows_op<T>(kb + col, kstride, ks, hh, L, false);
+          for (int sw = 0; sw < NW; ++sw)
+            if (w == sw) {
+#pragma unroll
+              for (int kk = 0; kk < C::KL; ++kk) ksel[kk] = kop[sw * C::KL + kk];
+            }
+          f32x16 kt = {};
+#pragma unroll
+          for (int kk = 0; kk < C::KL; ++kk) {
+            op_t id;
+#pragma unroll
+            for (int e = 0; e < E; ++e) id[e] = (T)(kk * KW + hh * E + e == li ? 1.0f : 0.0f);
+            kt = M::mma(ksel[kk], id, kt);
+          }
+#pragma unroll
+          for (int kk = 0; kk < C::KL; ++kk) ktop[kk] = acc_op<T>(kt, kk);
+        } else {
+#pragma unroll
+          for (int ks = 0; ks < C::KL; ++ks)
+            ktop[ks] = load_rows_op<T>(kb + col, kstride, ks, hh, L, false);
+        }
       }
     }
     const float gdl = ka.gd[((size_t)u * ka.nblk + blk) * kTile + li];
