@@ -390,6 +390,13 @@ __device__ inline float log_sigmoid(float a) {
 // format; the untyped loads and stores used here take no other field).
 constexpr int kBufferWord3 = 0x00020000;
 
+// A 16-byte piece per lane from a buffer straight into LDS: lane l's piece
+// goes to lds + 16 l (lds is the wave's base, uniform), read from the
+// buffer at voff (per lane) + soff (scalar).
+__device__ inline void buf_to_lds16(__amdgpu_buffer_rsrc_t r, void* lds, int voff, int soff) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, voff, soff, 0, 0);
+}
+
 __device__ inline void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
   __builtin_amdgcn_s_barrier();

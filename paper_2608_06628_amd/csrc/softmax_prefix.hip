@@ -342,10 +342,51 @@ __global__ __launch_bounds__(kWave* NG, 2) void hyb_sp_ring_kernel(SoftmaxPrefix
     __syncthreads();
   }
 
+  // Copies of a tile that lies wholly in the cached prefix: a buffer
+  // descriptor whose base is the tile's first row (a scalar) and, per lane
+  // and copy, the 32-bit offset of its 16-byte piece, which is the same for
+  // every tile.  Tiles that reach past the cache or the range take the
+  // general path below.
+  int voff[IPW];
+#pragma unroll
+  for (int u = 0; u < IPW; ++u) {
+    const int ins = w * IPW + u, i = ins % IK;
+    const int t = i * RPI + lane / CPR, pos = lane % CPR;
+    voff[u] = (int)(((size_t)t * kstride + (size_t)((pos ^ RG::swz(t)) * EPC)) * sizeof(bf16));
+  }
+  const int cend = min(hi, P);  // keys below this come from the cache
+  auto issue_fast = [&](int n, SpSlot<D>& sl) __attribute__((always_inline)) {
+    const int j0 = lo + n * kTile;
+    const bf16* kt = kc;
+    const bf16* vt = vc;
+    if constexpr (PAGED) {
+      const int pi = j0 >> a.page_shift;
+      const ptrdiff_t sh =
+          ((ptrdiff_t)__builtin_amdgcn_readfirstlane(pages[pi - p0]) - pi) * ((ptrdiff_t)kstride << a.page_shift);
+      kt += sh;
+      vt += sh;
+    }
+    kt += (size_t)j0 * kstride;
+    vt += (size_t)j0 * kstride;
+    const int span = (int)((size_t)kTile * kstride * sizeof(bf16));
+    const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(kt), 0, span, kBufferWord3);
+    const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(vt), 0, span, kBufferWord3);
+#pragma unroll
+    for (int u = 0; u < IPW; ++u) {
+      const int ins = w * IPW + u, kv = ins / IK, i = ins % IK;
+      bf16* dst = (kv == 0 ? sl.k : sl.v) + i * RPI * D;
+      buf_to_lds16(kv == 0 ? rk : rv, dst, voff[u], 0);
+    }
+  };
+
   // This wave's copies of tile n (keys past the range read the range's last
   // key, in bounds, and are masked below).
   auto issue = [&](int n, SpSlot<D>& sl) __attribute__((always_inline)) {
     const int j0 = lo + n * kTile;
+    if (j0 + kTile <= cend) {
+      issue_fast(n, sl);
+      return;
+    }
     const bf16* kcb = kc;
     const bf16* vcb = vc;
     if constexpr (PAGED) {
