@@ -415,10 +415,17 @@ __global__ __launch_bounds__(kWave* NG, 2) void hyb_sp_ring_kernel(SoftmaxPrefix
   };
 
   const float scale = 1.0f / sqrtf((float)D);
-  float m = -INFINITY, l = 0.0f;
-  f32x16 acc[NCT];
+  // The running sum of the weights comes from the MFMAs, as the product of
+  // P^T with a tile of ones (every row of lsum holds it; only row 0 is kept
+  // rescaled, the one that is read), so it is the sum of the same rounded
+  // weights that enter P V.
+  float m = -INFINITY;
+  f32x16 acc[NCT], lsum = {};
 #pragma unroll
   for (int ct = 0; ct < NCT; ++ct) acc[ct] = f32x16{};
+  op_t ones;
+#pragma unroll
+  for (int e = 0; e < E; ++e) ones[e] = (bf16)1.0f;
 
   auto compute = [&](int n, const SpSlot<D>& sl) __attribute__((always_inline)) {
     const int j0 = lo + n * kTile;
@@ -428,32 +435,29 @@ __global__ __launch_bounds__(kWave* NG, 2) void hyb_sp_ring_kernel(SoftmaxPrefix
       const int c = 2 * ks + hh;  // 16-byte chunk of elements ks*KW + hh*E
       sc = M::mma(load_op<bf16>(&sl.k[li * D + (c ^ RG::swz(li)) * EPC]), qop[ks], sc);
     }
-    const bool full = j0 + kTile <= hi;
     float p[16];
+    if (j0 + kTile <= hi) {  // (uniform) a full tile needs no range masks
+#pragma unroll
+      for (int i = 0; i < 16; ++i) p[i] = sc[i] * scale;
+    } else {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) p[i] = j0 + row_of(i, hh) < hi ? sc[i] * scale : -INFINITY;
+    }
     float mt = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      p[i] = (full || j0 + row_of(i, hh) < hi) ? sc[i] * scale : -INFINITY;
-      mt = fmaxf(mt, p[i]);
-    }
+    for (int i = 0; i < 16; ++i) mt = fmaxf(mt, p[i]);
     mt = fmaxf(mt, xor32(mt));
     const float mn = fmaxf(m, mt);
-    float ps = 0.0f;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      p[i] = as_operand<bf16>(fast_exp(p[i] - mn));
-      ps += p[i];
-    }
-    ps += xor32(ps);
+    for (int i = 0; i < 16; ++i) p[i] = fast_exp(p[i] - mn);
     if (__any(mn > m)) {
       const float corr = fast_exp(m - mn);
-      l *= corr;
+      lsum[0] *= corr;
 #pragma unroll
       for (int ct = 0; ct < NCT; ++ct)
 #pragma unroll
         for (int i = 0; i < 16; ++i) acc[ct][i] *= corr;
     }
-    l += ps;
     m = mn;
     // V^T operands by transposing reads: in each 16-lane quarter lane i
     // addresses key kb + i/4 at columns cb + 4*(i%4) .. +3 and receives
@@ -475,6 +479,8 @@ __global__ __launch_bounds__(kWave* NG, 2) void hyb_sp_ring_kernel(SoftmaxPrefix
         acc[ct] = M::mma(va, cvt_op<bf16>(&p[ks * E]), acc[ct]);
       }
     }
+#pragma unroll
+    for (int ks = 0; ks < KL; ++ks) lsum = M::mma(ones, cvt_op<bf16>(&p[ks * E]), lsum);
   };
 
   // Wait for this wave's copies of tile n, with `later` tiles issued after
@@ -509,6 +515,7 @@ __global__ __launch_bounds__(kWave* NG, 2) void hyb_sp_ring_kernel(SoftmaxPrefix
   }
 
   if (li >= L) return;
+  const float l = lsum[0];
   if (ns == 1) {
     // one range: the result is final, normalised here (no combine launch)
     const float inv = 1.0f / l;
