@@ -414,7 +414,10 @@ __global__ __launch_bounds__(kWave* NG, 2) void hyb_sp_ring_kernel(SoftmaxPrefix
     }
   };
 
-  const float scale = 1.0f / sqrtf((float)D);
+  // Scores and the running maximum m are kept in the log2 domain (scaled by
+  // log2 e with 1/sqrt(d)), so each weight is one subtraction and one exp2;
+  // m is converted back where it is written out for the combine.
+  const float scale = 1.4426950408889634f / sqrtf((float)D);
   // The running sum of the weights comes from the MFMAs, as the product of
   // P^T with a tile of ones (every row of lsum holds it; only row 0 is kept
   // rescaled, the one that is read), so it is the sum of the same rounded
@@ -449,9 +452,9 @@ __global__ __launch_bounds__(kWave* NG, 2) void hyb_sp_ring_kernel(SoftmaxPrefix
     mt = fmaxf(mt, xor32(mt));
     const float mn = fmaxf(m, mt);
 #pragma unroll
-    for (int i = 0; i < 16; ++i) p[i] = fast_exp(p[i] - mn);
+    for (int i = 0; i < 16; ++i) p[i] = __builtin_amdgcn_exp2f(p[i] - mn);
     if (__any(mn > m)) {
-      const float corr = fast_exp(m - mn);
+      const float corr = __builtin_amdgcn_exp2f(m - mn);
       lsum[0] *= corr;
 #pragma unroll
       for (int ct = 0; ct < NCT; ++ct)
@@ -540,7 +543,7 @@ __global__ __launch_bounds__(kWave* NG, 2) void hyb_sp_ring_kernel(SoftmaxPrefix
       *reinterpret_cast<f32x4*>(wacc + ct * kTile + row_of(i, hh)) =
           f32x4{acc[ct][i], acc[ct][i + 1], acc[ct][i + 2], acc[ct][i + 3]};
   if (hh == 0) {
-    wml[0] = m;
+    wml[0] = m * 0.6931471805599453f;  // back to the natural log
     wml[1] = l;
   }
 }
