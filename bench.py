@@ -738,13 +738,18 @@ COLD_BYTES = 384 << 20  # more than the 256 MB memory-side cache
 
 
 def median_ms(fn, n=20, warm=3):
-    """Median of n individually timed calls (HIP events around each)."""
+    """Median of n individually timed calls (HIP events around each).  Each
+    call is queued behind a short GPU sleep, so that the host's work for the
+    call (Python and the argument marshalling of the binding) overlaps the
+    sleep and the event pair brackets only queued GPU work: single calls of
+    about 10 us are otherwise timed with the host's time included."""
     for _ in range(warm):
         fn()
     torch.cuda.synchronize()
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
           for _ in range(n)]
     for a, b in ev:
+        torch.cuda._sleep(200_000)  # about 0.1 ms of GPU time
         a.record()
         fn()
         b.record()

@@ -369,7 +369,16 @@ __device__ inline void store_out1(void* out, size_t idx, float v, bool f32) {
     ((bf16*)out)[idx] = (bf16)v;
 }
 
-__device__ inline float xor32(float x) { return __shfl_xor(x, 32); }
+// The value of lane l ^ 32.  One v_permlane32_swap of x with itself leaves
+// the lower half repeated in its first result and the upper half repeated in
+// its second, so each lane picks the other half's copy: no LDS round trip
+// (as a cross-lane shuffle through ds_bpermute would take).  Waves are 64
+// lanes and blocks one-dimensional, so bit 5 of the thread index is the half.
+__device__ inline float xor32(float x) {
+  const int v = __builtin_bit_cast(int, x);
+  const auto r = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return __builtin_bit_cast(float, (threadIdx.x & 32) ? r[0] : r[1]);
+}
 
 __device__ inline float fast_exp(float x) {
   // e^x = 2^(x log2 e); v_exp_f32 is exact to about 1 ulp.
