@@ -93,7 +93,17 @@ struct Mma16<float> {
   __device__ static inline op_t zero() { return 0.0f; }
 };
 
-__device__ inline float xor16(float x) { return __shfl_xor(x, 16); }
+// The value of lane l ^ 16.  v_permlane16_swap exchanges the odd 16-lane rows
+// of its first operand with the even rows of its second: applied to x and x,
+// the first result holds rows (0, 0, 2, 2) and the second rows (1, 1, 3, 3),
+// so each lane picks the other row of its pair (as xor32 below, no LDS round
+// trip).  Blocks are one-dimensional, so bit 4 of the thread index is the
+// row's parity.
+__device__ inline float xor16(float x) {
+  const int v = __builtin_bit_cast(int, x);
+  const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  return __builtin_bit_cast(float, (threadIdx.x & 16) ? r[0] : r[1]);
+}
 
 // Row of accumulator register i (0..15) held by lane half hh.
 __device__ __host__ constexpr int row_of(int i, int hh) {
