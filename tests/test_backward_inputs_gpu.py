@@ -43,6 +43,10 @@ SHAPES = [
     (1, 1024, 4, 2, 128, 32, 64, "bf16"),   # 8 sequence segments
     (1, 35, 2, 1, 64, 5, 32, "bf16"),       # odd block length
     (1, 32, 2, 1, 128, 32, 64, "bf16"),     # one block: softmax attention only
+    # 13 blocks: 3 segments of 5, increments in pieces of 3 blocks; the last
+    # segment's second reverse piece is empty
+    (1, 416, 2, 1, 64, 32, 32, "bf16"),
+    (1, 416, 2, 1, 64, 32, 32, "f32"),
 ]
 
 
