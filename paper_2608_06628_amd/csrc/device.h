@@ -395,6 +395,11 @@ __device__ inline float fast_exp(float x) {
   return __builtin_amdgcn_exp2f(x * 1.4426950408889634f);
 }
 
+constexpr float kLog2e = 1.4426950408889634f;
+
+// 1 / x by the hardware reciprocal (about 1 ulp).
+__device__ inline float fast_rcp(float x) { return __builtin_amdgcn_rcpf(x); }
+
 // log(sigmoid(a)) without overflow for any a.
 __device__ inline float log_sigmoid(float a) {
   return a >= 0.0f ? -log1pf(expf(-a)) : a - log1pf(expf(a));

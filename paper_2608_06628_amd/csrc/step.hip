@@ -324,6 +324,26 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
     }
   };
 
+  // The same transposing reads over rows of another staged tile whose
+  // columns are features: lane (c16, quad) gets rows key(0..7, quad) of
+  // column col0 + c16 (col0 a multiple of 16), i.e. the phi(K)^T A operand
+  // of features col0 .. col0+15 in the key order of vt_op.
+  auto rows_op = [&](const T* rows, int col0) -> op_t {
+    if constexpr (C::DMA_QK) {
+      typedef short s16x4 __attribute__((ext_vector_type(4)));
+      const int col = col0 + 4 * (c16 % 4);
+      auto piece = [&](int t) {
+        const T* src = rows + t * D + ((col / C::EPC) ^ C::swz(t)) * C::EPC + col % C::EPC;
+        return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (__attribute__((address_space(3))) s16x4*)src);
+      };
+      const s16x4 lo = piece(quad * 4 + c16 / 4), hi = piece(16 + quad * 4 + c16 / 4);
+      return __builtin_bit_cast(op_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    } else {
+      return M::zero();
+    }
+  };
+
   // K and W_h operands (the block wave's step; the state wave's phi(K) in
   // the commit), z at this lane's features in phi-register order (block
   // wave), phi(K)^T operands (commit, state wave).
@@ -402,20 +422,22 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
   };
 
   // EARLY commit of column block cb (fp32 state in buf): S^T of the block
-  // += (phi(K)^T V)^T, the phi(K)^T operands (hi, lo) read from the block
-  // wave's staging space.  Run rn of the block holds, in lane (c16, quad),
-  // features rn*16 + quad*4 .. +3 of column column(cb, c16): the accumulator
-  // layout of the 16 x 16 tile (features rn*16 .., columns of cb).
+  // += (phi(K)^T V)^T, the phi(K)^T operands (hi, lo) read by transposing
+  // reads from the phi(K) rows the block wave left in its staging space (hi
+  // parts over the staged K rows, lo parts in the head area).  Run rn of the
+  // block holds, in lane (c16, quad), features rn*16 + quad*4 .. +3 of
+  // column column(cb, c16): the accumulator layout of the 16 x 16 tile
+  // (features rn*16 .., columns of cb).
   auto update = [&](int cb) {
     if (!slot_ok || Lb == 0) return;
-    const op_t* __restrict__ pkh = reinterpret_cast<const op_t*>(sh.wl[w].qk + 32 * D);
-    const op_t* __restrict__ pkl = reinterpret_cast<const op_t*>(&sh.hd[w]);
+    const T* const pkh = sh.wl[w].qk + 32 * D;
+    const T* const pkl = reinterpret_cast<const T*>(&sh.hd[w]);
     float* __restrict__ Sw = const_cast<float*>(a.S) + sbase * f * D;
     const op_t va = vt_op(cb, 0);
 #pragma unroll
     for (int rn = 0; rn < RUNS; ++rn) {
-      f32x4 acc = M::mma(pkh[rn * kWave + lane], va, buf[cb % NBUF][rn]);
-      acc = M::mma(pkl[rn * kWave + lane], va, acc);
+      f32x4 acc = M::mma(rows_op(pkh, rn * 16), va, buf[cb % NBUF][rn]);
+      acc = M::mma(rows_op(pkl, rn * 16), va, acc);
       *reinterpret_cast<f32x4*>(Sw + (size_t)C::column(cb, c16) * f + C::feature(rn * 4, quad)) = acc;
     }
   };
@@ -532,11 +554,15 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
     // loads first; a plain barrier (no fence, no wait) holds their stream
     // until the block waves' requests are queued ahead of it.
     if constexpr (C::EARLY) __builtin_amdgcn_s_barrier();
-    const float lw = log_sigmoid(alpha_h);
+    float alpha_v = alpha_h;
     if constexpr (C::DMA_QK) {
       // The copies are counted by vmcnt alone and the compiler does not
       // track them: wait for every load of this wave, then read the operands.
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      // alpha is used only below this wait: without the opaque step the
+      // compiler computes log sigmoid(alpha) between the copies and waits
+      // there for every copy issued so far (a second memory round trip).
+      asm volatile("" : "+v"(alpha_v));
 #pragma unroll
       for (int r = 0; r < 2; ++r)
 #pragma unroll
@@ -551,25 +577,80 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
     }
     if constexpr (C::EARLY) {
       // phi(K) for the commit, over the K rows just read (Q is read after
-      // it, to keep registers free); z takes the sum of the same values
-      // (z_old is in zr: lane (c16, quad) holds features fbk*16 + quad*4 + r);
-      // then the state waves may start.
-      float zs[C::NFB];
-      op_t* const pkh = reinterpret_cast<op_t*>(kst);
-      op_t* const pkl = reinterpret_cast<op_t*>(&sh.hd[w]);
-      phi_k(std::integral_constant<int, 2>{}, zs, [&](int fbk, int part, int kb, const float* x4) {
-        typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
-        const bf16x4_t v{(bf16)x4[0], (bf16)x4[1], (bf16)x4[2], (bf16)x4[3]};
-        *reinterpret_cast<bf16x4_t*>(reinterpret_cast<char*>(part == 0 ? pkh : pkl) +
-                                     (fbk * kWave + lane) * 16 + kb * 8) = v;
-      });
+      // it, to keep registers free), one key per lane as phi(Q) below:
+      // U_K^T = W_h^T K^T puts features fb*16 + quad*4 + r of key
+      // kb*16 + c16 in lane (c16, quad), so each sign's softmax reduces over
+      // the four lane quarters; padding keys get phi = 0.  Each key's phi
+      // goes to LDS as a row, bf16 hi parts over the staged K rows and lo
+      // parts (the rounding remainder) in the head area, chunk-swizzled like
+      // the staged V rows; the state wave reads its phi(K)^T operands from
+      // them by transposing reads.  z takes the sum of the same rounded
+      // values, on the MFMAs (phi(K)^T against a block of ones); z_old is in
+      // zr (lane (c16, quad) holds features fbk*16 + quad*4 + r).  Then the
+      // state waves may start.
+      typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+      T* const pkh = kst;
+      T* const pkl = reinterpret_cast<T*>(&sh.hd[w]);
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) {
+        float u[4 * FB];
+#pragma unroll
+        for (int fb = 0; fb < FB; ++fb) {
+          f32x4 acc = {};
+#pragma unroll
+          for (int ks = 0; ks < C::KD; ++ks) acc = M::mma(wop[fb][ks], kop[kb][ks], acc);
+#pragma unroll
+          for (int r = 0; r < 4; ++r) u[fb * 4 + r] = acc[r] * kLog2e;
+        }
+        float mx = -INFINITY, mn = INFINITY;
+#pragma unroll
+        for (int j = 0; j < 4 * FB; ++j) {
+          mx = fmaxf(mx, u[j]);
+          mn = fminf(mn, u[j]);
+        }
+        mx = qmax(mx);
+        mn = qmin(mn);
+        float ph[2][4 * FB];
+        float sp = 0.0f, sn = 0.0f;
+#pragma unroll
+        for (int j = 0; j < 4 * FB; ++j) {
+          ph[0][j] = __builtin_amdgcn_exp2f(u[j] - mx);
+          ph[1][j] = __builtin_amdgcn_exp2f(mn - u[j]);
+          sp += ph[0][j];
+          sn += ph[1][j];
+        }
+        const int t = kb * 16 + c16;
+        const float kv = t < Lb ? 1.0f : 0.0f;
+        const float ip = kv * fast_rcp(qsum(sp)), in = kv * fast_rcp(qsum(sn));
+#pragma unroll
+        for (int sg = 0; sg < 2; ++sg)
+#pragma unroll
+          for (int fb = 0; fb < FB; ++fb) {
+            const int col = sg * F + fb * 16 + quad * 4;
+            const int off = t * D + ((col / C::EPC) ^ C::swz(t)) * C::EPC + col % C::EPC;
+            float x[4], lo[4];
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              x[r] = ph[sg][fb * 4 + r] * (sg ? in : ip);
+              lo[r] = x[r] - as_operand<T>(x[r]);
+            }
+            *reinterpret_cast<bf16x4_t*>(pkh + off) = bf16x4_t{(bf16)x[0], (bf16)x[1], (bf16)x[2], (bf16)x[3]};
+            *reinterpret_cast<bf16x4_t*>(pkl + off) = bf16x4_t{(bf16)lo[0], (bf16)lo[1], (bf16)lo[2], (bf16)lo[3]};
+          }
+      }
+      asm volatile("" ::: "memory");  // the rows above, then the reads below
       if (slot_ok && Lb > 0) {
+        op_t ones;
+#pragma unroll
+        for (int e = 0; e < E; ++e) set_elem<T>(ones, e, 1.0f);
         float* __restrict__ zw = const_cast<float*>(a.z) + sbase * f;
 #pragma unroll
         for (int fbk = 0; fbk < C::NFB; ++fbk) {
+          f32x4 zs = M::mma(rows_op(pkh, fbk * 16), ones, f32x4{});
+          zs = M::mma(rows_op(pkl, fbk * 16), ones, zs);
           f32x4 zn;
 #pragma unroll
-          for (int r = 0; r < 4; ++r) zn[r] = zr[fbk][r] + __shfl(zs[fbk], quad * 4 + r);
+          for (int r = 0; r < 4; ++r) zn[r] = zr[fbk][r] + zs[r];
           if (c16 == 0) *reinterpret_cast<f32x4*>(zw + fbk * 16 + quad * 4) = zn;
         }
       }
@@ -581,6 +662,8 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
 #pragma unroll
         for (int ks = 0; ks < C::KD; ++ks) qop[r][ks] = staged_op(qst, r * 16 + c16, quad + 4 * ks);
     }
+    // log2 sigmoid(alpha): the merge coefficients are formed in base 2.
+    const float lw2 = log_sigmoid(alpha_v) * kLog2e;
 
     // 2. Without the staged copies: V^T of the KV head into this wave's LDS
     //    area (keys padded to 0).
@@ -600,7 +683,9 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
 
     // 3. Block scores Sc^T = K Q^T; softmax of query qb*16 + c16 over its 32
     //    keys (8 in this lane, the rest in the other three lane quarters).
-    const float scale = 1.0f / sqrtf((float)D);
+    //    Scores are kept in base-2 units (times log2 e), so each weight is
+    //    one subtraction and one exp2; m is the maximum in those units.
+    const float scale = kLog2e / sqrtf((float)D);
     float p[QB][8], m[QB], den[QB];
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
@@ -621,7 +706,7 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
       den[qb] = 0.0f;
 #pragma unroll
       for (int j = 0; j < 8; ++j) {
-        p[qb][j] = C::key(j, quad) < Lb ? fast_exp(p[qb][j] - m[qb]) : 0.0f;
+        p[qb][j] = C::key(j, quad) < Lb ? __builtin_amdgcn_exp2f(p[qb][j] - m[qb]) : 0.0f;
         den[qb] += p[qb][j];
       }
       den[qb] = qsum(den[qb]);
@@ -641,10 +726,11 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb)
 #pragma unroll
-        for (int r = 0; r < 4; ++r) uu[qb][fb * 4 + r] = acc[qb][r];
+        for (int r = 0; r < 4; ++r) uu[qb][fb * 4 + r] = acc[qb][r] * kLog2e;
     }
 
-    // 5. Per query block: phi = [softmax(U), softmax(-U)], lin_den = phi z,
+    // 5. Per query block: phi = [softmax(U), softmax(-U)] (U in base-2
+    //    units: one subtraction and one exp2 per feature), lin_den = phi z,
     //    the coefficients a and b; a scales P, b phi goes to LDS.
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb) {
@@ -660,25 +746,28 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
       float sp = 0.0f, sn = 0.0f, zp = 0.0f, zn = 0.0f;
 #pragma unroll
       for (int j = 0; j < 4 * FB; ++j) {
-        phi[j] = fast_exp(uu[qb][j] - mx);
-        phi[4 * FB + j] = fast_exp(mn - uu[qb][j]);
+        phi[j] = __builtin_amdgcn_exp2f(uu[qb][j] - mx);
+        phi[4 * FB + j] = __builtin_amdgcn_exp2f(mn - uu[qb][j]);
         sp += phi[j];
         sn += phi[4 * FB + j];
         zp += phi[j] * zr[j / 4][j % 4];
         zn += phi[4 * FB + j] * zr[(4 * FB + j) / 4][j % 4];
       }
-      const float ip = 1.0f / qsum(sp), in = 1.0f / qsum(sn);
+      const float ip = fast_rcp(qsum(sp)), in = fast_rcp(qsum(sn));
       const float lden = qsum(zp) * ip + qsum(zn) * in;
+      // In base 2: la = log2 w + m, lb = log2 lin_den, c = max(la, lb);
+      // a = 2^(la-c) / (2^(la-c) den + 2^(lb-c)) and
+      // b = 2^(lb-c) / (lin_den (...)) = 2^(-c) / (...).
       float ca, cb;
       if (lden > 0.0f) {
-        const float la = lw + m[qb], lb = logf(lden);
+        const float la = lw2 + m[qb], lb = __builtin_amdgcn_logf(lden);
         const float c = fmaxf(la, lb);
-        const float ea = expf(la - c), eb = expf(lb - c);
-        const float inv = 1.0f / (ea * den[qb] + eb);
+        const float ea = __builtin_amdgcn_exp2f(la - c), eb = __builtin_amdgcn_exp2f(lb - c);
+        const float inv = fast_rcp(ea * den[qb] + eb);
         ca = ea * inv;
-        cb = eb * inv / lden;
+        cb = __builtin_amdgcn_exp2f(-c) * inv;
       } else {
-        ca = 1.0f / den[qb];
+        ca = fast_rcp(den[qb]);
         cb = 0.0f;
       }
       if (!slot_ok) ca = cb = __builtin_nanf("");
