@@ -644,14 +644,30 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
 #pragma unroll
         for (int e = 0; e < E; ++e) set_elem<T>(ones, e, 1.0f);
         float* __restrict__ zw = const_cast<float*>(a.z) + sbase * f;
+        // Four feature blocks at a time: every operand read issued before
+        // the products, the stores after them.
+        constexpr int ZB = C::NFB < 4 ? C::NFB : 4;
+        static_assert(C::NFB % ZB == 0, "feature blocks in groups");
 #pragma unroll
-        for (int fbk = 0; fbk < C::NFB; ++fbk) {
-          f32x4 zs = M::mma(rows_op(pkh, fbk * 16), ones, f32x4{});
-          zs = M::mma(rows_op(pkl, fbk * 16), ones, zs);
-          f32x4 zn;
+        for (int f0 = 0; f0 < C::NFB; f0 += ZB) {
+          op_t ah[ZB], al[ZB];
 #pragma unroll
-          for (int r = 0; r < 4; ++r) zn[r] = zr[fbk][r] + zs[r];
-          if (c16 == 0) *reinterpret_cast<f32x4*>(zw + fbk * 16 + quad * 4) = zn;
+          for (int i = 0; i < ZB; ++i) {
+            ah[i] = rows_op(pkh, (f0 + i) * 16);
+            al[i] = rows_op(pkl, (f0 + i) * 16);
+          }
+          f32x4 zn[ZB];
+#pragma unroll
+          for (int i = 0; i < ZB; ++i) {
+            const f32x4 zs = M::mma(al[i], ones, M::mma(ah[i], ones, f32x4{}));
+#pragma unroll
+            for (int r = 0; r < 4; ++r) zn[i][r] = zr[f0 + i][r] + zs[r];
+          }
+          if (c16 == 0) {
+#pragma unroll
+            for (int i = 0; i < ZB; ++i)
+              *reinterpret_cast<f32x4*>(zw + (f0 + i) * 16 + quad * 4) = zn[i];
+          }
         }
       }
       lds_barrier_nodrain();
@@ -782,8 +798,8 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
     }
 
     // 6. a P V into accumulators, then over this wave's head area (with
-    //    the early commit, once the state wave is done with phi(K)).
-    if constexpr (C::EARLY) lds_barrier_nodrain();
+    //    the early commit, once the state wave is done with phi(K): the
+    //    products are formed before that barrier, only the stores wait).
     f32x4 acc[CB][QB];
 #pragma unroll
     for (int cbk = 0; cbk < CB; ++cbk) {
@@ -797,6 +813,7 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
           acc[cbk][qb] = mma16_split_b<T>(va, &p[qb][ks * E], acc[cbk][qb]);
       }
     }
+    if constexpr (C::EARLY) lds_barrier_nodrain();
 #pragma unroll
     for (int cbk = 0; cbk < CB; ++cbk)
 #pragma unroll
