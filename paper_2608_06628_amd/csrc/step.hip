@@ -126,9 +126,14 @@ struct StepCfg {
   // second pass after the outputs.
   static constexpr bool EARLY = CM && DMA_QK && f <= D;
   static_assert(!EARLY || f * 64 <= (int)sizeof(HeadLds), "phi(K) lo parts in the head area");
-  // Column blocks held as bf16 readout operands: KPACK, or all of them with
-  // the early commit (each is updated and converted as it arrives).
-  static constexpr int NPACK = EARLY ? CB : KPACK;
+  // Column blocks held as bf16 readout operands (those converted before b
+  // phi(Q) is in LDS; with the early commit the later ones are folded as
+  // they arrive).
+  static constexpr int NPACK = KPACK;
+  // With the early commit, the refill that would request the last column
+  // block inside the conversion loop (if one does) waits until b phi(Q) is
+  // in LDS and the converted blocks are folded.
+  static constexpr bool DEFER = EARLY && CB - 1 - NBUF >= 0 && CB - 1 - NBUF < KPACK;
   struct alignas(16) SmemBase {
     HeadLds hd[NW];  // W_h rows (staged), then V^T, then a P V and outputs
     WaveLds wl[NW];
@@ -451,6 +456,29 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
     return cvt_op<T>(sv);
   };
 
+  const bool of32 = sizeof(T) == 4 || a.s.out_f32;
+  // Outputs of the column-block pair pr into the pair's staging area of this
+  // head's area: the lane holds query qb*16 + c16 and the 8 consecutive
+  // columns 32 pr + 8 quad .. +7 (see column()); acc[0] holds the first
+  // block's four, acc[1] the second's.
+  auto stage_pair = [&](int pr, const f32x4 (&acc)[2][QB]) {
+    char* stg = reinterpret_cast<char*>(&sh.hd[w].apv[2 * pr][0][0]);
+#pragma unroll
+    for (int qb = 0; qb < QB; ++qb) {
+      const f32x4 lo = acc[0][qb], hi = acc[1][qb];
+      const int row = qb * 16 + c16;
+      if (of32) {
+        f32x4* d = reinterpret_cast<f32x4*>(stg + (row * 32 + quad * 8) * 4);
+        d[0] = lo;
+        d[1] = hi;
+      } else {
+        *reinterpret_cast<bf16x8*>(stg + (row * 32 + quad * 8) * 2) =
+            bf16x8{(bf16)lo[0], (bf16)lo[1], (bf16)lo[2], (bf16)lo[3],
+                   (bf16)hi[0], (bf16)hi[1], (bf16)hi[2], (bf16)hi[3]};
+      }
+    }
+  };
+
   if (state_wave) {
     if constexpr (C::EARLY) __builtin_amdgcn_s_barrier();  // block requests first
 #pragma unroll
@@ -468,18 +496,47 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
         const uint4 t = *reinterpret_cast<const uint4*>(&sop[cb][ks]);
         asm volatile("" ::"v"(t.x), "v"(t.y), "v"(t.z), "v"(t.w) : "memory");
       }
-      if (cb + NBUF < CB) issue(cb + NBUF);
+      // (with the early commit the last refill waits for the fold below:
+      // its buffer is what the converted blocks need until then)
+      if (cb + NBUF < CB && !(C::DEFER && cb + NBUF == CB - 1)) issue(cb + NBUF);
     }
     if constexpr (C::EARLY) {
-      // The rest as it arrives, then the head area may take a P V.
+      // 7. With the early commit the readout folds run inside the update
+      //    stream: once b phi(Q) is in LDS, S^T (b phi)^T of the blocks
+      //    converted so far, from zero; then each later block is updated,
+      //    converted and folded as it arrives.  a P V is added at the end.
+      lds_barrier_nodrain();  // b phi(Q) is in LDS
+      if constexpr (C::DEFER) issue(CB - 1);
+      // (b phi operands are read per column block, not held: the state
+      // buffers in flight and the converted blocks fill the registers)
+      f32x4 fo[CB][QB];
 #pragma unroll
-      for (int cb = C::KPACK; cb < CB; ++cb) {
-        update(cb);
+      for (int cb = 0; cb < CB; ++cb) {
+        if (cb >= C::KPACK) update(cb);
 #pragma unroll
-        for (int ks = 0; ks < C::KF; ++ks) sop[cb][ks] = convert(cb, ks);
-        if (cb + NBUF < CB) issue(cb + NBUF);
+        for (int qb = 0; qb < QB; ++qb) fo[cb][qb] = f32x4{};
+#pragma unroll
+        for (int ks = 0; ks < C::KF; ++ks) {
+          const op_t sa = cb < C::KPACK ? sop[cb < C::KPACK ? cb : 0][ks] : convert(cb, ks);
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb)
+            fo[cb][qb] = M::mma(sa, sh.wl[w].phib[qb][ks][lane], fo[cb][qb]);
+        }
+        if (cb >= C::KPACK && cb + NBUF < CB) issue(cb + NBUF);
       }
-      lds_barrier_nodrain();
+      lds_barrier_nodrain();  // done with phi(K): the head area may take a P V
+      lds_barrier_nodrain();  // a P V is in LDS
+#pragma unroll
+      for (int pr = 0; pr < CB / 2; ++pr) {
+        f32x4 acc[2][QB];
+#pragma unroll
+        for (int h2 = 0; h2 < 2; ++h2)
+#pragma unroll
+          for (int qb = 0; qb < QB; ++qb)
+            acc[h2][qb] = sh.hd[w].apv[2 * pr + h2][qb][lane] + fo[2 * pr + h2][qb];
+        stage_pair(pr, acc);
+      }
+      lds_barrier();  // outputs staged
     }
   } else {
     // ---------------- block wave ----------------
@@ -796,6 +853,7 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
       for (int ks = 0; ks < C::KF; ++ks)
         sh.wl[w].phib[qb][ks][lane] = cvt_op<T>(&phi[ks * E]);
     }
+    if constexpr (C::EARLY) lds_barrier_nodrain();  // b phi(Q) is in LDS
 
     // 6. a P V into accumulators, then over this wave's head area (with
     //    the early commit, once the state wave is done with phi(K): the
@@ -818,17 +876,19 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
     for (int cbk = 0; cbk < CB; ++cbk)
 #pragma unroll
       for (int qb = 0; qb < QB; ++qb) sh.hd[w].apv[cbk][qb][lane] = acc[cbk][qb];
+    if constexpr (C::EARLY) {
+      lds_barrier_nodrain();  // a P V is in LDS
+      lds_barrier();          // outputs staged
+    }
   }
-  if constexpr (C::EARLY)
-    lds_barrier_nodrain();
-  else
-    lds_barrier();
+  if constexpr (!C::EARLY) lds_barrier();
 
-  const bool of32 = sizeof(T) == 4 || a.s.out_f32;
-  if (state_wave) {
-    // 7. out^T = a P V + S^T (b phi)^T, a pair of column blocks at a time;
-    //    column blocks past KPACK are converted as they land, and each such
-    //    buffer is refilled with column block cb + NBUF if not yet requested.
+  if (!C::EARLY && state_wave) {
+    // 7. out^T = a P V + S^T (b phi)^T, a pair of column blocks at a time:
+    //    the fold from zero, then a P V added (the arithmetic of the early
+    //    commit's fold, so the fused call gives the same bits); column
+    //    blocks past KPACK are converted as they land, and each such buffer
+    //    is refilled with column block cb + NBUF if not yet requested.
     op_t phib[QB][C::KF];
 #pragma unroll
     for (int qb = 0; qb < QB; ++qb)
@@ -840,38 +900,22 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
 #pragma unroll
       for (int h2 = 0; h2 < 2; ++h2) {
         const int cbk = 2 * pr + h2;
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb) acc[h2][qb] = sh.hd[w].apv[cbk][qb][lane];
+        f32x4 fd[QB] = {};
 #pragma unroll
         for (int ks = 0; ks < C::KF; ++ks) {
           const op_t sa = cbk < C::NPACK ? sop[cbk < C::NPACK ? cbk : 0][ks] : convert(cbk, ks);
 #pragma unroll
-          for (int qb = 0; qb < QB; ++qb)
-            acc[h2][qb] = M::mma(sa, phib[qb][ks], acc[h2][qb]);
+          for (int qb = 0; qb < QB; ++qb) fd[qb] = M::mma(sa, phib[qb][ks], fd[qb]);
         }
-        if (!C::EARLY && cbk >= C::KPACK && cbk + NBUF < CB) issue(cbk + NBUF);
-      }
-      // The lane holds query qb*16 + c16 and the 8 consecutive columns
-      // 32 pr + 8 quad .. +7 (see column()); they go to the pair's staging
-      // area, over its a P V just read.
-      char* stg = reinterpret_cast<char*>(&sh.hd[w].apv[2 * pr][0][0]);
 #pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
-        const f32x4 lo = acc[0][qb], hi = acc[1][qb];
-        const int row = qb * 16 + c16;
-        if (of32) {
-          f32x4* d = reinterpret_cast<f32x4*>(stg + (row * 32 + quad * 8) * 4);
-          d[0] = lo;
-          d[1] = hi;
-        } else {
-          *reinterpret_cast<bf16x8*>(stg + (row * 32 + quad * 8) * 2) =
-              bf16x8{(bf16)lo[0], (bf16)lo[1], (bf16)lo[2], (bf16)lo[3],
-                     (bf16)hi[0], (bf16)hi[1], (bf16)hi[2], (bf16)hi[3]};
-        }
+        for (int qb = 0; qb < QB; ++qb) acc[h2][qb] = sh.hd[w].apv[cbk][qb][lane] + fd[qb];
+        if (cbk >= C::KPACK && cbk + NBUF < CB) issue(cbk + NBUF);
       }
+      // Over the pair's a P V just read.
+      stage_pair(pr, acc);
     }
   }
-  lds_barrier();
+  if constexpr (!C::EARLY) lds_barrier();
 
   // 8. Store: each wave writes whole tokens (the NW heads of a token are
   //    contiguous, NW * D outputs), 16 bytes per lane; the output is not read
