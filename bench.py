@@ -416,7 +416,7 @@ def cpu_baseline_1core(dims, plens, n_req=4, budget_s=6.0):
 
 def bench_small_batch(gen, dev, batches=(1, 8, 16, 32)):
     """decode1 (B = 1) and the Table 3 batches: one step (16q/4kv, d = 128,
-    f = 128, block 32, bf16) with each of the step's two kernels and with the
+    f = 128, block 32, bf16) with each of the step's three kernels and with the
     library's choice; median of 20 individually timed calls on cold states
     (HIP events around each call, so the launch's own latency is included;
     the rocprofv3 kernel trace of `--only-small-batch` gives kernel time)."""
@@ -436,7 +436,7 @@ def bench_small_batch(gen, dev, batches=(1, 8, 16, 32)):
         v = (torch.randn((B, L, Hkv, d), generator=gen, device=dev) * sc).to(torch.bfloat16)
         out = torch.empty_like(q)
         row = {"B": B, "bytes": step_bytes(B, Hq, Hkv, d, L, f)}
-        for kern in ("split", "whole", None):
+        for kern in ("split", "whole", "halves", None):
             it = [0]
 
             def fn():
@@ -451,7 +451,7 @@ def bench_small_batch(gen, dev, batches=(1, 8, 16, 32)):
             row[f"{kern or 'auto'}_us"] = median_ms(fn) * 1e3
         rows.append(row)
         log(f"small batch B={B:2d}: split {row['split_us']:.1f} us, whole {row['whole_us']:.1f} us, "
-            f"library's choice {row['auto_us']:.1f} us")
+            f"halves {row['halves_us']:.1f} us, library's choice {row['auto_us']:.1f} us")
         del states
         torch.cuda.empty_cache()
     return {"workload": "one hybrid step, 16q/4kv, d=128, f=128, block 32, bf16, cold states; "

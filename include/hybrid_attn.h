@@ -121,16 +121,23 @@ typedef struct {
  * bit for bit. */
 #define HYB_OUT_F32 1
 /* flags of hybrid_attn_step only (any other entry point rejects them): which
- * of its two kernels runs.  HYB_STEP_SPLIT: one wave per (request, query
+ * of its three kernels runs.  HYB_STEP_SPLIT: one wave per (request, query
  * head, 32-column slice of d), for batches too small to fill the chip with
  * HYB_STEP_WHOLE: one workgroup per group of query heads sharing a KV head,
- * each streaming its heads' whole states.  Neither: the library picks by the
- * batch (SPLIT while its B * Hq * d/32 waves fit on the chip at once, 1024
- * of them).  Both: rejected.
+ * each streaming its heads' whole states.  HYB_STEP_HALVES: two workgroups
+ * per group of four query heads, each streaming half of every head's state
+ * columns and writing half of its output columns (bf16, feat_dim <= 128,
+ * n_q_heads / n_kv_heads a multiple of 4; otherwise HYB_EUNSUPPORTED).  None:
+ * the library picks by the batch (HALVES where it is supported and its
+ * workgroups fill 128 to 256 compute units; else SPLIT while its
+ * B * Hq * d/32 waves fit on the chip at once, 1024 of them; else HALVES
+ * while its workgroups fit on the 256 compute units; else WHOLE).  More than
+ * one: rejected.
  * Results agree to the same bound against the definition; they need not
  * agree bit for bit. */
 #define HYB_STEP_SPLIT 2
 #define HYB_STEP_WHOLE 4
+#define HYB_STEP_HALVES 8
 
 /* One denoising step of the active block (Section 3.1: within-block
  * softmax branch, linear readout of the committed state, gated merge with a

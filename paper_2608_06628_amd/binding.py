@@ -18,8 +18,9 @@ LIB_PATH = os.path.join(_PKG, "libhybattn.so")
 
 HYB_F32, HYB_BF16 = 0, 1
 HYB_OUT_F32 = 1
-HYB_STEP_SPLIT, HYB_STEP_WHOLE = 2, 4
-_STEP_KERNEL = {None: 0, "auto": 0, "split": HYB_STEP_SPLIT, "whole": HYB_STEP_WHOLE}
+HYB_STEP_SPLIT, HYB_STEP_WHOLE, HYB_STEP_HALVES = 2, 4, 8
+_STEP_KERNEL = {None: 0, "auto": 0, "split": HYB_STEP_SPLIT, "whole": HYB_STEP_WHOLE,
+                "halves": HYB_STEP_HALVES}
 OP_STEP, OP_COMMIT, OP_PREFILL, OP_SOFTMAX_PREFIX, OP_BACKWARD, OP_BACKWARD_FULL = 0, 1, 2, 3, 4, 5
 STATUS = {0: "HYB_OK", 1: "HYB_ENULL", 2: "HYB_EINVAL", 3: "HYB_EALIGN",
           4: "HYB_EDTYPE", 5: "HYB_EUNSUPPORTED", 6: "HYB_EWORKSPACE",
@@ -134,8 +135,8 @@ def hybrid_attn_step(q, k, v, W, alpha, S, z, slots=None, out=None, out_f32=Fals
     S [n_slots][Hq][d][f] f32 (S_h transposed), z [n_slots][Hq][f] f32 -> out [B][L][Hq][d]
     in q's dtype (fp32 with out_f32).  block_len [B] int32 (device): active rows
     per request; rows past it of out are left as they were.  kernel: None or
-    "auto" (the library picks), "split" or "whole" (HYB_STEP_SPLIT /
-    HYB_STEP_WHOLE)."""
+    "auto" (the library picks), "split", "whole" or "halves" (HYB_STEP_SPLIT /
+    HYB_STEP_WHOLE / HYB_STEP_HALVES)."""
     lib = load()
     B, L, Hq, d = q.shape
     act = q.dtype

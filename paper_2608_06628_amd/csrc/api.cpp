@@ -60,21 +60,32 @@ int check_dims(const hyb_dims_t* d, bool need_state, hyb::Shape* s) {
     return fail(HYB_EINVAL, "n_slots %d < 1", d->n_slots);
   if ((long long)d->batch * d->n_q_heads > 0x7fffffffLL)
     return fail(HYB_EINVAL, "batch * n_q_heads exceeds the grid limit");
-  if (d->flags & ~(HYB_OUT_F32 | HYB_STEP_SPLIT | HYB_STEP_WHOLE))
+  if (d->flags & ~(HYB_OUT_F32 | HYB_STEP_SPLIT | HYB_STEP_WHOLE | HYB_STEP_HALVES))
     return fail(HYB_EINVAL, "unknown flags 0x%x", d->flags);
-  if ((d->flags & HYB_STEP_SPLIT) && (d->flags & HYB_STEP_WHOLE))
-    return fail(HYB_EINVAL, "HYB_STEP_SPLIT and HYB_STEP_WHOLE together");
+  {
+    const int kf = d->flags & (HYB_STEP_SPLIT | HYB_STEP_WHOLE | HYB_STEP_HALVES);
+    if (kf & (kf - 1))
+      return fail(HYB_EINVAL, "more than one of HYB_STEP_SPLIT, HYB_STEP_WHOLE, HYB_STEP_HALVES");
+  }
   *s = hyb::Shape{d->batch,    d->n_q_heads,    d->n_kv_heads,
                   d->head_dim, d->block,        d->feat_dim / 2,
                   d->dtype,    d->n_slots,      (d->flags & HYB_OUT_F32) ? 1 : 0};
-  s->step_kernel = (d->flags & HYB_STEP_SPLIT) ? 1 : (d->flags & HYB_STEP_WHOLE) ? 2 : 0;
+  s->step_kernel = (d->flags & HYB_STEP_SPLIT)    ? 1
+                   : (d->flags & HYB_STEP_WHOLE)  ? 2
+                   : (d->flags & HYB_STEP_HALVES) ? 3
+                                                  : 0;
+  if (s->step_kernel == 3 && !hyb::step_halves_supported(*s))
+    return fail(HYB_EUNSUPPORTED,
+                "HYB_STEP_HALVES needs bf16, feat_dim <= 128 and n_q_heads / n_kv_heads a "
+                "multiple of 4");
   return HYB_OK;
 }
 
 // The step-kernel flags belong to hybrid_attn_step alone.
 int no_step_flags(const hyb_dims_t* d) {
-  if (d && (d->flags & (HYB_STEP_SPLIT | HYB_STEP_WHOLE)))
-    return fail(HYB_EINVAL, "HYB_STEP_SPLIT / HYB_STEP_WHOLE apply to hybrid_attn_step only");
+  if (d && (d->flags & (HYB_STEP_SPLIT | HYB_STEP_WHOLE | HYB_STEP_HALVES)))
+    return fail(HYB_EINVAL,
+                "HYB_STEP_SPLIT / HYB_STEP_WHOLE / HYB_STEP_HALVES apply to hybrid_attn_step only");
   return HYB_OK;
 }
 

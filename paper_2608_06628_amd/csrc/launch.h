@@ -11,7 +11,7 @@ namespace hyb {
 struct Shape {
   int B, Hq, Hkv, D, L, F, dtype, n_slots;  // F = feat_dim / 2
   int out_f32;                              // out is fp32 whatever dtype is
-  int step_kernel = 0;                      // step: 0 auto, 1 split, 2 whole
+  int step_kernel = 0;                      // step: 0 auto, 1 split, 2 whole, 3 halves
 };
 
 // block_len (nullable, device [B]): request b uses its first block_len[b]
@@ -84,6 +84,11 @@ hipError_t launch_step(const StepArgs& a, hipStream_t st);
 hipError_t launch_step_small(const StepArgs& a, hipStream_t st);
 // Whether the automatic choice takes the split kernel for these dims.
 bool step_prefers_split(const Shape& s);
+// The column-split step (two workgroups per group of four query heads, each
+// streaming half of every head's state columns): whether a shape can take
+// it, and whether the automatic choice does.
+bool step_halves_supported(const Shape& s);
+bool step_prefers_halves(const Shape& s);
 // The step fused with the commit of the same block: S and z are updated in
 // place after the step has read them (the StepArgs state pointers must be
 // writable).

@@ -51,7 +51,10 @@
 
 namespace hyb {
 
-template <typename T, int D, int F, int NW, bool CM = false>
+// CS > 1 splits each head's output columns (and state columns) over CS
+// workgroups: each streams 1/CS of the state and writes 1/CS of the outputs,
+// and repeats the per-query block math (small batches, plain step only).
+template <typename T, int D, int F, int NW, bool CM = false, int CS = 1>
 struct StepCfg {
   typedef Mma16<T> M;
   typedef typename M::op_t op_t;
@@ -64,7 +67,8 @@ struct StepCfg {
   static constexpr int KD = D / KW;       // k-steps over head_dim
   static constexpr int KF = f / KW;       // k-steps over features
   static constexpr int KL = 32 / KW;      // k-steps over block keys
-  static constexpr int CB = D / 16;       // 16-column blocks of the output
+  static constexpr int CBF = D / 16;      // 16-column blocks of the output
+  static constexpr int CB = CBF / CS;     // ... taken by one workgroup
   static constexpr int RUNS = NPHI / 4;   // 16-byte state runs per column block
   // Column blocks a state wave keeps in flight: 128 registers' worth.
   static constexpr int NBUF0 = 128 / (RUNS * 4);
@@ -82,7 +86,7 @@ struct StepCfg {
   // outputs ([32 queries][32 columns], output type).
   union alignas(16) HeadLds {
     T vt[D][VT_LD];
-    f32x4 apv[CB][QB][kWave];
+    f32x4 apv[CBF][QB][kWave];
   };
   static_assert(2 * QB * kWave * 16 >= 32 * 32 * 4, "output staging");
   static_assert(CB % 2 == 0, "output columns are stored in pairs of blocks");
@@ -246,9 +250,10 @@ __device__ inline float rsum16(float x) {
   return row_reduce16(x, [](float a, float b) { return a + b; });
 }
 
-template <typename T, int D, int F, int NW, bool CM>
+template <typename T, int D, int F, int NW, bool CM, int CS = 1>
 __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a) {
-  typedef StepCfg<T, D, F, NW, CM> C;
+  typedef StepCfg<T, D, F, NW, CM, CS> C;
+  static_assert(CS == 1 || (!CM && sizeof(T) == 2), "column split: plain bf16 step only");
   typedef typename C::M M;
   typedef typename C::op_t op_t;
   constexpr int f = C::f, E = C::E, KW = C::KW, FB = C::FB, QB = C::QB,
@@ -263,7 +268,12 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
   const int c16 = lane & 15, quad = lane >> 4;
   const int Hq = a.s.Hq, Hkv = a.s.Hkv, L = a.s.L;
   const int ngrp = Hq / NW;
-  const int u = xcd_unit(blockIdx.x, a.s.B * ngrp);
+  const int uc = xcd_unit(blockIdx.x, a.s.B * ngrp * CS);
+  // Column part of a split workgroup: output and state columns coff ..
+  // coff + 16 CB - 1.  Pairs of column blocks are whole, so column(cb, i) +
+  // coff is the column of local block cb.
+  const int coff = (uc % CS) * 16 * C::CB;
+  const int u = uc / CS;
   const int hg = u % ngrp, b = u / ngrp;
   const int h = hg * NW + w, g = (hg * NW) / (Hq / Hkv);
   // (uniform through readfirstlane: the state base is then a scalar and
@@ -282,12 +292,12 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
   // State wave: column block cb of S_h^T; lane (c16, quad) reads the RUNS
   // 16-byte runs of column column(cb, c16) at features feature(4 rn, quad).
   f32x4 buf[NBUF][RUNS];
-  const float* __restrict__ St = a.S + sbase * f * D;
+  const float* __restrict__ St = a.S + sbase * f * D + (size_t)coff * f;
   // Buffer loads over the head's state: the column block's part of the
   // offset is a scalar, the lane's part one VGPR, the run's part the
   // immediate, so a load needs no address arithmetic of its own.
   const __amdgpu_buffer_rsrc_t srs = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<float*>(St), 0, f * D * 4, kBufferWord3);
+      const_cast<float*>(St), 0, f * 16 * C::CB * 4, kBufferWord3);
   const int slane = (C::column(0, c16) * f + C::feature(0, quad)) * 4;  // bytes
   auto issue = [&](int cb) {
 #pragma unroll
@@ -316,7 +326,7 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
     if constexpr (C::DMA_QK) {
       static_assert(C::KL == 1, "one k-step over the block keys");
       typedef short s16x4 __attribute__((ext_vector_type(4)));
-      const int col = C::column(cbk, 4 * (c16 % 4));
+      const int col = C::column(cbk, 4 * (c16 % 4)) + coff;
       auto piece = [&](int t) {
         const T* src = vst + t * D + ((col / C::EPC) ^ C::swz(t)) * C::EPC + col % C::EPC;
         return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
@@ -325,7 +335,7 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
       const s16x4 lo = piece(quad * 4 + c16 / 4), hi = piece(16 + quad * 4 + c16 / 4);
       return __builtin_bit_cast(op_t, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
     } else {
-      return lds_keys_op<T>(&vt[C::column(cbk, c16)][0], ks, quad);
+      return lds_keys_op<T>(&vt[C::column(cbk, c16) + coff][0], ks, quad);
     }
   };
 
@@ -923,10 +933,10 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
   {
     typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
     const int osz = of32 ? 4 : 2;
-    const int cph = D * osz / 16;  // 16-byte chunks per head
+    const int cph = 16 * C::CB * osz / 16;  // 16-byte chunks per head (this part)
     for (int t = wv; t < Lb; t += 2 * NW) {
       char* orow = reinterpret_cast<char*>(a.out) +
-                   (((size_t)b * L + t) * Hq + hg * NW) * D * osz;
+                   ((((size_t)b * L + t) * Hq + hg * NW) * D + coff) * osz;
       for (int c = lane; c < NW * cph; c += kWave) {
         const int hh = c / cph, col0 = (c % cph) * (16 / osz);
         const char* src = reinterpret_cast<const char*>(&sh.hd[hh].apv[2 * (col0 / 32)][0][0]) +
@@ -1070,9 +1080,47 @@ bool step_prefers_split(const Shape& s) {
   return (long)s.B * s.Hq * (s.D / kTile) <= 1024 && (long)s.B * s.Hq / 4 < 256;
 }
 
+// The column-split step: bf16, four query heads per workgroup (G a multiple
+// of 4, F <= 64, the shapes whose per-head-group kernel takes 4 heads).
+bool step_halves_supported(const Shape& s) {
+  return s.dtype == 1 && s.F <= 64 && s.Hkv > 0 && (s.Hq / s.Hkv) % 4 == 0;
+}
+
+// While the two workgroups per head group fit on the 256 compute units at
+// once (the per-head-group grid would leave half of them idle or more).
+bool step_prefers_halves(const Shape& s) {
+  return step_halves_supported(s) && (long)s.B * (s.Hq / 4) * 2 <= 256;
+}
+
+template <int D, int F>
+static hipError_t step_halves_go(const StepArgs& a, hipStream_t st) {
+  static_assert(sizeof(typename StepCfg<bf16, D, F, 4, false, 2>::Smem) <= 160 * 1024, "LDS");
+  const dim3 grid(a.s.B * (a.s.Hq / 4) * 2);
+  hipLaunchKernelGGL((hyb_step_kernel<bf16, D, F, 4, false, 2>), grid, dim3(kWave * 8), 0, st, a);
+  return hipGetLastError();
+}
+
+static hipError_t step_halves(const StepArgs& a, hipStream_t st) {
+  if (!step_halves_supported(a.s)) return hipErrorInvalidValue;
+  if (a.s.D == 64) return a.s.F == 32 ? step_halves_go<64, 32>(a, st) : step_halves_go<64, 64>(a, st);
+  if (a.s.D == 128) return a.s.F == 32 ? step_halves_go<128, 32>(a, st) : step_halves_go<128, 64>(a, st);
+  return hipErrorInvalidValue;
+}
+
+// Automatic choice: the column split while its workgroups fill at least
+// half of the compute units and at most all of them (measured, 16q/4kv,
+// d = 128, f = 128, bf16, event-timed calls: B = 12 split 12.1 us against
+// halves 12.8; B = 16 split 13.9, halves 12.9; B = 32 whole 18.4, halves
+// 14.8), else the split kernel while its waves fit, else one workgroup per
+// head group.
 hipError_t launch_step(const StepArgs& a, hipStream_t st) {
-  if (a.s.step_kernel == 1 || (a.s.step_kernel == 0 && step_prefers_split(a.s)))
-    return launch_step_small(a, st);
+  int k = a.s.step_kernel;  // 0 auto, 1 split, 2 whole, 3 halves
+  if (k == 0) {
+    const bool halves = step_prefers_halves(a.s) && (long)a.s.B * (a.s.Hq / 4) * 2 >= 128;
+    k = halves ? 3 : step_prefers_split(a.s) ? 1 : step_prefers_halves(a.s) ? 3 : 2;
+  }
+  if (k == 1) return launch_step_small(a, st);
+  if (k == 3) return step_halves(a, st);
   return a.s.dtype == 1 ? step_d<bf16, false>(a, st) : step_d<float, false>(a, st);
 }
 

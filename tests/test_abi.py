@@ -354,8 +354,16 @@ def test_step_kernel_flags():
     p = [_addr(i) for i in range(11)]
     step = lambda dims: lib.hybrid_attn_step(ctypes.byref(dims), *p[:7], None, None, p[10], None)
     assert step(_dims(flags=hb.HYB_STEP_SPLIT | hb.HYB_STEP_WHOLE)) == 2
-    assert "together" in hb.last_error()
-    assert step(_dims(flags=8)) == 2
+    assert "more than one" in hb.last_error()
+    assert step(_dims(flags=hb.HYB_STEP_WHOLE | hb.HYB_STEP_HALVES)) == 2
+    assert step(_dims(flags=16)) == 2
+    # the column-split kernel: bf16, feat_dim <= 128, Hq / Hkv a multiple of 4
+    for kw in (dict(dtype=hb.HYB_F32), dict(feat_dim=256), dict(n_kv_heads=8)):
+        assert step(_dims(flags=hb.HYB_STEP_HALVES, **kw)) == 5, kw
+        assert "HYB_STEP_HALVES" in hb.last_error()
+    d = _dims(flags=hb.HYB_STEP_HALVES)
+    assert lib.hybrid_state_commit(ctypes.byref(d), *p[:5], None, None, None) == 2
+    assert "hybrid_attn_step only" in hb.last_error()
     # the other entry points reject them
     d = _dims(flags=hb.HYB_STEP_SPLIT)
     assert lib.hybrid_state_commit(ctypes.byref(d), *p[:5], None, None, None) == 2

@@ -111,6 +111,12 @@ def test_block_len_step_fused_commit(shape):
                         block_len=bld, kernel="whole")
     torch.cuda.synchronize()
     _check_out(out, outs, lens, dt, "step [whole]")
+    if dt == "bf16" and dims.F <= 64 and (dims.Hq // dims.Hkv) % 4 == 0:
+        outh = _out_buf(q)
+        hb.hybrid_attn_step(q, k, v, W, al, state_dev(c["S"]), f32(c["z"]), slots=sd, out=outh,
+                            block_len=bld, kernel="halves")
+        torch.cuda.synchronize()
+        _check_out(outh, outs, lens, dt, "step [halves]")
     # the fused step+commit: the same output, and the state as the commits
     S1, z1 = state_dev(c["S"]), f32(c["z"])
     outf = _out_buf(q)
@@ -142,7 +148,7 @@ def test_full_block_len_equals_null(dt):
     a = hb.hybrid_attn_step(q, k, v, W, al, state_dev(c["S"]), f32(c["z"]), out_f32=True)
     b = hb.hybrid_attn_step(q, k, v, W, al, state_dev(c["S"]), f32(c["z"]), out_f32=True,
                             block_len=full)
-    for kern in ("split", "whole"):
+    for kern in ("split", "whole") + (("halves",) if dt == "bf16" else ()):
         x = hb.hybrid_attn_step(q, k, v, W, al, state_dev(c["S"]), f32(c["z"]), out_f32=True,
                                 kernel=kern)
         y = hb.hybrid_attn_step(q, k, v, W, al, state_dev(c["S"]), f32(c["z"]), out_f32=True,

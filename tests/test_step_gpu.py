@@ -14,9 +14,17 @@ from _helpers import (act, announce, assert_close, check_outputs, f32, host, i32
 pytestmark = pytest.mark.gpu
 
 
-# The step's two kernels: one wave per (request, head, 32-column slice),
-# and one workgroup per group of heads.  Every parity case runs both.
-KERNELS = ["split", "whole"]
+# The step's three kernels: one wave per (request, head, 32-column slice),
+# one workgroup per group of heads, and two workgroups per group of four
+# heads each taking half of the columns.  Every parity case runs each one
+# the shape supports (the column split: bf16, f <= 128, Hq / Hkv a multiple
+# of 4).
+KERNELS = ["split", "whole", "halves"]
+
+
+def kernels_for(dims):
+    ok = dims.dtype == "bf16" and dims.F <= 64 and (dims.Hq // dims.Hkv) % 4 == 0
+    return [k for k in KERNELS if k != "halves" or ok]
 
 
 def step_call(c, dims, slots=None, kernel=None):
@@ -34,7 +42,7 @@ def run_step(c, dims, slots=None, kernel=None):
 
 def check_step(c, dims, what, slots=None):
     ref = ref_step(c, slots)
-    for kernel in KERNELS:
+    for kernel in kernels_for(dims):
         check_outputs(step_call(c, dims, slots, kernel), ref, dims.dtype, f"{what} [{kernel}]")
 
 
@@ -123,8 +131,9 @@ def test_large_scores(dt):
     check_step(c, dims, "step large scores")
 
 
-def test_slots_and_bad_slot():
-    dims = synth.Dims(B=3, Hq=4, Hkv=2, d=128, L=32, F=64, dtype="bf16")
+@pytest.mark.parametrize("Hq", [4, 8])
+def test_slots_and_bad_slot(Hq):
+    dims = synth.Dims(B=3, Hq=Hq, Hkv=2, d=128, L=32, F=64, dtype="bf16")
     slots = np.array([4, 0, 2], np.int32)
     announce("step slots")
     c = make_case(dims, 64, seed=21, peaky=True, n_slots=5, slots=slots)
@@ -132,7 +141,7 @@ def test_slots_and_bad_slot():
     announce("step bad slot")
     bad = np.array([4, 7, -1], np.int32)
     good = ref_step(c, np.array([4, 0, 0], np.int32))[:1]
-    for kernel in KERNELS:
+    for kernel in kernels_for(dims):
         out = host(step_call(c, dims, bad, kernel)(True))
         assert np.isnan(out[1:]).all()
         assert_close(out[:1], good, "bf16", f"step valid row next to bad slots [{kernel}]")
@@ -170,16 +179,21 @@ def test_matches_commit_free_brute_force():
     check_outputs(step_call(c, dims), ref, "f32", "step tiny vs brute")
 
 
-@pytest.mark.parametrize("B", [1, 8, 16, 32])
+@pytest.mark.parametrize("B", [1, 8, 16, 20, 32, 48])
 def test_small_batch_kernels(B):
     """Batch sizes of decode1 and the paper's Table 3 (B = 8, 32), serving
-    shapes, peaky inputs, both kernels; the library's own choice is the split
-    kernel while its B * Hq * d/32 waves fit on the chip (1024), else the
-    per-head kernel."""
+    shapes, peaky inputs, every kernel; the library's own choice is the
+    column split while its 2 B Hq/4 workgroups fill 128 to 256 compute units,
+    else the split kernel while its B * Hq * d/32 waves fit on the chip
+    (1024), else the column split while its workgroups fit, else the per-head
+    kernel."""
     dims = synth.DECODE1.with_(B=B)
     announce(f"step small batch B={B}")
     c = make_case(dims, 96, seed=40 + B, peaky=True)
     check_step(c, dims, f"step B={B}")
     auto = run_step(c, dims)
-    want = "split" if B * dims.Hq * (dims.d // 32) <= 1024 else "whole"
+    groups2 = 2 * B * (dims.Hq // 4)
+    want = ("halves" if 128 <= groups2 <= 256
+            else "split" if B * dims.Hq * (dims.d // 32) <= 1024
+            else "halves" if groups2 <= 256 else "whole")
     assert np.array_equal(auto, run_step(c, dims, kernel=want)), f"automatic choice is not {want}"
