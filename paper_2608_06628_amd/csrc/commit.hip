@@ -189,6 +189,7 @@ static hipError_t commit_d(const CommitArgs& a, hipStream_t st) {
 }
 
 hipError_t launch_commit(const CommitArgs& a, hipStream_t st) {
+  if (commit_grouped_supported(a.s)) return launch_commit_grouped(a, st);
   return a.s.dtype == 1 ? commit_d<bf16>(a, st) : commit_d<float>(a, st);
 }
 

@@ -93,6 +93,11 @@ bool step_prefers_halves(const Shape& s);
 // place after the step has read them (the StepArgs state pointers must be
 // writable).
 hipError_t launch_step_commit(const StepArgs& a, hipStream_t st);
+// hybrid_state_commit with four query heads per workgroup sharing their K
+// and V (bf16, f <= d, Hq / Hkv a multiple of 4, F <= 64; otherwise the
+// per-head commit kernel).
+bool commit_grouped_supported(const Shape& s);
+hipError_t launch_commit_grouped(const CommitArgs& a, hipStream_t st);
 hipError_t launch_commit(const CommitArgs& a, hipStream_t st);
 hipError_t launch_prefill(const PrefillArgs& a, hipStream_t st);
 hipError_t launch_softmax_prefix(const SoftmaxPrefixArgs& a, hipStream_t st);

@@ -54,7 +54,9 @@ namespace hyb {
 // CS > 1 splits each head's output columns (and state columns) over CS
 // workgroups: each streams 1/CS of the state and writes 1/CS of the outputs,
 // and repeats the per-query block math (small batches, plain step only).
-template <typename T, int D, int F, int NW, bool CM = false, int CS = 1>
+// CO: the commit alone (hybrid_state_commit's grouped kernel): the block
+// waves form phi(K) and z, the state waves update S as it lands; no output.
+template <typename T, int D, int F, int NW, bool CM = false, int CS = 1, bool CO = false>
 struct StepCfg {
   typedef Mma16<T> M;
   typedef typename M::op_t op_t;
@@ -70,13 +72,14 @@ struct StepCfg {
   static constexpr int CBF = D / 16;      // 16-column blocks of the output
   static constexpr int CB = CBF / CS;     // ... taken by one workgroup
   static constexpr int RUNS = NPHI / 4;   // 16-byte state runs per column block
-  // Column blocks a state wave keeps in flight: 128 registers' worth.
-  static constexpr int NBUF0 = 128 / (RUNS * 4);
+  // Column blocks a state wave keeps in flight: 128 registers' worth (192
+  // for the commit alone, which holds no readout operands).
+  static constexpr int NBUF0 = (CO ? 192 : 128) / (RUNS * 4);
   static constexpr int NBUF = NBUF0 < 1 ? 1 : (NBUF0 > CB ? CB : NBUF0);
   // Column blocks converted to operands before the barrier (bf16 only):
   // enough to have every column block requested, within 64 registers.
   static constexpr int KPK0 = CB - NBUF, KPK1 = 64 / (KF * 4);
-  static constexpr int KPACK = E == 1 ? 0 : (KPK0 < KPK1 ? KPK0 : KPK1);
+  static constexpr int KPACK = (E == 1 || CO) ? 0 : (KPK0 < KPK1 ? KPK0 : KPK1);
   static constexpr int EPC = 16 / (int)sizeof(T);  // elements per 16 bytes
   static constexpr int VT_LD = 36;        // V^T row length (keys, padded)
   static constexpr int VITEMS = 16 * (D / EPC);    // (key pair, column group)
@@ -250,9 +253,10 @@ __device__ inline float rsum16(float x) {
   return row_reduce16(x, [](float a, float b) { return a + b; });
 }
 
-template <typename T, int D, int F, int NW, bool CM, int CS = 1>
+template <typename T, int D, int F, int NW, bool CM, int CS = 1, bool CO = false>
 __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a) {
-  typedef StepCfg<T, D, F, NW, CM, CS> C;
+  typedef StepCfg<T, D, F, NW, CM, CS, CO> C;
+  static_assert(!CO || (CM && C::EARLY), "the commit alone: early-commit shapes only");
   static_assert(CS == 1 || (!CM && sizeof(T) == 2), "column split: plain bf16 step only");
   typedef typename C::M M;
   typedef typename C::op_t op_t;
@@ -510,7 +514,15 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
       // its buffer is what the converted blocks need until then)
       if (cb + NBUF < CB && !(C::DEFER && cb + NBUF == CB - 1)) issue(cb + NBUF);
     }
-    if constexpr (C::EARLY) {
+    if constexpr (CO) {
+      // The commit alone: each column block is updated as it lands.
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb) {
+        update(cb);
+        if (cb + NBUF < CB) issue(cb + NBUF);
+      }
+      return;
+    } else if constexpr (C::EARLY) {
       // 7. With the early commit the readout folds run inside the update
       //    stream: once b phi(Q) is in LDS, S^T (b phi)^T of the blocks
       //    converted so far, from zero; then each later block is updated,
@@ -569,7 +581,7 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
             vb0 + (size_t)min(2 * kp + 1, Lc) * kstride + cg * C::EPC);
       }
     }
-    const float alpha_h = a.alpha[h];
+    const float alpha_h = CO ? 0.0f : a.alpha[h];
     op_t qop[QB][C::KD];
     T* const wst = reinterpret_cast<T*>(&sh.hd[w]);
     T* const qst = sh.wl[w].qk;
@@ -591,7 +603,7 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
     };
     if constexpr (C::DMA_W) stage(Wt_h, D, F, F - 1, wst);
     if constexpr (C::DMA_QK) {
-      stage(qb0, qstride, 32, Lc, qst);
+      if constexpr (!CO) stage(qb0, qstride, 32, Lc, qst);
       stage(kb0, kstride, 32, Lc, kst);
       stage(vb0, kstride, 32, Lc, vst);
     } else {
@@ -739,6 +751,7 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
       }
       lds_barrier_nodrain();
     }
+    if constexpr (CO) return;  // the commit alone: phi(K) and z were all
     if constexpr (C::DMA_QK) {
 #pragma unroll
       for (int r = 0; r < 2; ++r)
@@ -1122,6 +1135,39 @@ hipError_t launch_step(const StepArgs& a, hipStream_t st) {
   if (k == 1) return launch_step_small(a, st);
   if (k == 3) return step_halves(a, st);
   return a.s.dtype == 1 ? step_d<bf16, false>(a, st) : step_d<float, false>(a, st);
+}
+
+// hybrid_state_commit with four query heads per workgroup (bf16, f <= d,
+// Hq / Hkv a multiple of 4, F <= 64): the fused kernel's early commit
+// without the step, so K and V are read once per KV head group, phi(K) is
+// formed while the state streams in, and each state column block is
+// updated as it lands.
+bool commit_grouped_supported(const Shape& s) {
+  return s.dtype == 1 && s.F <= 64 && 2 * s.F <= s.D && s.Hkv > 0 && (s.Hq / s.Hkv) % 4 == 0;
+}
+
+template <int D, int F>
+static hipError_t commit_grouped_go(const StepArgs& a, hipStream_t st) {
+  static_assert(sizeof(typename StepCfg<bf16, D, F, 4, true, 1, true>::Smem) <= 160 * 1024, "LDS");
+  hipLaunchKernelGGL((hyb_step_kernel<bf16, D, F, 4, true, 1, true>), dim3(a.s.B * (a.s.Hq / 4)),
+                     dim3(kWave * 8), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_commit_grouped(const CommitArgs& c, hipStream_t st) {
+  if (!commit_grouped_supported(c.s)) return hipErrorInvalidValue;
+  StepArgs a{};
+  a.s = c.s;
+  a.k = c.k;
+  a.v = c.v;
+  a.W = c.W;
+  a.S = c.S;
+  a.z = c.z;
+  a.slots = c.slots;
+  a.block_len = c.block_len;
+  if (c.s.D == 128) return c.s.F == 32 ? commit_grouped_go<128, 32>(a, st) : commit_grouped_go<128, 64>(a, st);
+  if (c.s.D == 64 && c.s.F == 32) return commit_grouped_go<64, 32>(a, st);
+  return hipErrorInvalidValue;
 }
 
 // The step of a block's last denoising pass fused with its commit (the
