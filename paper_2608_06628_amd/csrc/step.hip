@@ -133,6 +133,11 @@ struct StepCfg {
   // second pass after the outputs.
   static constexpr bool EARLY = CM && DMA_QK && f <= D;
   static_assert(!EARLY || f * 64 <= (int)sizeof(HeadLds), "phi(K) lo parts in the head area");
+  // The early commit's staging of an updated column block (16 columns of f
+  // floats) in the head area, after the phi(K) lo rows.
+  static constexpr int UPD_STG = 32 * D * (int)sizeof(T);
+  static_assert(!EARLY || UPD_STG + 16 * f * 4 <= (int)sizeof(HeadLds), "update staging");
+  static_assert(!EARLY || (f / 4) % 16 == 0, "update staging swizzle");
   // Column blocks held as bf16 readout operands (those converted before b
   // phi(Q) is in LDS; with the early commit the later ones are folded as
   // they arrive).
@@ -451,13 +456,42 @@ __global__ __launch_bounds__(kWave * 2 * NW, 1) void hyb_step_kernel(StepArgs a)
     if (!slot_ok || Lb == 0) return;
     const T* const pkh = sh.wl[w].qk + 32 * D;
     const T* const pkl = reinterpret_cast<const T*>(&sh.hd[w]);
-    float* __restrict__ Sw = const_cast<float*>(a.S) + sbase * f * D;
     const op_t va = vt_op(cb, 0);
+    // The updated block goes out through LDS (the second half of the head
+    // area, free until a P V): in registers each lane holds 16 bytes of a
+    // column, so a direct store would write half-lines; staged as the
+    // block's 16 columns of f floats (16-byte chunk k of column i at
+    // k ^ (i % 16), conflict-free) it leaves as whole columns, 32 lanes per
+    // 512 contiguous bytes.
+    // (The commit alone; the fused kernel stores directly: its registers
+    // are taken by the readout operands.)
+    constexpr int CPC = f / 4;  // 16-byte chunks per column
+    f32x4* const stg = reinterpret_cast<f32x4*>(reinterpret_cast<char*>(&sh.hd[w]) + C::UPD_STG);
 #pragma unroll
     for (int rn = 0; rn < RUNS; ++rn) {
       f32x4 acc = M::mma(rows_op(pkh, rn * 16), va, buf[cb % NBUF][rn]);
       acc = M::mma(rows_op(pkl, rn * 16), va, acc);
-      *reinterpret_cast<f32x4*>(Sw + (size_t)C::column(cb, c16) * f + C::feature(rn * 4, quad)) = acc;
+      if constexpr (CO)
+        stg[c16 * CPC + ((rn * 4 + quad) ^ c16)] = acc;
+      else
+        __builtin_amdgcn_raw_buffer_store_b128(
+            __builtin_bit_cast(u32x4, acc), srs, slane + (C::feature(rn * 4, 0) - C::feature(0, 0)) * 4,
+            (C::column(cb, 0) - C::column(0, 0)) * f * 4, 0);
+    }
+    if constexpr (!CO) return;
+    // (buffer stores over the head's state: the block's column offset in
+    // the scalar offset, the lane's part in one VGPR; one chunk at a time)
+    const int rows = kWave / CPC;  // columns per instruction
+    const int c0 = lane / CPC, ch = lane % CPC;
+#pragma unroll
+    for (int j = 0; j < 16 / (kWave / CPC); ++j) {
+      const int col = j * rows + c0;
+      const f32x4 x = stg[col * CPC + (ch ^ col)];
+      __builtin_amdgcn_raw_buffer_store_b128(
+          __builtin_bit_cast(u32x4, x), srs,
+          ((C::column(0, col) - C::column(0, 0)) * f + ch * 4) * 4,
+          (C::column(cb, 0) - C::column(0, 0)) * f * 4, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
 
