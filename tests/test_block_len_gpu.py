@@ -30,6 +30,9 @@ CASES = [
     (4, 4, 2, 64, 17, 128, "bf16", 34, [17, 9, 3, 0], None),
     (3, 4, 1, 128, 32, 32, "bf16", 40, [-3, 40, 13], [2, 1, 0]),
     (2, 2, 2, 128, 16, 64, "f32", 48, [15, 7], None),
+    # four heads per KV head, f = 128: the grouped commit, the column-split
+    # step and the fused kernel's early commit, with slots
+    (4, 8, 2, 128, 32, 64, "bf16", 64, [32, 0, 19, 1], [1, 4, 0, 2]),
 ]
 
 

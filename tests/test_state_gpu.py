@@ -28,6 +28,10 @@ SHAPES = [
     (2, 16, 4, 128, 32, 64, "bf16", 256),
     (3, 4, 1, 64, 5, 64, "bf16", 20),
     (2, 8, 8, 128, 32, 128, "bf16", 64),
+    # the grouped commit kernel at its other shapes (bf16, four heads per KV
+    # head, f <= d): d = 64 with f = 64, and f = 64 with a 7-token block
+    (2, 8, 2, 64, 32, 32, "bf16", 48),
+    (1, 4, 1, 128, 7, 32, "bf16", 16),
 ]
 
 
@@ -44,8 +48,10 @@ def test_commit(shape):
     assert_state_delta(state_host(S), host(z), c["S"], c["z"], Sr, zr, dt, f"commit {shape}")
 
 
-def test_commit_slots_and_bad_slot():
-    dims = synth.Dims(B=3, Hq=4, Hkv=2, d=128, L=32, F=64, dtype="bf16")
+@pytest.mark.parametrize("Hq", [4, 8])
+def test_commit_slots_and_bad_slot(Hq):
+    """Hq = 4 over 2 KV heads takes the per-head kernel, Hq = 8 the grouped one."""
+    dims = synth.Dims(B=3, Hq=Hq, Hkv=2, d=128, L=32, F=64, dtype="bf16")
     slots = np.array([3, 0, 5], np.int32)
     announce("commit slots")
     c = make_case(dims, 32, seed=8, peaky=True, n_slots=6, slots=slots)
