@@ -133,11 +133,11 @@ struct StepCfg {
   // second pass after the outputs.
   static constexpr bool EARLY = CM && DMA_QK && f <= D;
   static_assert(!EARLY || f * 64 <= (int)sizeof(HeadLds), "phi(K) lo parts in the head area");
-  // The early commit's staging of an updated column block (16 columns of f
-  // floats) in the head area, after the phi(K) lo rows.
+  // The grouped commit's staging of an updated column block (16 columns of
+  // f floats) in the head area, after the phi(K) lo rows.
   static constexpr int UPD_STG = 32 * D * (int)sizeof(T);
-  static_assert(!EARLY || UPD_STG + 16 * f * 4 <= (int)sizeof(HeadLds), "update staging");
-  static_assert(!EARLY || (f / 4) % 16 == 0, "update staging swizzle");
+  static_assert(!CO || UPD_STG + 16 * f * 4 <= (int)sizeof(HeadLds), "update staging");
+  static_assert(!CO || (f / 4) % 16 == 0, "update staging swizzle");
   // Column blocks held as bf16 readout operands (those converted before b
   // phi(Q) is in LDS; with the early commit the later ones are folded as
   // they arrive).
