@@ -42,14 +42,24 @@ __global__ __launch_bounds__(kWave) void hyb_step_small_kernel(StepArgs a) {
   constexpr int f = 2 * F;
 
   const int lane = threadIdx.x, li = lane & 31, hh = lane >> 5;
+  // Every kernel argument in one round of scalar loads: fetched where each
+  // is first used, the later fields would wait behind the earlier ones, one
+  // round trip each, before the first global load could issue.
+  asm volatile("" ::"s"(a.s.B), "s"(a.s.Hq), "s"(a.s.Hkv), "s"(a.s.D), "s"(a.s.L), "s"(a.s.F), "s"(a.s.dtype),
+               "s"(a.s.n_slots), "s"(a.s.out_f32),
+               "s"(a.slots), "s"(a.block_len), "s"(a.out), "s"(a.alpha));
   const int Hq = a.s.Hq, Hkv = a.s.Hkv, L = a.s.L;
   // units (b, h, s): the slices of a head, then the heads of a KV group,
   // are neighbours (one XCD, one L2 for the Q, K, V and W rows they share)
   const int u = xcd_unit(blockIdx.x, a.s.B * Hq * NS);
   const int s = u % NS, bh = u / NS, b = bh / Hq, h = bh % Hq, g = h / (Hq / Hkv);
-  const int slot = __builtin_amdgcn_readfirstlane(a.slots ? a.slots[b] : b);
+  // the slot and the block length, both requested before either is waited for
+  int slot_v = b, lb_v = L;
+  if (a.slots) slot_v = a.slots[b];
+  if (a.block_len) lb_v = min(max(a.block_len[b], 0), L);
+  const int slot = __builtin_amdgcn_readfirstlane(slot_v);
   const bool slot_ok = slot >= 0 && slot < a.s.n_slots;
-  const int Lb = __builtin_amdgcn_readfirstlane(a.block_len ? min(max(a.block_len[b], 0), L) : L);
+  const int Lb = __builtin_amdgcn_readfirstlane(lb_v);
   if (Lb == 0) return;  // nothing to answer (uniform per wave)
   const int Lc = Lb - 1;
   const size_t qstride = (size_t)Hq * D, kstride = (size_t)Hkv * D;
@@ -61,9 +71,12 @@ __global__ __launch_bounds__(kWave) void hyb_step_small_kernel(StepArgs a) {
 
   // 1. Block operands (rows past Lb read row Lb-1, in bounds, then zeroed),
   //    then the state slice, so the block math can start while the state
-  //    is in flight.
-  op_t wop[NT][KD];
-  WFM::load_w((const T*)a.W + (size_t)h * F * D, li, hh, wop);
+  //    is in flight.  The loads are issued in the order of their first use
+  //    (loads return in order) and, on the bf16 path, number fewer than the
+  //    63 a wave can have outstanding, so that none of them waits for an
+  //    earlier one to return before it can issue: V and z arrive as whole
+  //    rows (two and one loads per lane) and are put into operand order
+  //    through LDS.
   // (padding rows and keys are masked after every load has been issued: a
   // select next to its load would make the wave wait for it there)
   op_t qop[KD], kop[KD], vop[KL];
@@ -75,17 +88,23 @@ __global__ __launch_bounds__(kWave) void hyb_step_small_kernel(StepArgs a) {
       qop[ks] = load_op<T>(qrow + ks * KW);
       kop[ks] = load_op<T>(krow + ks * KW);
     }
-    // V^T operand: column c0 + li at keys row_of(ks*E + e, hh), clamped
+  }
+  op_t wop[NT][KD];
+  WFM::load_w((const T*)a.W + (size_t)h * F * D, li, hh, wop);
+  // V rows: on bf16, key (lane / 4) + 16 j, columns c0 + 8 (lane % 4) + 0..7
+  // (rows past Lb read row Lb-1); on fp32 the V^T operand is gathered
+  // directly (column c0 + li at keys row_of(ks, hh))
+  constexpr int VR = E == 1 ? 1 : 2;
+  bf16x8 vraw[VR];
+  if constexpr (E == 1) {
     const T* vcol = vb + c0 + li;
 #pragma unroll
-    for (int ks = 0; ks < KL; ++ks) {
-      if constexpr (E == 1) {
-        vop[ks] = vcol[(size_t)min(row_of(ks, hh), Lc) * kstride];
-      } else {
+    for (int ks = 0; ks < KL; ++ks) vop[ks] = vcol[(size_t)min(row_of(ks, hh), Lc) * kstride];
+  } else {
 #pragma unroll
-        for (int e = 0; e < E; ++e) vop[ks][e] = vcol[(size_t)min(row_of(ks * E + e, hh), Lc) * kstride];
-      }
-    }
+    for (int j = 0; j < VR; ++j)
+      vraw[j] = *reinterpret_cast<const bf16x8*>(vb + (size_t)min((lane >> 2) + 16 * j, Lc) * kstride + c0 +
+                                                 8 * (lane & 3));
   }
   // State slice: column c0 + li of S_h (row c0 + li of the stored S_h^T),
   // features in the order of the phi registers (32p + row_of(ks*E + e, hh)
@@ -94,6 +113,22 @@ __global__ __launch_bounds__(kWave) void hyb_step_small_kernel(StepArgs a) {
   const size_t sbase = (size_t)(slot_ok ? slot : 0) * Hq + h;
   const float* __restrict__ srow = a.S + (sbase * D + c0 + li) * f;
   const float* __restrict__ zh = a.z + sbase * f;
+  // z: f/64 consecutive values per lane (put into the order of the phi
+  // registers through LDS), ahead of the state, which is needed last
+  constexpr int ZPL = f / kWave;
+  static_assert(ZPL == 1 || ZPL == 2 || ZPL == 4, "z is loaded as 1, 2 or 4 values per lane");
+  float zv[ZPL];
+  if constexpr (ZPL == 4) {
+    const f32x4 t = *reinterpret_cast<const f32x4*>(zh + 4 * lane);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) zv[e] = t[e];
+  } else if constexpr (ZPL == 2) {
+    const float2 t = *reinterpret_cast<const float2*>(zh + 2 * lane);
+    zv[0] = t.x;
+    zv[1] = t.y;
+  } else {
+    zv[0] = zh[lane];
+  }
   constexpr int NKF = f / KW;  // k-steps over the features
   float sv[NKF][E];
 #pragma unroll
@@ -112,14 +147,7 @@ __global__ __launch_bounds__(kWave) void hyb_step_small_kernel(StepArgs a) {
     }
   }
 
-  // z in the order of the phi registers, and the gate logit
-  f32x4 zr[NPAIR][4];
-#pragma unroll
-  for (int pp = 0; pp < NPAIR; ++pp)
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      zr[pp][j] = *reinterpret_cast<const f32x4*>(zh + pp * kTile + row_of(4 * j, hh));
-  const float alpha_h = a.alpha[h];
+  const float alpha_h = a.alpha[h];  // the gate logit
   // Every load is issued here, ahead of the block math: moved to their uses
   // (as the compiler would) the state and z loads would wait behind it, a
   // second round trip to memory.
@@ -130,15 +158,10 @@ __global__ __launch_bounds__(kWave) void hyb_step_small_kernel(StepArgs a) {
     qop[ks] = keep_if<T>(row_ok, qop[ks]);
     kop[ks] = keep_if<T>(row_ok, kop[ks]);
   }
+  if constexpr (E == 1) {
 #pragma unroll
-  for (int ks = 0; ks < KL; ++ks) {
-    if constexpr (E == 1) {
+    for (int ks = 0; ks < KL; ++ks)
       if (row_of(ks, hh) >= Lb) vop[ks] = 0.0f;
-    } else {
-#pragma unroll
-      for (int e = 0; e < E; ++e)
-        if (row_of(ks * E + e, hh) >= Lb) vop[ks][e] = (T)0.0f;
-    }
   }
 
   // 2. Scores of query li against the block keys (keys in rows), softmax.
@@ -161,6 +184,35 @@ __global__ __launch_bounds__(kWave) void hyb_step_small_kernel(StepArgs a) {
     den += p[i];
   }
   den += xor32(den);
+
+  // V^T of the slice ([column][key], rows padded against bank conflicts)
+  // and z through LDS, read back in operand order.  (One wave per
+  // workgroup: the barrier only orders the LDS accesses.)
+  __shared__ float zs[f];
+  __shared__ T vt[kTile][kTile + 4];
+#pragma unroll
+  for (int e = 0; e < ZPL; ++e) zs[ZPL * lane + e] = zv[e];
+  if constexpr (E != 1) {
+#pragma unroll
+    for (int j = 0; j < VR; ++j)
+#pragma unroll
+      for (int c = 0; c < 8; ++c) vt[8 * (lane & 3) + c][(lane >> 2) + 16 * j] = vraw[j][c];
+  }
+  __syncthreads();
+  f32x4 zr[NPAIR][4];
+#pragma unroll
+  for (int pp = 0; pp < NPAIR; ++pp)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) zr[pp][j] = *reinterpret_cast<const f32x4*>(&zs[pp * kTile + row_of(4 * j, hh)]);
+  if constexpr (E != 1) {
+#pragma unroll
+    for (int ks = 0; ks < KL; ++ks) {
+      vop[ks] = lds_op_perm<T>(&vt[li][0], ks, hh, 0);
+#pragma unroll
+      for (int e = 0; e < E; ++e)
+        if (row_of(ks * E + e, hh) >= Lb) vop[ks][e] = (T)0.0f;
+    }
+  }
 
   // 3. phi(q_li) and lin_den = phi(q_li) . z.
   float phi[NPAIR][16];
